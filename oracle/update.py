@@ -1,0 +1,145 @@
+"""Oracle of the delayed optimizer update (Alg. 1 of §2) with AdamW as the update function u,
+the Error-Feedback correction of §3.2 and its lambda-scaled form (App. A.4).
+
+TEST INFRASTRUCTURE: only the tests, the smoke check and the bench's CPU-baseline leg may use this
+package.  It shares no code with the HIP path.
+
+Alg. 1, one iteration t (g_{-1} = 0, u_{-1} = 0):
+    compute g_t at x_t
+    feed g_{t-1} to the optimizer statistics and form u_{t-1}(g_{t-1})
+    standard async, or t <= 1:  x_{t+1} = x_t - u_{t-1}
+    Error Feedback:             x_{t+1} = x_t - u_{t-1} - lambda (u_{t-1} - u_{t-2})
+(lambda = 1 is the equation of §3.2; lambda = 0 is standard async.)  With delay 0 the same
+update consumes g_t instead, which is plain synchronous AdamW.
+
+u is decoupled AdamW (§2: beta = (0.9, 0.95); App. E.1: weight decay 0.1, clipping at 1.0):
+    g <- c g,  c = min(1, clip / (||g||_2 + 1e-6))        (global norm over the stage)
+    m <- b1 m + (1 - b1) g;   v <- b2 v + (1 - b2) g^2
+    u  = lr ( (m / (1 - b1^k)) / (sqrt(v / (1 - b2^k)) + eps) + wd x_t )
+with k the number of updates applied so far including this one, weight decay on the current
+weights x_t (the form Alg. 2 of §4 writes, U = eta (O + lambda X_t)), and the following readings
+where the paper is silent: eps = 1e-8; the clip epsilon 1e-6; weight decay on every parameter;
+step t = 0 changes nothing (the zero gradient g_{-1} is not fed to the statistics, so the first
+real update has k = 1); the EF buffer holds the whole previous update u_{t-2}, learning rate and
+weight decay included.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import Dict, Optional
+
+import numpy as np
+
+
+@dataclass
+class HParams:
+    lr: float = 1e-3
+    beta1: float = 0.9
+    beta2: float = 0.95
+    eps: float = 1e-8
+    weight_decay: float = 0.1
+    clip_norm: float = 1.0       # <= 0 disables clipping
+    ef_lambda: float = 0.0       # 0: standard async; 1: Error Feedback of §3.2
+    delay: int = 1               # 1: Alg. 1; 0: synchronous
+
+
+class NonFiniteGradient(Exception):
+    pass
+
+
+def global_norm(grads: Dict[str, np.ndarray]) -> float:
+    """||g||_2 over every tensor of the stage, accumulated in float64."""
+    return math.sqrt(sum(float(np.sum(np.square(g.astype(np.float64)))) for g in grads.values()))
+
+
+def clip_coefficient(norm: float, clip: float) -> float:
+    """c = min(1, clip / (norm + 1e-6)); 1 when clipping is off."""
+    if clip <= 0:
+        return 1.0
+    return min(1.0, clip / (norm + 1e-6))
+
+
+def adamw_u(x, g, m, v, k: int, hp: HParams):
+    """One AdamW evaluation on already-clipped g.  Returns (u, m_new, v_new)."""
+    m1 = hp.beta1 * m + (1.0 - hp.beta1) * g
+    v1 = hp.beta2 * v + (1.0 - hp.beta2) * g * g
+    mhat = m1 / (1.0 - hp.beta1 ** k)
+    vhat = v1 / (1.0 - hp.beta2 ** k)
+    u = hp.lr * (mhat / (np.sqrt(vhat) + hp.eps) + hp.weight_decay * x)
+    return u, m1, v1
+
+
+def apply_update(x, u, u_prev, ef: bool, lam: float):
+    """x_{t+1} from x_t: standard x - u, or the lambda-scaled EF form x - u - lam (u - u_prev)."""
+    if ef:
+        return x - u - lam * (u - u_prev)
+    return x - u
+
+
+@dataclass
+class OptState:
+    """Everything Alg. 1 carries from one iteration to the next."""
+    x: Dict[str, np.ndarray]
+    m: Dict[str, np.ndarray]
+    v: Dict[str, np.ndarray]
+    u_prev: Dict[str, np.ndarray]           # u_{t-2} at iteration t (zero before any update)
+    pending: Optional[Dict[str, np.ndarray]] = None  # g_{t-1}, not yet consumed
+    n_updates: int = 0                      # updates applied so far
+    t: int = 0                              # next iteration index
+
+    @staticmethod
+    def create(x: Dict[str, np.ndarray], dt=np.float64) -> "OptState":
+        xx = {k: np.array(v, dtype=dt) for k, v in x.items()}
+        z = {k: np.zeros_like(v) for k, v in xx.items()}
+        return OptState(xx, {k: v.copy() for k, v in z.items()}, {k: v.copy() for k, v in z.items()},
+                        {k: v.copy() for k, v in z.items()})
+
+    def copy(self) -> "OptState":
+        cp = lambda d: None if d is None else {k: v.copy() for k, v in d.items()}
+        return OptState(cp(self.x), cp(self.m), cp(self.v), cp(self.u_prev), cp(self.pending),
+                        self.n_updates, self.t)
+
+
+def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> dict:
+    """Second half of iteration t of Alg. 1, after g_t has been computed at x_t.
+
+    Mutates st into the state at iteration t+1 and returns diagnostics (applied, norm, clip)."""
+    if hp.delay not in (0, 1):
+        raise ValueError("delay must be 0 or 1")
+    if hp.delay == 0 and hp.ef_lambda != 0.0:
+        raise ValueError("Error Feedback needs a delayed gradient (delay 1)")
+    if hp.delay == 1:
+        g_use = st.pending
+    else:
+        g_use = g_t
+    info = dict(applied=False, norm=0.0, clip=1.0)
+    if g_use is not None:
+        norm = global_norm(g_use)
+        if not math.isfinite(norm):
+            raise NonFiniteGradient(f"non-finite gradient norm at iteration {st.t}")
+        c = clip_coefficient(norm, hp.clip_norm)
+        k = st.n_updates + 1
+        ef = hp.ef_lambda != 0.0 and st.n_updates >= 1   # "t <= 1": the first update is standard
+        for name in st.x:
+            g = g_use[name] * c
+            u, st.m[name], st.v[name] = adamw_u(st.x[name], g, st.m[name], st.v[name], k, hp)
+            st.x[name] = apply_update(st.x[name], u, st.u_prev[name], ef, hp.ef_lambda)
+            st.u_prev[name] = u
+        st.n_updates = k
+        info.update(applied=True, norm=norm, clip=c)
+    st.pending = {k: v.copy() for k, v in g_t.items()} if hp.delay == 1 else None
+    st.t += 1
+    return info
+
+
+def flat_update(x, g, m, v, u_prev, t: int, hp: HParams, clip_scale: float = 1.0):
+    """Elementwise form on flat arrays for a fixed delay-1 run: iteration t consumes g (= g_{t-1}).
+
+    t = 0 is a no-op; the update is the k = t-th; EF applies from t = 2 on.  Returns the new
+    (x, m, v, u_prev)."""
+    if t == 0:
+        return x, m, v, u_prev
+    u, m1, v1 = adamw_u(x, g * clip_scale, m, v, t, hp)
+    ef = hp.ef_lambda != 0.0 and t >= 2
+    return apply_update(x, u, u_prev, ef, hp.ef_lambda), m1, v1, u
