@@ -1,0 +1,166 @@
+/*
+ * asyncstage.h - C ABI of one pipeline stage's training step under a one-step gradient delay,
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The method (One-Step Gradient Delay is Not a Barrier for Large-Scale Asynchronous Pipeline
+ * Parallel LLM Pretraining):
+ *   - §2, Alg. 1 (Delayed Gradient Update): iteration t computes g_t at x_t, feeds g_{t-1} to the
+ *     optimizer statistics and sets x_{t+1} = x_t - u_{t-1}(g_{t-1}); g_{-1} = 0, u_{-1} = 0.
+ *   - §3.2, Error-Feedback equation: x_{t+1} = x_t - 2 u_{t-1}(g_{t-1}) + u_{t-2}(g_{t-2}) for
+ *     t >= 2, and App. A.4 its lambda-scaled form x_{t+1} = x_t - u_{t-1} - lambda (u_{t-1} - u_{t-2}).
+ *   - §2 and App. E.1: u is decoupled AdamW, betas (0.9, 0.95), weight decay 0.1, global-norm
+ *     gradient clipping at 1.0; Alg. 2 (§4) puts the weight decay on the current weights x_t.
+ *   - §2 / App. F.1: PipeDream-2BW keeps one stashed weight version, so a stage holds two compute
+ *     copies of its weights (versions t mod 2) and two gradient buffers (g_t being accumulated,
+ *     g_{t-1} being consumed).
+ *   - App. E.2: the stage is a stack of Llama-style decoder blocks (pre-norm RMSNorm, grouped-query
+ *     causal attention with RoPE, SwiGLU feed-forward, no biases); a first stage owns the token
+ *     embedding, a last stage the tied LM head with next-token cross-entropy (App. E).
+ *
+ * Conventions
+ *   - Every function returns a stage_status; no C++ exception crosses the ABI.  On error,
+ *     stage_last_error() returns a message (thread-local, valid until the next call).
+ *   - The library never allocates device memory.  The caller allocates one arena of
+ *     stage_required_bytes() and every input/output buffer; all pointers stay owned by the caller.
+ *   - All device work is enqueued asynchronously on the HIP stream given to stage_init (or to
+ *     delayed_update_flat).  Host pointers are never retained.  The caller synchronises.
+ *   - Device pointers must be 16-byte aligned.  Layouts are row-major, last index contiguous.
+ *   - Token ids are int32 in [0, vocab); ids outside that range give STAGE_EINVAL only when the
+ *     caller asks for validation (stage_validate_tokens); the kernels clamp nothing.
+ *   - One stage_t per host thread; calls on one stage_t must not overlap.
+ */
+#ifndef ASYNCSTAGE_H
+#define ASYNCSTAGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct stage stage_t; /* opaque */
+
+typedef enum {
+  STAGE_OK = 0,
+  STAGE_EINVAL = -1,     /* bad argument or shape                                  */
+  STAGE_ENOSPACE = -2,   /* arena smaller than stage_required_bytes()              */
+  STAGE_EHIP = -3,       /* a HIP runtime call failed                              */
+  STAGE_ESTATE = -4,     /* call out of the documented order                       */
+  STAGE_ENONFINITE = -5  /* reported by stage_poll_nonfinite                       */
+} stage_status;
+
+typedef enum { STAGE_DT_F32 = 0, STAGE_DT_BF16 = 1, STAGE_DT_I32 = 2 } stage_dtype;
+
+/* Shape of one stage.  dtype 0: fp32 compute and storage; 1: bf16 compute copies, bf16
+ * activations, fp32 accumulation, fp32 master weights / optimizer state / gradients.
+ * vocab > 0 requires first_stage (token embedding [vocab, d_model]); last_stage requires
+ * tie_embedding and vocab > 0 (logits = RMSNorm(x) E^T).  head_dim in {32, 64, 128};
+ * n_heads a multiple of n_kv_heads; d_model a multiple of 64.  max_inflight >= 1 is the number
+ * of activation slots (microbatches whose backward is pending). */
+typedef struct {
+  int32_t n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ffn;
+  int32_t vocab, first_stage, last_stage, tie_embedding;
+  int32_t seq_len, micro_batch, max_inflight;
+  int32_t dtype;
+  float rms_eps, rope_theta;
+} stage_shape_t;
+
+/* Hyper-parameters of one update.  clip_norm <= 0 disables clipping.  ef_lambda = 0 is standard
+ * delayed training, 1 the Error-Feedback equation of §3.2.  delay 1 is Alg. 1; delay 0 is
+ * synchronous AdamW (requires ef_lambda = 0). */
+typedef struct {
+  float lr, beta1, beta2, eps, weight_decay, clip_norm, ef_lambda;
+  int32_t delay;
+} update_hparams_t;
+
+/* Bytes of device memory the stage needs (weights, optimizer state, two gradient buffers, two
+ * compute versions, the activation ring and scratch).  0 on an invalid shape. */
+size_t stage_required_bytes(const stage_shape_t* shape);
+
+/* Carve the arena (device memory, >= stage_required_bytes, 256-byte aligned) and zero the
+ * optimizer state.  The master weights are left for the caller to fill through stage_tensor(),
+ * followed by stage_sync_weights().  hip_stream: a hipStream_t (NULL = default stream). */
+int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void* hip_stream,
+               stage_t** out);
+
+/* Number of named tensors exposed by stage_tensor. */
+int stage_num_tensors(const stage_t* s, int32_t* count);
+
+/* Tensor idx: name, device pointer, element count and dtype (stage_dtype).  Names:
+ *   "embed", "blk{i}.attn_norm|wq|wk|wv|wo|ffn_norm|wgate|wup|wdown", "final_norm"  - fp32
+ *   master weights [out, in]; the same names prefixed "m.", "v.", "u_prev.", "grad0.", "grad1."
+ *   (fp32 optimizer state, EF buffer, the two gradient buffers) and "w0.", "w1." (the two
+ *   compute versions, bf16 or fp32); "flat.master|m|v|u_prev|grad0|grad1|w0|w1" for the whole
+ *   flat vectors (padding between tensors is zero and stays zero);
+ *   "act{slot}.blk{i}.{x|rstd1|n1|qkv|o|lse|h|rstd2|n2|gu|z}" and "act{slot}.{x0|y|logits}"
+ *   for the saved activations of an activation slot. */
+int stage_tensor(const stage_t* s, int32_t idx, const char** name, void** dev_ptr,
+                 int64_t* numel, int32_t* dtype);
+
+/* Look a tensor up by name; STAGE_EINVAL if absent. */
+int stage_tensor_by_name(const stage_t* s, const char* name, void** dev_ptr, int64_t* numel,
+                         int32_t* dtype);
+
+/* Copy the fp32 master weights into both compute versions (after the caller wrote them). */
+int stage_sync_weights(stage_t* s);
+
+/* Forward of one microbatch of optimizer step `step` at the weights x_step (compute version
+ * step mod 2), saving activations in slot `slot` (0 <= slot < max_inflight).
+ *   tokens  [micro_batch, seq_len] int32, device  (first stage; else NULL)
+ *   x_in    [micro_batch, seq_len, d_model] bf16/fp32 per dtype, device (non-first; else NULL)
+ *   targets [micro_batch, seq_len] int32, device  (last stage; else NULL)
+ *   y_out   [micro_batch, seq_len, d_model] device (non-last; may be NULL to keep it in the slot)
+ *   loss_dev one float, device (last stage: mean cross-entropy of this microbatch; else NULL)
+ * STAGE_ESTATE if compute version step mod 2 does not hold x_step. */
+int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens, const void* x_in,
+                  const int32_t* targets, void* y_out, float* loss_dev);
+
+/* Backward of the microbatch saved in `slot`; its parameter gradient is added to gradient buffer
+ * (step mod 2) - the first backward of a step overwrites it.  dy: upstream gradient
+ * [micro_batch, seq_len, d_model] (non-last stage; NULL on a last stage, whose loss is the mean
+ * cross-entropy divided by microbatches_per_step).  dx_out: gradient w.r.t. x_in (non-first
+ * stage; may be NULL).  STAGE_ESTATE if the slot holds no pending forward. */
+int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out,
+                   int32_t microbatches_per_step);
+
+/* Second half of iteration t of Alg. 1: with delay 1 consume g_{t-1} (the gradient of step t-1,
+ * complete), with delay 0 consume g_t; clip by the global norm; AdamW; standard or lambda-EF
+ * update of the master weights (EF from the second applied update on, the "t <= 1" rule); write
+ * x_{t+1} to compute version (t+1) mod 2.  Must be called once per t in increasing order; with
+ * delay 1 and t = 0 (no pending gradient) the weights are unchanged (u_{-1} = 0).  A non-finite
+ * gradient norm leaves x, m, v and the EF buffer untouched (x_{t+1} = x_t) and is counted on the
+ * device; see stage_poll_nonfinite.  STAGE_ESTATE on out-of-order t or an incomplete gradient. */
+int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp);
+
+/* Stateless fused update over flat device vectors of n elements (the update kernel alone):
+ * iteration t of a delay-1 run consumes g_prev (= g_{t-1}; fp32, or bf16 when g_is_bf16), with
+ * k = t the AdamW bias-correction index and EF from t >= 2; t = 0 only writes x_shadow.
+ * x, m, v, u_prev fp32 (read and written; u_prev may be NULL when ef_lambda = 0); x_shadow
+ * (written, bf16 when shadow_is_bf16 else fp32; may be NULL).  clip_scale_dev: device float
+ * multiplying g_prev, or NULL for 1.  hp->delay must be 1. */
+int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf16, float* m,
+                        float* v, float* u_prev, void* x_shadow, int32_t shadow_is_bf16,
+                        int64_t t, const update_hparams_t* hp, const float* clip_scale_dev,
+                        void* hip_stream);
+
+/* Ascending unique token ids of the microbatch in `slot` and their counts (after its backward
+ * on a first stage).  ids, counts: device int32 arrays of >= micro_batch*seq_len entries;
+ * n_unique: device int32. */
+int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts,
+                        int32_t* n_unique);
+
+/* Synchronise the stream and report how many updates were skipped for a non-finite gradient
+ * norm since the last poll (STAGE_ENONFINITE if any). */
+int stage_poll_nonfinite(stage_t* s, int64_t* skipped);
+
+/* Global L2 norm of gradient buffer `which` (0/1), computed on device into norm_dev (float). */
+int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev);
+
+const char* stage_last_error(void);
+void stage_destroy(stage_t* s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ASYNCSTAGE_H */

@@ -105,7 +105,9 @@ def stage_forward(params: Dict[str, np.ndarray], inp: Dict[str, np.ndarray], w, 
     else:
         out["y"] = x
         if "dy" in inp:
-            out["loss"] = float(np.sum(x.astype(np.float64) * inp["dy"].astype(np.float64)))
+            prod = x.astype(np.float64) * inp["dy"].astype(np.float64)
+            out["loss"] = float(np.sum(prod))
+            out["loss_abs"] = float(np.sum(np.abs(prod)))  # condition of the sum, for comparisons
     return out, saves
 
 

@@ -1,0 +1,75 @@
+// Host-side launchers of the stage's gfx950 kernels (internal to the library).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+// ------------------------------------------------------------------ update (update.hip)
+struct UpdateScalars {
+  float lr, b1, b2, omb1, omb2, bc1, bc2, eps, wd, lam, one_plus_lam;
+  int ef;     // 1: Error-Feedback form this call
+  int apply;  // 0: write the compute copy only (no pending gradient)
+};
+size_t norm_scratch_bytes();
+void launch_grad_norm(const void* g, bool g_bf16, int64_t n, float clip, double* partial,
+                      float* out2, int* flag, unsigned long long* skipped, hipStream_t st);
+void launch_fused_update(int64_t n, float* x, const void* g, bool g_bf16, float* m, float* v,
+                         float* up, void* shadow, int shadow_kind, const UpdateScalars& hs,
+                         const float* clip, const int* flag, hipStream_t st);
+void launch_cast_copy(int64_t n, const float* src, void* dst, bool dst_bf16, hipStream_t st);
+void launch_zero(void* p, int64_t bytes, hipStream_t st);
+
+// ------------------------------------------------------------------ elementwise (elementwise.hip)
+// `bf` selects bf16 storage (else fp32) for every activation / weight pointer of the call.
+void launch_embed_gather(bool bf, const int32_t* tok, const void* table, void* x0, int rows, int d,
+                         hipStream_t st);
+void launch_rmsnorm_fwd(bool bf, const void* x, const void* gamma, void* y, float* rstd, int rows,
+                        int d, float eps, hipStream_t st);
+// dx = resid + rstd * (dn*gamma - xhat * mean(dn*gamma*xhat)); dgamma partial sums per chunk of
+// RMS_CHUNK rows into partial[chunk][d].
+constexpr int RMS_CHUNK = 32;
+void launch_rmsnorm_bwd(bool bf, const void* dn, const void* x, const float* rstd,
+                        const void* gamma, const void* resid, void* dx, float* partial, int rows,
+                        int d, hipStream_t st);
+void launch_colsum_partials(const float* partial, int nchunks, int d, float* out, bool accumulate,
+                            hipStream_t st);
+void launch_rope(bool bf, void* qkv, int rows, int seq_len, int n_rot_heads, int head_dim, int ld,
+                 const float* cos_t, const float* sin_t, bool inverse, hipStream_t st);
+void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st);
+void launch_swiglu_bwd(bool bf, const void* dz, const void* gu, void* dgu, int rows, int f,
+                       hipStream_t st);
+// token sort for the embedding gradient: keys (tok << 14 | pos) ascending; n <= 16384
+void launch_token_sort(const int32_t* tok, int n, uint32_t* sorted, hipStream_t st);
+void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_start,
+                       int32_t* ids, int32_t* counts, int32_t* n_unique, hipStream_t st);
+void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted,
+                          const int32_t* row_start, int vocab, int d, float* de, bool accumulate,
+                          hipStream_t st);
+// cross-entropy rows: dlogits = (softmax - onehot) * scale (stored bf16/fp32), row_loss fp32
+void launch_ce_rows(bool bf, const float* logits, const int32_t* targets, int rows, int vocab,
+                    float scale, void* dlogits, float* row_loss, hipStream_t st);
+void launch_mean(const float* v, int n, float* out, hipStream_t st);
+
+// ------------------------------------------------------------------ GEMM (gemm.hip)
+// C[m, n] (+)= sum_k A(m, k) B(n, k).  A(m,k) = a_kmajor ? A[m*lda + k] : A[k*lda + m];
+// B(n,k) = b_kmajor ? B[n*ldb + k] : B[k*ldb + n].  Inputs bf16 or fp32 (bf), accumulation fp32.
+// out_f32: C is fp32 (beta 0: overwrite, 1: accumulate); else C has the input type.
+// resid (input type, leading dimension ldc) is added when non-null.
+struct GemmArgs {
+  int M, N, K;
+  const void* A; int lda; bool a_kmajor;
+  const void* B; int ldb; bool b_kmajor;
+  void* C; int ldc; bool out_f32; float beta;
+  const void* resid;
+};
+void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st);
+
+// ------------------------------------------------------------------ attention (attention.hip)
+// Causal grouped-query attention on the packed projection buffer qkv [B*s, (Hq + 2 Hkv) hd]
+// (query heads, then key heads, then value heads); o [B*s, Hq hd]; lse fp32 [B, Hq, s].
+struct AttnArgs {
+  int B, S, Hq, Hkv, hd;
+  const void* qkv; void* o; float* lse;
+  const void* dout; void* dqkv; float* delta;  // backward only; delta fp32 [B, Hq, s]
+};
+void launch_attention_fwd(bool bf, const AttnArgs& a, hipStream_t st);
+void launch_attention_bwd(bool bf, const AttnArgs& a, hipStream_t st);

@@ -1,0 +1,639 @@
+// Host side of the stage library: arena layout, named tensors, the weight-version and
+// gradient-buffer bookkeeping of the delayed update, and the kernel sequences of forward,
+// backward and update.  Every device operation is a kernel of this library on the stage's stream.
+//
+// Bookkeeping (PipeDream-2BW, §2; Alg. 1): compute version v = step mod 2 holds x_step while the
+// microbatches of that step run forward and backward; gradient buffer step mod 2 accumulates g_step;
+// delayed_update(t) reads g_{t-1} (delay 1) and writes x_{t+1} into version (t+1) mod 2, which
+// no pending microbatch reads any more.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/asyncstage.h"
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define HIP_OK(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess) return fail(STAGE_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t ALIGN = 256;
+size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+struct BlockOff {  // element offsets of one block's weights in the flat parameter vector
+  int64_t attn_norm, wqkv, wo, ffn_norm, wgu, wdown;
+};
+
+struct BlockAct {
+  void *x, *n1, *qkv, *o, *h, *n2, *gu, *z;
+  float *rstd1, *lse, *rstd2;
+};
+
+struct Slot {
+  std::vector<BlockAct> blk;
+  void* y;          // output of the last block [T, d]
+  void *hf;         // final norm output (last stage)
+  float *rstdf, *logits;
+  int32_t *tokens, *targets;
+  int64_t step = -1;
+  bool pending = false;
+};
+
+}  // namespace
+
+struct stage {
+  stage_shape_t sh;
+  hipStream_t st;
+  bool bf;
+  size_t esz;  // bytes per compute element
+  int T, qkvw, hqd;
+  // flat parameter layout
+  int64_t n_flat = 0, off_embed = -1, off_final = -1;
+  std::vector<BlockOff> boff;
+  // flat vectors
+  float *master, *m, *v, *u_prev, *grad[2];
+  void* ver[2];
+  // scratch
+  void *dA, *dB, *dh, *dn, *dz, *dgu, *do_, *dqkv, *dlog, *dhf;
+  float *delta, *rms_part, *row_loss, *cos_t, *sin_t, *norm_out;
+  double* norm_part;
+  int* flag;
+  unsigned long long* skipped;
+  uint32_t* sorted;
+  int32_t* row_start;
+  std::vector<Slot> slots;
+  // bookkeeping
+  int64_t version_step[2] = {-1, -1};
+  int64_t grad_step[2] = {-1, -1};
+  int grad_count[2] = {0, 0};
+  bool grad_consumed[2] = {true, true};
+  int64_t next_t = 0;
+  int64_t n_updates = 0;
+  unsigned long long skipped_seen = 0;
+  // named tensors
+  struct Named { std::string name; void* ptr; int64_t numel; int32_t dtype; };
+  std::vector<Named> named;
+
+  void* wptr(int ver_idx, int64_t off) const { return (char*)ver[ver_idx] + off * esz; }
+};
+
+namespace {
+
+int validate(const stage_shape_t* s) {
+  if (!s) return fail(STAGE_EINVAL, "null shape");
+  if (s->n_blocks < 0 || s->d_model <= 0 || s->n_heads <= 0 || s->n_kv_heads <= 0 ||
+      s->d_ffn <= 0 || s->seq_len <= 0 || s->micro_batch <= 0 || s->max_inflight <= 0)
+    return fail(STAGE_EINVAL, "non-positive dimension");
+  if (s->head_dim != 32 && s->head_dim != 64 && s->head_dim != 128)
+    return fail(STAGE_EINVAL, "head_dim must be 32, 64 or 128");
+  if (s->n_heads % s->n_kv_heads) return fail(STAGE_EINVAL, "n_heads % n_kv_heads != 0");
+  if (s->d_model % 64 || s->d_ffn % 64) return fail(STAGE_EINVAL, "d_model, d_ffn must be multiples of 64");
+  if (s->d_model > 4096) return fail(STAGE_EINVAL, "d_model > 4096 not supported");
+  if (s->dtype != 0 && s->dtype != 1) return fail(STAGE_EINVAL, "dtype must be 0 (fp32) or 1 (bf16)");
+  if (s->vocab < 0 || s->vocab >= (1 << 17)) return fail(STAGE_EINVAL, "vocab out of range");
+  if (s->vocab > 0 && !s->first_stage) return fail(STAGE_EINVAL, "embedding requires first_stage");
+  if (s->first_stage && s->vocab == 0) return fail(STAGE_EINVAL, "first_stage requires vocab > 0");
+  if (s->last_stage && (!s->tie_embedding || !s->first_stage))
+    return fail(STAGE_EINVAL, "a last stage needs the tied embedding (first_stage, tie_embedding)");
+  const int64_t T = (int64_t)s->seq_len * s->micro_batch;
+  if (T > (1 << 24)) return fail(STAGE_EINVAL, "too many tokens per microbatch");
+  if (s->first_stage && T > 16384) return fail(STAGE_EINVAL, "first stage: at most 16384 tokens per microbatch");
+  return STAGE_OK;
+}
+
+// Lays the arena out; with base == nullptr only computes the size.
+size_t layout(stage* S, char* base) {
+  const stage_shape_t& sh = S->sh;
+  const int64_t d = sh.d_model, f = sh.d_ffn, hd = sh.head_dim;
+  const int64_t T = (int64_t)sh.seq_len * sh.micro_batch;
+  const int64_t qkvw = (int64_t)(sh.n_heads + 2 * sh.n_kv_heads) * hd, hqd = (int64_t)sh.n_heads * hd;
+  const size_t esz = sh.dtype == 1 ? 2 : 4;
+  // flat parameter vector: groups aligned to 64 elements (256 bytes of fp32)
+  int64_t n = 0;
+  auto take = [&](int64_t cnt) { int64_t o = n; n += (cnt + 63) / 64 * 64; return o; };
+  S->boff.clear();
+  S->off_embed = sh.vocab > 0 ? take((int64_t)sh.vocab * d) : -1;
+  for (int i = 0; i < sh.n_blocks; ++i) {
+    BlockOff b;
+    b.attn_norm = take(d);
+    b.wqkv = take(qkvw * d);
+    b.wo = take(d * hqd);
+    b.ffn_norm = take(d);
+    b.wgu = take(2 * f * d);
+    b.wdown = take(d * f);
+    S->boff.push_back(b);
+  }
+  S->off_final = sh.last_stage ? take(d) : -1;
+  S->n_flat = n;
+  size_t off = 0;
+  auto carve = [&](size_t bytes) -> void* { void* p = base ? base + off : nullptr; off += up(bytes); return p; };
+  S->master = (float*)carve(n * 4);
+  S->m = (float*)carve(n * 4);
+  S->v = (float*)carve(n * 4);
+  S->u_prev = (float*)carve(n * 4);
+  S->grad[0] = (float*)carve(n * 4);
+  S->grad[1] = (float*)carve(n * 4);
+  S->ver[0] = carve(n * esz);
+  S->ver[1] = carve(n * esz);
+  // activation slots
+  S->slots.assign(sh.max_inflight, Slot());
+  for (auto& sl : S->slots) {
+    sl.blk.resize(sh.n_blocks);
+    for (auto& b : sl.blk) {
+      b.x = carve(T * d * esz);
+      b.rstd1 = (float*)carve(T * 4);
+      b.n1 = carve(T * d * esz);
+      b.qkv = carve(T * qkvw * esz);
+      b.o = carve(T * hqd * esz);
+      b.lse = (float*)carve((int64_t)sh.micro_batch * sh.n_heads * sh.seq_len * 4);
+      b.h = carve(T * d * esz);
+      b.rstd2 = (float*)carve(T * 4);
+      b.n2 = carve(T * d * esz);
+      b.gu = carve(T * 2 * f * esz);
+      b.z = carve(T * f * esz);
+    }
+    sl.y = carve(T * d * esz);
+    sl.tokens = sh.first_stage ? (int32_t*)carve(T * 4) : nullptr;
+    sl.targets = sh.last_stage ? (int32_t*)carve(T * 4) : nullptr;
+    sl.hf = sh.last_stage ? carve(T * d * esz) : nullptr;
+    sl.rstdf = sh.last_stage ? (float*)carve(T * 4) : nullptr;
+    sl.logits = sh.last_stage ? (float*)carve(T * (int64_t)sh.vocab * 4) : nullptr;
+  }
+  // scratch shared by all calls
+  S->dA = carve(T * d * esz);
+  S->dB = carve(T * d * esz);
+  S->dh = carve(T * d * esz);
+  S->dn = carve(T * d * esz);
+  S->dz = carve(T * f * esz);
+  S->dgu = carve(T * 2 * f * esz);
+  S->do_ = carve(T * hqd * esz);
+  S->dqkv = carve(T * qkvw * esz);
+  S->delta = (float*)carve((int64_t)sh.micro_batch * sh.n_heads * sh.seq_len * 4);
+  S->rms_part = (float*)carve(cdiv(T, RMS_CHUNK) * d * 4);
+  S->norm_part = (double*)carve(norm_scratch_bytes());
+  S->norm_out = (float*)carve(2 * 4);
+  S->flag = (int*)carve(4);
+  S->skipped = (unsigned long long*)carve(8);
+  S->cos_t = (float*)carve((int64_t)sh.seq_len * (hd / 2) * 4);
+  S->sin_t = (float*)carve((int64_t)sh.seq_len * (hd / 2) * 4);
+  S->sorted = sh.first_stage ? (uint32_t*)carve(T * 4) : nullptr;
+  S->row_start = sh.first_stage ? (int32_t*)carve(((int64_t)sh.vocab + 1) * 4) : nullptr;
+  S->dlog = sh.last_stage ? carve(T * (int64_t)sh.vocab * esz) : nullptr;
+  S->dhf = sh.last_stage ? carve(T * d * esz) : nullptr;
+  S->row_loss = sh.last_stage ? (float*)carve(T * 4) : nullptr;
+  return off;
+}
+
+void register_tensors(stage* S) {
+  const stage_shape_t& sh = S->sh;
+  const int64_t d = sh.d_model, f = sh.d_ffn, hd = sh.head_dim;
+  const int64_t T = (int64_t)sh.seq_len * sh.micro_batch;
+  const int32_t cdt = S->bf ? STAGE_DT_BF16 : STAGE_DT_F32;
+  struct P { std::string name; int64_t off, numel; };
+  std::vector<P> ps;
+  if (S->off_embed >= 0) ps.push_back({"embed", S->off_embed, (int64_t)sh.vocab * d});
+  for (int i = 0; i < sh.n_blocks; ++i) {
+    const BlockOff& b = S->boff[i];
+    const std::string p = "blk" + std::to_string(i) + ".";
+    const int64_t nq = (int64_t)sh.n_heads * hd * d, nk = (int64_t)sh.n_kv_heads * hd * d;
+    ps.push_back({p + "attn_norm", b.attn_norm, d});
+    ps.push_back({p + "wq", b.wqkv, nq});
+    ps.push_back({p + "wk", b.wqkv + nq, nk});
+    ps.push_back({p + "wv", b.wqkv + nq + nk, nk});
+    ps.push_back({p + "wo", b.wo, d * sh.n_heads * hd});
+    ps.push_back({p + "ffn_norm", b.ffn_norm, d});
+    ps.push_back({p + "wgate", b.wgu, f * d});
+    ps.push_back({p + "wup", b.wgu + f * d, f * d});
+    ps.push_back({p + "wdown", b.wdown, d * f});
+  }
+  if (S->off_final >= 0) ps.push_back({"final_norm", S->off_final, d});
+  struct V { std::string pre; void* base; size_t es; int32_t dt; };
+  const std::vector<V> vs = {{"", S->master, 4, STAGE_DT_F32},     {"m.", S->m, 4, STAGE_DT_F32},
+                             {"v.", S->v, 4, STAGE_DT_F32},        {"u_prev.", S->u_prev, 4, STAGE_DT_F32},
+                             {"grad0.", S->grad[0], 4, STAGE_DT_F32}, {"grad1.", S->grad[1], 4, STAGE_DT_F32},
+                             {"w0.", S->ver[0], S->esz, cdt},      {"w1.", S->ver[1], S->esz, cdt}};
+  for (const auto& vv : vs)
+    for (const auto& p : ps)
+      S->named.push_back({vv.pre + p.name, (char*)vv.base + p.off * vv.es, p.numel, vv.dt});
+  const char* flat_names[] = {"flat.master", "flat.m", "flat.v", "flat.u_prev", "flat.grad0", "flat.grad1", "flat.w0", "flat.w1"};
+  for (size_t k = 0; k < vs.size(); ++k)
+    S->named.push_back({flat_names[k], vs[k].base, S->n_flat, vs[k].dt});
+  const int64_t lse_n = (int64_t)sh.micro_batch * sh.n_heads * sh.seq_len;
+  for (size_t si = 0; si < S->slots.size(); ++si) {
+    const Slot& sl = S->slots[si];
+    const std::string a = "act" + std::to_string(si) + ".";
+    for (int i = 0; i < sh.n_blocks; ++i) {
+      const BlockAct& b = sl.blk[i];
+      const std::string p = a + "blk" + std::to_string(i) + ".";
+      S->named.push_back({p + "x", b.x, T * d, cdt});
+      S->named.push_back({p + "rstd1", b.rstd1, T, STAGE_DT_F32});
+      S->named.push_back({p + "n1", b.n1, T * d, cdt});
+      S->named.push_back({p + "qkv", b.qkv, T * S->qkvw, cdt});
+      S->named.push_back({p + "o", b.o, T * S->hqd, cdt});
+      S->named.push_back({p + "lse", b.lse, lse_n, STAGE_DT_F32});
+      S->named.push_back({p + "h", b.h, T * d, cdt});
+      S->named.push_back({p + "rstd2", b.rstd2, T, STAGE_DT_F32});
+      S->named.push_back({p + "n2", b.n2, T * d, cdt});
+      S->named.push_back({p + "gu", b.gu, T * 2 * f, cdt});
+      S->named.push_back({p + "z", b.z, T * f, cdt});
+    }
+    S->named.push_back({a + "x0", sh.n_blocks > 0 ? sl.blk[0].x : sl.y, T * d, cdt});
+    S->named.push_back({a + "y", sl.y, T * d, cdt});
+    if (sl.logits) S->named.push_back({a + "logits", sl.logits, T * (int64_t)sh.vocab, STAGE_DT_F32});
+  }
+}
+
+GemmArgs gemm(int M, int N, int K, const void* A, int lda, bool ak, const void* B, int ldb, bool bk,
+              void* C, int ldc, bool out_f32 = false, float beta = 0.f, const void* resid = nullptr) {
+  GemmArgs g;
+  g.M = M; g.N = N; g.K = K;
+  g.A = A; g.lda = lda; g.a_kmajor = ak;
+  g.B = B; g.ldb = ldb; g.b_kmajor = bk;
+  g.C = C; g.ldc = ldc; g.out_f32 = out_f32; g.beta = beta; g.resid = resid;
+  return g;
+}
+
+AttnArgs attn_args(const stage* S, const BlockAct& b) {
+  AttnArgs a;
+  a.B = S->sh.micro_batch; a.S = S->sh.seq_len; a.Hq = S->sh.n_heads; a.Hkv = S->sh.n_kv_heads;
+  a.hd = S->sh.head_dim; a.qkv = b.qkv; a.o = b.o; a.lse = b.lse;
+  a.dout = nullptr; a.dqkv = nullptr; a.delta = nullptr;
+  return a;
+}
+
+void block_forward(stage* S, int vi, BlockAct& b, const BlockOff& w, void* y) {
+  const stage_shape_t& sh = S->sh;
+  const int T = S->T, d = sh.d_model, f = sh.d_ffn;
+  const bool bf = S->bf;
+  hipStream_t st = S->st;
+  launch_rmsnorm_fwd(bf, b.x, S->wptr(vi, w.attn_norm), b.n1, b.rstd1, T, d, sh.rms_eps, st);
+  launch_gemm(bf, gemm(T, S->qkvw, d, b.n1, d, true, S->wptr(vi, w.wqkv), d, true, b.qkv, S->qkvw), st);
+  launch_rope(bf, b.qkv, T, sh.seq_len, sh.n_heads + sh.n_kv_heads, sh.head_dim, S->qkvw, S->cos_t,
+              S->sin_t, false, st);
+  launch_attention_fwd(bf, attn_args(S, b), st);
+  launch_gemm(bf, gemm(T, d, S->hqd, b.o, S->hqd, true, S->wptr(vi, w.wo), S->hqd, true, b.h, d,
+                       false, 0.f, b.x), st);
+  launch_rmsnorm_fwd(bf, b.h, S->wptr(vi, w.ffn_norm), b.n2, b.rstd2, T, d, sh.rms_eps, st);
+  launch_gemm(bf, gemm(T, 2 * f, d, b.n2, d, true, S->wptr(vi, w.wgu), d, true, b.gu, 2 * f), st);
+  launch_swiglu_fwd(bf, b.gu, b.z, T, f, st);
+  launch_gemm(bf, gemm(T, d, f, b.z, f, true, S->wptr(vi, w.wdown), f, true, y, d, false, 0.f, b.h), st);
+}
+
+// dy: gradient of the block output; writes the gradient of the block input into dx.
+void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void* dy, void* dx,
+                    float* g, bool first) {
+  const stage_shape_t& sh = S->sh;
+  const int T = S->T, d = sh.d_model, f = sh.d_ffn;
+  const bool bf = S->bf;
+  const float beta = first ? 0.f : 1.f;
+  hipStream_t st = S->st;
+  const int nch = (int)cdiv(T, RMS_CHUNK);
+  // down projection: dz = dy Wd ; dWd (+)= dy^T z
+  launch_gemm(bf, gemm(T, f, d, dy, d, true, S->wptr(vi, w.wdown), f, false, S->dz, f), st);
+  launch_gemm(bf, gemm(d, f, T, dy, d, false, b.z, f, false, g + w.wdown, f, true, beta), st);
+  launch_swiglu_bwd(bf, S->dz, b.gu, S->dgu, T, f, st);
+  // gate/up: dn2 = dgu Wgu ; dWgu (+)= dgu^T n2
+  launch_gemm(bf, gemm(T, d, 2 * f, S->dgu, 2 * f, true, S->wptr(vi, w.wgu), d, false, S->dn, d), st);
+  launch_gemm(bf, gemm(2 * f, d, T, S->dgu, 2 * f, false, b.n2, d, false, g + w.wgu, d, true, beta), st);
+  launch_rmsnorm_bwd(bf, S->dn, b.h, b.rstd2, S->wptr(vi, w.ffn_norm), dy, S->dh, S->rms_part, T, d, st);
+  launch_colsum_partials(S->rms_part, nch, d, g + w.ffn_norm, !first, st);
+  // output projection: do = dh Wo ; dWo (+)= dh^T o
+  launch_gemm(bf, gemm(T, S->hqd, d, S->dh, d, true, S->wptr(vi, w.wo), S->hqd, false, S->do_, S->hqd), st);
+  launch_gemm(bf, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta), st);
+  AttnArgs a = attn_args(S, b);
+  a.dout = S->do_; a.dqkv = S->dqkv; a.delta = S->delta;
+  launch_attention_bwd(bf, a, st);
+  launch_rope(bf, S->dqkv, T, sh.seq_len, sh.n_heads + sh.n_kv_heads, sh.head_dim, S->qkvw, S->cos_t,
+              S->sin_t, true, st);
+  // qkv projection: dn1 = dqkv Wqkv ; dWqkv (+)= dqkv^T n1
+  launch_gemm(bf, gemm(T, d, S->qkvw, S->dqkv, S->qkvw, true, S->wptr(vi, w.wqkv), d, false, S->dn, d), st);
+  launch_gemm(bf, gemm(S->qkvw, d, T, S->dqkv, S->qkvw, false, b.n1, d, false, g + w.wqkv, d, true, beta), st);
+  launch_rmsnorm_bwd(bf, S->dn, b.x, b.rstd1, S->wptr(vi, w.attn_norm), S->dh, dx, S->rms_part, T, d, st);
+  launch_colsum_partials(S->rms_part, nch, d, g + w.attn_norm, !first, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* stage_last_error(void) { return g_err.c_str(); }
+
+size_t stage_required_bytes(const stage_shape_t* shape) {
+  if (validate(shape) != STAGE_OK) return 0;
+  stage tmp;
+  tmp.sh = *shape;
+  return layout(&tmp, nullptr);
+}
+
+int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void* hip_stream,
+               stage_t** out) {
+  if (!out) return fail(STAGE_EINVAL, "null out");
+  *out = nullptr;
+  int rc = validate(shape);
+  if (rc) return rc;
+  if (!arena || ((uintptr_t)arena % ALIGN)) return fail(STAGE_EINVAL, "arena must be 256-byte aligned");
+  stage* S = new stage();
+  S->sh = *shape;
+  S->st = (hipStream_t)hip_stream;
+  S->bf = shape->dtype == 1;
+  S->esz = S->bf ? 2 : 4;
+  S->T = shape->seq_len * shape->micro_batch;
+  S->qkvw = (shape->n_heads + 2 * shape->n_kv_heads) * shape->head_dim;
+  S->hqd = shape->n_heads * shape->head_dim;
+  const size_t need = layout(S, nullptr);
+  if (arena_bytes < need) {
+    delete S;
+    return fail(STAGE_ENOSPACE, "arena holds " + std::to_string(arena_bytes) + " bytes, needs " + std::to_string(need));
+  }
+  layout(S, (char*)arena);
+  register_tensors(S);
+  launch_zero(arena, (int64_t)need, S->st);
+  // RoPE tables: angle(p, i) = p * theta^(-2i/hd), evaluated in double
+  const int half = shape->head_dim / 2;
+  std::vector<float> c((size_t)shape->seq_len * half), s(c.size());
+  for (int p = 0; p < shape->seq_len; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double ang = p * std::pow((double)shape->rope_theta, -2.0 * i / shape->head_dim);
+      c[(size_t)p * half + i] = (float)std::cos(ang);
+      s[(size_t)p * half + i] = (float)std::sin(ang);
+    }
+  hipError_t e = hipMemcpyAsync(S->cos_t, c.data(), c.size() * 4, hipMemcpyHostToDevice, S->st);
+  if (e == hipSuccess) e = hipMemcpyAsync(S->sin_t, s.data(), s.size() * 4, hipMemcpyHostToDevice, S->st);
+  if (e == hipSuccess) e = hipStreamSynchronize(S->st);
+  if (e == hipSuccess) e = hipGetLastError();
+  if (e != hipSuccess) {
+    delete S;
+    return fail(STAGE_EHIP, std::string("stage_init: ") + hipGetErrorString(e));
+  }
+  *out = S;
+  return STAGE_OK;
+}
+
+int stage_num_tensors(const stage_t* s, int32_t* count) {
+  if (!s || !count) return fail(STAGE_EINVAL, "null argument");
+  *count = (int32_t)s->named.size();
+  return STAGE_OK;
+}
+
+int stage_tensor(const stage_t* s, int32_t idx, const char** name, void** dev_ptr, int64_t* numel,
+                 int32_t* dtype) {
+  if (!s || idx < 0 || idx >= (int32_t)s->named.size()) return fail(STAGE_EINVAL, "bad tensor index");
+  const auto& t = s->named[idx];
+  if (name) *name = t.name.c_str();
+  if (dev_ptr) *dev_ptr = t.ptr;
+  if (numel) *numel = t.numel;
+  if (dtype) *dtype = t.dtype;
+  return STAGE_OK;
+}
+
+int stage_tensor_by_name(const stage_t* s, const char* name, void** dev_ptr, int64_t* numel,
+                         int32_t* dtype) {
+  if (!s || !name) return fail(STAGE_EINVAL, "null argument");
+  for (const auto& t : s->named)
+    if (t.name == name) {
+      if (dev_ptr) *dev_ptr = t.ptr;
+      if (numel) *numel = t.numel;
+      if (dtype) *dtype = t.dtype;
+      return STAGE_OK;
+    }
+  return fail(STAGE_EINVAL, std::string("no tensor named ") + name);
+}
+
+int stage_sync_weights(stage_t* s) {
+  if (!s) return fail(STAGE_EINVAL, "null stage");
+  for (int k = 0; k < 2; ++k) launch_cast_copy(s->n_flat, s->master, s->ver[k], s->bf, s->st);
+  HIP_OK(hipGetLastError());
+  s->version_step[s->next_t % 2] = s->next_t;
+  s->version_step[(s->next_t + 1) % 2] = -1;
+  return STAGE_OK;
+}
+
+int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens, const void* x_in,
+                  const int32_t* targets, void* y_out, float* loss_dev) {
+  if (!s) return fail(STAGE_EINVAL, "null stage");
+  const stage_shape_t& sh = s->sh;
+  if (slot < 0 || slot >= sh.max_inflight) return fail(STAGE_EINVAL, "slot out of range");
+  if (step < 0 || s->version_step[step % 2] != step)
+    return fail(STAGE_ESTATE, "weights of step " + std::to_string(step) + " are not resident");
+  if (sh.first_stage && !tokens) return fail(STAGE_EINVAL, "first stage needs tokens");
+  if (!sh.first_stage && !x_in) return fail(STAGE_EINVAL, "non-first stage needs x_in");
+  if (sh.last_stage && (!targets || !loss_dev)) return fail(STAGE_EINVAL, "last stage needs targets and loss_dev");
+  Slot& sl = s->slots[slot];
+  if (sl.pending) return fail(STAGE_ESTATE, "slot holds a microbatch whose backward is pending");
+  const int vi = (int)(step % 2);
+  const int T = s->T, d = sh.d_model;
+  hipStream_t st = s->st;
+  void* x0 = sh.n_blocks > 0 ? sl.blk[0].x : sl.y;
+  if (sh.first_stage) {
+    HIP_OK(hipMemcpyAsync(sl.tokens, tokens, (size_t)T * 4, hipMemcpyDeviceToDevice, st));
+    launch_embed_gather(s->bf, sl.tokens, s->wptr(vi, s->off_embed), x0, T, d, st);
+  } else {
+    HIP_OK(hipMemcpyAsync(x0, x_in, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
+  }
+  for (int i = 0; i < sh.n_blocks; ++i) {
+    void* y = i + 1 < sh.n_blocks ? sl.blk[i + 1].x : sl.y;
+    block_forward(s, vi, sl.blk[i], s->boff[i], y);
+  }
+  if (sh.last_stage) {
+    HIP_OK(hipMemcpyAsync(sl.targets, targets, (size_t)T * 4, hipMemcpyDeviceToDevice, st));
+    launch_rmsnorm_fwd(s->bf, sl.y, s->wptr(vi, s->off_final), sl.hf, sl.rstdf, T, d, sh.rms_eps, st);
+    launch_gemm(s->bf, gemm(T, sh.vocab, d, sl.hf, d, true, s->wptr(vi, s->off_embed), d, true,
+                            sl.logits, sh.vocab, true, 0.f), st);
+    launch_ce_rows(s->bf, sl.logits, sl.targets, T, sh.vocab, 1.0f / T, s->dlog, s->row_loss, st);
+    launch_mean(s->row_loss, T, loss_dev, st);
+  }
+  if (y_out && !sh.last_stage)
+    HIP_OK(hipMemcpyAsync(y_out, sl.y, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
+  HIP_OK(hipGetLastError());
+  sl.step = step;
+  sl.pending = true;
+  return STAGE_OK;
+}
+
+int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32_t microbatches_per_step) {
+  if (!s) return fail(STAGE_EINVAL, "null stage");
+  const stage_shape_t& sh = s->sh;
+  if (slot < 0 || slot >= sh.max_inflight) return fail(STAGE_EINVAL, "slot out of range");
+  Slot& sl = s->slots[slot];
+  if (!sl.pending) return fail(STAGE_ESTATE, "slot holds no pending forward");
+  if (!sh.last_stage && !dy) return fail(STAGE_EINVAL, "non-last stage needs dy");
+  if (microbatches_per_step <= 0) return fail(STAGE_EINVAL, "microbatches_per_step must be positive");
+  const int64_t step = sl.step;
+  const int gb = (int)(step % 2), vi = gb;
+  if (s->grad_step[gb] != step) {
+    if (s->grad_step[gb] >= 0 && !s->grad_consumed[gb])
+      return fail(STAGE_ESTATE, "gradient buffer still holds the unconsumed gradient of step " +
+                                    std::to_string(s->grad_step[gb]));
+    s->grad_step[gb] = step;
+    s->grad_count[gb] = 0;
+    s->grad_consumed[gb] = false;
+  }
+  const bool first = s->grad_count[gb] == 0;
+  float* g = s->grad[gb];
+  const int T = s->T, d = sh.d_model;
+  const bool bf = s->bf;
+  hipStream_t st = s->st;
+  const void* cur = dy;
+  bool head_wrote_embed = false;
+  if (sh.last_stage) {
+    launch_ce_rows(bf, sl.logits, sl.targets, T, sh.vocab, 1.0f / ((float)T * microbatches_per_step),
+                   s->dlog, s->row_loss, st);
+    // dhf = dlogits E ; dE (+)= dlogits^T hf
+    launch_gemm(bf, gemm(T, d, sh.vocab, s->dlog, sh.vocab, true, s->wptr(vi, s->off_embed), d, false,
+                         s->dhf, d), st);
+    launch_gemm(bf, gemm(sh.vocab, d, T, s->dlog, sh.vocab, false, sl.hf, d, false, g + s->off_embed, d,
+                         true, first ? 0.f : 1.f), st);
+    head_wrote_embed = true;
+    launch_rmsnorm_bwd(bf, s->dhf, sl.y, sl.rstdf, s->wptr(vi, s->off_final), nullptr, s->dA,
+                       s->rms_part, T, d, st);
+    launch_colsum_partials(s->rms_part, (int)cdiv(T, RMS_CHUNK), d, g + s->off_final, !first, st);
+    cur = s->dA;
+  }
+  for (int i = sh.n_blocks - 1; i >= 0; --i) {
+    void* out = (cur == s->dA) ? s->dB : s->dA;
+    block_backward(s, vi, sl.blk[i], s->boff[i], cur, out, g, first);
+    cur = out;
+  }
+  if (sh.first_stage) {
+    const void* dx0 = cur;
+    launch_token_sort(sl.tokens, T, s->sorted, st);
+    launch_token_runs(s->sorted, T, sh.vocab, s->row_start, nullptr, nullptr, nullptr, st);
+    launch_embed_scatter(bf, dx0, s->sorted, s->row_start, sh.vocab, d, g + s->off_embed,
+                         head_wrote_embed || !first, st);
+  } else if (dx_out) {
+    HIP_OK(hipMemcpyAsync(dx_out, cur, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
+  }
+  HIP_OK(hipGetLastError());
+  s->grad_count[gb] += 1;
+  sl.pending = false;
+  return STAGE_OK;
+}
+
+int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
+  if (!s || !hp) return fail(STAGE_EINVAL, "null argument");
+  if (hp->delay != 0 && hp->delay != 1) return fail(STAGE_EINVAL, "delay must be 0 or 1");
+  if (hp->delay == 0 && hp->ef_lambda != 0.f) return fail(STAGE_EINVAL, "Error Feedback needs delay 1");
+  if (t != s->next_t) return fail(STAGE_ESTATE, "delayed_update: expected t = " + std::to_string(s->next_t));
+  const int64_t gstep = hp->delay == 1 ? t - 1 : t;  // the gradient this iteration consumes
+  bool apply = gstep >= 0;
+  int gb = 0;
+  if (apply) {
+    gb = (int)(gstep % 2);
+    if (s->grad_step[gb] != gstep || s->grad_count[gb] == 0 || s->grad_consumed[gb])
+      return fail(STAGE_ESTATE, "gradient of step " + std::to_string(gstep) + " is not available");
+    for (const auto& sl : s->slots)
+      if (sl.pending && sl.step == gstep)
+        return fail(STAGE_ESTATE, "a microbatch of step " + std::to_string(gstep) + " has not run backward");
+  }
+  const int vout = (int)((t + 1) % 2);
+  for (const auto& sl : s->slots)
+    if (sl.pending && sl.step % 2 == vout)
+      return fail(STAGE_ESTATE, "a pending microbatch still reads the version being overwritten");
+  UpdateScalars hs{};
+  const int64_t k = s->n_updates + 1;
+  hs.lr = hp->lr; hs.b1 = hp->beta1; hs.b2 = hp->beta2;
+  hs.omb1 = 1.0f - hp->beta1; hs.omb2 = 1.0f - hp->beta2;
+  hs.bc1 = (float)(1.0 - std::pow((double)hp->beta1, (double)k));
+  hs.bc2 = (float)(1.0 - std::pow((double)hp->beta2, (double)k));
+  hs.eps = hp->eps; hs.wd = hp->weight_decay; hs.lam = hp->ef_lambda;
+  hs.one_plus_lam = 1.0f + hp->ef_lambda;
+  hs.ef = (apply && hp->ef_lambda != 0.f && s->n_updates >= 1) ? 1 : 0;
+  hs.apply = apply ? 1 : 0;
+  const float* clip = nullptr;
+  const int* flag = nullptr;
+  if (apply && hp->clip_norm > 0.f) {
+    launch_grad_norm(s->grad[gb], false, s->n_flat, hp->clip_norm, s->norm_part, s->norm_out, s->flag,
+                     s->skipped, s->st);
+    clip = s->norm_out + 1;
+    flag = s->flag;
+  }
+  launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v,
+                      hp->ef_lambda != 0.f ? s->u_prev : nullptr, s->ver[vout], s->bf ? 2 : 1, hs,
+                      clip, flag, s->st);
+  HIP_OK(hipGetLastError());
+  if (apply) {
+    s->grad_consumed[gb] = true;
+    s->n_updates = k;
+  }
+  s->version_step[vout] = t + 1;
+  s->next_t = t + 1;
+  return STAGE_OK;
+}
+
+int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf16, float* m, float* v,
+                        float* u_prev, void* x_shadow, int32_t shadow_is_bf16, int64_t t,
+                        const update_hparams_t* hp, const float* clip_scale_dev, void* hip_stream) {
+  if (!hp || n < 0 || t < 0) return fail(STAGE_EINVAL, "bad argument");
+  if (hp->delay != 1) return fail(STAGE_EINVAL, "delayed_update_flat implements delay 1");
+  if (n == 0) return STAGE_OK;
+  if (!x || !g_prev || !m || !v) return fail(STAGE_EINVAL, "null vector");
+  if (hp->ef_lambda != 0.f && !u_prev) return fail(STAGE_EINVAL, "Error Feedback needs u_prev");
+  if (((uintptr_t)x | (uintptr_t)m | (uintptr_t)v | (uintptr_t)u_prev | (uintptr_t)x_shadow) % 16 ||
+      (uintptr_t)g_prev % 8)
+    return fail(STAGE_EINVAL, "vectors must be 16-byte aligned (g_prev 8-byte)");
+  UpdateScalars hs{};
+  const double k = (double)t;
+  hs.lr = hp->lr; hs.b1 = hp->beta1; hs.b2 = hp->beta2;
+  hs.omb1 = 1.0f - hp->beta1; hs.omb2 = 1.0f - hp->beta2;
+  hs.bc1 = t > 0 ? (float)(1.0 - std::pow((double)hp->beta1, k)) : 1.f;
+  hs.bc2 = t > 0 ? (float)(1.0 - std::pow((double)hp->beta2, k)) : 1.f;
+  hs.eps = hp->eps; hs.wd = hp->weight_decay; hs.lam = hp->ef_lambda;
+  hs.one_plus_lam = 1.0f + hp->ef_lambda;
+  hs.ef = (hp->ef_lambda != 0.f && t >= 2) ? 1 : 0;
+  hs.apply = t > 0 ? 1 : 0;
+  launch_fused_update(n, x, g_prev, g_is_bf16 != 0, m, v, hp->ef_lambda != 0.f ? u_prev : nullptr,
+                      x_shadow, x_shadow ? (shadow_is_bf16 ? 2 : 1) : 0, hs, clip_scale_dev, nullptr,
+                      (hipStream_t)hip_stream);
+  HIP_OK(hipGetLastError());
+  return STAGE_OK;
+}
+
+int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts, int32_t* n_unique) {
+  if (!s || !ids || !counts || !n_unique) return fail(STAGE_EINVAL, "null argument");
+  if (!s->sh.first_stage) return fail(STAGE_EINVAL, "not a first stage");
+  if (slot < 0 || slot >= s->sh.max_inflight) return fail(STAGE_EINVAL, "slot out of range");
+  const Slot& sl = s->slots[slot];
+  if (sl.step < 0) return fail(STAGE_ESTATE, "slot has not run forward");
+  launch_token_sort(sl.tokens, s->T, s->sorted, s->st);
+  launch_token_runs(s->sorted, s->T, s->sh.vocab, s->row_start, ids, counts, n_unique, s->st);
+  HIP_OK(hipGetLastError());
+  return STAGE_OK;
+}
+
+int stage_poll_nonfinite(stage_t* s, int64_t* skipped) {
+  if (!s) return fail(STAGE_EINVAL, "null stage");
+  HIP_OK(hipStreamSynchronize(s->st));
+  unsigned long long now = 0;
+  HIP_OK(hipMemcpy(&now, s->skipped, 8, hipMemcpyDeviceToHost));
+  const unsigned long long d = now - s->skipped_seen;
+  s->skipped_seen = now;
+  if (skipped) *skipped = (int64_t)d;
+  return d ? fail(STAGE_ENONFINITE, "non-finite gradient norm: update skipped") : STAGE_OK;
+}
+
+int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev) {
+  if (!s || !norm_dev || (which != 0 && which != 1)) return fail(STAGE_EINVAL, "bad argument");
+  launch_grad_norm(s->grad[which], false, s->n_flat, 0.f, s->norm_part, s->norm_out, nullptr, nullptr,
+                   s->st);
+  HIP_OK(hipMemcpyAsync(norm_dev, s->norm_out, 4, hipMemcpyDeviceToDevice, s->st));
+  HIP_OK(hipGetLastError());
+  return STAGE_OK;
+}
+
+void stage_destroy(stage_t* s) { delete s; }
+
+}  // extern "C"

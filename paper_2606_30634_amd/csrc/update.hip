@@ -1,0 +1,219 @@
+// Delayed optimizer update: global gradient norm (two deterministic passes) and the fused,
+// HBM-bound AdamW + delay + Error-Feedback pass over the flat fp32 master vector.
+//
+// Per element, iteration t consuming the gradient g of the previous step (Alg. 1, §2):
+//   g <- c g                                  c = min(1, clip / (||g|| + 1e-6))   (App. E.1)
+//   m <- b1 m + (1 - b1) g ;  v <- b2 v + (1 - b2) g^2                          (AdamW, §2)
+//   u  = lr ( (m / bc1) / (sqrt(v / bc2) + eps) + wd x_t )   bc_i = 1 - b_i^k   (Alg. 2 puts
+//                                                             the decay on x_t)
+//   x_{t+1} = x_t - u                      standard, or the first update ("t <= 1" of Alg. 1)
+//   x_{t+1} = x_t - (1 + lam) u + lam u_prev   Error Feedback (§3.2; lam-scaled form App. A.4)
+//   u_prev <- u ;  shadow <- cast(x_{t+1})    compute copy for the next step's forward
+// Memory traffic per element (fp32 g, EF, bf16 shadow): x, m, v, u_prev read+write (32 B),
+// g read (4 B), shadow write (2 B) = 38 B.  Every access is a 16-byte vector per thread,
+// consecutive threads on consecutive addresses.
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int NORM_BLOCKS = 1024;
+constexpr int NORM_THREADS = 256;
+
+template <typename G>
+__device__ __forceinline__ void load4(const G* p, int64_t i, float r[4]);
+template <>
+__device__ __forceinline__ void load4<float>(const float* p, int64_t i, float r[4]) {
+  float4 v = *reinterpret_cast<const float4*>(p + i);
+  r[0] = v.x; r[1] = v.y; r[2] = v.z; r[3] = v.w;
+}
+template <>
+__device__ __forceinline__ void load4<bf16>(const bf16* p, int64_t i, float r[4]) {
+  bf16x4 v = *reinterpret_cast<const bf16x4*>(p + i);
+  r[0] = (float)v[0]; r[1] = (float)v[1]; r[2] = (float)v[2]; r[3] = (float)v[3];
+}
+template <typename S>
+__device__ __forceinline__ void store4(S* p, int64_t i, const float r[4]);
+template <>
+__device__ __forceinline__ void store4<float>(float* p, int64_t i, const float r[4]) {
+  *reinterpret_cast<float4*>(p + i) = make_float4(r[0], r[1], r[2], r[3]);
+}
+template <>
+__device__ __forceinline__ void store4<bf16>(bf16* p, int64_t i, const float r[4]) {
+  bf16x4 v;
+  v[0] = (bf16)r[0]; v[1] = (bf16)r[1]; v[2] = (bf16)r[2]; v[3] = (bf16)r[3];
+  *reinterpret_cast<bf16x4*>(p + i) = v;
+}
+
+// Pass 1: block b sums g^2 over its contiguous range in double; partial[b].
+template <typename G>
+__global__ void __launch_bounds__(NORM_THREADS) sumsq_partial(const G* __restrict__ g, int64_t n,
+                                                              double* __restrict__ partial) {
+  __shared__ double sm[16];
+  const int64_t per = ((n + gridDim.x - 1) / gridDim.x + 3) & ~int64_t(3);
+  const int64_t lo = per * blockIdx.x;
+  const int64_t hi = lo + per < n ? lo + per : n;
+  double acc = 0.0;
+  int64_t i = lo + 4 * threadIdx.x;
+  for (; i + 3 < hi; i += 4 * blockDim.x) {
+    float r[4];
+    load4<G>(g, i, r);
+    acc += (double)r[0] * r[0] + (double)r[1] * r[1] + (double)r[2] * r[2] + (double)r[3] * r[3];
+  }
+  for (; i < hi; ++i) { float r = to_f32(g[i]); acc += (double)r * r; }  // ragged tail
+  acc = block_sum<double>(acc, sm);
+  if (threadIdx.x == 0) partial[blockIdx.x] = acc;
+}
+
+// Pass 2: one block sums the partials in a fixed order and derives the clip coefficient and the
+// non-finite flag.  out[0] = ||g||, out[1] = clip scale c; flag[0] = 1 when ||g|| is not finite;
+// skipped[0] counts non-finite norms.
+__global__ void __launch_bounds__(1024) norm_finish(const double* __restrict__ partial, int np,
+                                                   float clip, float* __restrict__ out,
+                                                   int* __restrict__ flag,
+                                                   unsigned long long* __restrict__ skipped) {
+  __shared__ double sm[16];
+  double acc = 0.0;
+  for (int i = threadIdx.x; i < np; i += blockDim.x) acc += partial[i];
+  acc = block_sum<double>(acc, sm);
+  if (threadIdx.x == 0) {
+    const double nrm = sqrt(acc);
+    const bool bad = !isfinite(nrm);
+    float c = 1.0f;
+    if (clip > 0.0f && !bad) c = (float)fmin(1.0, (double)clip / (nrm + 1e-6));
+    out[0] = (float)nrm;
+    out[1] = c;
+    if (flag) flag[0] = bad ? 1 : 0;
+    if (bad && skipped) skipped[0] += 1ull;
+  }
+}
+
+template <typename G, typename S, bool EF>
+__global__ void __launch_bounds__(256) fused_update(int64_t n, float* __restrict__ x,
+                                                    const G* __restrict__ g,
+                                                    float* __restrict__ m, float* __restrict__ v,
+                                                    float* __restrict__ up, S* __restrict__ shadow,
+                                                    UpdateScalars hs, const float* __restrict__ clip,
+                                                    const int* __restrict__ skip_flag) {
+  const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+  if (i >= n) return;
+  const bool skip = hs.apply == 0 || (skip_flag && skip_flag[0] != 0);
+  const float c = clip ? clip[0] : 1.0f;
+  if (i + 3 < n) {
+    float xr[4];
+    load4<float>(x, i, xr);
+    if (!skip) {
+      float gr[4], mr[4], vr[4], ur[4];
+      load4<G>(g, i, gr);
+      load4<float>(m, i, mr);
+      load4<float>(v, i, vr);
+      if (EF) load4<float>(up, i, ur);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float gg = gr[j] * c;
+        mr[j] = hs.b1 * mr[j] + hs.omb1 * gg;
+        vr[j] = hs.b2 * vr[j] + hs.omb2 * (gg * gg);
+        const float mhat = mr[j] / hs.bc1;
+        const float vhat = vr[j] / hs.bc2;
+        const float u = hs.lr * (mhat / (sqrtf(vhat) + hs.eps) + hs.wd * xr[j]);
+        if (EF && hs.ef) xr[j] = xr[j] - hs.one_plus_lam * u + hs.lam * ur[j];
+        else xr[j] = xr[j] - u;
+        ur[j] = u;
+      }
+      store4<float>(x, i, xr);
+      store4<float>(m, i, mr);
+      store4<float>(v, i, vr);
+      if (EF) store4<float>(up, i, ur);
+    }
+    if (shadow) store4<S>(shadow, i, xr);
+  } else {
+    for (int64_t k = i; k < n; ++k) {  // ragged tail of a flat vector whose length is not 4k
+      float xv = x[k];
+      if (!skip) {
+        const float gg = to_f32(g[k]) * c;
+        const float mm = hs.b1 * m[k] + hs.omb1 * gg;
+        const float vv = hs.b2 * v[k] + hs.omb2 * (gg * gg);
+        const float u = hs.lr * ((mm / hs.bc1) / (sqrtf(vv / hs.bc2) + hs.eps) + hs.wd * xv);
+        if (EF && hs.ef) xv = xv - hs.one_plus_lam * u + hs.lam * up[k];
+        else xv = xv - u;
+        m[k] = mm;
+        v[k] = vv;
+        if (EF) up[k] = u;
+        x[k] = xv;
+      }
+      if (shadow) shadow[k] = from_f32<S>(xv);
+    }
+  }
+}
+
+template <typename S>
+__global__ void __launch_bounds__(256) cast_copy(int64_t n, const float* __restrict__ src,
+                                                 S* __restrict__ dst) {
+  const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+  if (i + 3 < n) {
+    float r[4];
+    load4<float>(src, i, r);
+    store4<S>(dst, i, r);
+  } else {
+    for (int64_t k = i; k < n; ++k) dst[k] = from_f32<S>(src[k]);
+  }
+}
+
+__global__ void __launch_bounds__(256) zero_bytes(int64_t n16, int4* __restrict__ p) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n16) p[i] = make_int4(0, 0, 0, 0);
+}
+
+template <typename G, typename S, bool EF>
+void launch_update_t(int64_t n, float* x, const void* g, float* m, float* v, float* up,
+                     void* shadow, const UpdateScalars& hs, const float* clip, const int* flag,
+                     hipStream_t st) {
+  const int64_t threads = cdiv(n, 4);
+  const dim3 grid((unsigned)cdiv(threads, 256));
+  fused_update<G, S, EF><<<grid, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow, hs, clip,
+                                               flag);
+}
+
+}  // namespace
+
+size_t norm_scratch_bytes() { return NORM_BLOCKS * sizeof(double); }
+
+void launch_grad_norm(const void* g, bool g_bf16, int64_t n, float clip, double* partial,
+                      float* out2, int* flag, unsigned long long* skipped, hipStream_t st) {
+  if (g_bf16)
+    sumsq_partial<bf16><<<NORM_BLOCKS, NORM_THREADS, 0, st>>>((const bf16*)g, n, partial);
+  else
+    sumsq_partial<float><<<NORM_BLOCKS, NORM_THREADS, 0, st>>>((const float*)g, n, partial);
+  norm_finish<<<1, 1024, 0, st>>>(partial, NORM_BLOCKS, clip, out2, flag, skipped);
+}
+
+void launch_fused_update(int64_t n, float* x, const void* g, bool g_bf16, float* m, float* v,
+                         float* up, void* shadow, int shadow_kind, const UpdateScalars& hs,
+                         const float* clip, const int* flag, hipStream_t st) {
+  // shadow_kind: 0 none, 1 fp32, 2 bf16.  EF instantiation whenever an EF buffer is present.
+  const bool ef = up != nullptr;
+#define UPD(G, S, E) launch_update_t<G, S, E>(n, x, g, m, v, up, shadow, hs, clip, flag, st)
+  if (g_bf16) {
+    if (shadow_kind == 2) { if (ef) UPD(bf16, bf16, true); else UPD(bf16, bf16, false); }
+    else if (shadow_kind == 1) { if (ef) UPD(bf16, float, true); else UPD(bf16, float, false); }
+    else { if (ef) UPD(bf16, float, true); else UPD(bf16, float, false); }
+  } else {
+    if (shadow_kind == 2) { if (ef) UPD(float, bf16, true); else UPD(float, bf16, false); }
+    else if (shadow_kind == 1) { if (ef) UPD(float, float, true); else UPD(float, float, false); }
+    else { if (ef) UPD(float, float, true); else UPD(float, float, false); }
+  }
+#undef UPD
+}
+
+void launch_cast_copy(int64_t n, const float* src, void* dst, bool dst_bf16, hipStream_t st) {
+  const dim3 grid((unsigned)cdiv(cdiv(n, 4), 256));
+  if (dst_bf16) cast_copy<bf16><<<grid, 256, 0, st>>>(n, src, (bf16*)dst);
+  else cast_copy<float><<<grid, 256, 0, st>>>(n, src, (float*)dst);
+}
+
+void launch_zero(void* p, int64_t bytes, hipStream_t st) {
+  // bytes must be a multiple of 16 (every region the stage clears is 256-byte aligned)
+  const int64_t n16 = bytes / 16;
+  if (n16 == 0) return;
+  zero_bytes<<<(unsigned)cdiv(n16, 256), 256, 0, st>>>(n16, (int4*)p);
+}

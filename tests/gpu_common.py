@@ -1,0 +1,139 @@
+"""Helpers of the GPU parity tests: drive the HIP stage through the C ABI for T iterations of
+Alg. 1 and record what the oracle records (losses, outputs, gradients, final state)."""
+from __future__ import annotations
+
+import sys
+from typing import Dict, Iterable, List, Optional
+
+import numpy as np
+
+import datagen
+import oracle
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def rel(a, b) -> float:
+    """Norm-wise relative error ||a - b|| / max(||b||, 1e-30), in float64."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-30))
+
+
+def shape_of(w):
+    from paper_2606_30634_amd.stage import make_shape
+    return make_shape(w.n_blocks, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ffn, w.vocab,
+                      w.first_stage, w.last_stage, w.tie_embedding, w.seq_len, w.micro_batch,
+                      w.max_inflight, bf16=(w.dtype == "bf16"), rms_eps=w.rms_eps,
+                      rope_theta=w.rope_theta)
+
+
+def hp_of(w, **kw):
+    from paper_2606_30634_amd.stage import hparams
+    base = dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay,
+                clip_norm=w.clip_norm, ef_lambda=w.ef_lambda, delay=1)
+    base.update(kw)
+    return hparams(**base)
+
+
+def to_device(inp: Dict[str, np.ndarray], w, dev):
+    import torch
+    out = {}
+    for k, v in inp.items():
+        if v.dtype == np.int32:
+            out[k] = torch.from_numpy(v).to(dev)
+        else:
+            t = torch.from_numpy(np.ascontiguousarray(v, dtype=np.float32))
+            out[k] = t.to(dev).to(torch.bfloat16 if w.dtype == "bf16" else torch.float32)
+    return out
+
+
+def schedule_1f1b(M: int, warm: int):
+    """Order of (kind, microbatch) on one stage for one step of a 1F1B schedule with `warm` forwards
+    ahead of the first backward (no cross-step overlap)."""
+    order = []
+    f = b = 0
+    for _ in range(min(warm, M)):
+        order.append(("F", f)); f += 1
+    while b < M:
+        if f < M:
+            order.append(("F", f)); f += 1
+        order.append(("B", b)); b += 1
+    return order
+
+
+def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps: Iterable[int] = (),
+            device: str = "cuda:0"):
+    """T iterations of Alg. 1 on the GPU stage.  Returns losses (per step, per microbatch), outputs
+    at y_steps, gradient tensors at grad_steps and the final master / m / v / u_prev."""
+    import torch
+    from paper_2606_30634_amd.stage import Stage
+    dev = torch.device(device)
+    st = Stage(shape_of(w), device)
+    st.load_master(params0)
+    names = list(params0)
+    grad_steps, y_steps = set(grad_steps), set(y_steps)
+    M = w.microbatches_per_step
+    res = dict(losses=[], ys={}, grads={})
+    for t in range(steps):
+        inps = [to_device(datagen.step_inputs(w, t, i), w, dev) for i in range(M)]
+        losses = [None] * M
+        ys = [None] * M
+        loss_t = [torch.zeros(1, device=dev) for _ in range(M)]
+        y_t = [None] * M
+        order = schedule_1f1b(M, w.max_inflight - 1) if M > 1 else [("F", 0), ("B", 0)]
+        for kind, i in order:
+            slot = i % w.max_inflight
+            inp = inps[i]
+            if kind == "F":
+                if not w.last_stage:
+                    y_t[i] = torch.empty_like(inp["dy"])
+                st.forward(slot, t, tokens=inp.get("tokens"), x_in=inp.get("x_in"),
+                           targets=inp.get("targets"), y_out=y_t[i],
+                           loss=loss_t[i] if w.last_stage else None)
+            else:
+                st.backward(slot, dy=inp.get("dy"), microbatches_per_step=M)
+        if t in grad_steps:
+            res["grads"][t] = {n: st.view(f"grad{t % 2}.{n}").float().cpu().numpy().reshape(params0[n].shape)
+                               for n in names}
+        for i in range(M):
+            if w.last_stage:
+                losses[i] = float(loss_t[i].item())
+            else:
+                yv = y_t[i].float().cpu().numpy().astype(np.float64)
+                losses[i] = float(np.sum(yv * inps[i]["dy"].float().cpu().numpy().astype(np.float64)))
+                if t in y_steps:
+                    ys[i] = yv
+        if t in y_steps:
+            res["ys"][t] = ys
+        res["losses"].append(losses)
+        st.update(t, hp)
+    torch.cuda.synchronize(dev)
+    final = {}
+    for pre in ("", "m.", "v.", "u_prev."):
+        final[pre] = {n: st.view(pre + n).float().cpu().numpy().reshape(params0[n].shape) for n in names}
+    res["final"] = final
+    rc, skipped = __import__("paper_2606_30634_amd.binding", fromlist=["x"]).stage_poll_nonfinite(st.handle)
+    res["skipped"] = skipped
+    st.close()
+    return res
+
+
+def run_oracle(w, steps: int, hp_oracle, params0, grad_steps=(), y_steps=(), dt=np.float64):
+    grad_steps, y_steps = set(grad_steps), set(y_steps)
+    res = dict(losses=[], ys={}, grads={})
+
+    def rec(t, info):
+        res["losses"].append([float(l) for l in info["losses"]])
+        res.setdefault("loss_abs", []).append([o.get("loss_abs") for o in info["outs"]])
+        if t in grad_steps:
+            res["grads"][t] = info["grads"]
+        if t in y_steps:
+            res["ys"][t] = [o.get("y") for o in info["outs"]]
+
+    st = oracle.run(w, steps, hp_oracle, params0, lambda t, i: datagen.step_inputs(w, t, i), dt, rec)
+    res["final"] = {"": st.x, "m.": st.m, "v.": st.v, "u_prev.": st.u_prev}
+    return res
