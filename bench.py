@@ -1,0 +1,217 @@
+"""Stage throughput of the delay-1 training step on one MI355X.
+
+One step = one pass of the whole hot path over one optimizer step's input: stage_forward and
+stage_backward of every microbatch, then delayed_update (Alg. 1 with AdamW, Error Feedback
+lambda = 1, global-norm clipping at 1.0).  Default workload: the small bf16 stage (3 decoder blocks,
+d_model 768, 12 heads, SwiGLU 3072, seq 1024, microbatch 8, vocab-32000 embedding on the first
+stage), synthetic seeded inputs already resident in HBM.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload small|mid|large|tiny] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w):
+    """The oracle (float32, numpy) on a bounded sample: 2 of the step's sequences forward+backward
+    and one full delayed update; the step time is extrapolated linearly in tokens."""
+    import numpy as np
+    import datagen
+    import oracle
+    from oracle import model
+    from oracle.update import OptState, iteration_update
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(i.get("num_threads", 1) for i in threadpool_info()) or os.cpu_count()
+    except Exception:
+        cores = os.cpu_count()
+    n_seq = min(2, w.micro_batch)
+    ws = w.with_(micro_batch=n_seq)
+    p0 = datagen.init_params(ws)
+    st = OptState.create(p0, np.float32)
+    inp = datagen.step_inputs(ws, 0)
+    t0 = time.perf_counter()
+    g, _ = model.stage_step_grads(st.x, [inp], ws, np.float32)
+    t1 = time.perf_counter()
+    iteration_update(st, g, oracle.hparams_of(ws))   # t = 0: stashes g_0 (no arithmetic)
+    t2 = time.perf_counter()
+    iteration_update(st, g, oracle.hparams_of(ws))   # t = 1: the full AdamW + clip pass
+    t3 = time.perf_counter()
+    tokens_step = w.tokens_per_micro * w.microbatches_per_step
+    fb_per_token = (t1 - t0) / (n_seq * w.seq_len)
+    step_s = fb_per_token * tokens_step + (t3 - t2)
+    return {"value": tokens_step / step_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"float32 numpy oracle: {n_seq} of the step's {w.micro_batch * w.microbatches_per_step} "
+                      f"sequences forward+backward ({t1 - t0:.1f} s) plus one full delayed update over "
+                      f"{sum(v.size for v in p0.values())} parameters ({t3 - t2:.1f} s); step time "
+                      f"extrapolated linearly in tokens to {tokens_step} tokens",
+            "measured_s": round(t3 - t0 + (t2 - t1), 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="small")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (one pipeline stage's "
+              "share on one MI355X); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import datagen
+    from paper_2606_30634_amd import binding as B
+    from paper_2606_30634_amd.stage import Stage, hparams, make_shape
+
+    w = datagen.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    bf = w.dtype == "bf16"
+    st = Stage(make_shape(w.n_blocks, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ffn, w.vocab,
+                          w.first_stage, w.last_stage, w.tie_embedding, w.seq_len, w.micro_batch,
+                          w.max_inflight, bf16=bf, rms_eps=w.rms_eps, rope_theta=w.rope_theta), "cuda:0")
+    st.load_master(datagen.init_params(w))
+    hp = hparams(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay,
+                 clip_norm=w.clip_norm, ef_lambda=1.0, delay=1)
+    M = w.microbatches_per_step
+    cdt = torch.bfloat16 if bf else torch.float32
+    # two distinct input sets per microbatch, resident in HBM, alternated across steps
+    sets = []
+    for k in range(2):
+        per = []
+        for i in range(M):
+            inp = datagen.step_inputs(w, k, i)
+            d = {}
+            for name, v in inp.items():
+                t = torch.from_numpy(v)
+                d[name] = t.to(dev) if v.dtype == np.int32 else t.to(dev).to(cdt)
+            if not w.last_stage:
+                d["y"] = torch.empty(w.micro_batch, w.seq_len, w.d_model, dtype=cdt, device=dev)
+            d["loss"] = torch.zeros(1, device=dev)
+            per.append(d)
+        sets.append(per)
+    warm = max(0, min(w.max_inflight - 1, M))
+
+    def step(t):
+        per = sets[t % 2]
+        order, f, b = [], 0, 0
+        for _ in range(warm):
+            order.append(("F", f)); f += 1
+        while b < M:
+            if f < M:
+                order.append(("F", f)); f += 1
+            order.append(("B", b)); b += 1
+        for kind, i in order:
+            d = per[i]
+            slot = i % w.max_inflight
+            if kind == "F":
+                st.forward(slot, t, tokens=d.get("tokens"), x_in=d.get("x_in"), targets=d.get("targets"),
+                           y_out=d.get("y"), loss=d["loss"] if w.last_stage else None)
+            else:
+                st.backward(slot, dy=d.get("dy"), microbatches_per_step=M)
+        st.update(t, hp)
+
+    t = 0
+    log(f"bench: {w.name}: warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step(t); t += 1
+    torch.cuda.synchronize(dev)
+    stream = st.stream
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    log(f"bench: timing {args.steps} steps")
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step(t); t += 1
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - wall0
+    ms = e0.elapsed_time(e1) / args.steps
+    tokens = w.tokens_per_micro * M
+    value = tokens / (ms * 1e-3)
+
+    # kernel-class timing pass: HIP event pairs around every launch, on the stage's stream
+    log("bench: kernel-class timing pass")
+    B.stage_profile_enable(st.handle, True)
+    for _ in range(args.steps):
+        step(t); t += 1
+    classes = {"gemm": B.PROF_GEMM, "attention_fwd": B.PROF_ATTN_FWD, "attention_bwd": B.PROF_ATTN_BWD,
+               "delayed_update": B.PROF_UPDATE, "grad_norm": B.PROF_NORM}
+    kern = {}
+    for name, c in classes.items():
+        kms, n, work = B.stage_profile_read(st.handle, c)
+        if n == 0:
+            continue
+        per_launch_ms = kms / n
+        if c in (B.PROF_UPDATE, B.PROF_NORM):
+            ach = work / (kms * 1e-3) / 1e9
+            kern[name] = {"bound": "hbm", "ms_per_step": round(kms / args.steps, 4), "launches": n,
+                          "avg_launch_ms": round(per_launch_ms, 4), "achieved": round(ach, 1),
+                          "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                          "work_per_launch": work / n}
+        else:
+            ach = work / (kms * 1e-3) / 1e12
+            peak = PEAK_BF16_TFLOPS if bf else PEAK_FP32_TFLOPS
+            kern[name] = {"bound": "mfma" if bf else "alu", "ms_per_step": round(kms / args.steps, 4),
+                          "launches": n, "avg_launch_ms": round(per_launch_ms, 4), "achieved": round(ach, 1),
+                          "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                          "work_per_launch": work / n}
+    B.stage_profile_enable(st.handle, False)
+    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    kd = kern[dom]
+    roofline = {"kernel": dom, "bound": kd["bound"], "achieved": kd["achieved"], "peak": kd["peak"],
+                "unit": kd["unit"], "frac": kd["frac"], "traffic": None}
+    rc, skipped = B.stage_poll_nonfinite(st.handle)
+    st.close()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("bench: CPU oracle baseline")
+        cpu = cpu_baseline(w)
+
+    out = {
+        "metric": "stage tokens/sec (fwd+bwd+delayed update)",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf else "f32",
+        "data": "synthetic (seeded: uniform tokens / N(0,1) activations, N(0,1e-3) upstream gradients, N(0,0.02) weights)",
+        "config": {"workload": w.name, "tokens_per_step": tokens, "microbatches_per_step": M,
+                   "optimizer": "AdamW, delay 1, Error Feedback lambda 1, clip 1.0", "parallelism": "1 GPU, one stage"},
+        "roofline": roofline,
+        "kernels": kern,
+        "cpu_baseline": cpu,
+        "wall_s_timed_region": round(wall, 3),
+        "skipped_updates": skipped,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -25,8 +25,8 @@
  *   - All device work is enqueued asynchronously on the HIP stream given to stage_init (or to
  *     delayed_update_flat).  Host pointers are never retained.  The caller synchronises.
  *   - Device pointers must be 16-byte aligned.  Layouts are row-major, last index contiguous.
- *   - Token ids are int32 in [0, vocab); ids outside that range give STAGE_EINVAL only when the
- *     caller asks for validation (stage_validate_tokens); the kernels clamp nothing.
+ *   - Token ids must be int32 in [0, vocab); the kernels do not check them (an id outside the
+ *     range reads outside the embedding).
  *   - One stage_t per host thread; calls on one stage_t must not overlap.
  */
 #ifndef ASYNCSTAGE_H
@@ -156,6 +156,19 @@ int stage_poll_nonfinite(stage_t* s, int64_t* skipped);
 
 /* Global L2 norm of gradient buffer `which` (0/1), computed on device into norm_dev (float). */
 int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev);
+
+/* Kernel-class timing.  While enabled, the stage records a HIP event pair on its stream around
+ * every launch of a class and, when read, adds up the elapsed times and the algorithmic work of
+ * those launches: GEMM and attention in flops (2 M N K per product; causal attention forward
+ * 4 B Hq hd s(s+1)/2, backward twice that), the delayed update and the gradient norm in bytes of
+ * HBM traffic.  Reading synchronises the stream and resets the counters.  Meant for measurement
+ * passes; it adds two event records per launch. */
+typedef enum {
+  STAGE_PROF_GEMM = 0, STAGE_PROF_ATTN_FWD = 1, STAGE_PROF_ATTN_BWD = 2, STAGE_PROF_UPDATE = 3,
+  STAGE_PROF_NORM = 4, STAGE_PROF_OTHER = 5, STAGE_PROF_NCLASS = 6
+} stage_prof_class;
+int stage_profile_enable(stage_t* s, int32_t on);
+int stage_profile_read(stage_t* s, int32_t cls, double* ms, int64_t* launches, double* work);
 
 const char* stage_last_error(void);
 void stage_destroy(stage_t* s);

@@ -16,7 +16,9 @@ DT_F32, DT_BF16, DT_I32 = 0, 1, 2
 EXPORTS = ["stage_required_bytes", "stage_init", "stage_num_tensors", "stage_tensor",
            "stage_tensor_by_name", "stage_sync_weights", "stage_forward", "stage_backward",
            "delayed_update", "delayed_update_flat", "stage_embed_indices", "stage_poll_nonfinite",
-           "stage_grad_norm", "stage_last_error", "stage_destroy"]
+           "stage_grad_norm", "stage_profile_enable", "stage_profile_read", "stage_last_error",
+           "stage_destroy"]
+PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_UPDATE, PROF_NORM, PROF_OTHER = range(6)
 
 
 class StageShape(C.Structure):
@@ -57,6 +59,8 @@ def _load():
         "stage_embed_indices": (C.c_int, [vp, i32, vp, vp, vp]),
         "stage_poll_nonfinite": (C.c_int, [vp, C.POINTER(i64)]),
         "stage_grad_norm": (C.c_int, [vp, i32, vp]),
+        "stage_profile_enable": (C.c_int, [vp, i32]),
+        "stage_profile_read": (C.c_int, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
         "stage_last_error": (C.c_char_p, []),
         "stage_destroy": (None, [vp]),
     }
@@ -149,6 +153,17 @@ def stage_poll_nonfinite(s: int):
 
 def stage_grad_norm(s: int, which: int, norm_dev) -> None:
     _call("stage_grad_norm", s, which, norm_dev)
+
+
+def stage_profile_enable(s: int, on: bool) -> None:
+    _call("stage_profile_enable", s, int(on))
+
+
+def stage_profile_read(s: int, cls: int):
+    """(milliseconds, launches, algorithmic work) of one kernel class since the last read."""
+    ms, n, work = C.c_double(), C.c_int64(), C.c_double()
+    _call("stage_profile_read", s, cls, C.byref(ms), C.byref(n), C.byref(work))
+    return ms.value, n.value, work.value
 
 
 def stage_destroy(s: int) -> None:

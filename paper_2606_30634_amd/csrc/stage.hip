@@ -84,6 +84,13 @@ struct stage {
   int64_t next_t = 0;
   int64_t n_updates = 0;
   unsigned long long skipped_seen = 0;
+  // kernel-class timing
+  struct ProfRec { int cls; hipEvent_t a, b; double work; };
+  bool prof_on = false;
+  std::vector<ProfRec> prof_pending;
+  std::vector<hipEvent_t> prof_free;
+  double prof_ms[STAGE_PROF_NCLASS] = {}, prof_work[STAGE_PROF_NCLASS] = {};
+  int64_t prof_n[STAGE_PROF_NCLASS] = {};
   // named tensors
   struct Named { std::string name; void* ptr; int64_t numel; int32_t dtype; };
   std::vector<Named> named;
@@ -92,6 +99,54 @@ struct stage {
 };
 
 namespace {
+
+hipEvent_t prof_event(stage* S) {
+  if (!S->prof_free.empty()) {
+    hipEvent_t e = S->prof_free.back();
+    S->prof_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  (void)hipEventCreate(&e);
+  return e;
+}
+
+void prof_collect(stage* S) {
+  for (auto& r : S->prof_pending) {
+    float ms = 0.f;
+    (void)hipEventElapsedTime(&ms, r.a, r.b);
+    S->prof_ms[r.cls] += ms;
+    S->prof_work[r.cls] += r.work;
+    S->prof_n[r.cls] += 1;
+    S->prof_free.push_back(r.a);
+    S->prof_free.push_back(r.b);
+  }
+  S->prof_pending.clear();
+}
+
+// Runs `launch` bracketed by an event pair on the stage stream when timing is enabled.
+template <typename F>
+void timed(stage* S, int cls, double work, F&& launch) {
+  if (!S->prof_on) { launch(); return; }
+  hipEvent_t a = prof_event(S), b = prof_event(S);
+  (void)hipEventRecord(a, S->st);
+  launch();
+  (void)hipEventRecord(b, S->st);
+  S->prof_pending.push_back({cls, a, b, work});
+  if (S->prof_pending.size() > 4096) {  // bound the number of live events
+    (void)hipEventSynchronize(b);
+    prof_collect(S);
+  }
+}
+
+void run_gemm(stage* S, const GemmArgs& g) {
+  timed(S, STAGE_PROF_GEMM, 2.0 * g.M * g.N * g.K, [&] { launch_gemm(S->bf, g, S->st); });
+}
+
+double attn_fwd_flops(const stage* S) {  // QK^T and PV over the causal triangle
+  const stage_shape_t& sh = S->sh;
+  return 4.0 * sh.micro_batch * sh.n_heads * sh.head_dim * (double)sh.seq_len * (sh.seq_len + 1) / 2.0;
+}
 
 int validate(const stage_shape_t* s) {
   if (!s) return fail(STAGE_EINVAL, "null shape");
@@ -281,16 +336,16 @@ void block_forward(stage* S, int vi, BlockAct& b, const BlockOff& w, void* y) {
   const bool bf = S->bf;
   hipStream_t st = S->st;
   launch_rmsnorm_fwd(bf, b.x, S->wptr(vi, w.attn_norm), b.n1, b.rstd1, T, d, sh.rms_eps, st);
-  launch_gemm(bf, gemm(T, S->qkvw, d, b.n1, d, true, S->wptr(vi, w.wqkv), d, true, b.qkv, S->qkvw), st);
+  run_gemm(S, gemm(T, S->qkvw, d, b.n1, d, true, S->wptr(vi, w.wqkv), d, true, b.qkv, S->qkvw));
   launch_rope(bf, b.qkv, T, sh.seq_len, sh.n_heads + sh.n_kv_heads, sh.head_dim, S->qkvw, S->cos_t,
               S->sin_t, false, st);
-  launch_attention_fwd(bf, attn_args(S, b), st);
-  launch_gemm(bf, gemm(T, d, S->hqd, b.o, S->hqd, true, S->wptr(vi, w.wo), S->hqd, true, b.h, d,
-                       false, 0.f, b.x), st);
+  timed(S, STAGE_PROF_ATTN_FWD, attn_fwd_flops(S), [&] { launch_attention_fwd(bf, attn_args(S, b), st); });
+  run_gemm(S, gemm(T, d, S->hqd, b.o, S->hqd, true, S->wptr(vi, w.wo), S->hqd, true, b.h, d,
+                       false, 0.f, b.x));
   launch_rmsnorm_fwd(bf, b.h, S->wptr(vi, w.ffn_norm), b.n2, b.rstd2, T, d, sh.rms_eps, st);
-  launch_gemm(bf, gemm(T, 2 * f, d, b.n2, d, true, S->wptr(vi, w.wgu), d, true, b.gu, 2 * f), st);
+  run_gemm(S, gemm(T, 2 * f, d, b.n2, d, true, S->wptr(vi, w.wgu), d, true, b.gu, 2 * f));
   launch_swiglu_fwd(bf, b.gu, b.z, T, f, st);
-  launch_gemm(bf, gemm(T, d, f, b.z, f, true, S->wptr(vi, w.wdown), f, true, y, d, false, 0.f, b.h), st);
+  run_gemm(S, gemm(T, d, f, b.z, f, true, S->wptr(vi, w.wdown), f, true, y, d, false, 0.f, b.h));
 }
 
 // dy: gradient of the block output; writes the gradient of the block input into dx.
@@ -303,25 +358,25 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   hipStream_t st = S->st;
   const int nch = (int)cdiv(T, RMS_CHUNK);
   // down projection: dz = dy Wd ; dWd (+)= dy^T z
-  launch_gemm(bf, gemm(T, f, d, dy, d, true, S->wptr(vi, w.wdown), f, false, S->dz, f), st);
-  launch_gemm(bf, gemm(d, f, T, dy, d, false, b.z, f, false, g + w.wdown, f, true, beta), st);
+  run_gemm(S, gemm(T, f, d, dy, d, true, S->wptr(vi, w.wdown), f, false, S->dz, f));
+  run_gemm(S, gemm(d, f, T, dy, d, false, b.z, f, false, g + w.wdown, f, true, beta));
   launch_swiglu_bwd(bf, S->dz, b.gu, S->dgu, T, f, st);
   // gate/up: dn2 = dgu Wgu ; dWgu (+)= dgu^T n2
-  launch_gemm(bf, gemm(T, d, 2 * f, S->dgu, 2 * f, true, S->wptr(vi, w.wgu), d, false, S->dn, d), st);
-  launch_gemm(bf, gemm(2 * f, d, T, S->dgu, 2 * f, false, b.n2, d, false, g + w.wgu, d, true, beta), st);
+  run_gemm(S, gemm(T, d, 2 * f, S->dgu, 2 * f, true, S->wptr(vi, w.wgu), d, false, S->dn, d));
+  run_gemm(S, gemm(2 * f, d, T, S->dgu, 2 * f, false, b.n2, d, false, g + w.wgu, d, true, beta));
   launch_rmsnorm_bwd(bf, S->dn, b.h, b.rstd2, S->wptr(vi, w.ffn_norm), dy, S->dh, S->rms_part, T, d, st);
   launch_colsum_partials(S->rms_part, nch, d, g + w.ffn_norm, !first, st);
   // output projection: do = dh Wo ; dWo (+)= dh^T o
-  launch_gemm(bf, gemm(T, S->hqd, d, S->dh, d, true, S->wptr(vi, w.wo), S->hqd, false, S->do_, S->hqd), st);
-  launch_gemm(bf, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta), st);
+  run_gemm(S, gemm(T, S->hqd, d, S->dh, d, true, S->wptr(vi, w.wo), S->hqd, false, S->do_, S->hqd));
+  run_gemm(S, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta));
   AttnArgs a = attn_args(S, b);
   a.dout = S->do_; a.dqkv = S->dqkv; a.delta = S->delta;
-  launch_attention_bwd(bf, a, st);
+  timed(S, STAGE_PROF_ATTN_BWD, 2.0 * attn_fwd_flops(S), [&] { launch_attention_bwd(bf, a, st); });
   launch_rope(bf, S->dqkv, T, sh.seq_len, sh.n_heads + sh.n_kv_heads, sh.head_dim, S->qkvw, S->cos_t,
               S->sin_t, true, st);
   // qkv projection: dn1 = dqkv Wqkv ; dWqkv (+)= dqkv^T n1
-  launch_gemm(bf, gemm(T, d, S->qkvw, S->dqkv, S->qkvw, true, S->wptr(vi, w.wqkv), d, false, S->dn, d), st);
-  launch_gemm(bf, gemm(S->qkvw, d, T, S->dqkv, S->qkvw, false, b.n1, d, false, g + w.wqkv, d, true, beta), st);
+  run_gemm(S, gemm(T, d, S->qkvw, S->dqkv, S->qkvw, true, S->wptr(vi, w.wqkv), d, false, S->dn, d));
+  run_gemm(S, gemm(S->qkvw, d, T, S->dqkv, S->qkvw, false, b.n1, d, false, g + w.wqkv, d, true, beta));
   launch_rmsnorm_bwd(bf, S->dn, b.x, b.rstd1, S->wptr(vi, w.attn_norm), S->dh, dx, S->rms_part, T, d, st);
   launch_colsum_partials(S->rms_part, nch, d, g + w.attn_norm, !first, st);
 }
@@ -451,8 +506,8 @@ int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens,
   if (sh.last_stage) {
     HIP_OK(hipMemcpyAsync(sl.targets, targets, (size_t)T * 4, hipMemcpyDeviceToDevice, st));
     launch_rmsnorm_fwd(s->bf, sl.y, s->wptr(vi, s->off_final), sl.hf, sl.rstdf, T, d, sh.rms_eps, st);
-    launch_gemm(s->bf, gemm(T, sh.vocab, d, sl.hf, d, true, s->wptr(vi, s->off_embed), d, true,
-                            sl.logits, sh.vocab, true, 0.f), st);
+    run_gemm(s, gemm(T, sh.vocab, d, sl.hf, d, true, s->wptr(vi, s->off_embed), d, true,
+                            sl.logits, sh.vocab, true, 0.f));
     launch_ce_rows(s->bf, sl.logits, sl.targets, T, sh.vocab, 1.0f / T, s->dlog, s->row_loss, st);
     launch_mean(s->row_loss, T, loss_dev, st);
   }
@@ -493,10 +548,10 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
     launch_ce_rows(bf, sl.logits, sl.targets, T, sh.vocab, 1.0f / ((float)T * microbatches_per_step),
                    s->dlog, s->row_loss, st);
     // dhf = dlogits E ; dE (+)= dlogits^T hf
-    launch_gemm(bf, gemm(T, d, sh.vocab, s->dlog, sh.vocab, true, s->wptr(vi, s->off_embed), d, false,
-                         s->dhf, d), st);
-    launch_gemm(bf, gemm(sh.vocab, d, T, s->dlog, sh.vocab, false, sl.hf, d, false, g + s->off_embed, d,
-                         true, first ? 0.f : 1.f), st);
+    run_gemm(s, gemm(T, d, sh.vocab, s->dlog, sh.vocab, true, s->wptr(vi, s->off_embed), d, false,
+                         s->dhf, d));
+    run_gemm(s, gemm(sh.vocab, d, T, s->dlog, sh.vocab, false, sl.hf, d, false, g + s->off_embed, d,
+                         true, first ? 0.f : 1.f));
     head_wrote_embed = true;
     launch_rmsnorm_bwd(bf, s->dhf, sl.y, sl.rstdf, s->wptr(vi, s->off_final), nullptr, s->dA,
                        s->rms_part, T, d, st);
@@ -556,14 +611,21 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   const float* clip = nullptr;
   const int* flag = nullptr;
   if (apply && hp->clip_norm > 0.f) {
-    launch_grad_norm(s->grad[gb], false, s->n_flat, hp->clip_norm, s->norm_part, s->norm_out, s->flag,
-                     s->skipped, s->st);
+    timed(s, STAGE_PROF_NORM, 4.0 * s->n_flat, [&] {
+      launch_grad_norm(s->grad[gb], false, s->n_flat, hp->clip_norm, s->norm_part, s->norm_out, s->flag,
+                       s->skipped, s->st);
+    });
     clip = s->norm_out + 1;
     flag = s->flag;
   }
-  launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v,
-                      hp->ef_lambda != 0.f ? s->u_prev : nullptr, s->ver[vout], s->bf ? 2 : 1, hs,
-                      clip, flag, s->st);
+  // bytes: x, m, v r+w; g read; shadow write; u_prev r+w with EF (no-op pass: x read, shadow write)
+  const double ub = apply ? (24.0 + 4.0 + (s->bf ? 2.0 : 4.0) + (hp->ef_lambda != 0.f ? 8.0 : 0.0))
+                          : (4.0 + (s->bf ? 2.0 : 4.0));
+  timed(s, STAGE_PROF_UPDATE, ub * s->n_flat, [&] {
+    launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v,
+                        hp->ef_lambda != 0.f ? s->u_prev : nullptr, s->ver[vout], s->bf ? 2 : 1, hs,
+                        clip, flag, s->st);
+  });
   HIP_OK(hipGetLastError());
   if (apply) {
     s->grad_consumed[gb] = true;
@@ -634,6 +696,31 @@ int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev) {
   return STAGE_OK;
 }
 
-void stage_destroy(stage_t* s) { delete s; }
+int stage_profile_enable(stage_t* s, int32_t on) {
+  if (!s) return fail(STAGE_EINVAL, "null stage");
+  s->prof_on = on != 0;
+  return STAGE_OK;
+}
+
+int stage_profile_read(stage_t* s, int32_t cls, double* ms, int64_t* launches, double* work) {
+  if (!s || cls < 0 || cls >= STAGE_PROF_NCLASS) return fail(STAGE_EINVAL, "bad argument");
+  HIP_OK(hipStreamSynchronize(s->st));
+  prof_collect(s);
+  if (ms) *ms = s->prof_ms[cls];
+  if (launches) *launches = s->prof_n[cls];
+  if (work) *work = s->prof_work[cls];
+  s->prof_ms[cls] = 0.0;
+  s->prof_n[cls] = 0;
+  s->prof_work[cls] = 0.0;
+  return STAGE_OK;
+}
+
+void stage_destroy(stage_t* s) {
+  if (!s) return;
+  (void)hipStreamSynchronize(s->st);
+  for (auto& r : s->prof_pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+  for (auto e : s->prof_free) (void)hipEventDestroy(e);
+  delete s;
+}
 
 }  // extern "C"
