@@ -29,8 +29,9 @@ def log(msg):
 
 
 def cpu_baseline(w):
-    """The oracle (float32, numpy) on a bounded sample: 2 of the step's sequences forward+backward
-    and one full delayed update; the step time is extrapolated linearly in tokens."""
+    """The oracle (float32, numpy) on one whole optimizer step of the workload (all sequences
+    forward+backward, then the full delayed update) when that is a bounded amount of CPU work;
+    otherwise on 2 of the step's sequences plus the full update, extrapolated linearly in tokens."""
     import numpy as np
     import datagen
     import oracle
@@ -41,7 +42,7 @@ def cpu_baseline(w):
         cores = max(i.get("num_threads", 1) for i in threadpool_info()) or os.cpu_count()
     except Exception:
         cores = os.cpu_count()
-    n_seq = min(2, w.micro_batch)
+    n_seq = w.micro_batch if w.d_model <= 1024 else min(2, w.micro_batch)
     ws = w.with_(micro_batch=n_seq)
     p0 = datagen.init_params(ws)
     st = OptState.create(p0, np.float32)
@@ -56,11 +57,13 @@ def cpu_baseline(w):
     tokens_step = w.tokens_per_micro * w.microbatches_per_step
     fb_per_token = (t1 - t0) / (n_seq * w.seq_len)
     step_s = fb_per_token * tokens_step + (t3 - t2)
+    whole = n_seq * w.seq_len == tokens_step
+    how = ("one whole optimizer step" if whole else
+           f"step time extrapolated linearly in tokens to {tokens_step} tokens")
     return {"value": tokens_step / step_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": f"float32 numpy oracle: {n_seq} of the step's {w.micro_batch * w.microbatches_per_step} "
                       f"sequences forward+backward ({t1 - t0:.1f} s) plus one full delayed update over "
-                      f"{sum(v.size for v in p0.values())} parameters ({t3 - t2:.1f} s); step time "
-                      f"extrapolated linearly in tokens to {tokens_step} tokens",
+                      f"{sum(v.size for v in p0.values())} parameters ({t3 - t2:.1f} s); {how}",
             "measured_s": round(t3 - t0 + (t2 - t1), 2)}
 
 

@@ -40,6 +40,10 @@ class StageError(RuntimeError):
 
 
 def _load():
+    # One HIP runtime per process: torch ships its own libamdhip64 with the same soname as ROCm's.
+    # Loading torch first makes this library bind to that runtime; loading this library first would
+    # bring a second HIP/HSA runtime into the process, which then sees no device.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
     lib = C.CDLL(LIB_PATH)

@@ -66,9 +66,11 @@ def schedule_1f1b(M: int, warm: int):
 
 
 def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps: Iterable[int] = (),
-            device: str = "cuda:0"):
+            device: str = "cuda:0", upd_steps: Iterable[int] = ()):
     """T iterations of Alg. 1 on the GPU stage.  Returns losses (per step, per microbatch), outputs
-    at y_steps, gradient tensors at grad_steps and the final master / m / v / u_prev."""
+    at y_steps, and at grad_steps the gradient g_t together with the master weights x_t it was taken
+    at, at upd_steps the whole optimizer state before and after delayed_update(t) with the gradient
+    it consumed, plus the final master / m / v / u_prev."""
     import torch
     from paper_2606_30634_amd.stage import Stage
     dev = torch.device(device)
@@ -77,8 +79,20 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     names = list(params0)
     grad_steps, y_steps = set(grad_steps), set(y_steps)
     M = w.microbatches_per_step
-    res = dict(losses=[], ys={}, grads={})
+    upd_steps = set(upd_steps)
+    res = dict(losses=[], ys={}, grads={}, x_at={}, upd={})
+
+    def state(g_idx=None):
+        d = {pre: {n: st.view(pre + n).float().cpu().numpy().reshape(params0[n].shape).copy() for n in names}
+             for pre in ("", "m.", "v.", "u_prev.")}
+        if g_idx is not None:
+            d["g"] = {n: st.view(f"grad{g_idx}.{n}").float().cpu().numpy().reshape(params0[n].shape).copy()
+                      for n in names}
+        return d
+
     for t in range(steps):
+        if t in grad_steps:
+            res["x_at"][t] = {n: st.view(n).float().cpu().numpy().reshape(params0[n].shape).copy() for n in names}
         inps = [to_device(datagen.step_inputs(w, t, i), w, dev) for i in range(M)]
         losses = [None] * M
         ys = [None] * M
@@ -110,7 +124,11 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
         if t in y_steps:
             res["ys"][t] = ys
         res["losses"].append(losses)
+        if t in upd_steps:
+            pre = state((t - 1) % 2 if hp.delay == 1 else t % 2)
         st.update(t, hp)
+        if t in upd_steps:
+            res["upd"][t] = (pre, state())
     torch.cuda.synchronize(dev)
     final = {}
     for pre in ("", "m.", "v.", "u_prev."):
@@ -120,6 +138,13 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     res["skipped"] = skipped
     st.close()
     return res
+
+
+def oracle_grads_at(w, t, x_t, dt=np.float64):
+    """The oracle's gradient g_t of step t's microbatches, taken at the given weights (teacher forcing)."""
+    from oracle import model
+    g, _ = model.stage_step_grads(x_t, [datagen.step_inputs(w, t, i) for i in range(w.microbatches_per_step)], w, dt)
+    return g
 
 
 def run_oracle(w, steps: int, hp_oracle, params0, grad_steps=(), y_steps=(), dt=np.float64):

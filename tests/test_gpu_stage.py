@@ -6,16 +6,19 @@ import pytest
 
 import datagen
 import oracle
-from gpu_common import hp_of, log, rel, run_gpu, run_oracle
+from gpu_common import hp_of, log, oracle_grads_at, rel, run_gpu, run_oracle
 
 pytestmark = pytest.mark.gpu
 
 
-def _compare(w, g, o, tol, grad_steps, label, lam=1.0):
-    """Losses per step (a head's mean CE: scalar relative; a middle stage's surrogate sum(Y dY):
-    error relative to sum |Y dY|, the sum's condition), outputs Y, gradients at grad_steps and the
-    final master / m / v / u_prev, all norm-wise relative.  Every failure is reported."""
-    errs, bad = {}, []
+def _compare(w, g, o, tol, grad_steps, label, lam=1.0, state_tol=None):
+    """Free-running trajectories (each side its own x_t): per-step losses (a head's mean CE: scalar
+    relative; a middle stage's surrogate sum(Y dY): error relative to sum |Y dY|, the condition of
+    the sum), outputs Y and the final master weights at `tol`; final m, v and the EF buffer at
+    `state_tol`.  Gradients teacher-forced: the GPU's g_t against the oracle's gradient at the GPU's
+    own x_t, at `tol`.  All norm-wise relative; every failure is reported."""
+    state_tol = tol if state_tol is None else state_tol
+    errs, tols = {}, {}
     for t, (lg, lo) in enumerate(zip(g["losses"], o["losses"])):
         for i, (a, b) in enumerate(zip(lg, lo)):
             scale = abs(b) if w.last_stage else o["loss_abs"][t][i]
@@ -24,16 +27,36 @@ def _compare(w, g, o, tol, grad_steps, label, lam=1.0):
         for i, y in enumerate(o["ys"][t]):
             errs[f"y[{t}][{i}]"] = rel(g["ys"][t][i], y)
     for t in grad_steps:
-        for n in o["grads"][t]:
-            errs[f"grad[{t}].{n}"] = rel(g["grads"][t][n], o["grads"][t][n])
-    for pre in ("", "m.", "v.", "u_prev."):
-        if pre == "u_prev." and not lam:
-            continue  # standard async keeps no EF buffer
+        ref = oracle_grads_at(w, t, g["x_at"][t])
+        for n in ref:
+            errs[f"grad[{t}].{n}"] = rel(g["grads"][t][n], ref[n])
+    for pre in ("", "m.", "v."):
         for n, ref in o["final"][pre].items():
-            errs[f"final.{pre}{n}"] = rel(g["final"][pre][n], ref)
-    bad = {k: v for k, v in errs.items() if not v <= tol}
-    worst = max(errs, key=errs.get)
-    log(f"{label}: {len(errs)} comparisons, worst {worst} = {errs[worst]:.3e} (tol {tol})")
+            k = f"final.{pre}{n}"
+            errs[k] = rel(g["final"][pre][n], ref)
+            if pre:
+                tols[k] = state_tol
+    # the update in place: the oracle's rule applied to the GPU's own state before delayed_update(t)
+    # and the gradient it consumed, against the GPU's state after it (fp32 vs float64 arithmetic)
+    from oracle.update import OptState, iteration_update
+    for t, (pre, post) in g.get("upd", {}).items():
+        ost = OptState({n: v.astype(np.float64) for n, v in pre[""].items()},
+                       {n: v.astype(np.float64) for n, v in pre["m."].items()},
+                       {n: v.astype(np.float64) for n, v in pre["v."].items()},
+                       {n: v.astype(np.float64) for n, v in pre["u_prev."].items()},
+                       pending={n: v.astype(np.float64) for n, v in pre["g"].items()},
+                       n_updates=max(t - 1, 0), t=t)
+        iteration_update(ost, {n: np.zeros_like(v) for n, v in ost.x.items()}, oracle.hparams_of(w, ef_lambda=lam))
+        for key, ref in (("", ost.x), ("m.", ost.m), ("v.", ost.v), ("u_prev.", ost.u_prev)):
+            if key == "u_prev." and not lam:
+                continue  # standard async keeps no EF buffer
+            for n in ref:
+                k = f"update[{t}].{key}{n}"
+                errs[k] = rel(post[key][n], ref[n])
+                tols[k] = 1e-5
+    bad = {k: v for k, v in errs.items() if not v <= tols.get(k, tol)}
+    worst = sorted(errs, key=errs.get, reverse=True)[:6]
+    log(f"{label}: {len(errs)} comparisons; worst " + ", ".join(f"{k}={errs[k]:.2e}" for k in worst))
     assert not bad, f"{label}: {len(bad)} over tolerance: " + ", ".join(f"{k}={v:.2e}" for k, v in sorted(bad.items(), key=lambda kv: -kv[1])[:12])
 
 
@@ -42,7 +65,7 @@ def test_tiny_fp32_20_steps(lam):
     w = datagen.TINY
     p0 = datagen.init_params(w)
     log(f"tiny fp32 20 steps lambda={lam}")
-    g = run_gpu(w, 20, hp_of(w, ef_lambda=lam), p0, grad_steps=(0, 1, 19))
+    g = run_gpu(w, 20, hp_of(w, ef_lambda=lam), p0, grad_steps=(0, 1, 19), upd_steps=(1, 2, 19))
     o = run_oracle(w, 20, oracle.hparams_of(w, ef_lambda=lam), p0, grad_steps=(0, 1, 19))
     _compare(w, g, o, 1e-4, (0, 1, 19), f"tiny lambda={lam}", lam)
 
@@ -64,6 +87,10 @@ def test_reduced_bf16_stages(w):
     p0 = datagen.init_params(w)
     log(f"{w.name}: {steps} steps")
     ys = (0, steps - 1) if not w.last_stage else ()
-    g = run_gpu(w, steps, hp_of(w), p0, grad_steps=(0, 1, steps - 1), y_steps=ys)
+    g = run_gpu(w, steps, hp_of(w), p0, grad_steps=(0, 1, steps - 1), y_steps=ys, upd_steps=(1, 2, steps - 1))
     o = run_oracle(w, steps, oracle.hparams_of(w), p0, grad_steps=(0, 1, steps - 1), y_steps=ys)
-    _compare(w, g, o, 2e-2, (0, 1, steps - 1), w.name)
+    # bf16 free-running optimizer state: Adam turns noise-level gradient differences into lr-sized
+    # differences of m / sqrt(v) wherever a gradient element is near zero, so m and v drift further
+    # than the weights; they are held to 5e-2.  The EF buffer (the last update, sign-like wherever a
+    # gradient is at noise level) is checked teacher-forced only.
+    _compare(w, g, o, 2e-2, (0, 1, steps - 1), w.name, state_tol=5e-2)
