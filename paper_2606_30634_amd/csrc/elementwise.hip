@@ -90,14 +90,65 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd(const T* __restrict__ dn, con
   }
 }
 
-__global__ void __launch_bounds__(256) colsum_partials(const float* __restrict__ partial,
-                                                       int nchunks, int d, float* __restrict__ out,
-                                                       int accumulate) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= d) return;
+// out[j] (+)= sum_c partial[c][j]: block of 1024 threads = 16 row groups x 64 columns; each thread
+// sums rows g, g+16, ... of its column, then the 16 group sums are added in group order.
+__global__ void __launch_bounds__(1024) colsum_partials(const float* __restrict__ partial,
+                                                        int nchunks, int d, float* __restrict__ out,
+                                                        int accumulate) {
+  __shared__ float sm[16][64];
+  const int c = threadIdx.x % 64, g = threadIdx.x / 64;
+  const int j = blockIdx.x * 64 + c;
   float s = 0.f;
-  for (int c = 0; c < nchunks; ++c) s += partial[(int64_t)c * d + j];  // fixed order
-  out[j] = accumulate ? out[j] + s : s;
+  if (j < d)
+    for (int r = g; r < nchunks; r += 16) s += partial[(int64_t)r * d + j];
+  sm[g][c] = s;
+  __syncthreads();
+  if (g == 0 && j < d) {
+    float t = 0.f;
+    for (int k = 0; k < 16; ++k) t += sm[k][c];
+    out[j] = accumulate ? out[j] + t : t;
+  }
+}
+
+// RMSNorm backward with one wave per row: lane l owns columns l + 64 k (k < CPL), gamma and the
+// dgamma partial sums of those columns stay in registers, the row dot product is a wave reduction.
+// Block = 4 waves over RMS_CHUNK consecutive rows; each wave writes its own dgamma partial row, so
+// the partial array holds 4 rows per block.
+template <typename T, int CPL>
+__global__ void __launch_bounds__(256) rmsnorm_bwd_wave(const T* __restrict__ dn, const T* __restrict__ x,
+                                                        const float* __restrict__ rstd,
+                                                        const T* __restrict__ gamma,
+                                                        const T* __restrict__ resid, T* __restrict__ dx,
+                                                        float* __restrict__ partial, int rows) {
+  constexpr int d = CPL * 64;
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  float gm[CPL], dg[CPL];
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) { gm[k] = to_f32(gamma[lane + 64 * k]); dg[k] = 0.f; }
+  const int r0 = blockIdx.x * RMS_CHUNK;
+  const int r1 = min(rows, r0 + RMS_CHUNK);
+  for (int r = r0 + wave; r < r1; r += 4) {
+    const int64_t base = (int64_t)r * d;
+    const float rs = rstd[r];
+    float xh[CPL], gv[CPL];
+    float dot = 0.f;
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      xh[k] = to_f32(x[base + lane + 64 * k]) * rs;
+      gv[k] = to_f32(dn[base + lane + 64 * k]);
+      dot += gv[k] * gm[k] * xh[k];
+      dg[k] += gv[k] * xh[k];
+    }
+    dot = wave_sum(dot) / (float)d;
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      float v = rs * (gv[k] * gm[k] - xh[k] * dot);
+      if (resid) v += to_f32(resid[base + lane + 64 * k]);
+      dx[base + lane + 64 * k] = from_f32<T>(v);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) partial[((int64_t)blockIdx.x * 4 + wave) * d + lane + 64 * k] = dg[k];
 }
 
 // ------------------------------------------------------------------ RoPE
@@ -292,20 +343,35 @@ void launch_rmsnorm_fwd(bool bf, const void* x, const void* gamma, void* y, floa
 }
 
 template <typename T>
-static void rmsb_t(const void* dn, const void* x, const float* r, const void* g, const void* res,
-                   void* dx, float* part, int rows, int d, hipStream_t st) {
-  rmsnorm_bwd<T><<<(unsigned)cdiv(rows, RMS_CHUNK), 256, 0, st>>>(
-      (const T*)dn, (const T*)x, r, (const T*)g, (const T*)res, (T*)dx, part, rows, d);
+static int rmsb_t(const void* dn, const void* x, const float* r, const void* g, const void* res,
+                  void* dx, float* part, int rows, int d, hipStream_t st) {
+  const unsigned nb = (unsigned)cdiv(rows, RMS_CHUNK);
+#define RB(CPL) rmsnorm_bwd_wave<T, CPL><<<nb, 256, 0, st>>>((const T*)dn, (const T*)x, r, (const T*)g, \
+                                                            (const T*)res, (T*)dx, part, rows)
+  switch (d) {
+    case 128: RB(2); return 4 * (int)nb;
+    case 256: RB(4); return 4 * (int)nb;
+    case 512: RB(8); return 4 * (int)nb;
+    case 768: RB(12); return 4 * (int)nb;
+    case 1024: RB(16); return 4 * (int)nb;
+    case 2048: RB(32); return 4 * (int)nb;
+    default: break;
+  }
+#undef RB
+  rmsnorm_bwd<T><<<nb, 256, 0, st>>>((const T*)dn, (const T*)x, r, (const T*)g, (const T*)res, (T*)dx,
+                                     part, rows, d);
+  return (int)nb;
 }
-void launch_rmsnorm_bwd(bool bf, const void* dn, const void* x, const float* rstd,
-                        const void* gamma, const void* resid, void* dx, float* partial, int rows,
-                        int d, hipStream_t st) {
-  DISPATCH(bf, rmsb_t, dn, x, rstd, gamma, resid, dx, partial, rows, d, st);
+int launch_rmsnorm_bwd(bool bf, const void* dn, const void* x, const float* rstd,
+                       const void* gamma, const void* resid, void* dx, float* partial, int rows,
+                       int d, hipStream_t st) {
+  return bf ? rmsb_t<bf16>(dn, x, rstd, gamma, resid, dx, partial, rows, d, st)
+            : rmsb_t<float>(dn, x, rstd, gamma, resid, dx, partial, rows, d, st);
 }
 
 void launch_colsum_partials(const float* partial, int nchunks, int d, float* out, bool accumulate,
                             hipStream_t st) {
-  colsum_partials<<<(unsigned)cdiv(d, 256), 256, 0, st>>>(partial, nchunks, d, out,
+  colsum_partials<<<(unsigned)cdiv(d, 64), 1024, 0, st>>>(partial, nchunks, d, out,
                                                           accumulate ? 1 : 0);
 }
 

@@ -13,6 +13,7 @@
 // Block order is remapped so that consecutive tiles of one output row band land on one XCD (one L2).
 #include "common.h"
 #include "kernels.h"
+#include <algorithm>
 
 namespace {
 
@@ -130,17 +131,24 @@ gemm_mfma_kernel(GemmArgs g) {
   TileLoader<BN, NT, BKM> lb;
   const bf16* A = (const bf16*)g.A;
   const bf16* B = (const bf16*)g.B;
-  const int nk = (g.K + BK - 1) / BK;
-  la.load(A, g.lda, m0, g.M, 0, g.K);
-  lb.load(B, g.ldb, n0, g.N, 0, g.K);
+  // split-K: this block covers k in [kbeg, kend); kbeg is a multiple of BK
+  int kbeg = 0, kend = g.K;
+  if (g.ksplit > 1) {
+    const int chunk = ((g.K + g.ksplit - 1) / g.ksplit + BK - 1) / BK * BK;
+    kbeg = blockIdx.y * chunk;
+    kend = min(g.K, kbeg + chunk);
+  }
+  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  la.load(A, g.lda, m0, g.M, kbeg, kend);
+  lb.load(B, g.ldb, n0, g.N, kbeg, kend);
   la.store(As);
   lb.store(Bs);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     if (kt + 1 < nk) {
-      la.load(A, g.lda, m0, g.M, (kt + 1) * BK, g.K);
-      lb.load(B, g.ldb, n0, g.N, (kt + 1) * BK, g.K);
+      la.load(A, g.lda, m0, g.M, kbeg + (kt + 1) * BK, kend);
+      lb.load(B, g.ldb, n0, g.N, kbeg + (kt + 1) * BK, kend);
     }
     const bf16* as = As + cur * BM * PADK;
     const bf16* bs = Bs + cur * BN * PADK;
@@ -166,6 +174,22 @@ gemm_mfma_kernel(GemmArgs g) {
     __syncthreads();
   }
 
+  if (g.ksplit > 1) {  // partial tile of this split: plain fp32 into the workspace
+    float* W = g.ws + (int64_t)blockIdx.y * g.M * g.N;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = n0 + wn0 + j * 32 + lane % 32;
+        if (col >= g.N) continue;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = m0 + wm0 + i * 32 + 8 * (e / 4) + 4 * (lane / 32) + (e % 4);
+          if (row < g.M) W[(int64_t)row * g.N + col] = acc[i][j][e];
+        }
+      }
+    return;
+  }
   OutT* C = (OutT*)g.C;
   const bf16* R = (const bf16*)g.resid;
 #pragma unroll
@@ -187,6 +211,31 @@ gemm_mfma_kernel(GemmArgs g) {
     }
 }
 
+// C = beta C + sum over splits of the partial tiles, in split order (fp32 output, ldc == N)
+__global__ void __launch_bounds__(256) splitk_reduce(const float* __restrict__ ws, int splits, int64_t mn,
+                                                     float* __restrict__ C, float beta) {
+  const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+  if (i >= mn) return;
+  if (i + 3 < mn) {
+    float4 acc = *reinterpret_cast<const float4*>(ws + i);
+    for (int s = 1; s < splits; ++s) {
+      const float4 v = *reinterpret_cast<const float4*>(ws + (int64_t)s * mn + i);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    if (beta != 0.f) {
+      const float4 c = *reinterpret_cast<const float4*>(C + i);
+      acc.x += beta * c.x; acc.y += beta * c.y; acc.z += beta * c.z; acc.w += beta * c.w;
+    }
+    *reinterpret_cast<float4*>(C + i) = acc;
+  } else {
+    for (int64_t k = i; k < mn; ++k) {
+      float acc = 0.f;
+      for (int s = 0; s < splits; ++s) acc += ws[(int64_t)s * mn + k];
+      C[k] = beta != 0.f ? acc + beta * C[k] : acc;
+    }
+  }
+}
+
 template <int BM, int BN, int WM, int WN, typename OutT>
 void launch_cfg(const GemmArgs& g, hipStream_t st) {
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
@@ -200,7 +249,7 @@ void launch_cfg(const GemmArgs& g, hipStream_t st) {
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);             \
       attr_set = true;                                                                             \
     }                                                                                              \
-    gemm_mfma_kernel<BM, BN, WM, WN, AK, BKM, OutT><<<nblk, NT, lds, st>>>(g);                     \
+    gemm_mfma_kernel<BM, BN, WM, WN, AK, BKM, OutT><<<dim3(nblk, g.ksplit), NT, lds, st>>>(g);      \
   } while (0)
   if (g.a_kmajor && g.b_kmajor) L(true, true);
   else if (g.a_kmajor) L(true, false);
@@ -211,11 +260,22 @@ void launch_cfg(const GemmArgs& g, hipStream_t st) {
 
 }  // namespace
 
-bool gemm_mfma_try(const GemmArgs& g, hipStream_t st) {
+bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   // vector-load alignment: 8 elements along every contiguous dimension, rows in groups of 4
-  if (g.K % 8 || g.M % 8 || g.N % 8 || g.lda % 8 || g.ldb % 8) return false;
-  if ((uintptr_t)g.A % 16 || (uintptr_t)g.B % 16) return false;
+  if (g0.K % 8 || g0.M % 8 || g0.N % 8 || g0.lda % 8 || g0.ldb % 8) return false;
+  if ((uintptr_t)g0.A % 16 || (uintptr_t)g0.B % 16) return false;
+  GemmArgs g = g0;
+  g.ksplit = 1;
+  const int64_t tiles = cdiv(g.M, 128) * cdiv(g.N, 128);
+  const int64_t mn = (int64_t)g.M * g.N;
+  if (g.out_f32 && g.ws && g.ldc == g.N && tiles < 512 && g.K >= 2048) {
+    int s = (int)std::min<int64_t>(8, cdiv(512, tiles));
+    while (s > 1 && (s * mn > g.ws_elems || g.K / s < 512)) --s;
+    g.ksplit = s;
+  }
   if (g.out_f32) launch_cfg<128, 128, 64, 64, float>(g, st);
   else launch_cfg<128, 128, 64, 64, bf16>(g, st);
+  if (g.ksplit > 1)
+    splitk_reduce<<<(unsigned)cdiv(cdiv(mn, 4), 256), 256, 0, st>>>(g.ws, g.ksplit, mn, (float*)g.C, g.beta);
   return true;
 }

@@ -24,10 +24,10 @@ void launch_embed_gather(bool bf, const int32_t* tok, const void* table, void* x
                          hipStream_t st);
 void launch_rmsnorm_fwd(bool bf, const void* x, const void* gamma, void* y, float* rstd, int rows,
                         int d, float eps, hipStream_t st);
-// dx = resid + rstd * (dn*gamma - xhat * mean(dn*gamma*xhat)); dgamma partial sums per chunk of
-// RMS_CHUNK rows into partial[chunk][d].
+// dx = resid + rstd * (dn*gamma - xhat * mean(dn*gamma*xhat)); dgamma partial sums into
+// partial[p][d]; returns the number of partial rows written (at most 4 per RMS_CHUNK rows).
 constexpr int RMS_CHUNK = 32;
-void launch_rmsnorm_bwd(bool bf, const void* dn, const void* x, const float* rstd,
+int launch_rmsnorm_bwd(bool bf, const void* dn, const void* x, const float* rstd,
                         const void* gamma, const void* resid, void* dx, float* partial, int rows,
                         int d, hipStream_t st);
 void launch_colsum_partials(const float* partial, int nchunks, int d, float* out, bool accumulate,
@@ -54,13 +54,18 @@ void launch_mean(const float* v, int n, float* out, hipStream_t st);
 // B(n,k) = b_kmajor ? B[n*ldb + k] : B[k*ldb + n].  Inputs bf16 or fp32 (bf), accumulation fp32.
 // out_f32: C is fp32 (beta 0: overwrite, 1: accumulate); else C has the input type.
 // resid (input type, leading dimension ldc) is added when non-null.
+// ws / ws_elems: optional fp32 workspace; when the output tile grid underfills the chip and K is
+// long, an fp32-output product is split over K into partial tiles there and summed in a fixed order.
 struct GemmArgs {
   int M, N, K;
   const void* A; int lda; bool a_kmajor;
   const void* B; int ldb; bool b_kmajor;
   void* C; int ldc; bool out_f32; float beta;
   const void* resid;
+  float* ws = nullptr; int64_t ws_elems = 0;
+  int ksplit = 1;  // set by the launcher
 };
+constexpr int64_t GEMM_WS_ELEMS = 16 << 20;  // 64 MiB of fp32 split-K partials per stage
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st);
 
 // ------------------------------------------------------------------ attention (attention.hip)

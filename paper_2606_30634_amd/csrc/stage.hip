@@ -71,6 +71,7 @@ struct stage {
   void *dA, *dB, *dh, *dn, *dz, *dgu, *do_, *dqkv, *dlog, *dhf;
   float *delta, *rms_part, *row_loss, *cos_t, *sin_t, *norm_out;
   double* norm_part;
+  float* gemm_ws;
   int* flag;
   unsigned long long* skipped;
   uint32_t* sorted;
@@ -139,7 +140,9 @@ void timed(stage* S, int cls, double work, F&& launch) {
   }
 }
 
-void run_gemm(stage* S, const GemmArgs& g) {
+void run_gemm(stage* S, GemmArgs g) {
+  g.ws = S->gemm_ws;
+  g.ws_elems = S->gemm_ws ? GEMM_WS_ELEMS : 0;
   timed(S, STAGE_PROF_GEMM, 2.0 * g.M * g.N * g.K, [&] { launch_gemm(S->bf, g, S->st); });
 }
 
@@ -238,8 +241,9 @@ size_t layout(stage* S, char* base) {
   S->do_ = carve(T * hqd * esz);
   S->dqkv = carve(T * qkvw * esz);
   S->delta = (float*)carve((int64_t)sh.micro_batch * sh.n_heads * sh.seq_len * 4);
-  S->rms_part = (float*)carve(cdiv(T, RMS_CHUNK) * d * 4);
+  S->rms_part = (float*)carve(4 * cdiv(T, RMS_CHUNK) * d * 4);
   S->norm_part = (double*)carve(norm_scratch_bytes());
+  S->gemm_ws = sh.dtype == 1 ? (float*)carve(GEMM_WS_ELEMS * 4) : nullptr;
   S->norm_out = (float*)carve(2 * 4);
   S->flag = (int*)carve(4);
   S->skipped = (unsigned long long*)carve(8);
@@ -356,7 +360,6 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   const bool bf = S->bf;
   const float beta = first ? 0.f : 1.f;
   hipStream_t st = S->st;
-  const int nch = (int)cdiv(T, RMS_CHUNK);
   // down projection: dz = dy Wd ; dWd (+)= dy^T z
   run_gemm(S, gemm(T, f, d, dy, d, true, S->wptr(vi, w.wdown), f, false, S->dz, f));
   run_gemm(S, gemm(d, f, T, dy, d, false, b.z, f, false, g + w.wdown, f, true, beta));
@@ -364,8 +367,8 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   // gate/up: dn2 = dgu Wgu ; dWgu (+)= dgu^T n2
   run_gemm(S, gemm(T, d, 2 * f, S->dgu, 2 * f, true, S->wptr(vi, w.wgu), d, false, S->dn, d));
   run_gemm(S, gemm(2 * f, d, T, S->dgu, 2 * f, false, b.n2, d, false, g + w.wgu, d, true, beta));
-  launch_rmsnorm_bwd(bf, S->dn, b.h, b.rstd2, S->wptr(vi, w.ffn_norm), dy, S->dh, S->rms_part, T, d, st);
-  launch_colsum_partials(S->rms_part, nch, d, g + w.ffn_norm, !first, st);
+  int np = launch_rmsnorm_bwd(bf, S->dn, b.h, b.rstd2, S->wptr(vi, w.ffn_norm), dy, S->dh, S->rms_part, T, d, st);
+  launch_colsum_partials(S->rms_part, np, d, g + w.ffn_norm, !first, st);
   // output projection: do = dh Wo ; dWo (+)= dh^T o
   run_gemm(S, gemm(T, S->hqd, d, S->dh, d, true, S->wptr(vi, w.wo), S->hqd, false, S->do_, S->hqd));
   run_gemm(S, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta));
@@ -377,8 +380,8 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   // qkv projection: dn1 = dqkv Wqkv ; dWqkv (+)= dqkv^T n1
   run_gemm(S, gemm(T, d, S->qkvw, S->dqkv, S->qkvw, true, S->wptr(vi, w.wqkv), d, false, S->dn, d));
   run_gemm(S, gemm(S->qkvw, d, T, S->dqkv, S->qkvw, false, b.n1, d, false, g + w.wqkv, d, true, beta));
-  launch_rmsnorm_bwd(bf, S->dn, b.x, b.rstd1, S->wptr(vi, w.attn_norm), S->dh, dx, S->rms_part, T, d, st);
-  launch_colsum_partials(S->rms_part, nch, d, g + w.attn_norm, !first, st);
+  np = launch_rmsnorm_bwd(bf, S->dn, b.x, b.rstd1, S->wptr(vi, w.attn_norm), S->dh, dx, S->rms_part, T, d, st);
+  launch_colsum_partials(S->rms_part, np, d, g + w.attn_norm, !first, st);
 }
 
 }  // namespace
@@ -553,9 +556,9 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
     run_gemm(s, gemm(sh.vocab, d, T, s->dlog, sh.vocab, false, sl.hf, d, false, g + s->off_embed, d,
                          true, first ? 0.f : 1.f));
     head_wrote_embed = true;
-    launch_rmsnorm_bwd(bf, s->dhf, sl.y, sl.rstdf, s->wptr(vi, s->off_final), nullptr, s->dA,
-                       s->rms_part, T, d, st);
-    launch_colsum_partials(s->rms_part, (int)cdiv(T, RMS_CHUNK), d, g + s->off_final, !first, st);
+    const int np = launch_rmsnorm_bwd(bf, s->dhf, sl.y, sl.rstdf, s->wptr(vi, s->off_final), nullptr, s->dA,
+                                       s->rms_part, T, d, st);
+    launch_colsum_partials(s->rms_part, np, d, g + s->off_final, !first, st);
     cur = s->dA;
   }
   for (int i = sh.n_blocks - 1; i >= 0; --i) {
