@@ -74,6 +74,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="small")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="run one plain 1 GiB device-to-device copy first (a known-size reference for "
+                         "the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (one pipeline stage's "
@@ -133,6 +136,13 @@ def main():
                 st.backward(slot, dy=d.get("dy"), microbatches_per_step=M)
         st.update(t, hp)
 
+    if args.calib_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize(dev)
+        dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        del src, dst
     t = 0
     log(f"bench: {w.name}: warmup {args.warmup}")
     for _ in range(args.warmup):

@@ -2,15 +2,19 @@
 //
 // v_mfma_f32_32x32x16_bf16: lane l supplies row (l mod 32) of A and of B with the 8 consecutive k
 // values 8*(l/32)..+7, and receives C rows 8*(i/4) + 4*(l/32) + (i mod 4), column l mod 32 in
-// accumulator i.  Both operands must therefore sit in LDS as [row][k], k contiguous.
+// accumulator i.  Both operands therefore sit in LDS as [row][k], k contiguous.
 //   - an operand whose global layout is k-contiguous (x W^T's x and W, dy W's dy) is copied in
 //     16-byte chunks;
 //   - an operand whose global layout is row-contiguous (W in dy W, both operands of dy^T x) is
 //     read 4 rows x 8 k per thread with 8-byte coalesced loads and transposed in registers.
-// Block tile BM x BN x 64, waves WM x WN each, two LDS stages: the next k-slice is fetched into
+// Block tile BM x BN x 64 over 4 waves of WM x WN, two LDS stages: the next k-slice is fetched into
 // registers while the current one feeds the MFMAs, then written to the other stage; one barrier per
-// k-slice.  Rows are padded by 16 bytes so the 16-byte fragment reads of 32 rows spread over banks.
-// Block order is remapped so that consecutive tiles of one output row band land on one XCD (one L2).
+// k-slice.  Inside a k-slice the fragments of the next 16-deep step are read from LDS while the
+// MFMAs of the current one run.  Rows are padded by 16 bytes so the 16-byte fragment reads of 32
+// rows spread over the banks.  Full tiles use loaders without bounds checks.  The epilogue stages
+// each wave's tile through LDS, 32 rows at a time, and writes 16-byte rows (residual and beta
+// terms read the same way).  Block order is remapped so that consecutive tiles of one output row
+// band land on one XCD (one L2).  Deterministic split-K for underfilled fp32-output products.
 #include "common.h"
 #include "kernels.h"
 #include <algorithm>
@@ -23,16 +27,16 @@ constexpr int PADK = BK + 8;  // LDS row pitch in elements
 __device__ __forceinline__ uint32_t lo_pair(uint32_t x, uint32_t y) { return (x & 0xffffu) | (y << 16); }
 __device__ __forceinline__ uint32_t hi_pair(uint32_t x, uint32_t y) { return (x >> 16) | (y & 0xffff0000u); }
 
-template <int ROWS, int NT, bool KMAJ>
+template <int ROWS, int NT, bool KMAJ, bool CHECK>
 struct TileLoader;
 
 // k-contiguous operand: chunks of 8 consecutive k of one row (16-byte loads and stores)
-template <int ROWS, int NT>
-struct TileLoader<ROWS, NT, true> {
+template <int ROWS, int NT, bool CHECK>
+struct TileLoader<ROWS, NT, true, CHECK> {
   static constexpr int CHUNKS = ROWS * BK / 8;
   static constexpr int PER = CHUNKS / NT;
   static_assert(CHUNKS % NT == 0, "tile does not split evenly over the threads");
-  uint4 r[PER];
+  u32x4 r[PER];
 
   __device__ __forceinline__ void load(const bf16* __restrict__ G, int ld, int row0, int nrows, int k0,
                                        int K) {
@@ -40,27 +44,28 @@ struct TileLoader<ROWS, NT, true> {
     for (int p = 0; p < PER; ++p) {
       const int c = threadIdx.x + p * NT;
       const int gr = row0 + c / (BK / 8), gk = k0 + (c % (BK / 8)) * 8;
-      r[p] = (gr < nrows && gk < K) ? *reinterpret_cast<const uint4*>(G + (int64_t)gr * ld + gk)
-                                    : make_uint4(0u, 0u, 0u, 0u);
+      const bool ok = !CHECK || (gr < nrows && gk < K);
+      const u32x4 v = ok ? *reinterpret_cast<const u32x4*>(G + (int64_t)gr * ld + gk) : u32x4{0u, 0u, 0u, 0u};
+      r[p] = v;
     }
   }
   __device__ __forceinline__ void store(bf16* __restrict__ S) const {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int c = threadIdx.x + p * NT;
-      *reinterpret_cast<uint4*>(S + (c / (BK / 8)) * PADK + (c % (BK / 8)) * 8) = r[p];
+      *reinterpret_cast<u32x4*>(S + (c / (BK / 8)) * PADK + (c % (BK / 8)) * 8) = r[p];
     }
   }
 };
 
 // row-contiguous operand: chunks of 4 rows x 8 k; eight 8-byte loads (one per k, lanes along rows)
 // are transposed in registers into four 16-byte rows of 8 k
-template <int ROWS, int NT>
-struct TileLoader<ROWS, NT, false> {
+template <int ROWS, int NT, bool CHECK>
+struct TileLoader<ROWS, NT, false, CHECK> {
   static constexpr int CHUNKS = ROWS * BK / 32;
   static constexpr int PER = CHUNKS / NT;
   static_assert(CHUNKS % NT == 0, "tile does not split evenly over the threads");
-  uint2 r[PER][8];  // r[p][j] = rows 0..3 of the chunk at its k offset j
+  u32x2 r[PER][8];  // r[p][j] = rows 0..3 of the chunk at its k offset j
 
   __device__ __forceinline__ void load(const bf16* __restrict__ G, int ld, int row0, int nrows, int k0,
                                        int K) {
@@ -69,9 +74,10 @@ struct TileLoader<ROWS, NT, false> {
       const int c = threadIdx.x + p * NT;
       const int gr = row0 + (c % (ROWS / 4)) * 4, kb = k0 + (c / (ROWS / 4)) * 8;
 #pragma unroll
-      for (int j = 0; j < 8; ++j)  // nrows is a multiple of 4: the 4 rows are in bounds together
-        r[p][j] = (gr < nrows && kb + j < K) ? *reinterpret_cast<const uint2*>(G + (int64_t)(kb + j) * ld + gr)
-                                             : make_uint2(0u, 0u);
+      for (int j = 0; j < 8; ++j) {  // nrows is a multiple of 4: the 4 rows are in bounds together
+        const bool ok = !CHECK || (gr < nrows && kb + j < K);
+        r[p][j] = ok ? *reinterpret_cast<const u32x2*>(G + (int64_t)(kb + j) * ld + gr) : u32x2{0u, 0u};
+      }
     }
   }
   __device__ __forceinline__ void store(bf16* __restrict__ S) const {
@@ -79,7 +85,7 @@ struct TileLoader<ROWS, NT, false> {
     for (int p = 0; p < PER; ++p) {
       const int c = threadIdx.x + p * NT;
       bf16* base = S + ((c % (ROWS / 4)) * 4) * PADK + (c / (ROWS / 4)) * 8;
-      uint4 o0, o1, o2, o3;
+      u32x4 o0, o1, o2, o3;
       o0.x = lo_pair(r[p][0].x, r[p][1].x); o0.y = lo_pair(r[p][2].x, r[p][3].x);
       o0.z = lo_pair(r[p][4].x, r[p][5].x); o0.w = lo_pair(r[p][6].x, r[p][7].x);
       o1.x = hi_pair(r[p][0].x, r[p][1].x); o1.y = hi_pair(r[p][2].x, r[p][3].x);
@@ -88,20 +94,31 @@ struct TileLoader<ROWS, NT, false> {
       o2.z = lo_pair(r[p][4].y, r[p][5].y); o2.w = lo_pair(r[p][6].y, r[p][7].y);
       o3.x = hi_pair(r[p][0].y, r[p][1].y); o3.y = hi_pair(r[p][2].y, r[p][3].y);
       o3.z = hi_pair(r[p][4].y, r[p][5].y); o3.w = hi_pair(r[p][6].y, r[p][7].y);
-      *reinterpret_cast<uint4*>(base) = o0;
-      *reinterpret_cast<uint4*>(base + PADK) = o1;
-      *reinterpret_cast<uint4*>(base + 2 * PADK) = o2;
-      *reinterpret_cast<uint4*>(base + 3 * PADK) = o3;
+      *reinterpret_cast<u32x4*>(base) = o0;
+      *reinterpret_cast<u32x4*>(base + PADK) = o1;
+      *reinterpret_cast<u32x4*>(base + 2 * PADK) = o2;
+      *reinterpret_cast<u32x4*>(base + 3 * PADK) = o3;
     }
   }
 };
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT>
+template <int BM, int BN, int WM, int WN>
+struct Cfg {
+  static constexpr int NW = (BM / WM) * (BN / WN);
+  static constexpr int NT = NW * 64;
+  static constexpr int FM = WM / 32, FN = WN / 32;
+  static constexpr size_t main_lds = (size_t)2 * (BM + BN) * PADK * sizeof(bf16);
+  static constexpr int EP = WN + 4;  // epilogue staging pitch (fp32 elements)
+  static constexpr size_t epi_lds = (size_t)NW * 32 * EP * sizeof(float);
+  static constexpr size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
+};
+
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, bool CHECK>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 gemm_mfma_kernel(GemmArgs g) {
+  using C_ = Cfg<BM, BN, WM, WN>;
   constexpr int WAVES_N = BN / WN;
-  constexpr int NT = (BM / WM) * (BN / WN) * 64;
-  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int NT = C_::NT, FM = C_::FM, FN = C_::FN;
   extern __shared__ __align__(16) unsigned char smem[];
   bf16* As = reinterpret_cast<bf16*>(smem);                 // [2][BM][PADK]
   bf16* Bs = As + 2 * BM * PADK;                            // [2][BN][PADK]
@@ -127,8 +144,8 @@ gemm_mfma_kernel(GemmArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  TileLoader<BM, NT, AK> la;
-  TileLoader<BN, NT, BKM> lb;
+  TileLoader<BM, NT, AK, CHECK> la;
+  TileLoader<BN, NT, BKM, CHECK> lb;
   const bf16* A = (const bf16*)g.A;
   const bf16* B = (const bf16*)g.B;
   // split-K: this block covers k in [kbeg, kend); kbeg is a multiple of BK
@@ -144,29 +161,36 @@ gemm_mfma_kernel(GemmArgs g) {
   la.store(As);
   lb.store(Bs);
   __syncthreads();
+  const int frow = lane % 32, fk = 8 * (lane / 32);
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     if (kt + 1 < nk) {
       la.load(A, g.lda, m0, g.M, kbeg + (kt + 1) * BK, kend);
       lb.load(B, g.ldb, n0, g.N, kbeg + (kt + 1) * BK, kend);
     }
-    const bf16* as = As + cur * BM * PADK;
-    const bf16* bs = Bs + cur * BN * PADK;
+    const bf16* as = As + cur * BM * PADK + (wm0 + frow) * PADK + fk;
+    const bf16* bs = Bs + cur * BN * PADK + (wn0 + frow) * PADK + fk;
+    bf16x8 af[2][FM], bfr[2][FN];
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      bf16x8 af[FM], bfr[FN];
+    for (int i = 0; i < FM; ++i) af[0][i] = *reinterpret_cast<const bf16x8*>(as + i * 32 * PADK);
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(as + (wm0 + i * 32 + lane % 32) * PADK + kk + 8 * (lane / 32));
+    for (int j = 0; j < FN; ++j) bfr[0][j] = *reinterpret_cast<const bf16x8*>(bs + j * 32 * PADK);
+    static_for<BK / 16>([&](auto KS) {
+      constexpr int ks = KS, c = ks & 1;
+      if constexpr (ks + 1 < BK / 16) {  // next 16-deep step's fragments while these MFMAs run
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(bs + (wn0 + j * 32 + lane % 32) * PADK + kk + 8 * (lane / 32));
+        for (int i = 0; i < FM; ++i)
+          af[c ^ 1][i] = *reinterpret_cast<const bf16x8*>(as + i * 32 * PADK + (ks + 1) * 16);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          bfr[c ^ 1][j] = *reinterpret_cast<const bf16x8*>(bs + j * 32 * PADK + (ks + 1) * 16);
+      }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
+    });
     if (kt + 1 < nk) {
       la.store(As + (cur ^ 1) * BM * PADK);
       lb.store(Bs + (cur ^ 1) * BN * PADK);
@@ -174,41 +198,59 @@ gemm_mfma_kernel(GemmArgs g) {
     __syncthreads();
   }
 
-  if (g.ksplit > 1) {  // partial tile of this split: plain fp32 into the workspace
-    float* W = g.ws + (int64_t)blockIdx.y * g.M * g.N;
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int col = n0 + wn0 + j * 32 + lane % 32;
-        if (col >= g.N) continue;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int row = m0 + wm0 + i * 32 + 8 * (e / 4) + 4 * (lane / 32) + (e % 4);
-          if (row < g.M) W[(int64_t)row * g.N + col] = acc[i][j][e];
-        }
-      }
-    return;
-  }
+  // epilogue: per 32-row slice of the wave tile, stage fp32 through LDS and write 16-byte rows
+  float* stg = reinterpret_cast<float*>(smem) + wave * 32 * C_::EP;
+  const bool split = g.ksplit > 1;
+  float* W = split ? g.ws + (int64_t)blockIdx.y * g.M * g.N : nullptr;
   OutT* C = (OutT*)g.C;
   const bf16* R = (const bf16*)g.resid;
+  constexpr int VEC = sizeof(OutT) == 2 ? 8 : 4;  // elements per 16-byte store
+  static_for<FM>([&](auto I) {
+    constexpr int i = I;
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int col = n0 + wn0 + j * 32 + lane % 32;
-      if (col >= g.N) continue;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm0 + i * 32 + 8 * (e / 4) + 4 * (lane / 32) + (e % 4);
-        if (row >= g.M) continue;
+      for (int e = 0; e < 16; ++e)
+        stg[(8 * (e / 4) + 4 * (lane / 32) + (e % 4)) * C_::EP + j * 32 + lane % 32] = acc[i][j][e];
+    __syncthreads();
+    const int rbase = m0 + wm0 + i * 32;
+    if (split) {
+      for (int c = lane; c < 32 * WN / 4; c += 64) {
+        const int r = c / (WN / 4), cc = (c % (WN / 4)) * 4;
+        const int row = rbase + r, col = n0 + wn0 + cc;
+        if (!CHECK || (row < g.M && col < g.N))
+          *reinterpret_cast<float4*>(W + (int64_t)row * g.N + col) = *reinterpret_cast<const float4*>(stg + r * C_::EP + cc);
+      }
+    } else {
+      for (int c = lane; c < 32 * WN / VEC; c += 64) {
+        const int r = c / (WN / VEC), cc = (c % (WN / VEC)) * VEC;
+        const int row = rbase + r, col = n0 + wn0 + cc;
+        if (CHECK && (row >= g.M || col >= g.N)) continue;  // N is a multiple of 8
         const int64_t o = (int64_t)row * g.ldc + col;
-        float v = acc[i][j][e];
-        if (sizeof(OutT) == 4 && g.beta != 0.f) v += g.beta * to_f32(C[o]);
-        if (R) v += (float)R[o];
-        C[o] = from_f32<OutT>(v);
+        float v[VEC];
+#pragma unroll
+        for (int q = 0; q < VEC; ++q) v[q] = stg[r * C_::EP + cc + q];
+        if constexpr (sizeof(OutT) == 4) {
+          if (g.beta != 0.f) {
+            const float4 old = *reinterpret_cast<const float4*>((const float*)C + o);
+            v[0] += g.beta * old.x; v[1] += g.beta * old.y; v[2] += g.beta * old.z; v[3] += g.beta * old.w;
+          }
+          *reinterpret_cast<float4*>((float*)C + o) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          if (R) {
+            const bf16x8 rr = *reinterpret_cast<const bf16x8*>(R + o);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] += (float)rr[q];
+          }
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
+          *reinterpret_cast<bf16x8*>((bf16*)C + o) = ov;
+        }
       }
     }
+    __syncthreads();
+  });
 }
 
 // C = beta C + sum over splits of the partial tiles, in split order (fp32 output, ldc == N)
@@ -236,20 +278,28 @@ __global__ void __launch_bounds__(256) splitk_reduce(const float* __restrict__ w
   }
 }
 
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, bool CHECK>
+void launch_one(const GemmArgs& g, int nblk, hipStream_t st) {
+  using C_ = Cfg<BM, BN, WM, WN>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)gemm_mfma_kernel<BM, BN, WM, WN, AK, BKM, OutT, CHECK>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)C_::lds);
+    attr_set = true;
+  }
+  gemm_mfma_kernel<BM, BN, WM, WN, AK, BKM, OutT, CHECK><<<dim3(nblk, g.ksplit), C_::NT, C_::lds, st>>>(g);
+}
+
 template <int BM, int BN, int WM, int WN, typename OutT>
 void launch_cfg(const GemmArgs& g, hipStream_t st) {
-  constexpr int NT = (BM / WM) * (BN / WN) * 64;
-  const size_t lds = (size_t)2 * (BM + BN) * PADK * sizeof(bf16);
   const int nblk = (int)(cdiv(g.M, BM) * cdiv(g.N, BN));
-#define L(AK, BKM)                                                                                 \
-  do {                                                                                             \
-    static bool attr_set = false;                                                                  \
-    if (!attr_set) {                                                                               \
-      (void)hipFuncSetAttribute((const void*)gemm_mfma_kernel<BM, BN, WM, WN, AK, BKM, OutT>,      \
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);             \
-      attr_set = true;                                                                             \
-    }                                                                                              \
-    gemm_mfma_kernel<BM, BN, WM, WN, AK, BKM, OutT><<<dim3(nblk, g.ksplit), NT, lds, st>>>(g);      \
+  // full tiles and whole k-slices everywhere (each split covers a whole number of slices)
+  const bool even = g.M % BM == 0 && g.N % BN == 0 && g.K % BK == 0 &&
+                    (g.ksplit == 1 || (g.K / BK) % g.ksplit == 0);
+#define L(AK, BKM)                                                                        \
+  do {                                                                                    \
+    if (even) launch_one<BM, BN, WM, WN, AK, BKM, OutT, false>(g, nblk, st);              \
+    else launch_one<BM, BN, WM, WN, AK, BKM, OutT, true>(g, nblk, st);                    \
   } while (0)
   if (g.a_kmajor && g.b_kmajor) L(true, true);
   else if (g.a_kmajor) L(true, false);
@@ -262,19 +312,27 @@ void launch_cfg(const GemmArgs& g, hipStream_t st) {
 
 bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   // vector-load alignment: 8 elements along every contiguous dimension, rows in groups of 4
-  if (g0.K % 8 || g0.M % 8 || g0.N % 8 || g0.lda % 8 || g0.ldb % 8) return false;
-  if ((uintptr_t)g0.A % 16 || (uintptr_t)g0.B % 16) return false;
+  if (g0.K % 8 || g0.M % 8 || g0.N % 8 || g0.lda % 8 || g0.ldb % 8 || g0.ldc % 8) return false;
+  if ((uintptr_t)g0.A % 16 || (uintptr_t)g0.B % 16 || (uintptr_t)g0.C % 16 || (uintptr_t)g0.resid % 16)
+    return false;
   GemmArgs g = g0;
   g.ksplit = 1;
-  const int64_t tiles = cdiv(g.M, 128) * cdiv(g.N, 128);
   const int64_t mn = (int64_t)g.M * g.N;
+  // 256x256 tiles when the product is deep enough to amortise them and still fills the chip
+  const bool big = g.K >= 2048 && cdiv(g.M, 256) * cdiv(g.N, 256) >= 256;
+  const int64_t tiles = big ? cdiv(g.M, 256) * cdiv(g.N, 256) : cdiv(g.M, 128) * cdiv(g.N, 128);
   if (g.out_f32 && g.ws && g.ldc == g.N && tiles < 512 && g.K >= 2048) {
     int s = (int)std::min<int64_t>(8, cdiv(512, tiles));
     while (s > 1 && (s * mn > g.ws_elems || g.K / s < 512)) --s;
     g.ksplit = s;
   }
-  if (g.out_f32) launch_cfg<128, 128, 64, 64, float>(g, st);
-  else launch_cfg<128, 128, 64, 64, bf16>(g, st);
+  if (big) {
+    if (g.out_f32) launch_cfg<256, 256, 128, 128, float>(g, st);
+    else launch_cfg<256, 256, 128, 128, bf16>(g, st);
+  } else {
+    if (g.out_f32) launch_cfg<128, 128, 64, 64, float>(g, st);
+    else launch_cfg<128, 128, 64, 64, bf16>(g, st);
+  }
   if (g.ksplit > 1)
     splitk_reduce<<<(unsigned)cdiv(cdiv(mn, 4), 256), 256, 0, st>>>(g.ws, g.ksplit, mn, (float*)g.C, g.beta);
   return true;
