@@ -67,6 +67,54 @@ def cpu_baseline(w):
             "measured_s": round(t3 - t0 + (t2 - t1), 2)}
 
 
+def update_workload(steps):
+    """The update-only workload: delayed_update_flat over a flat 1.0e9-element fp32 vector (x, m, v,
+    EF buffer), one bf16 gradient N(0, 1e-3), bf16 compute copy; `steps` iterations timed with HIP
+    events on the stream.  36 algorithmic bytes per element.  A plain device copy of 4 GiB is timed
+    in the same process as the practical HBM ceiling."""
+    import torch
+    from paper_2606_30634_amd import binding as B
+    from paper_2606_30634_amd.stage import hparams
+    n = 1_000_000_000
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+    x = torch.randn(n, device=dev, generator=gen).mul_(0.02)
+    g = torch.randn(n, device=dev, generator=gen).mul_(1e-3).to(torch.bfloat16)
+    m = torch.zeros(n, device=dev)
+    v = torch.zeros(n, device=dev)
+    up = torch.zeros(n, device=dev)
+    sh = torch.empty(n, device=dev, dtype=torch.bfloat16)
+    hp = hparams(lr=1e-3, ef_lambda=1.0, clip_norm=0.0)
+    stream = torch.cuda.current_stream(dev)
+    call = lambda t: B.delayed_update_flat(n, x.data_ptr(), g.data_ptr(), True, m.data_ptr(), v.data_ptr(),
+                                           up.data_ptr(), sh.data_ptr(), True, t, hp, None, stream.cuda_stream)
+    call(1)  # warm-up (t = 1: a real update)
+    torch.cuda.synchronize(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for t in range(2, 2 + steps):
+        call(t)
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    ms = e0.elapsed_time(e1) / steps
+    gbs = 36.0 * n / (ms * 1e-3) / 1e9
+    del g, m, v, up, sh
+    src = x[: 1 << 30]  # 4 GiB
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize(dev)
+    e0.record(stream)
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    copy_gbs = 2.0 * src.numel() * 4 / (e0.elapsed_time(e1) / 5 * 1e-3) / 1e9
+    return {"elements": n, "steps": steps, "bytes_per_element": 36, "ms_per_step": round(ms, 4),
+            "achieved_GBs": round(gbs, 1), "peak_GBs": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "plain_copy_GBs": round(copy_gbs, 1), "frac_of_copy": round(gbs / copy_gbs, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -74,6 +122,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="small")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--update-steps", type=int, default=50,
+                    help="iterations of the update-only workload (1.0e9 fp32 elements); 0 skips it")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one plain 1 GiB device-to-device copy first (a known-size reference for "
                          "the FETCH_SIZE / WRITE_SIZE counters)")
@@ -197,6 +247,8 @@ def main():
     rc, skipped = B.stage_poll_nonfinite(st.handle)
     st.close()
 
+    upd = update_workload(args.update_steps) if args.update_steps > 0 else None
+
     cpu = None
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline")
@@ -219,6 +271,7 @@ def main():
                    "optimizer": "AdamW, delay 1, Error Feedback lambda 1, clip 1.0", "parallelism": "1 GPU, one stage"},
         "roofline": roofline,
         "kernels": kern,
+        "update_workload": upd,
         "cpu_baseline": cpu,
         "wall_s_timed_region": round(wall, 3),
         "skipped_updates": skipped,

@@ -25,7 +25,6 @@ constexpr int KB = 64;    // rows per streamed tile
 constexpr int NT = 256;   // 4 waves
 constexpr float LOG2E = 1.4426950408889634f;
 
-typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
   bf16 x = (bf16)a, y = (bf16)b;
@@ -39,21 +38,6 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 __device__ __forceinline__ bf16x8 frag_rows(const bf16* T, int P, int r0, int k0) {
   const int l = threadIdx.x % 64;
   return *reinterpret_cast<const bf16x8*>(T + (r0 + l % 32) * P + k0 + 8 * (l / 32));
-}
-
-// fragment whose row index runs along the columns of a [k][row] tile (pitch P elements):
-// row r0 + lane mod 32, k = k0 + 8 (lane / 32) .. +7; two transposing reads of 4 k each.
-__device__ __forceinline__ bf16x8 frag_tr(const bf16* T, int P, int r0, int k0) {
-  const int l = threadIdx.x % 64, g = l / 16, i = l % 16;
-  const int r = r0 + 16 * (g & 1) + 4 * (i & 3);
-  const int k = k0 + 8 * (g >> 1) + (i >> 2);
-  typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(T + k * P + r));
-  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(T + (k + 4) * P + r));
-  bf16x8 f;
-  __builtin_memcpy(&f, &lo, 8);
-  __builtin_memcpy(reinterpret_cast<char*>(&f) + 8, &hi, 8);
-  return f;
 }
 
 // B operand (8 consecutive k at column lane mod 32) from a 32x32 accumulator whose rows are the k
@@ -414,13 +398,20 @@ __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows(Qs, P, t * 32, ks * 16), kf[ks], s, 0, 0, 0);
         dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows(Ds, P, t * 32, ks * 16), vf[ks], dp, 0, 0, 0);
       }
+      // accumulator rows of this lane: t*32 + 8 (e/4) + 4 half + (e mod 4): four runs of 4
+      // consecutive query rows, so lse and delta arrive as 16-byte reads
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = t * 32 + 8 * (e / 4) + 4 * half + (e % 4);  // query row within the block
-        const int q = qs0 + r;
-        const float p = (q >= mykey && q < a.S) ? exp2f(s[e] * sl2 - Ls[r]) : 0.f;
-        s[e] = p;
-        dp[e] = p * (dp[e] - Dl[r]);
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int r0 = t * 32 + 8 * e4 + 4 * half;
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(Ls + r0);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + r0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int e = 4 * e4 + j, q = qs0 + r0 + j;
+          const float p = (q >= mykey && q < a.S) ? exp2f(s[e] * sl2 - l4[j]) : 0.f;
+          s[e] = p;
+          dp[e] = p * (dp[e] - d4[j]);
+        }
       }
 #pragma unroll
       for (int g2 = 0; g2 < 2; ++g2) {

@@ -52,6 +52,25 @@ __device__ __forceinline__ T block_sum(T v, T* smem /* >= 16 entries */) {
 
 static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// MFMA fragment (v_mfma_f32_32x32x16_bf16 operand) whose row index runs along the columns of a
+// [k][row] LDS tile of pitch P elements: row r0 + lane mod 32, k = k0 + 8 (lane / 32) .. +7.
+// ds_read_b64_tr_b16 lets each 16-lane group read a 4 x 16 block (lanes 4r..4r+3 supply row r,
+// 4 consecutive elements each) and hands column j to lane j; two such reads give 8 k.
+// Addresses must be 8-byte aligned (r0 and P multiples of 4).
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x8 frag_tr(const bf16* T, int P, int r0, int k0) {
+  const int l = threadIdx.x % 64, g = l / 16, i = l % 16;
+  const int r = r0 + 16 * (g & 1) + 4 * (i & 3);
+  const int k = k0 + 8 * (g >> 1) + (i >> 2);
+  typedef __attribute__((address_space(3))) v4i16_t lds_v4i16;
+  const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(T + k * P + r));
+  const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(T + (k + 4) * P + r));
+  bf16x8 f;
+  __builtin_memcpy(&f, &lo, 8);
+  __builtin_memcpy(reinterpret_cast<char*>(&f) + 8, &hi, 8);
+  return f;
+}
+
 // Compile-time loop: f(std::integral_constant<int, 0>) ... f(<N-1>).  Keeps register-array indices
 // constant even where a loop body holds a barrier (which can stop the unroller).
 #include <utility>

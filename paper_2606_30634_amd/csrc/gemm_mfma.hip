@@ -6,7 +6,8 @@
 //   - an operand whose global layout is k-contiguous (x W^T's x and W, dy W's dy) is copied in
 //     16-byte chunks;
 //   - an operand whose global layout is row-contiguous (W in dy W, both operands of dy^T x) is
-//     read 4 rows x 8 k per thread with 8-byte coalesced loads and transposed in registers.
+//     staged as it sits in memory ([k][row], 16-byte chunks) and its fragments are read with
+//     gfx950's transposing LDS read ds_read_b64_tr_b16.
 // Block tile BM x BN x 64 over 4 waves of WM x WN, two LDS stages: the next k-slice is fetched into
 // registers while the current one feeds the MFMAs, then written to the other stage; one barrier per
 // k-slice.  Inside a k-slice the fragments of the next 16-deep step are read from LDS while the
@@ -23,9 +24,6 @@ namespace {
 
 constexpr int BK = 64;
 constexpr int PADK = BK + 8;  // LDS row pitch in elements
-
-__device__ __forceinline__ uint32_t lo_pair(uint32_t x, uint32_t y) { return (x & 0xffffu) | (y << 16); }
-__device__ __forceinline__ uint32_t hi_pair(uint32_t x, uint32_t y) { return (x >> 16) | (y & 0xffff0000u); }
 
 template <int ROWS, int NT, bool KMAJ, bool CHECK>
 struct TileLoader;
@@ -58,56 +56,61 @@ struct TileLoader<ROWS, NT, true, CHECK> {
   }
 };
 
-// row-contiguous operand: chunks of 4 rows x 8 k; eight 8-byte loads (one per k, lanes along rows)
-// are transposed in registers into four 16-byte rows of 8 k
+// row-contiguous operand: kept as it sits in memory, a [k][row] tile of pitch ROWS + 16 filled
+// with 16-byte chunks of 8 rows; its MFMA fragments are read with transposing LDS reads (the
+// 16-element pad puts the 4 rows of one transposing read on distinct banks)
+template <int ROWS>
+constexpr int row_pitch() { return ROWS + 16; }
+
 template <int ROWS, int NT, bool CHECK>
 struct TileLoader<ROWS, NT, false, CHECK> {
-  static constexpr int CHUNKS = ROWS * BK / 32;
+  static constexpr int CHUNKS = ROWS * BK / 8;
   static constexpr int PER = CHUNKS / NT;
+  static constexpr int PR = row_pitch<ROWS>();
   static_assert(CHUNKS % NT == 0, "tile does not split evenly over the threads");
-  u32x2 r[PER][8];  // r[p][j] = rows 0..3 of the chunk at its k offset j
+  u32x4 r[PER];
 
   __device__ __forceinline__ void load(const bf16* __restrict__ G, int ld, int row0, int nrows, int k0,
                                        int K) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int c = threadIdx.x + p * NT;
-      const int gr = row0 + (c % (ROWS / 4)) * 4, kb = k0 + (c / (ROWS / 4)) * 8;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {  // nrows is a multiple of 4: the 4 rows are in bounds together
-        const bool ok = !CHECK || (gr < nrows && kb + j < K);
-        r[p][j] = ok ? *reinterpret_cast<const u32x2*>(G + (int64_t)(kb + j) * ld + gr) : u32x2{0u, 0u};
-      }
+      const int gk = k0 + c / (ROWS / 8), gr = row0 + (c % (ROWS / 8)) * 8;
+      const bool ok = !CHECK || (gr < nrows && gk < K);  // nrows is a multiple of 8
+      r[p] = ok ? *reinterpret_cast<const u32x4*>(G + (int64_t)gk * ld + gr) : u32x4{0u, 0u, 0u, 0u};
     }
   }
   __device__ __forceinline__ void store(bf16* __restrict__ S) const {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int c = threadIdx.x + p * NT;
-      bf16* base = S + ((c % (ROWS / 4)) * 4) * PADK + (c / (ROWS / 4)) * 8;
-      u32x4 o0, o1, o2, o3;
-      o0.x = lo_pair(r[p][0].x, r[p][1].x); o0.y = lo_pair(r[p][2].x, r[p][3].x);
-      o0.z = lo_pair(r[p][4].x, r[p][5].x); o0.w = lo_pair(r[p][6].x, r[p][7].x);
-      o1.x = hi_pair(r[p][0].x, r[p][1].x); o1.y = hi_pair(r[p][2].x, r[p][3].x);
-      o1.z = hi_pair(r[p][4].x, r[p][5].x); o1.w = hi_pair(r[p][6].x, r[p][7].x);
-      o2.x = lo_pair(r[p][0].y, r[p][1].y); o2.y = lo_pair(r[p][2].y, r[p][3].y);
-      o2.z = lo_pair(r[p][4].y, r[p][5].y); o2.w = lo_pair(r[p][6].y, r[p][7].y);
-      o3.x = hi_pair(r[p][0].y, r[p][1].y); o3.y = hi_pair(r[p][2].y, r[p][3].y);
-      o3.z = hi_pair(r[p][4].y, r[p][5].y); o3.w = hi_pair(r[p][6].y, r[p][7].y);
-      *reinterpret_cast<u32x4*>(base) = o0;
-      *reinterpret_cast<u32x4*>(base + PADK) = o1;
-      *reinterpret_cast<u32x4*>(base + 2 * PADK) = o2;
-      *reinterpret_cast<u32x4*>(base + 3 * PADK) = o3;
+      *reinterpret_cast<u32x4*>(S + (c / (ROWS / 8)) * PR + (c % (ROWS / 8)) * 8) = r[p];
     }
   }
 };
 
-template <int BM, int BN, int WM, int WN>
+// LDS elements of one stage of an operand tile
+template <int ROWS, bool KMAJ>
+constexpr int stage_elems() { return KMAJ ? ROWS * PADK : BK * row_pitch<ROWS>(); }
+
+// MFMA fragment: row r0 + lane mod 32 of the tile, k = k0 + 8 (lane / 32) .. +7
+template <int ROWS, bool KMAJ>
+__device__ __forceinline__ bf16x8 frag(const bf16* T, int r0, int k0) {
+  if constexpr (KMAJ) {
+    const int l = threadIdx.x % 64;
+    return *reinterpret_cast<const bf16x8*>(T + (r0 + l % 32) * PADK + k0 + 8 * (l / 32));
+  } else {
+    return frag_tr(T, row_pitch<ROWS>(), r0, k0);
+  }
+}
+
+template <int BM, int BN, int WM, int WN, bool AK = true, bool BKM = true>
 struct Cfg {
   static constexpr int NW = (BM / WM) * (BN / WN);
   static constexpr int NT = NW * 64;
   static constexpr int FM = WM / 32, FN = WN / 32;
-  static constexpr size_t main_lds = (size_t)2 * (BM + BN) * PADK * sizeof(bf16);
+  static constexpr int SA = stage_elems<BM, AK>(), SB = stage_elems<BN, BKM>();
+  static constexpr size_t main_lds = (size_t)2 * (SA + SB) * sizeof(bf16);
   static constexpr int EP = WN + 4;  // epilogue staging pitch (fp32 elements)
   static constexpr size_t epi_lds = (size_t)NW * 32 * EP * sizeof(float);
   static constexpr size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
@@ -116,12 +119,12 @@ struct Cfg {
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, bool CHECK>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 gemm_mfma_kernel(GemmArgs g) {
-  using C_ = Cfg<BM, BN, WM, WN>;
+  using C_ = Cfg<BM, BN, WM, WN, AK, BKM>;
   constexpr int WAVES_N = BN / WN;
-  constexpr int NT = C_::NT, FM = C_::FM, FN = C_::FN;
+  constexpr int NT = C_::NT, FM = C_::FM, FN = C_::FN, SA = C_::SA, SB = C_::SB;
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16* As = reinterpret_cast<bf16*>(smem);                 // [2][BM][PADK]
-  bf16* Bs = As + 2 * BM * PADK;                            // [2][BN][PADK]
+  bf16* As = reinterpret_cast<bf16*>(smem);                 // [2][SA]
+  bf16* Bs = As + 2 * SA;                                   // [2][SB]
 
   // XCD-aware tile order: hardware places block b on XCD b mod 8; give each XCD a contiguous run
   // of tiles (in row-band order) so the tiles sharing A rows share that XCD's L2.
@@ -161,29 +164,26 @@ gemm_mfma_kernel(GemmArgs g) {
   la.store(As);
   lb.store(Bs);
   __syncthreads();
-  const int frow = lane % 32, fk = 8 * (lane / 32);
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     if (kt + 1 < nk) {
       la.load(A, g.lda, m0, g.M, kbeg + (kt + 1) * BK, kend);
       lb.load(B, g.ldb, n0, g.N, kbeg + (kt + 1) * BK, kend);
     }
-    const bf16* as = As + cur * BM * PADK + (wm0 + frow) * PADK + fk;
-    const bf16* bs = Bs + cur * BN * PADK + (wn0 + frow) * PADK + fk;
+    const bf16* as = As + cur * SA;
+    const bf16* bs = Bs + cur * SB;
     bf16x8 af[2][FM], bfr[2][FN];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) af[0][i] = *reinterpret_cast<const bf16x8*>(as + i * 32 * PADK);
+    for (int i = 0; i < FM; ++i) af[0][i] = frag<BM, AK>(as, wm0 + i * 32, 0);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) bfr[0][j] = *reinterpret_cast<const bf16x8*>(bs + j * 32 * PADK);
+    for (int j = 0; j < FN; ++j) bfr[0][j] = frag<BN, BKM>(bs, wn0 + j * 32, 0);
     static_for<BK / 16>([&](auto KS) {
       constexpr int ks = KS, c = ks & 1;
       if constexpr (ks + 1 < BK / 16) {  // next 16-deep step's fragments while these MFMAs run
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
-          af[c ^ 1][i] = *reinterpret_cast<const bf16x8*>(as + i * 32 * PADK + (ks + 1) * 16);
+        for (int i = 0; i < FM; ++i) af[c ^ 1][i] = frag<BM, AK>(as, wm0 + i * 32, (ks + 1) * 16);
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-          bfr[c ^ 1][j] = *reinterpret_cast<const bf16x8*>(bs + j * 32 * PADK + (ks + 1) * 16);
+        for (int j = 0; j < FN; ++j) bfr[c ^ 1][j] = frag<BN, BKM>(bs, wn0 + j * 32, (ks + 1) * 16);
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -192,8 +192,8 @@ gemm_mfma_kernel(GemmArgs g) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
     });
     if (kt + 1 < nk) {
-      la.store(As + (cur ^ 1) * BM * PADK);
-      lb.store(Bs + (cur ^ 1) * BN * PADK);
+      la.store(As + (cur ^ 1) * SA);
+      lb.store(Bs + (cur ^ 1) * SB);
     }
     __syncthreads();
   }
@@ -280,7 +280,7 @@ __global__ void __launch_bounds__(256) splitk_reduce(const float* __restrict__ w
 
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, bool CHECK>
 void launch_one(const GemmArgs& g, int nblk, hipStream_t st) {
-  using C_ = Cfg<BM, BN, WM, WN>;
+  using C_ = Cfg<BM, BN, WM, WN, AK, BKM>;
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute((const void*)gemm_mfma_kernel<BM, BN, WM, WN, AK, BKM, OutT, CHECK>,

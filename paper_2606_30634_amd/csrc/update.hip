@@ -20,29 +20,34 @@ namespace {
 constexpr int NORM_BLOCKS = 1024;
 constexpr int NORM_THREADS = 256;
 
+// Streaming accesses: every byte of the pass is touched once, so loads and stores are
+// non-temporal (they bypass the caches' retention policy) and use native 16- / 8-byte vectors.
 template <typename G>
 __device__ __forceinline__ void load4(const G* p, int64_t i, float r[4]);
 template <>
 __device__ __forceinline__ void load4<float>(const float* p, int64_t i, float r[4]) {
-  float4 v = *reinterpret_cast<const float4*>(p + i);
-  r[0] = v.x; r[1] = v.y; r[2] = v.z; r[3] = v.w;
+  const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + i));
+  r[0] = v[0]; r[1] = v[1]; r[2] = v[2]; r[3] = v[3];
 }
 template <>
 __device__ __forceinline__ void load4<bf16>(const bf16* p, int64_t i, float r[4]) {
-  bf16x4 v = *reinterpret_cast<const bf16x4*>(p + i);
-  r[0] = (float)v[0]; r[1] = (float)v[1]; r[2] = (float)v[2]; r[3] = (float)v[3];
+  const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p + i));
+  r[0] = __uint_as_float(v[0] << 16); r[1] = __uint_as_float(v[0] & 0xffff0000u);
+  r[2] = __uint_as_float(v[1] << 16); r[3] = __uint_as_float(v[1] & 0xffff0000u);
 }
 template <typename S>
 __device__ __forceinline__ void store4(S* p, int64_t i, const float r[4]);
 template <>
 __device__ __forceinline__ void store4<float>(float* p, int64_t i, const float r[4]) {
-  *reinterpret_cast<float4*>(p + i) = make_float4(r[0], r[1], r[2], r[3]);
+  __builtin_nontemporal_store(f32x4{r[0], r[1], r[2], r[3]}, reinterpret_cast<f32x4*>(p + i));
 }
 template <>
 __device__ __forceinline__ void store4<bf16>(bf16* p, int64_t i, const float r[4]) {
   bf16x4 v;
   v[0] = (bf16)r[0]; v[1] = (bf16)r[1]; v[2] = (bf16)r[2]; v[3] = (bf16)r[3];
-  *reinterpret_cast<bf16x4*>(p + i) = v;
+  u32x2 u;
+  __builtin_memcpy(&u, &v, 8);
+  __builtin_nontemporal_store(u, reinterpret_cast<u32x2*>(p + i));
 }
 
 // Pass 1: block b sums g^2 over its contiguous range in double; partial[b].
@@ -89,16 +94,12 @@ __global__ void __launch_bounds__(1024) norm_finish(const double* __restrict__ p
 }
 
 template <typename G, typename S, bool EF>
-__global__ void __launch_bounds__(256) fused_update(int64_t n, float* __restrict__ x,
-                                                    const G* __restrict__ g,
-                                                    float* __restrict__ m, float* __restrict__ v,
-                                                    float* __restrict__ up, S* __restrict__ shadow,
-                                                    UpdateScalars hs, const float* __restrict__ clip,
-                                                    const int* __restrict__ skip_flag) {
-  const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+__device__ __forceinline__ void update_group(int64_t n, int64_t i, float* __restrict__ x,
+                                             const G* __restrict__ g, float* __restrict__ m,
+                                             float* __restrict__ v, float* __restrict__ up,
+                                             S* __restrict__ shadow, const UpdateScalars& hs, float c,
+                                             bool skip) {
   if (i >= n) return;
-  const bool skip = hs.apply == 0 || (skip_flag && skip_flag[0] != 0);
-  const float c = clip ? clip[0] : 1.0f;
   if (i + 3 < n) {
     float xr[4];
     load4<float>(x, i, xr);
@@ -146,6 +147,23 @@ __global__ void __launch_bounds__(256) fused_update(int64_t n, float* __restrict
   }
 }
 
+// Each thread owns V groups of 4 consecutive elements, the groups one block-width apart so that
+// every load instruction of a wave covers contiguous memory.
+template <typename G, typename S, bool EF, int V>
+__global__ void __launch_bounds__(256) fused_update(int64_t n, float* __restrict__ x,
+                                                    const G* __restrict__ g,
+                                                    float* __restrict__ m, float* __restrict__ v,
+                                                    float* __restrict__ up, S* __restrict__ shadow,
+                                                    UpdateScalars hs, const float* __restrict__ clip,
+                                                    const int* __restrict__ skip_flag) {
+  const bool skip = hs.apply == 0 || (skip_flag && skip_flag[0] != 0);
+  const float c = clip ? clip[0] : 1.0f;
+  const int64_t i0 = 4 * ((int64_t)blockIdx.x * blockDim.x * V + threadIdx.x);
+#pragma unroll
+  for (int k = 0; k < V; ++k)
+    update_group<G, S, EF>(n, i0 + 4 * (int64_t)k * blockDim.x, x, g, m, v, up, shadow, hs, c, skip);
+}
+
 template <typename S>
 __global__ void __launch_bounds__(256) cast_copy(int64_t n, const float* __restrict__ src,
                                                  S* __restrict__ dst) {
@@ -164,14 +182,14 @@ __global__ void __launch_bounds__(256) zero_bytes(int64_t n16, int4* __restrict_
   if (i < n16) p[i] = make_int4(0, 0, 0, 0);
 }
 
-template <typename G, typename S, bool EF>
+template <typename G, typename S, bool EF, int V = 1>
 void launch_update_t(int64_t n, float* x, const void* g, float* m, float* v, float* up,
                      void* shadow, const UpdateScalars& hs, const float* clip, const int* flag,
                      hipStream_t st) {
-  const int64_t threads = cdiv(n, 4);
-  const dim3 grid((unsigned)cdiv(threads, 256));
-  fused_update<G, S, EF><<<grid, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow, hs, clip,
-                                               flag);
+  const int64_t groups = cdiv(n, 4);
+  const dim3 grid((unsigned)cdiv(groups, 256 * V));
+  fused_update<G, S, EF, V><<<grid, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow, hs, clip,
+                                                  flag);
 }
 
 }  // namespace
