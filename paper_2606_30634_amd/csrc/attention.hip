@@ -247,4 +247,7 @@ void launch_attention_fwd(bool bf, const AttnArgs& a, hipStream_t st) {
 void launch_attention_bwd(bool bf, const AttnArgs& a, hipStream_t st) {
   if (bf && attention_mfma_bwd_try(a, st)) return;
   launch_attention_bwd_ref(bf, a, st);
+  if (a.rope_cos)  // dq, dk back through the rotation (query heads and key heads are contiguous)
+    launch_rope(bf, a.dqkv, a.B * a.S, a.S, a.Hq + a.Hkv, a.hd, (a.Hq + 2 * a.Hkv) * a.hd, a.rope_cos,
+                a.rope_sin, true, st);
 }

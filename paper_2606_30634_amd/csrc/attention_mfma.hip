@@ -41,21 +41,29 @@ __device__ __forceinline__ bf16x8 frag_rows(const bf16* T, int P, int r0, int k0
 }
 
 // B operand (8 consecutive k at column lane mod 32) from a 32x32 accumulator whose rows are the k
-// index, for the 16-row group starting at accumulator index ib (0 or 8): one lane-pair swap.
-__device__ __forceinline__ bf16x8 acc_rows_to_b(const f32x16& s, int ib, int half) {
-  const uint32_t own0 = pack2(s[ib + 4 * half + 0], s[ib + 4 * half + 1]);
-  const uint32_t own1 = pack2(s[ib + 4 * half + 2], s[ib + 4 * half + 3]);
-  const uint32_t snd0 = pack2(s[ib + 4 * (1 - half) + 0], s[ib + 4 * (1 - half) + 1]);
-  const uint32_t snd1 = pack2(s[ib + 4 * (1 - half) + 2], s[ib + 4 * (1 - half) + 3]);
-  const uint32_t rcv0 = __shfl_xor(snd0, 32, 64);
-  const uint32_t rcv1 = __shfl_xor(snd1, 32, 64);
+// index, for the 16-row group starting at accumulator index ib (0 or 8).  Lane half h holds rows
+// ib+4h..ib+4h+3 of the group; the operand wants rows 8h..8h+7, so each half keeps its own four and
+// takes the other four from its partner lane (l ^ 32).  All accumulator indices are compile-time
+// constants; the half selects between two packed candidates.
+template <int IB>
+__device__ __forceinline__ bf16x8 acc_rows_to_b(const f32x16& s, int half) {
+  const uint32_t lo0 = pack2(s[IB + 0], s[IB + 1]), lo1 = pack2(s[IB + 2], s[IB + 3]);
+  const uint32_t hi0 = pack2(s[IB + 4], s[IB + 5]), hi1 = pack2(s[IB + 6], s[IB + 7]);
+  const bool h = half != 0;
+  const uint32_t own0 = h ? hi0 : lo0, own1 = h ? hi1 : lo1;
+  const uint32_t rcv0 = __shfl_xor(h ? lo0 : hi0, 32, 64);
+  const uint32_t rcv1 = __shfl_xor(h ? lo1 : hi1, 32, 64);
   uint32_t pw[4];
-  if (half == 0) { pw[0] = own0; pw[1] = own1; pw[2] = rcv0; pw[3] = rcv1; }
-  else { pw[0] = rcv0; pw[1] = rcv1; pw[2] = own0; pw[3] = own1; }
+  pw[0] = h ? rcv0 : own0;
+  pw[1] = h ? rcv1 : own1;
+  pw[2] = h ? own0 : rcv0;
+  pw[3] = h ? own1 : rcv1;
   bf16x8 r;
   __builtin_memcpy(&r, pw, 16);
   return r;
 }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // KB rows x HD of a head (row stride ld) through registers into an LDS tile of pitch P;
 // rows at or beyond S are zero.
@@ -85,21 +93,42 @@ struct RowTile {
 
 // Writes a wave's 32 columns of X^T (accumulators: rows d, column = the wave's 32 rows) as rows of
 // out (row stride ldo) through the LDS staging area, scaled.  Ends with all staging reads done.
+// With rope tables the rows are gradients w.r.t. RoPE-rotated vectors and leave rotated back by
+// -angle(position, i) (position = row within the sequence): the gradient w.r.t. the unrotated ones.
 template <int HD>
-__device__ __forceinline__ void store_rows_from_t(bf16* __restrict__ stage, const f32x16* acc, float scale,
-                                                  bf16* __restrict__ out, int ldo, int row0_wg, int S) {
-  constexpr int OP = HD + 8;
+__device__ __forceinline__ void store_rows_from_t(float* __restrict__ stage, const f32x16* acc, float scale,
+                                                  bf16* __restrict__ out, int ldo, int row0_wg, int S,
+                                                  const float* rope_cos = nullptr,
+                                                  const float* rope_sin = nullptr) {
+  constexpr int OP = HD + 4;  // fp32 staging pitch
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64, half = lane / 32, col = lane % 32;
 #pragma unroll
   for (int dt = 0; dt < HD / 32; ++dt)
 #pragma unroll
     for (int e = 0; e < 16; ++e)
-      stage[(wave * 32 + col) * OP + dt * 32 + 8 * (e / 4) + 4 * half + (e % 4)] = (bf16)(acc[dt][e] * scale);
+      stage[(wave * 32 + col) * OP + dt * 32 + 8 * (e / 4) + 4 * half + (e % 4)] = acc[dt][e] * scale;
   __syncthreads();
   for (int c = threadIdx.x; c < QB * HD / 8; c += NT) {
     const int r = c / (HD / 8), d = (c % (HD / 8)) * 8;
-    if (row0_wg + r < S)
-      *reinterpret_cast<u32x4*>(out + (int64_t)(row0_wg + r) * ldo + d) = *reinterpret_cast<const u32x4*>(stage + r * OP + d);
+    const int row = row0_wg + r;
+    if (row >= S) continue;
+    const float* sr = stage + r * OP;
+    bf16x8 ov;
+    if (rope_cos) {
+      constexpr int HH = HD / 2;
+      const bool first = d < HH;
+      const int i0 = d % HH;
+      const float* xp = sr + (first ? d + HH : d - HH);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float cs = rope_cos[row * HH + i0 + q], sn = rope_sin[row * HH + i0 + q];
+        ov[q] = (bf16)(first ? sr[d + q] * cs + xp[q] * sn : sr[d + q] * cs - xp[q] * sn);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) ov[q] = (bf16)sr[d + q];
+    }
+    *reinterpret_cast<bf16x8*>(out + (int64_t)row * ldo + d) = ov;
   }
   __syncthreads();
 }
@@ -108,7 +137,7 @@ template <int HD>
 struct Lds {
   static constexpr int P = HD + 8;       // tile pitch (elements)
   static constexpr int TSZ = KB * P;     // one [KB][HD] tile
-  static constexpr size_t out_bytes = (size_t)QB * (HD + 8) * 2;
+  static constexpr size_t out_bytes = (size_t)QB * (HD + 4) * 4;  // fp32 output staging
   static constexpr size_t fwd_bytes() { const size_t t = (size_t)4 * TSZ * 2; return t > out_bytes ? t : out_bytes; }
   static constexpr size_t dq_bytes() { return fwd_bytes(); }
   static constexpr size_t dkv_bytes() {
@@ -190,26 +219,28 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
         }
       bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
       const float mn = fmaxf(m, bm);  // every query of the wave sees key0 here, so mn is finite
-      const float corr = (m == -INFINITY) ? 0.f : exp2f(m - mn);
+      const float corr = (m == -INFINITY) ? 0.f : fast_exp2(m - mn);
       float rs = 0.f;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const float p = exp2f(s[t][e] - mn);
+          const float p = fast_exp2(s[t][e] - mn);
           s[t][e] = p;
           rs += p;
         }
       rs += __shfl_xor(rs, 32, 64);
       lsum = lsum * corr + rs;
       m = mn;
+      if (__any(corr != 1.0f)) {  // the running maximum moved for some query of the wave
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) o[dt][e] *= corr;
+          for (int e = 0; e < 16; ++e) o[dt][e] *= corr;
+      }
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 pf = acc_rows_to_b(s[kk / 2], 8 * (kk % 2), half);
+        const bf16x8 pf = (kk % 2) ? acc_rows_to_b<8>(s[kk / 2], half) : acc_rows_to_b<0>(s[kk / 2], half);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr(Vs, P, dt * 32, kk * 16), pf, o[dt], 0, 0, 0);
@@ -224,7 +255,7 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
   if (half == 0 && myq < a.S)
     a.lse[((int64_t)b * a.Hq + h) * a.S + myq] = (m + log2f(lsum)) * 0.6931471805599453f;
   const float inv = lsum > 0.f ? 1.0f / lsum : 0.f;
-  store_rows_from_t<HD>(reinterpret_cast<bf16*>(smem), o, inv,
+  store_rows_from_t<HD>(reinterpret_cast<float*>(smem), o, inv,
                         (bf16*)a.o + (int64_t)b * a.S * a.Hq * HD + h * HD, a.Hq * HD, qb * QB, a.S);
 }
 
@@ -295,12 +326,12 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4);
-          const float p = key <= myq ? exp2f(s[e] * sl2 - lse2) : 0.f;
+          const float p = key <= myq ? fast_exp2(s[e] * sl2 - lse2) : 0.f;
           s[e] = p * (dp[e] - dl);
         }
 #pragma unroll
         for (int g2 = 0; g2 < 2; ++g2) {
-          const bf16x8 bop = acc_rows_to_b(s, 8 * g2, half);
+          const bf16x8 bop = g2 ? acc_rows_to_b<8>(s, half) : acc_rows_to_b<0>(s, half);
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
             dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr(Ks, P, dt * 32, t * 32 + g2 * 16), bop, dq[dt], 0, 0, 0);
@@ -313,8 +344,8 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
     }
     __syncthreads();
   }
-  store_rows_from_t<HD>(reinterpret_cast<bf16*>(smem), dq, 1.0f / sqrtf((float)HD),
-                        (bf16*)a.dqkv + (int64_t)b * a.S * ld + h * HD, ld, qb * QB, a.S);
+  store_rows_from_t<HD>(reinterpret_cast<float*>(smem), dq, 1.0f / sqrtf((float)HD),
+                        (bf16*)a.dqkv + (int64_t)b * a.S * ld + h * HD, ld, qb * QB, a.S, a.rope_cos, a.rope_sin);
 }
 
 // ------------------------------------------------------------------------------------------ dK, dV
@@ -408,15 +439,15 @@ __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int e = 4 * e4 + j, q = qs0 + r0 + j;
-          const float p = (q >= mykey && q < a.S) ? exp2f(s[e] * sl2 - l4[j]) : 0.f;
+          const float p = (q >= mykey && q < a.S) ? fast_exp2(s[e] * sl2 - l4[j]) : 0.f;
           s[e] = p;
           dp[e] = p * (dp[e] - d4[j]);
         }
       }
 #pragma unroll
       for (int g2 = 0; g2 < 2; ++g2) {
-        const bf16x8 pb = acc_rows_to_b(s, 8 * g2, half);
-        const bf16x8 sb = acc_rows_to_b(dp, 8 * g2, half);
+        const bf16x8 pb = g2 ? acc_rows_to_b<8>(s, half) : acc_rows_to_b<0>(s, half);
+        const bf16x8 sb = g2 ? acc_rows_to_b<8>(dp, half) : acc_rows_to_b<0>(dp, half);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
           dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr(Ds, P, dt * 32, t * 32 + g2 * 16), pb, dv[dt], 0, 0, 0);
@@ -428,9 +459,10 @@ __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
     __syncthreads();
   }
   bf16* outb = (bf16*)a.dqkv + (int64_t)b * a.S * ld;
-  store_rows_from_t<HD>(reinterpret_cast<bf16*>(smem), dk, 1.0f / sqrtf((float)HD), outb + (a.Hq + kvh) * HD, ld,
-                        kbk * QB, a.S);
-  store_rows_from_t<HD>(reinterpret_cast<bf16*>(smem), dv, 1.0f, outb + (a.Hq + a.Hkv + kvh) * HD, ld, kbk * QB, a.S);
+  store_rows_from_t<HD>(reinterpret_cast<float*>(smem), dk, 1.0f / sqrtf((float)HD), outb + (a.Hq + kvh) * HD, ld,
+                        kbk * QB, a.S, a.rope_cos, a.rope_sin);
+  store_rows_from_t<HD>(reinterpret_cast<float*>(smem), dv, 1.0f, outb + (a.Hq + a.Hkv + kvh) * HD, ld, kbk * QB,
+                        a.S);
 }
 
 // delta[b, h, i] = sum_d dO[b, i, h, d] O[b, i, h, d]; one thread per (token, head)

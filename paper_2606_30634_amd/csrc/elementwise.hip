@@ -4,7 +4,7 @@
 //  RMSNorm (App. E.2):   y = x r gamma, r = 1/sqrt(mean x^2 + eps)       one block per row
 //  RMSNorm backward:     dx = resid + r (dn gamma - xhat mean(dn gamma xhat)),  dgamma partials
 //  RoPE (rotate-half):   (a, b) <- (a cos - b sin, b cos + a sin), inverse with -sin
-//  SwiGLU:               z = silu(a) b;  da = dz b s (1 + a (1 - s)), db = dz silu(a)
+//  SwiGLU:               z = silu(a) b  (its backward runs in the down-projection GEMM epilogue)
 //  Embedding:            x0[i] = E[tok[i]];  dE[v] = sum_{i: tok[i] = v} dx0[i] in position order
 //  Cross-entropy:        dlogits = (softmax - onehot) * scale, row loss = lse - z[target]
 #include "common.h"
@@ -183,19 +183,6 @@ __global__ void __launch_bounds__(256) swiglu_fwd(const T* __restrict__ gu, T* _
   const int64_t r = idx / f, j = idx % f;
   const float a = to_f32(gu[r * 2 * f + j]), b = to_f32(gu[r * 2 * f + f + j]);
   z[idx] = from_f32<T>(a * sigm(a) * b);
-}
-
-template <typename T>
-__global__ void __launch_bounds__(256) swiglu_bwd(const T* __restrict__ dz, const T* __restrict__ gu,
-                                                  T* __restrict__ dgu, int rows, int f) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)rows * f) return;
-  const int64_t r = idx / f, j = idx % f;
-  const float a = to_f32(gu[r * 2 * f + j]), b = to_f32(gu[r * 2 * f + f + j]);
-  const float g = to_f32(dz[idx]);
-  const float s = sigm(a);
-  dgu[r * 2 * f + j] = from_f32<T>(g * b * s * (1.0f + a * (1.0f - s)));
-  dgu[r * 2 * f + f + j] = from_f32<T>(g * a * s);
 }
 
 // ------------------------------------------------------------------ token sort (bitonic, LDS)
@@ -394,17 +381,6 @@ static void swf_t(const void* gu, void* z, int rows, int f, hipStream_t st) {
 void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st) {
   DISPATCH(bf, swf_t, gu, z, rows, f, st);
 }
-template <typename T>
-static void swb_t(const void* dz, const void* gu, void* dgu, int rows, int f, hipStream_t st) {
-  swiglu_bwd<T><<<(unsigned)cdiv((int64_t)rows * f, 256), 256, 0, st>>>((const T*)dz,
-                                                                        (const T*)gu, (T*)dgu,
-                                                                        rows, f);
-}
-void launch_swiglu_bwd(bool bf, const void* dz, const void* gu, void* dgu, int rows, int f,
-                       hipStream_t st) {
-  DISPATCH(bf, swb_t, dz, gu, dgu, rows, f, st);
-}
-
 void launch_token_sort(const int32_t* tok, int n, uint32_t* sorted, hipStream_t st) {
   token_sort<<<1, 1024, 0, st>>>(tok, n, sorted);
 }

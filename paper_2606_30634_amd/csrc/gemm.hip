@@ -71,6 +71,14 @@ __global__ void __launch_bounds__(256) gemm_tiled(GemmArgs g) {
       if (n >= g.N) continue;
       const int64_t o = (int64_t)m * g.ldc + n;
       float v = acc[i][j];
+      if (g.epi == 1) {  // SwiGLU backward from dz = v
+        const T* gu = (const T*)g.aux + (int64_t)m * g.ld_aux + n;
+        const float a = to_f32(gu[0]), b = to_f32(gu[g.N]);
+        const float sg = 1.0f / (1.0f + expf(-a));
+        C[o] = from_f32<OutT>(v * b * sg * (1.0f + a * (1.0f - sg)));
+        C[o + g.N] = from_f32<OutT>(v * a * sg);
+        continue;
+      }
       if (g.out_f32 && g.beta != 0.f) v += g.beta * to_f32(C[o]);
       if (R) v += to_f32(R[o]);
       C[o] = from_f32<OutT>(v);
@@ -101,5 +109,13 @@ void launch_gemm_tiled(bool bf, const GemmArgs& g, hipStream_t st) {
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st) {
   if (g.M == 0 || g.N == 0) return;
   if (bf && gemm_mfma_try(g, st)) return;
+  if (g.epi == 2) {  // the reference tiling writes the products, then the rotation runs
+    GemmArgs p = g;
+    p.epi = 0;
+    launch_gemm_tiled(bf, p, st);
+    launch_rope(bf, g.C, g.M, g.rope_S, g.rope_cols / g.rope_hd, g.rope_hd, g.ldc, g.rope_cos, g.rope_sin,
+                false, st);
+    return;
+  }
   launch_gemm_tiled(bf, g, st);
 }

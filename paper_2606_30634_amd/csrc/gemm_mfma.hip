@@ -236,6 +236,33 @@ gemm_mfma_kernel(GemmArgs g) {
             v[0] += g.beta * old.x; v[1] += g.beta * old.y; v[2] += g.beta * old.z; v[3] += g.beta * old.w;
           }
           *reinterpret_cast<float4*>((float*)C + o) = make_float4(v[0], v[1], v[2], v[3]);
+        } else if (g.epi == 1) {  // SwiGLU backward from dz = v
+          const bf16* gu = (const bf16*)g.aux + (int64_t)row * g.ld_aux + col;
+          const bf16x8 av = *reinterpret_cast<const bf16x8*>(gu);
+          const bf16x8 bv = *reinterpret_cast<const bf16x8*>(gu + g.N);
+          bf16x8 da, db;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float a = (float)av[q], bb = (float)bv[q];
+            const float sg = 1.0f / (1.0f + __expf(-a));
+            da[q] = (bf16)(v[q] * bb * sg * (1.0f + a * (1.0f - sg)));
+            db[q] = (bf16)(v[q] * a * sg);
+          }
+          *reinterpret_cast<bf16x8*>((bf16*)C + o) = da;
+          *reinterpret_cast<bf16x8*>((bf16*)C + o + g.N) = db;
+        } else if (g.epi == 2 && col < g.rope_cols) {  // RoPE on the fp32 products
+          const int hd = g.rope_hd, hh = hd / 2;
+          const int c = col % hd, i0 = c % hh;
+          const bool first = c < hh;
+          const float* xp = stg + r * C_::EP + (first ? cc + hh : cc - hh);  // partner columns
+          const int64_t tb = (int64_t)(row % g.rope_S) * hh + i0;
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float cs = g.rope_cos[tb + q], sn = g.rope_sin[tb + q];
+            ov[q] = (bf16)(first ? v[q] * cs - xp[q] * sn : v[q] * cs + xp[q] * sn);
+          }
+          *reinterpret_cast<bf16x8*>((bf16*)C + o) = ov;
         } else {
           if (R) {
             const bf16x8 rr = *reinterpret_cast<const bf16x8*>(R + o);
@@ -313,6 +340,7 @@ void launch_cfg(const GemmArgs& g, hipStream_t st) {
 bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   // vector-load alignment: 8 elements along every contiguous dimension, rows in groups of 4
   if (g0.K % 8 || g0.M % 8 || g0.N % 8 || g0.lda % 8 || g0.ldb % 8 || g0.ldc % 8) return false;
+  if (g0.epi == 1 && (g0.out_f32 || g0.ld_aux % 8 || (uintptr_t)g0.aux % 16)) return false;
   if ((uintptr_t)g0.A % 16 || (uintptr_t)g0.B % 16 || (uintptr_t)g0.C % 16 || (uintptr_t)g0.resid % 16)
     return false;
   GemmArgs g = g0;
@@ -326,6 +354,10 @@ bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
     while (s > 1 && (s * mn > g.ws_elems || g.K / s < 512)) --s;
     g.ksplit = s;
   }
+  // RoPE in the epilogue needs every head whole inside one wave's columns
+  const int wn = big ? 128 : 64;
+  const bool rope_after = g.epi == 2 && (g.out_f32 || wn % g.rope_hd != 0);
+  if (rope_after) g.epi = 0;
   if (big) {
     if (g.out_f32) launch_cfg<256, 256, 128, 128, float>(g, st);
     else launch_cfg<256, 256, 128, 128, bf16>(g, st);
@@ -335,5 +367,8 @@ bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   }
   if (g.ksplit > 1)
     splitk_reduce<<<(unsigned)cdiv(cdiv(mn, 4), 256), 256, 0, st>>>(g.ws, g.ksplit, mn, (float*)g.C, g.beta);
+  if (rope_after)
+    launch_rope(!g.out_f32, g.C, g.M, g.rope_S, g.rope_cols / g.rope_hd, g.rope_hd, g.ldc, g.rope_cos,
+                g.rope_sin, false, st);
   return true;
 }

@@ -35,8 +35,6 @@ void launch_colsum_partials(const float* partial, int nchunks, int d, float* out
 void launch_rope(bool bf, void* qkv, int rows, int seq_len, int n_rot_heads, int head_dim, int ld,
                  const float* cos_t, const float* sin_t, bool inverse, hipStream_t st);
 void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st);
-void launch_swiglu_bwd(bool bf, const void* dz, const void* gu, void* dgu, int rows, int f,
-                       hipStream_t st);
 // token sort for the embedding gradient: keys (tok << 14 | pos) ascending; n <= 16384
 void launch_token_sort(const int32_t* tok, int n, uint32_t* sorted, hipStream_t st);
 void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_start,
@@ -64,6 +62,15 @@ struct GemmArgs {
   const void* resid;
   float* ws = nullptr; int64_t ws_elems = 0;
   int ksplit = 1;  // set by the launcher
+  // epilogue 1 (SwiGLU backward): the product is dz [M, N]; aux holds the saved gate|up
+  // pre-activations [M, 2N] (row stride ld_aux) and C receives dgate in columns [0, N) and dup in
+  // [N, 2N) (row stride ldc): da = dz b s (1 + a (1 - s)), db = dz a s, s = sigmoid(a).
+  // epilogue 2 (RoPE): columns [0, rope_cols) of the bf16 output are rotated in pairs
+  // (i, i + hd/2) of each hd-wide head by angle(p, i), p = row mod rope_S (tables [rope_S][hd/2]).
+  int epi = 0;
+  const void* aux = nullptr; int ld_aux = 0;
+  const float* rope_cos = nullptr; const float* rope_sin = nullptr;
+  int rope_cols = 0, rope_hd = 0, rope_S = 0;
 };
 constexpr int64_t GEMM_WS_ELEMS = 16 << 20;  // 64 MiB of fp32 split-K partials per stage
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st);
@@ -71,10 +78,13 @@ void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st);
 // ------------------------------------------------------------------ attention (attention.hip)
 // Causal grouped-query attention on the packed projection buffer qkv [B*s, (Hq + 2 Hkv) hd]
 // (query heads, then key heads, then value heads); o [B*s, Hq hd]; lse fp32 [B, Hq, s].
+// rope_cos / rope_sin (backward, optional): qkv holds RoPE-rotated q and k; the returned dq and
+// dk are then taken with respect to the unrotated projections (inverse rotation applied).
 struct AttnArgs {
   int B, S, Hq, Hkv, hd;
   const void* qkv; void* o; float* lse;
   const void* dout; void* dqkv; float* delta;  // backward only; delta fp32 [B, Hq, s]
+  const float* rope_cos = nullptr; const float* rope_sin = nullptr;
 };
 void launch_attention_fwd(bool bf, const AttnArgs& a, hipStream_t st);
 void launch_attention_bwd(bool bf, const AttnArgs& a, hipStream_t st);

@@ -68,7 +68,7 @@ struct stage {
   float *master, *m, *v, *u_prev, *grad[2];
   void* ver[2];
   // scratch
-  void *dA, *dB, *dh, *dn, *dz, *dgu, *do_, *dqkv, *dlog, *dhf;
+  void *dA, *dB, *dh, *dn, *dgu, *do_, *dqkv, *dlog, *dhf;
   float *delta, *rms_part, *row_loss, *cos_t, *sin_t, *norm_out;
   double* norm_part;
   float* gemm_ws;
@@ -236,7 +236,6 @@ size_t layout(stage* S, char* base) {
   S->dB = carve(T * d * esz);
   S->dh = carve(T * d * esz);
   S->dn = carve(T * d * esz);
-  S->dz = carve(T * f * esz);
   S->dgu = carve(T * 2 * f * esz);
   S->do_ = carve(T * hqd * esz);
   S->dqkv = carve(T * qkvw * esz);
@@ -340,9 +339,15 @@ void block_forward(stage* S, int vi, BlockAct& b, const BlockOff& w, void* y) {
   const bool bf = S->bf;
   hipStream_t st = S->st;
   launch_rmsnorm_fwd(bf, b.x, S->wptr(vi, w.attn_norm), b.n1, b.rstd1, T, d, sh.rms_eps, st);
-  run_gemm(S, gemm(T, S->qkvw, d, b.n1, d, true, S->wptr(vi, w.wqkv), d, true, b.qkv, S->qkvw));
-  launch_rope(bf, b.qkv, T, sh.seq_len, sh.n_heads + sh.n_kv_heads, sh.head_dim, S->qkvw, S->cos_t,
-              S->sin_t, false, st);
+  // QKV projection with RoPE on the query and key heads in the GEMM epilogue
+  GemmArgs gq = gemm(T, S->qkvw, d, b.n1, d, true, S->wptr(vi, w.wqkv), d, true, b.qkv, S->qkvw);
+  gq.epi = 2;
+  gq.rope_cos = S->cos_t;
+  gq.rope_sin = S->sin_t;
+  gq.rope_cols = (sh.n_heads + sh.n_kv_heads) * sh.head_dim;
+  gq.rope_hd = sh.head_dim;
+  gq.rope_S = sh.seq_len;
+  run_gemm(S, gq);
   timed(S, STAGE_PROF_ATTN_FWD, attn_fwd_flops(S), [&] { launch_attention_fwd(bf, attn_args(S, b), st); });
   run_gemm(S, gemm(T, d, S->hqd, b.o, S->hqd, true, S->wptr(vi, w.wo), S->hqd, true, b.h, d,
                        false, 0.f, b.x));
@@ -360,10 +365,14 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   const bool bf = S->bf;
   const float beta = first ? 0.f : 1.f;
   hipStream_t st = S->st;
-  // down projection: dz = dy Wd ; dWd (+)= dy^T z
-  run_gemm(S, gemm(T, f, d, dy, d, true, S->wptr(vi, w.wdown), f, false, S->dz, f));
+  // down projection: dz = dy Wd with the SwiGLU backward in its epilogue (-> dgate | dup);
+  // dWd (+)= dy^T z
+  GemmArgs gz = gemm(T, f, d, dy, d, true, S->wptr(vi, w.wdown), f, false, S->dgu, 2 * f);
+  gz.epi = 1;
+  gz.aux = b.gu;
+  gz.ld_aux = 2 * f;
+  run_gemm(S, gz);
   run_gemm(S, gemm(d, f, T, dy, d, false, b.z, f, false, g + w.wdown, f, true, beta));
-  launch_swiglu_bwd(bf, S->dz, b.gu, S->dgu, T, f, st);
   // gate/up: dn2 = dgu Wgu ; dWgu (+)= dgu^T n2
   run_gemm(S, gemm(T, d, 2 * f, S->dgu, 2 * f, true, S->wptr(vi, w.wgu), d, false, S->dn, d));
   run_gemm(S, gemm(2 * f, d, T, S->dgu, 2 * f, false, b.n2, d, false, g + w.wgu, d, true, beta));
@@ -374,9 +383,9 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   run_gemm(S, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta));
   AttnArgs a = attn_args(S, b);
   a.dout = S->do_; a.dqkv = S->dqkv; a.delta = S->delta;
+  a.rope_cos = S->cos_t;  // dq, dk come back w.r.t. the unrotated projections
+  a.rope_sin = S->sin_t;
   timed(S, STAGE_PROF_ATTN_BWD, 2.0 * attn_fwd_flops(S), [&] { launch_attention_bwd(bf, a, st); });
-  launch_rope(bf, S->dqkv, T, sh.seq_len, sh.n_heads + sh.n_kv_heads, sh.head_dim, S->qkvw, S->cos_t,
-              S->sin_t, true, st);
   // qkv projection: dn1 = dqkv Wqkv ; dWqkv (+)= dqkv^T n1
   run_gemm(S, gemm(T, d, S->qkvw, S->dqkv, S->qkvw, true, S->wptr(vi, w.wqkv), d, false, S->dn, d));
   run_gemm(S, gemm(S->qkvw, d, T, S->dqkv, S->qkvw, false, b.n1, d, false, g + w.wqkv, d, true, beta));
