@@ -107,9 +107,13 @@ int stage_sync_weights(stage_t* s);
 
 /* Forward of one microbatch of optimizer step `step` at the weights x_step (compute version
  * step mod 2), saving activations in slot `slot` (0 <= slot < max_inflight).
- *   tokens  [micro_batch, seq_len] int32, device  (first stage; else NULL)
+ *   tokens  [micro_batch, seq_len] int32, device  (first stage; else NULL).  Ids outside
+ *           [0, vocab) are not read: such a position embeds as a zero row and adds nothing to
+ *           the embedding gradient.
  *   x_in    [micro_batch, seq_len, d_model] bf16/fp32 per dtype, device (non-first; else NULL)
- *   targets [micro_batch, seq_len] int32, device  (last stage; else NULL)
+ *   targets [micro_batch, seq_len] int32, device  (last stage; else NULL).  A target outside
+ *           [0, vocab) is ignored: zero loss and zero gradient at that position (the mean still
+ *           divides by micro_batch*seq_len).
  *   y_out   [micro_batch, seq_len, d_model] device (non-last; may be NULL to keep it in the slot)
  *   loss_dev one float, device (last stage: mean cross-entropy of this microbatch; else NULL)
  * STAGE_ESTATE if compute version step mod 2 does not hold x_step. */

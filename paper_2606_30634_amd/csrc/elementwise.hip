@@ -13,14 +13,17 @@
 namespace {
 
 // ------------------------------------------------------------------ embedding gather
+// A token outside [0, vocab) embeds as a zero row.
 template <typename T>
 __global__ void __launch_bounds__(256) embed_gather(const int32_t* __restrict__ tok,
                                                     const T* __restrict__ E, T* __restrict__ x0,
-                                                    int d) {
+                                                    int d, int vocab) {
   const int row = blockIdx.x;
-  const int64_t src = (int64_t)tok[row] * d;
+  const int t = tok[row];
+  const bool ok = t >= 0 && t < vocab;
+  const int64_t src = (int64_t)(ok ? t : 0) * d;
   const int64_t dst = (int64_t)row * d;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) x0[dst + j] = E[src + j];
+  for (int j = threadIdx.x; j < d; j += blockDim.x) x0[dst + j] = ok ? E[src + j] : from_f32<T>(0.f);
 }
 
 // ------------------------------------------------------------------ RMSNorm
@@ -90,65 +93,118 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd(const T* __restrict__ dn, con
   }
 }
 
-// out[j] (+)= sum_c partial[c][j]: block of 1024 threads = 16 row groups x 64 columns; each thread
-// sums rows g, g+16, ... of its column, then the 16 group sums are added in group order.
-__global__ void __launch_bounds__(1024) colsum_partials(const float* __restrict__ partial,
-                                                        int nchunks, int d, float* __restrict__ out,
-                                                        int accumulate) {
-  __shared__ float sm[16][64];
-  const int c = threadIdx.x % 64, g = threadIdx.x / 64;
-  const int j = blockIdx.x * 64 + c;
+// Fixed-order column sums of a [nrows][d] fp32 array, one level of a two-level tree: thread j of
+// group g sums rows [g G, min(g G + G, nrows)) of column j in row order and writes dst[g][j]
+// (dst (+)= when accumulate, used for the last level whose single group covers every row).
+__global__ void __launch_bounds__(256) colsum_rows(const float* __restrict__ src, int nrows, int d, int G,
+                                                   float* __restrict__ dst, int accumulate) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= d) return;
+  const int r0 = blockIdx.y * G, r1 = min(nrows, r0 + G);
   float s = 0.f;
-  if (j < d)
-    for (int r = g; r < nchunks; r += 16) s += partial[(int64_t)r * d + j];
-  sm[g][c] = s;
-  __syncthreads();
-  if (g == 0 && j < d) {
-    float t = 0.f;
-    for (int k = 0; k < 16; ++k) t += sm[k][c];
-    out[j] = accumulate ? out[j] + t : t;
-  }
+#pragma unroll 8
+  for (int r = r0; r < r1; ++r) s += src[(int64_t)r * d + j];
+  float* o = dst + (int64_t)blockIdx.y * d + j;
+  *o = accumulate ? *o + s : s;
 }
 
-// RMSNorm backward with one wave per row: lane l owns columns l + 64 k (k < CPL), gamma and the
-// dgamma partial sums of those columns stay in registers, the row dot product is a wave reduction.
-// Block = 4 waves over RMS_CHUNK consecutive rows; each wave writes its own dgamma partial row, so
-// the partial array holds 4 rows per block.
-template <typename T, int CPL>
-__global__ void __launch_bounds__(256) rmsnorm_bwd_wave(const T* __restrict__ dn, const T* __restrict__ x,
-                                                        const float* __restrict__ rstd,
-                                                        const T* __restrict__ gamma,
-                                                        const T* __restrict__ resid, T* __restrict__ dx,
-                                                        float* __restrict__ partial, int rows) {
-  constexpr int d = CPL * 64;
+template <typename T, int V>
+struct Vec {
+  typedef T type __attribute__((ext_vector_type(V)));
+};
+
+// RMSNorm backward, one wave per row and U rows in flight per wave: lane l owns the V-element
+// vectors at columns (l + 64 k) V, k < NI, so every load and store is V elements wide; gamma and
+// the dgamma partial sums of those columns stay in registers and the row dot product is a wave
+// reduction.  A block covers RMS_ROWS_VEC consecutive rows (4 per wave) and writes one dgamma
+// partial row, the sum of its waves' rows in wave order.
+constexpr int RMS_ROWS_VEC = 16;
+template <typename T, int V, int NI>
+__global__ void __launch_bounds__(256) rmsnorm_bwd_vec(const T* __restrict__ dn, const T* __restrict__ x,
+                                                       const float* __restrict__ rstd,
+                                                       const T* __restrict__ gamma,
+                                                       const T* __restrict__ resid, T* __restrict__ dx,
+                                                       float* __restrict__ partial, int rows) {
+  constexpr int d = 64 * V * NI;
+  constexpr int U = V * NI <= 12 ? 2 : 1;  // two rows in flight while registers allow
+  using VT = typename Vec<T, V>::type;
+  __shared__ float red[d];
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-  float gm[CPL], dg[CPL];
+  float gm[NI][V], dg[NI][V];
 #pragma unroll
-  for (int k = 0; k < CPL; ++k) { gm[k] = to_f32(gamma[lane + 64 * k]); dg[k] = 0.f; }
-  const int r0 = blockIdx.x * RMS_CHUNK;
-  const int r1 = min(rows, r0 + RMS_CHUNK);
-  for (int r = r0 + wave; r < r1; r += 4) {
-    const int64_t base = (int64_t)r * d;
-    const float rs = rstd[r];
-    float xh[CPL], gv[CPL];
-    float dot = 0.f;
+  for (int k = 0; k < NI; ++k) {
+    const VT gv = *reinterpret_cast<const VT*>(gamma + (lane + 64 * k) * V);
 #pragma unroll
-    for (int k = 0; k < CPL; ++k) {
-      xh[k] = to_f32(x[base + lane + 64 * k]) * rs;
-      gv[k] = to_f32(dn[base + lane + 64 * k]);
-      dot += gv[k] * gm[k] * xh[k];
-      dg[k] += gv[k] * xh[k];
+    for (int q = 0; q < V; ++q) { gm[k][q] = to_f32(gv[q]); dg[k][q] = 0.f; }
+  }
+  const int r0 = blockIdx.x * RMS_ROWS_VEC + wave;
+#pragma unroll 1
+  for (int it = 0; it < RMS_ROWS_VEC / (4 * U); ++it) {
+    int r[U];
+    bool ok[U];
+    VT xv[U][NI], gv[U][NI], rv[U][NI];
+    float rs[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      r[u] = r0 + 4 * (U * it + u);
+      ok[u] = r[u] < rows;
+      const int64_t base = (int64_t)(ok[u] ? r[u] : 0) * d;
+      rs[u] = ok[u] ? rstd[r[u]] : 0.f;
+#pragma unroll
+      for (int k = 0; k < NI; ++k) {
+        const int64_t o = base + (lane + 64 * k) * V;
+        xv[u][k] = *reinterpret_cast<const VT*>(x + o);
+        gv[u][k] = *reinterpret_cast<const VT*>(dn + o);
+        if (resid) rv[u][k] = *reinterpret_cast<const VT*>(resid + o);
+      }
     }
-    dot = wave_sum(dot) / (float)d;
+    float dot[U];
 #pragma unroll
-    for (int k = 0; k < CPL; ++k) {
-      float v = rs * (gv[k] * gm[k] - xh[k] * dot);
-      if (resid) v += to_f32(resid[base + lane + 64 * k]);
-      dx[base + lane + 64 * k] = from_f32<T>(v);
+    for (int u = 0; u < U; ++u) {
+      dot[u] = 0.f;
+#pragma unroll
+      for (int k = 0; k < NI; ++k)
+#pragma unroll
+        for (int q = 0; q < V; ++q) {
+          const float xh = to_f32(xv[u][k][q]) * rs[u], g = to_f32(gv[u][k][q]);
+          dot[u] += g * gm[k][q] * xh;
+          dg[k][q] += g * xh;  // rs = 0 on a row past the end adds nothing
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) dot[u] = wave_sum(dot[u]) / (float)d;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (!ok[u]) continue;
+      const int64_t base = (int64_t)r[u] * d;
+#pragma unroll
+      for (int k = 0; k < NI; ++k) {
+        VT ov;
+#pragma unroll
+        for (int q = 0; q < V; ++q) {
+          const float xh = to_f32(xv[u][k][q]) * rs[u];
+          float v = rs[u] * (to_f32(gv[u][k][q]) * gm[k][q] - xh * dot[u]);
+          if (resid) v += to_f32(rv[u][k][q]);
+          ov[q] = from_f32<T>(v);
+        }
+        *reinterpret_cast<VT*>(dx + base + (lane + 64 * k) * V) = ov;
+      }
     }
   }
+  // dgamma partial of the block: wave 0's sums, then waves 1, 2, 3 added in that order
 #pragma unroll
-  for (int k = 0; k < CPL; ++k) partial[((int64_t)blockIdx.x * 4 + wave) * d + lane + 64 * k] = dg[k];
+  for (int w = 0; w < 4; ++w) {
+    if (wave == w)
+#pragma unroll
+      for (int k = 0; k < NI; ++k)
+#pragma unroll
+        for (int q = 0; q < V; ++q) {
+          float& e = red[(lane + 64 * k) * V + q];
+          e = (w == 0 ? 0.f : e) + dg[k][q];
+        }
+    __syncthreads();
+  }
+  for (int c = threadIdx.x; c < d; c += 256) partial[(int64_t)blockIdx.x * d + c] = red[c];
 }
 
 // ------------------------------------------------------------------ RoPE
@@ -185,31 +241,41 @@ __global__ void __launch_bounds__(256) swiglu_fwd(const T* __restrict__ gu, T* _
   z[idx] = from_f32<T>(a * sigm(a) * b);
 }
 
-// ------------------------------------------------------------------ token sort (bitonic, LDS)
-// keys (tok << 14) | pos are distinct, so the order is total; one block of 1024 threads.
+// ------------------------------------------------------------------ token sort (rank sort)
+// Key of position i: (token << 14) | i, with tokens outside [0, vocab) given the token value
+// vocab so that they sort after every valid one and belong to no embedding row.  The keys are
+// distinct, so key i goes to out[#{j : key_j < key_i}].  A block ranks 64 keys; each of its four
+// waves counts over a quarter of every LDS-staged chunk of keys (all lanes read the same word, a
+// broadcast) and the four counts are added.
 constexpr int SORT_MAX = 16384;
-__global__ void __launch_bounds__(1024) token_sort(const int32_t* __restrict__ tok, int n,
-                                                   uint32_t* __restrict__ out) {
-  __shared__ uint32_t k[SORT_MAX];
-  int np = 1;
-  while (np < n) np <<= 1;
-  for (int i = threadIdx.x; i < np; i += blockDim.x)
-    k[i] = i < n ? ((uint32_t)tok[i] << 14) | (uint32_t)i : 0xFFFFFFFFu;
-  __syncthreads();
-  for (int size = 2; size <= np; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = threadIdx.x; i < np; i += blockDim.x) {
-        const int j = i ^ stride;
-        if (j > i) {
-          const bool up = (i & size) == 0;
-          const uint32_t a = k[i], b = k[j];
-          if ((a > b) == up) { k[i] = b; k[j] = a; }
-        }
-      }
-      __syncthreads();
+constexpr int SORT_CHUNK = 4096;
+__device__ __forceinline__ uint32_t token_key(const int32_t* tok, int i, int vocab) {
+  const int t = tok[i];
+  return ((uint32_t)(t >= 0 && t < vocab ? t : vocab) << 14) | (uint32_t)i;
+}
+__global__ void __launch_bounds__(256) token_sort(const int32_t* __restrict__ tok, int n, int vocab,
+                                                  uint32_t* __restrict__ out) {
+  __shared__ u32x4 ks[SORT_CHUNK / 4];
+  __shared__ int cnt4[4][64];
+  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+  const int i = blockIdx.x * 64 + lane;
+  const uint32_t mine = i < n ? token_key(tok, i, vocab) : 0xFFFFFFFFu;
+  int cnt = 0;
+  for (int c0 = 0; c0 < n; c0 += SORT_CHUNK) {
+    const int m = min(SORT_CHUNK, n - c0);
+    const int m16 = (m + 15) & ~15;  // padded with keys that no valid key exceeds
+    __syncthreads();
+    uint32_t* kw = reinterpret_cast<uint32_t*>(ks);
+    for (int e = threadIdx.x; e < m16; e += 256) kw[e] = e < m ? token_key(tok, c0 + e, vocab) : 0xFFFFFFFFu;
+    __syncthreads();
+    for (int q = wave; q < m16 / 4; q += 4) {
+      const u32x4 k = ks[q];
+      cnt += (k.x < mine) + (k.y < mine) + (k.z < mine) + (k.w < mine);
     }
   }
-  for (int i = threadIdx.x; i < n; i += blockDim.x) out[i] = k[i];
+  cnt4[wave][lane] = cnt;
+  __syncthreads();
+  if (wave == 0 && i < n) out[cnt4[0][lane] + cnt4[1][lane] + cnt4[2][lane] + cnt4[3][lane]] = mine;
 }
 
 // row_start[v] = first sorted index with token >= v (binary search), v in [0, vocab]
@@ -276,6 +342,12 @@ __global__ void __launch_bounds__(256) ce_rows(const float* __restrict__ logits,
   __shared__ float sm[16];
   __shared__ float smx[16];
   const int64_t base = (int64_t)blockIdx.x * V;
+  const int t = tg[blockIdx.x];
+  if (t < 0 || t >= V) {  // a target outside [0, V) is ignored: zero loss, zero gradient
+    for (int j = threadIdx.x; j < V; j += blockDim.x) dlog[base + j] = from_f32<T>(0.f);
+    if (threadIdx.x == 0) row_loss[blockIdx.x] = 0.f;
+    return;
+  }
   float mx = -INFINITY;
   for (int j = threadIdx.x; j < V; j += blockDim.x) mx = fmaxf(mx, logits[base + j]);
   mx = wave_max(mx);
@@ -287,7 +359,6 @@ __global__ void __launch_bounds__(256) ce_rows(const float* __restrict__ logits,
   for (int j = threadIdx.x; j < V; j += blockDim.x) se += expf(logits[base + j] - mx);
   se = block_sum<float>(se, sm);
   const float lse = mx + logf(se);
-  const int t = tg[blockIdx.x];
   for (int j = threadIdx.x; j < V; j += blockDim.x) {
     float p = expf(logits[base + j] - lse);
     if (j == t) p -= 1.0f;
@@ -311,12 +382,13 @@ __global__ void __launch_bounds__(1024) mean_kernel(const float* __restrict__ v,
   do { if (bf) KERNEL<bf16>(__VA_ARGS__); else KERNEL<float>(__VA_ARGS__); } while (0)
 
 template <typename T>
-static void gather_t(const int32_t* tok, const void* E, void* x0, int rows, int d, hipStream_t st) {
-  embed_gather<T><<<rows, 256, 0, st>>>(tok, (const T*)E, (T*)x0, d);
+static void gather_t(const int32_t* tok, const void* E, void* x0, int rows, int d, int vocab,
+                     hipStream_t st) {
+  embed_gather<T><<<rows, 256, 0, st>>>(tok, (const T*)E, (T*)x0, d, vocab);
 }
 void launch_embed_gather(bool bf, const int32_t* tok, const void* table, void* x0, int rows, int d,
-                         hipStream_t st) {
-  DISPATCH(bf, gather_t, tok, table, x0, rows, d, st);
+                         int vocab, hipStream_t st) {
+  DISPATCH(bf, gather_t, tok, table, x0, rows, d, vocab, st);
 }
 
 template <typename T>
@@ -332,19 +404,30 @@ void launch_rmsnorm_fwd(bool bf, const void* x, const void* gamma, void* y, floa
 template <typename T>
 static int rmsb_t(const void* dn, const void* x, const float* r, const void* g, const void* res,
                   void* dx, float* part, int rows, int d, hipStream_t st) {
-  const unsigned nb = (unsigned)cdiv(rows, RMS_CHUNK);
-#define RB(CPL) rmsnorm_bwd_wave<T, CPL><<<nb, 256, 0, st>>>((const T*)dn, (const T*)x, r, (const T*)g, \
-                                                            (const T*)res, (T*)dx, part, rows)
+  const unsigned nv = (unsigned)cdiv(rows, RMS_ROWS_VEC);
+  // caller-owned rows (the incoming gradient, dx) may be less aligned than the vector width
+  const uintptr_t align = (uintptr_t)dn | (uintptr_t)x | (uintptr_t)g | (uintptr_t)res | (uintptr_t)dx;
+#define RB(V, NI)                                                                                    \
+  if (align % (V * sizeof(T)) == 0) {                                                                \
+    rmsnorm_bwd_vec<T, V, NI><<<nv, 256, 0, st>>>((const T*)dn, (const T*)x, r, (const T*)g,          \
+                                                  (const T*)res, (T*)dx, part, rows);                 \
+    return (int)nv;                                                                                  \
+  }
+  // 16-byte vectors where d allows (8 bf16 or 4 fp32 elements per lane), else 8 or 4 bytes; any
+  // other width, or rows not aligned to the vector, take the block-per-chunk kernel below
+  constexpr bool B = sizeof(T) == 2;
   switch (d) {
-    case 128: RB(2); return 4 * (int)nb;
-    case 256: RB(4); return 4 * (int)nb;
-    case 512: RB(8); return 4 * (int)nb;
-    case 768: RB(12); return 4 * (int)nb;
-    case 1024: RB(16); return 4 * (int)nb;
-    case 2048: RB(32); return 4 * (int)nb;
+    case 128: RB(2, 1) break;
+    case 256: RB(4, 1) break;
+    case 512: if (B) { RB(8, 1) } else { RB(4, 2) } break;
+    case 768: RB(4, 3) break;
+    case 1024: if (B) { RB(8, 2) } else { RB(4, 4) } break;
+    case 1536: if (B) { RB(8, 3) } else { RB(4, 6) } break;
+    case 2048: if (B) { RB(8, 4) } else { RB(4, 8) } break;
     default: break;
   }
 #undef RB
+  const unsigned nb = (unsigned)cdiv(rows, RMS_CHUNK);
   rmsnorm_bwd<T><<<nb, 256, 0, st>>>((const T*)dn, (const T*)x, r, (const T*)g, (const T*)res, (T*)dx,
                                      part, rows, d);
   return (int)nb;
@@ -356,10 +439,18 @@ int launch_rmsnorm_bwd(bool bf, const void* dn, const void* x, const float* rstd
             : rmsb_t<float>(dn, x, rstd, gamma, resid, dx, partial, rows, d, st);
 }
 
-void launch_colsum_partials(const float* partial, int nchunks, int d, float* out, bool accumulate,
+void launch_colsum_partials(float* partial, int nchunks, int d, float* out, bool accumulate,
                             hipStream_t st) {
-  colsum_partials<<<(unsigned)cdiv(d, 64), 1024, 0, st>>>(partial, nchunks, d, out,
-                                                          accumulate ? 1 : 0);
+  const unsigned cb = (unsigned)cdiv(d, 256);
+  if (nchunks <= 32) {
+    colsum_rows<<<dim3(cb, 1), 256, 0, st>>>(partial, nchunks, d, nchunks, out, accumulate ? 1 : 0);
+    return;
+  }
+  constexpr int G = 16;  // rows per first-level group; the group sums go after the partial rows
+  const int n1 = cdiv(nchunks, G);
+  float* tmp = partial + (int64_t)nchunks * d;
+  colsum_rows<<<dim3(cb, (unsigned)n1), 256, 0, st>>>(partial, nchunks, d, G, tmp, 0);
+  colsum_rows<<<dim3(cb, 1), 256, 0, st>>>(tmp, n1, d, n1, out, accumulate ? 1 : 0);
 }
 
 template <typename T>
@@ -381,8 +472,8 @@ static void swf_t(const void* gu, void* z, int rows, int f, hipStream_t st) {
 void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st) {
   DISPATCH(bf, swf_t, gu, z, rows, f, st);
 }
-void launch_token_sort(const int32_t* tok, int n, uint32_t* sorted, hipStream_t st) {
-  token_sort<<<1, 1024, 0, st>>>(tok, n, sorted);
+void launch_token_sort(const int32_t* tok, int n, int vocab, uint32_t* sorted, hipStream_t st) {
+  if (n > 0) token_sort<<<(unsigned)cdiv(n, 64), 256, 0, st>>>(tok, n, vocab, sorted);
 }
 void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_start, int32_t* ids,
                        int32_t* counts, int32_t* n_unique, hipStream_t st) {

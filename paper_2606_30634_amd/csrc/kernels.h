@@ -21,22 +21,30 @@ void launch_zero(void* p, int64_t bytes, hipStream_t st);
 // ------------------------------------------------------------------ elementwise (elementwise.hip)
 // `bf` selects bf16 storage (else fp32) for every activation / weight pointer of the call.
 void launch_embed_gather(bool bf, const int32_t* tok, const void* table, void* x0, int rows, int d,
-                         hipStream_t st);
+                         int vocab, hipStream_t st);
 void launch_rmsnorm_fwd(bool bf, const void* x, const void* gamma, void* y, float* rstd, int rows,
                         int d, float eps, hipStream_t st);
 // dx = resid + rstd * (dn*gamma - xhat * mean(dn*gamma*xhat)); dgamma partial sums into
-// partial[p][d]; returns the number of partial rows written (at most 4 per RMS_CHUNK rows).
+// partial[p][d]; returns the number of partial rows written (at most one per 16 rows).
 constexpr int RMS_CHUNK = 32;
 int launch_rmsnorm_bwd(bool bf, const void* dn, const void* x, const float* rstd,
                         const void* gamma, const void* resid, void* dx, float* partial, int rows,
                         int d, hipStream_t st);
-void launch_colsum_partials(const float* partial, int nchunks, int d, float* out, bool accumulate,
+// out (+)= the column sums of partial[0 .. nchunks), summed in a fixed order; the rows after
+// them are scratch for the first level of the sum.
+void launch_colsum_partials(float* partial, int nchunks, int d, float* out, bool accumulate,
                             hipStream_t st);
+// rows of d floats the partial buffer of launch_rmsnorm_bwd + launch_colsum_partials needs
+inline int64_t rms_partial_rows(int rows) {
+  const int64_t p = (rows + 15) / 16;
+  return p + (p + 15) / 16;
+}
 void launch_rope(bool bf, void* qkv, int rows, int seq_len, int n_rot_heads, int head_dim, int ld,
                  const float* cos_t, const float* sin_t, bool inverse, hipStream_t st);
 void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st);
-// token sort for the embedding gradient: keys (tok << 14 | pos) ascending; n <= 16384
-void launch_token_sort(const int32_t* tok, int n, uint32_t* sorted, hipStream_t st);
+// token sort for the embedding gradient: keys (tok << 14 | pos) ascending, tokens outside
+// [0, vocab) keyed as vocab; n <= 16384
+void launch_token_sort(const int32_t* tok, int n, int vocab, uint32_t* sorted, hipStream_t st);
 void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_start,
                        int32_t* ids, int32_t* counts, int32_t* n_unique, hipStream_t st);
 void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted,

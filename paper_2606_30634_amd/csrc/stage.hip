@@ -240,7 +240,7 @@ size_t layout(stage* S, char* base) {
   S->do_ = carve(T * hqd * esz);
   S->dqkv = carve(T * qkvw * esz);
   S->delta = (float*)carve((int64_t)sh.micro_batch * sh.n_heads * sh.seq_len * 4);
-  S->rms_part = (float*)carve(4 * cdiv(T, RMS_CHUNK) * d * 4);
+  S->rms_part = (float*)carve(rms_partial_rows(T) * d * 4);
   S->norm_part = (double*)carve(norm_scratch_bytes());
   S->gemm_ws = sh.dtype == 1 ? (float*)carve(GEMM_WS_ELEMS * 4) : nullptr;
   S->norm_out = (float*)carve(2 * 4);
@@ -507,7 +507,7 @@ int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens,
   void* x0 = sh.n_blocks > 0 ? sl.blk[0].x : sl.y;
   if (sh.first_stage) {
     HIP_OK(hipMemcpyAsync(sl.tokens, tokens, (size_t)T * 4, hipMemcpyDeviceToDevice, st));
-    launch_embed_gather(s->bf, sl.tokens, s->wptr(vi, s->off_embed), x0, T, d, st);
+    launch_embed_gather(s->bf, sl.tokens, s->wptr(vi, s->off_embed), x0, T, d, sh.vocab, st);
   } else {
     HIP_OK(hipMemcpyAsync(x0, x_in, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
   }
@@ -577,7 +577,7 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   }
   if (sh.first_stage) {
     const void* dx0 = cur;
-    launch_token_sort(sl.tokens, T, s->sorted, st);
+    launch_token_sort(sl.tokens, T, sh.vocab, s->sorted, st);
     launch_token_runs(s->sorted, T, sh.vocab, s->row_start, nullptr, nullptr, nullptr, st);
     launch_embed_scatter(bf, dx0, s->sorted, s->row_start, sh.vocab, d, g + s->off_embed,
                          head_wrote_embed || !first, st);
@@ -682,7 +682,7 @@ int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts,
   if (slot < 0 || slot >= s->sh.max_inflight) return fail(STAGE_EINVAL, "slot out of range");
   const Slot& sl = s->slots[slot];
   if (sl.step < 0) return fail(STAGE_ESTATE, "slot has not run forward");
-  launch_token_sort(sl.tokens, s->T, s->sorted, s->st);
+  launch_token_sort(sl.tokens, s->T, s->sh.vocab, s->sorted, s->st);
   launch_token_runs(s->sorted, s->T, s->sh.vocab, s->row_start, ids, counts, n_unique, s->st);
   HIP_OK(hipGetLastError());
   return STAGE_OK;
