@@ -23,10 +23,17 @@
  *   - The library never allocates device memory.  The caller allocates one arena of
  *     stage_required_bytes() and every input/output buffer; all pointers stay owned by the caller.
  *   - All device work is enqueued asynchronously on the HIP stream given to stage_init (or to
- *     delayed_update_flat).  Host pointers are never retained.  The caller synchronises.
+ *     delayed_update_flat), with one exception: delayed_update runs its kernels on a stream of
+ *     the stage's own (non-blocking, default priority).  It waits there only for the backwards
+ *     whose gradient it consumes and for the last use of the weight version it overwrites, so
+ *     it overlaps forward / backward work the caller enqueued before it; the stage stream then
+ *     waits for it, so everything enqueued after delayed_update returns sees its results.
+ *     Host pointers are never retained.  The caller synchronises.
+ *   - The caller may write master weights and optimizer state (stage_tensor views) only when no
+ *     update is in flight, and then calls stage_sync_weights() before the next delayed_update.
  *   - Device pointers must be 16-byte aligned.  Layouts are row-major, last index contiguous.
- *   - Token ids must be int32 in [0, vocab); the kernels do not check them (an id outside the
- *     range reads outside the embedding).
+ *   - Token ids are int32; an id outside [0, vocab) is never used as an index (see
+ *     stage_forward).
  *   - One stage_t per host thread; calls on one stage_t must not overlap.
  */
 #ifndef ASYNCSTAGE_H
@@ -161,8 +168,8 @@ int stage_poll_nonfinite(stage_t* s, int64_t* skipped);
 /* Global L2 norm of gradient buffer `which` (0/1), computed on device into norm_dev (float). */
 int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev);
 
-/* Kernel-class timing.  While enabled, the stage records a HIP event pair on its stream around
- * every launch of a class and, when read, adds up the elapsed times and the algorithmic work of
+/* Kernel-class timing.  While enabled, the stage records a HIP event pair on the launching
+ * stream around every launch of a class and, when read, adds up the elapsed times and the algorithmic work of
  * those launches: GEMM and attention in flops (2 M N K per product; causal attention forward
  * 4 B Hq hd s(s+1)/2, backward twice that), the delayed update and the gradient norm in bytes of
  * HBM traffic.  Reading synchronises the stream and resets the counters.  Meant for measurement

@@ -58,6 +58,14 @@ struct Slot {
 struct stage {
   stage_shape_t sh;
   hipStream_t st;
+  // The delayed update runs on its own stream: it reads the gradient of an earlier step and
+  // writes the master state and the other weight version, none of which the forward / backward
+  // of the current step touch, so the two overlap.  ev_bwd[p] marks the end of the last backward
+  // of a step of parity p (its gradient and its use of weight version p); ev_upd the end of the
+  // last update, which the stage stream waits for before anything enqueued after it.
+  hipStream_t ust = nullptr;
+  hipEvent_t ev_bwd[2] = {nullptr, nullptr}, ev_upd = nullptr, ev_now = nullptr;
+  bool ev_bwd_set[2] = {false, false};
   bool bf;
   size_t esz;  // bytes per compute element
   int T, qkvw, hqd;
@@ -69,8 +77,8 @@ struct stage {
   void* ver[2];
   // scratch
   void *dA, *dB, *dh, *dn, *dgu, *do_, *dqkv, *dlog, *dhf;
-  float *delta, *rms_part, *row_loss, *cos_t, *sin_t, *norm_out;
-  double* norm_part;
+  float *delta, *rms_part, *row_loss, *cos_t, *sin_t, *norm_out, *upd_norm_out;
+  double *norm_part, *upd_norm_part;
   float* gemm_ws;
   int* flag;
   unsigned long long* skipped;
@@ -125,14 +133,16 @@ void prof_collect(stage* S) {
   S->prof_pending.clear();
 }
 
-// Runs `launch` bracketed by an event pair on the stage stream when timing is enabled.
+// Runs `launch` bracketed by an event pair on its stream (the stage stream unless `on` is given)
+// when timing is enabled.
 template <typename F>
-void timed(stage* S, int cls, double work, F&& launch) {
+void timed(stage* S, int cls, double work, F&& launch, hipStream_t on = nullptr) {
   if (!S->prof_on) { launch(); return; }
+  if (!on) on = S->st;
   hipEvent_t a = prof_event(S), b = prof_event(S);
-  (void)hipEventRecord(a, S->st);
+  (void)hipEventRecord(a, on);
   launch();
-  (void)hipEventRecord(b, S->st);
+  (void)hipEventRecord(b, on);
   S->prof_pending.push_back({cls, a, b, work});
   if (S->prof_pending.size() > 4096) {  // bound the number of live events
     (void)hipEventSynchronize(b);
@@ -242,6 +252,8 @@ size_t layout(stage* S, char* base) {
   S->delta = (float*)carve((int64_t)sh.micro_batch * sh.n_heads * sh.seq_len * 4);
   S->rms_part = (float*)carve(rms_partial_rows(T) * d * 4);
   S->norm_part = (double*)carve(norm_scratch_bytes());
+  S->upd_norm_part = (double*)carve(norm_scratch_bytes());
+  S->upd_norm_out = (float*)carve(2 * 4);
   S->gemm_ws = sh.dtype == 1 ? (float*)carve(GEMM_WS_ELEMS * 4) : nullptr;
   S->norm_out = (float*)carve(2 * 4);
   S->flag = (int*)carve(4);
@@ -428,6 +440,16 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
   }
   layout(S, (char*)arena);
   register_tensors(S);
+  {
+    hipError_t e = hipStreamCreateWithFlags(&S->ust, hipStreamNonBlocking);
+    for (int k = 0; k < 2 && e == hipSuccess; ++k) e = hipEventCreateWithFlags(&S->ev_bwd[k], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_upd, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_now, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      stage_destroy(S);
+      return fail(STAGE_EHIP, std::string("stage_init: ") + hipGetErrorString(e));
+    }
+  }
   launch_zero(arena, (int64_t)need, S->st);
   // RoPE tables: angle(p, i) = p * theta^(-2i/hd), evaluated in double
   const int half = shape->head_dim / 2;
@@ -443,7 +465,7 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
   if (e == hipSuccess) e = hipStreamSynchronize(S->st);
   if (e == hipSuccess) e = hipGetLastError();
   if (e != hipSuccess) {
-    delete S;
+    stage_destroy(S);
     return fail(STAGE_EHIP, std::string("stage_init: ") + hipGetErrorString(e));
   }
   *out = S;
@@ -484,6 +506,8 @@ int stage_sync_weights(stage_t* s) {
   if (!s) return fail(STAGE_EINVAL, "null stage");
   for (int k = 0; k < 2; ++k) launch_cast_copy(s->n_flat, s->master, s->ver[k], s->bf, s->st);
   HIP_OK(hipGetLastError());
+  // the caller may have written the optimizer state: the next update waits for the whole stream
+  s->ev_bwd_set[0] = s->ev_bwd_set[1] = false;
   s->version_step[s->next_t % 2] = s->next_t;
   s->version_step[(s->next_t + 1) % 2] = -1;
   return STAGE_OK;
@@ -584,6 +608,8 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   } else if (dx_out) {
     HIP_OK(hipMemcpyAsync(dx_out, cur, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
   }
+  HIP_OK(hipEventRecord(s->ev_bwd[gb], st));
+  s->ev_bwd_set[gb] = true;
   HIP_OK(hipGetLastError());
   s->grad_count[gb] += 1;
   sl.pending = false;
@@ -620,14 +646,29 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   hs.one_plus_lam = 1.0f + hp->ef_lambda;
   hs.ef = (apply && hp->ef_lambda != 0.f && s->n_updates >= 1) ? 1 : 0;
   hs.apply = apply ? 1 : 0;
+  // Order the update after the backwards whose gradient it reads (parity gb) and after the last
+  // use of the version it overwrites (parity vout); with no such backward on record, after
+  // everything on the stage stream.
+  hipStream_t us = s->ust;
+  const int need[2] = {vout, apply ? gb : vout};
+  for (int k = 0; k < 2; ++k) {
+    if (k == 1 && need[1] == need[0]) break;
+    const int p = need[k];
+    if (s->ev_bwd_set[p]) {
+      HIP_OK(hipStreamWaitEvent(us, s->ev_bwd[p], 0));
+    } else {
+      HIP_OK(hipEventRecord(s->ev_now, s->st));
+      HIP_OK(hipStreamWaitEvent(us, s->ev_now, 0));
+    }
+  }
   const float* clip = nullptr;
   const int* flag = nullptr;
   if (apply && hp->clip_norm > 0.f) {
     timed(s, STAGE_PROF_NORM, 4.0 * s->n_flat, [&] {
-      launch_grad_norm(s->grad[gb], false, s->n_flat, hp->clip_norm, s->norm_part, s->norm_out, s->flag,
-                       s->skipped, s->st);
-    });
-    clip = s->norm_out + 1;
+      launch_grad_norm(s->grad[gb], false, s->n_flat, hp->clip_norm, s->upd_norm_part, s->upd_norm_out,
+                       s->flag, s->skipped, us);
+    }, us);
+    clip = s->upd_norm_out + 1;
     flag = s->flag;
   }
   // bytes: x, m, v r+w; g read; shadow write; u_prev r+w with EF (no-op pass: x read, shadow write)
@@ -636,9 +677,12 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   timed(s, STAGE_PROF_UPDATE, ub * s->n_flat, [&] {
     launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v,
                         hp->ef_lambda != 0.f ? s->u_prev : nullptr, s->ver[vout], s->bf ? 2 : 1, hs,
-                        clip, flag, s->st);
-  });
+                        clip, flag, us);
+  }, us);
   HIP_OK(hipGetLastError());
+  // everything enqueued on the stage stream from here on runs after the update
+  HIP_OK(hipEventRecord(s->ev_upd, us));
+  HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd, 0));
   if (apply) {
     s->grad_consumed[gb] = true;
     s->n_updates = k;
@@ -730,8 +774,12 @@ int stage_profile_read(stage_t* s, int32_t cls, double* ms, int64_t* launches, d
 void stage_destroy(stage_t* s) {
   if (!s) return;
   (void)hipStreamSynchronize(s->st);
+  if (s->ust) (void)hipStreamSynchronize(s->ust);
   for (auto& r : s->prof_pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
   for (auto e : s->prof_free) (void)hipEventDestroy(e);
+  for (hipEvent_t e : {s->ev_bwd[0], s->ev_bwd[1], s->ev_upd, s->ev_now})
+    if (e) (void)hipEventDestroy(e);
+  if (s->ust) (void)hipStreamDestroy(s->ust);
   delete s;
 }
 
