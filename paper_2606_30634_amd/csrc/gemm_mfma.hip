@@ -47,20 +47,22 @@ struct TileLoader<ROWS, NT, true, CHECK> {
       r[p] = v;
     }
   }
+  __device__ __forceinline__ void store_one(bf16* __restrict__ S, int p) const {
+    const int c = threadIdx.x + p * NT;
+    *reinterpret_cast<u32x4*>(S + (c / (BK / 8)) * PADK + (c % (BK / 8)) * 8) = r[p];
+  }
   __device__ __forceinline__ void store(bf16* __restrict__ S) const {
 #pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int c = threadIdx.x + p * NT;
-      *reinterpret_cast<u32x4*>(S + (c / (BK / 8)) * PADK + (c % (BK / 8)) * 8) = r[p];
-    }
+    for (int p = 0; p < PER; ++p) store_one(S, p);
   }
 };
 
-// row-contiguous operand: kept as it sits in memory, a [k][row] tile of pitch ROWS + 16 filled
-// with 16-byte chunks of 8 rows; its MFMA fragments are read with transposing LDS reads (the
-// 16-element pad puts the 4 rows of one transposing read on distinct banks)
+// row-contiguous operand: kept as it sits in memory, a [k][row] tile of pitch ROWS + 32 filled
+// with 16-byte chunks of 8 rows; its MFMA fragments are read with transposing LDS reads.  One
+// such read by half a wave covers 4 k-rows x 32 rows (16 dwords per k-row); a pitch of 16 dwords
+// mod 64 puts those four runs on disjoint banks.
 template <int ROWS>
-constexpr int row_pitch() { return ROWS + 16; }
+constexpr int row_pitch() { return ROWS + 32; }
 
 template <int ROWS, int NT, bool CHECK>
 struct TileLoader<ROWS, NT, false, CHECK> {
@@ -80,12 +82,13 @@ struct TileLoader<ROWS, NT, false, CHECK> {
       r[p] = ok ? *reinterpret_cast<const u32x4*>(G + (int64_t)gk * ld + gr) : u32x4{0u, 0u, 0u, 0u};
     }
   }
+  __device__ __forceinline__ void store_one(bf16* __restrict__ S, int p) const {
+    const int c = threadIdx.x + p * NT;
+    *reinterpret_cast<u32x4*>(S + (c / (ROWS / 8)) * PR + (c % (ROWS / 8)) * 8) = r[p];
+  }
   __device__ __forceinline__ void store(bf16* __restrict__ S) const {
 #pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int c = threadIdx.x + p * NT;
-      *reinterpret_cast<u32x4*>(S + (c / (ROWS / 8)) * PR + (c % (ROWS / 8)) * 8) = r[p];
-    }
+    for (int p = 0; p < PER; ++p) store_one(S, p);
   }
 };
 
@@ -116,8 +119,122 @@ struct Cfg {
   static constexpr size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
 };
 
+// Waves per SIMD the tile allows (accumulators and LDS stages): told to the compiler so that it
+// schedules for that occupancy instead of trading the fragment prefetch for registers.
+template <int BM, int BN>
+constexpr int tile_waves_per_simd() { return BM * BN >= 256 * 256 ? 1 : 2; }
+
+// XCD-aware tile order: hardware places block b on XCD b mod 8; give each XCD a contiguous run
+// of tiles, walked in groups of GM row tiles (down a group's rows, then to its next column), so
+// the blocks resident on one XCD at a time cover a compact patch of C and share their A and B
+// slices in that XCD's L2.
+template <int BM, int BN>
+__device__ __forceinline__ void tile_origin(const GemmArgs& g, int& m0, int& n0) {
+  constexpr int GM = 8;
+  const int tiles_n = (g.N + BN - 1) / BN;
+  const int tiles_m = (g.M + BM - 1) / BM;
+  const int nblk = tiles_m * tiles_n;
+  int b = blockIdx.x;
+  if ((nblk & 7) == 0) b = (b & 7) * (nblk >> 3) + (b >> 3);
+  const int first_m = (b / (GM * tiles_n)) * GM;
+  const int gsz = min(tiles_m - first_m, GM);
+  m0 = (first_m + (b % (GM * tiles_n)) % gsz) * BM;
+  n0 = ((b % (GM * tiles_n)) / gsz) * BN;
+}
+
+// Epilogue: per 32-row slice of the wave tile, stage the fp32 accumulators through LDS and write
+// 16-byte rows: split-K partials to the workspace, or C with the beta / residual / SwiGLU-backward
+// / RoPE terms.  LDS must be free (every wave past its last read of the operand stages).
+template <int BM, int BN, int WM, int WN, typename OutT, bool CHECK>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[WM / 32][WN / 32],
+                                              unsigned char* smem, int m0, int n0, int wm0, int wn0) {
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int EP = WN + 4;  // staging pitch (fp32 elements)
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  float* stg = reinterpret_cast<float*>(smem) + wave * 32 * EP;
+  const bool split = g.ksplit > 1;
+  float* W = split ? g.ws + (int64_t)blockIdx.y * g.M * g.N : nullptr;
+  OutT* C = (OutT*)g.C;
+  const bf16* R = (const bf16*)g.resid;
+  constexpr int VEC = sizeof(OutT) == 2 ? 8 : 4;  // elements per 16-byte store
+  static_for<FM>([&](auto I) {
+    constexpr int i = I;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        stg[(8 * (e / 4) + 4 * (lane / 32) + (e % 4)) * EP + j * 32 + lane % 32] = acc[i][j][e];
+    __syncthreads();
+    const int rbase = m0 + wm0 + i * 32;
+    if (split) {
+      for (int c = lane; c < 32 * WN / 4; c += 64) {
+        const int r = c / (WN / 4), cc = (c % (WN / 4)) * 4;
+        const int row = rbase + r, col = n0 + wn0 + cc;
+        if (!CHECK || (row < g.M && col < g.N))
+          *reinterpret_cast<float4*>(W + (int64_t)row * g.N + col) = *reinterpret_cast<const float4*>(stg + r * EP + cc);
+      }
+    } else {
+      for (int c = lane; c < 32 * WN / VEC; c += 64) {
+        const int r = c / (WN / VEC), cc = (c % (WN / VEC)) * VEC;
+        const int row = rbase + r, col = n0 + wn0 + cc;
+        if (CHECK && (row >= g.M || col >= g.N)) continue;  // N is a multiple of 8
+        const int64_t o = (int64_t)row * g.ldc + col;
+        float v[VEC];
+#pragma unroll
+        for (int q = 0; q < VEC; ++q) v[q] = stg[r * EP + cc + q];
+        if constexpr (sizeof(OutT) == 4) {
+          if (g.beta != 0.f) {
+            const float4 old = *reinterpret_cast<const float4*>((const float*)C + o);
+            v[0] += g.beta * old.x; v[1] += g.beta * old.y; v[2] += g.beta * old.z; v[3] += g.beta * old.w;
+          }
+          *reinterpret_cast<float4*>((float*)C + o) = make_float4(v[0], v[1], v[2], v[3]);
+        } else if (g.epi == 1) {  // SwiGLU backward from dz = v
+          const bf16* gu = (const bf16*)g.aux + (int64_t)row * g.ld_aux + col;
+          const bf16x8 av = *reinterpret_cast<const bf16x8*>(gu);
+          const bf16x8 bv = *reinterpret_cast<const bf16x8*>(gu + g.N);
+          bf16x8 da, db;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float a = (float)av[q], bb = (float)bv[q];
+            const float sg = 1.0f / (1.0f + __expf(-a));
+            da[q] = (bf16)(v[q] * bb * sg * (1.0f + a * (1.0f - sg)));
+            db[q] = (bf16)(v[q] * a * sg);
+          }
+          *reinterpret_cast<bf16x8*>((bf16*)C + o) = da;
+          *reinterpret_cast<bf16x8*>((bf16*)C + o + g.N) = db;
+        } else if (g.epi == 2 && col < g.rope_cols) {  // RoPE on the fp32 products
+          const int hd = g.rope_hd, hh = hd / 2;
+          const int c = col % hd, i0 = c % hh;
+          const bool first = c < hh;
+          const float* xp = stg + r * EP + (first ? cc + hh : cc - hh);  // partner columns
+          const int64_t tb = (int64_t)(row % g.rope_S) * hh + i0;
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float cs = g.rope_cos[tb + q], sn = g.rope_sin[tb + q];
+            ov[q] = (bf16)(first ? v[q] * cs - xp[q] * sn : v[q] * cs + xp[q] * sn);
+          }
+          *reinterpret_cast<bf16x8*>((bf16*)C + o) = ov;
+        } else {
+          if (R) {
+            const bf16x8 rr = *reinterpret_cast<const bf16x8*>(R + o);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] += (float)rr[q];
+          }
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
+          *reinterpret_cast<bf16x8*>((bf16*)C + o) = ov;
+        }
+      }
+    }
+    __syncthreads();
+  });
+}
+
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, bool CHECK>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(tile_waves_per_simd<BM, BN>(), tile_waves_per_simd<BM, BN>())))
 gemm_mfma_kernel(GemmArgs g) {
   using C_ = Cfg<BM, BN, WM, WN, AK, BKM>;
   constexpr int WAVES_N = BN / WN;
@@ -126,15 +243,8 @@ gemm_mfma_kernel(GemmArgs g) {
   bf16* As = reinterpret_cast<bf16*>(smem);                 // [2][SA]
   bf16* Bs = As + 2 * SA;                                   // [2][SB]
 
-  // XCD-aware tile order: hardware places block b on XCD b mod 8; give each XCD a contiguous run
-  // of tiles (in row-band order) so the tiles sharing A rows share that XCD's L2.
-  const int tiles_n = (g.N + BN - 1) / BN;
-  const int tiles_m = (g.M + BM - 1) / BM;
-  const int nblk = tiles_m * tiles_n;
-  int b = blockIdx.x;
-  if ((nblk & 7) == 0) b = (b & 7) * (nblk >> 3) + (b >> 3);
-  const int tm = b / tiles_n, tn = b % tiles_n;
-  const int m0 = tm * BM, n0 = tn * BN;
+  int m0, n0;
+  tile_origin<BM, BN>(g, m0, n0);
 
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
@@ -164,14 +274,23 @@ gemm_mfma_kernel(GemmArgs g) {
   la.store(As);
   lb.store(Bs);
   __syncthreads();
+  // Per k-slice, in this order (the compiler may not move instructions across the fences):
+  //   step 0: global loads of the next slice, then the fragment reads of step 1, then the MFMAs
+  //   steps 1, 2: fragment reads of the following step, then the MFMAs
+  //   step 3: the MFMAs, each followed by its share of the LDS writes of the next slice
+  // so every fragment read has a whole step of MFMAs to land, and the global loads three.
+  constexpr int NM = FM * FN;
+  constexpr int PA = decltype(la)::PER, PB = decltype(lb)::PER;
+  constexpr int WPM = (PA + PB + NM - 1) / NM;  // LDS writes per MFMA in the last step
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      la.load(A, g.lda, m0, g.M, kbeg + (kt + 1) * BK, kend);
-      lb.load(B, g.ldb, n0, g.N, kbeg + (kt + 1) * BK, kend);
-    }
+    // next slice (the last iteration reloads its own slice, unused, so the loads and the LDS
+    // writes are unconditional)
+    const int kn = kbeg + min(kt + 1, nk - 1) * BK;
     const bf16* as = As + cur * SA;
     const bf16* bs = Bs + cur * SB;
+    bf16* asn = As + (cur ^ 1) * SA;
+    bf16* bsn = Bs + (cur ^ 1) * SB;
     bf16x8 af[2][FM], bfr[2][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i) af[0][i] = frag<BM, AK>(as, wm0 + i * 32, 0);
@@ -179,105 +298,229 @@ gemm_mfma_kernel(GemmArgs g) {
     for (int j = 0; j < FN; ++j) bfr[0][j] = frag<BN, BKM>(bs, wn0 + j * 32, 0);
     static_for<BK / 16>([&](auto KS) {
       constexpr int ks = KS, c = ks & 1;
-      if constexpr (ks + 1 < BK / 16) {  // next 16-deep step's fragments while these MFMAs run
+      if constexpr (ks == 0) {
+        la.load(A, g.lda, m0, g.M, kn, kend);
+        lb.load(B, g.ldb, n0, g.N, kn, kend);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (ks + 1 < BK / 16) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) af[c ^ 1][i] = frag<BM, AK>(as, wm0 + i * 32, (ks + 1) * 16);
 #pragma unroll
         for (int j = 0; j < FN; ++j) bfr[c ^ 1][j] = frag<BN, BKM>(bs, wn0 + j * 32, (ks + 1) * 16);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+        static_for<NM>([&](auto Q) {
+          constexpr int q = Q, i = q / FN, j = q % FN;
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
+          static_for<WPM>([&](auto W) {
+            constexpr int w = q * WPM + W;
+            if constexpr (w < PA) la.store_one(asn, w);
+            else if constexpr (w < PA + PB) lb.store_one(bsn, w - PA);
+          });
+          __builtin_amdgcn_sched_barrier(0);
+        });
       }
+    });
+    __syncthreads();
+  }
+
+  gemm_epilogue<BM, BN, WM, WN, OutT, CHECK>(g, acc, smem, m0, n0, wm0, wn0);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Full-tile kernel with direct-to-LDS operand loads (gfx950 global_load_lds_dwordx4): each lane's
+// 16 bytes land at the wave's LDS base + 16 * lane, so a tile is written in lane order and the
+// bank spreading is an XOR swizzle of 16-byte chunks instead of padding:
+//   k-contiguous tile [ROWS][BKT]: chunk kc of row r sits at r * BKT/8 + (kc ^ ((r / (128/BKT)) mod
+//     BKT/8)), so the 16 rows one 16-lane group reads for a fragment cover all 64 banks;
+//   row-contiguous tile [BKT][ROWS]: chunk rc of k-row k sits at k * ROWS/8 + (rc ^ 4 (k mod 4)), so
+//     the 4 k-rows x 32 rows of one half-wave transposing read fall in 4 different 64-byte bank
+//     groups (ROWS >= 128, a whole number of 256-byte bank periods per k-row).
+// NS stages: the loads of slice kt + NS - 1 are issued while slice kt is consumed, so a load has
+// NS - 1 slices of MFMAs to land; one barrier per slice, after each thread has seen its own loads
+// of the slice complete (vmcnt), makes every thread's loads of it visible.
+template <int ROWS, int BKT, bool KMAJ, int NT>
+struct DmaTile {
+  static constexpr int CHUNKS = ROWS * BKT / 8;
+  static constexpr int PER = CHUNKS / NT;  // loads per thread and slice
+  static constexpr int ELEMS = ROWS * BKT;
+  static_assert(CHUNKS % NT == 0, "tile does not split evenly over the threads");
+  static_assert(KMAJ || ROWS >= 128, "row-contiguous swizzle needs 256-byte k-rows");
+  // element offset, from the tile origin in global memory, of the data for LDS chunk p
+  __device__ static int64_t src(int p, int ld) {
+    if constexpr (KMAJ) {
+      constexpr int CPR = BKT / 8, RPB = 128 / BKT;
+      const int r = p / CPR, kc = (p % CPR) ^ ((r / RPB) % CPR);
+      return (int64_t)r * ld + kc * 8;
+    } else {
+      constexpr int CPK = ROWS / 8;
+      const int k = p / CPK, rc = (p % CPK) ^ (4 * (k & 3));
+      return (int64_t)k * ld + rc * 8;
+    }
+  }
+  // MFMA fragment: row r0 + lane mod 32, k = k0 + 8 (lane / 32) .. +7
+  __device__ static bf16x8 frag(const bf16* T, int r0, int k0) {
+    const int l = threadIdx.x % 64;
+    if constexpr (KMAJ) {
+      constexpr int CPR = BKT / 8, RPB = 128 / BKT;
+      const int r = r0 + l % 32, kc = k0 / 8 + l / 32;
+      return *reinterpret_cast<const bf16x8*>(T + r * BKT + ((kc ^ ((r / RPB) % CPR)) << 3));
+    } else {
+      const int gq = l / 16, i = l % 16;
+      const int r = r0 + 16 * (gq & 1) + 4 * (i & 3);
+      const int k = k0 + 8 * (gq >> 1) + (i >> 2);  // k and k + 4 share k mod 4
+      const int col = (((r >> 3) ^ (4 * (k & 3))) << 3) + (r & 7);
+      typedef __attribute__((address_space(3))) v4i16_t lds_v4i16;
+      const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(T + k * ROWS + col));
+      const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(T + (k + 4) * ROWS + col));
+      bf16x8 f;
+      __builtin_memcpy(&f, &lo, 8);
+      __builtin_memcpy(reinterpret_cast<char*>(&f) + 8, &hi, 8);
+      return f;
+    }
+  }
+};
+
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, int BKT, int NS>
+struct DmaCfg {
+  static constexpr int NW = (BM / WM) * (BN / WN);
+  static constexpr int NT = NW * 64;
+  using TA = DmaTile<BM, BKT, AK, NT>;
+  using TB = DmaTile<BN, BKT, BKM, NT>;
+  static constexpr size_t main_lds = (size_t)NS * (TA::ELEMS + TB::ELEMS) * sizeof(bf16);
+  static constexpr size_t epi_lds = (size_t)NW * 32 * (WN + 4) * sizeof(float);
+  static constexpr size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
+};
+
+// s_waitcnt: at most N vector-memory operations and no LDS operation outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+}
+
+// One 16-byte global -> LDS load per lane (lane l writes lds + 16 l).  Issued as inline assembly so
+// that the compiler neither counts it in its own waits nor orders LDS reads after it: the kernel
+// waits for these loads itself (wait_vm_lds) before the barrier that publishes a stage.
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+}
+
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// waves per SIMD: the block's waves over the 4 SIMDs times the blocks the LDS lets a CU hold
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, int BKT, int NS>
+constexpr int dma_waves_per_simd() {
+  using C_ = DmaCfg<BM, BN, WM, WN, AK, BKM, BKT, NS>;
+  const int blocks = (int)(163840 / C_::lds);
+  const int w = (C_::NW / 4) * (blocks > 0 ? blocks : 1);
+  return w > 8 ? 8 : (w < 1 ? 1 : w);
+}
+
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, int BKT, int NS>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(dma_waves_per_simd<BM, BN, WM, WN, AK, BKM, BKT, NS>(),
+                                   dma_waves_per_simd<BM, BN, WM, WN, AK, BKM, BKT, NS>())))
+gemm_dma_kernel(GemmArgs g) {
+  using C_ = DmaCfg<BM, BN, WM, WN, AK, BKM, BKT, NS>;
+  using TA = typename C_::TA;
+  using TB = typename C_::TB;
+  constexpr int WAVES_N = BN / WN, NW = C_::NW;
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int PA = TA::PER, PB = TB::PER;
+  extern __shared__ __align__(16) unsigned char smem[];
+  bf16* As = reinterpret_cast<bf16*>(smem);  // [NS][TA::ELEMS]
+  bf16* Bs = As + NS * TA::ELEMS;            // [NS][TB::ELEMS]
+
+  int m0, n0;
+  tile_origin<BM, BN>(g, m0, n0);
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  // split-K: this block covers slices [s0, s0 + nk)
+  const int nslices = g.K / BKT;
+  const int per_split = nslices / g.ksplit;
+  const int s0 = blockIdx.y * per_split, nk = per_split;
+  // this thread's source pointers for slice s0 and the step between slices
+  const bf16* pa[PA];
+  const bf16* pb[PB];
+  const bf16* A = (const bf16*)g.A + (AK ? (int64_t)m0 * g.lda + (int64_t)s0 * BKT : (int64_t)s0 * BKT * g.lda + m0);
+  const bf16* B = (const bf16*)g.B + (BKM ? (int64_t)n0 * g.ldb + (int64_t)s0 * BKT : (int64_t)s0 * BKT * g.ldb + n0);
+#pragma unroll
+  for (int q = 0; q < PA; ++q) pa[q] = A + TA::src((q * NW + wave) * 64 + lane, g.lda);
+#pragma unroll
+  for (int q = 0; q < PB; ++q) pb[q] = B + TB::src((q * NW + wave) * 64 + lane, g.ldb);
+  const int64_t step_a = AK ? BKT : (int64_t)BKT * g.lda;
+  const int64_t step_b = BKM ? BKT : (int64_t)BKT * g.ldb;
+  // LDS byte addresses of this wave's first chunk in stage 0
+  typedef __attribute__((address_space(3))) bf16 lds_bf16;
+  const uint32_t la0 = (uint32_t)(uintptr_t)(lds_bf16*)(As + wave * 512);
+  const uint32_t lb0 = (uint32_t)(uintptr_t)(lds_bf16*)(Bs + wave * 512);
+  // slice s (clamped to the last one: the tail reloads it into a stage nobody reads again, which
+  // keeps the count of outstanding loads per slice uniform) into stage `stage`
+  auto issue = [&](int s, int stage) {
+    s = min(s, nk - 1);
+    const uint32_t ta = la0 + stage * TA::ELEMS * 2, tb = lb0 + stage * TB::ELEMS * 2;
+#pragma unroll
+    for (int q = 0; q < PA; ++q) dma16(pa[q] + s * step_a, ta + q * NW * 1024);
+#pragma unroll
+    for (int q = 0; q < PB; ++q) dma16(pb[q] + s * step_b, tb + q * NW * 1024);
+  };
+  if (nk > 0) {
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) issue(s, s);
+  }
+  for (int kt = 0; kt < nk; ++kt) {
+    wait_vm_lds<(NS - 2) * (PA + PB)>();  // this thread's loads of slice kt are in LDS
+    block_barrier();                        // ... and every thread's; stage kt - 1 is free
+    issue(kt + NS - 1, (kt + NS - 1) % NS);
+    const int cur = kt % NS;
+    const bf16* as = As + cur * TA::ELEMS;
+    const bf16* bs = Bs + cur * TB::ELEMS;
+    bf16x8 af[2][FM], bfr[2][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) af[0][i] = TA::frag(as, wm0 + i * 32, 0);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) bfr[0][j] = TB::frag(bs, wn0 + j * 32, 0);
+    static_for<BKT / 16>([&](auto KS) {
+      constexpr int ks = KS, c = ks & 1;
+      if constexpr (ks + 1 < BKT / 16) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[c ^ 1][i] = TA::frag(as, wm0 + i * 32, (ks + 1) * 16);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[c ^ 1][j] = TB::frag(bs, wn0 + j * 32, (ks + 1) * 16);
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     });
-    if (kt + 1 < nk) {
-      la.store(As + (cur ^ 1) * SA);
-      lb.store(Bs + (cur ^ 1) * SB);
-    }
-    __syncthreads();
   }
-
-  // epilogue: per 32-row slice of the wave tile, stage fp32 through LDS and write 16-byte rows
-  float* stg = reinterpret_cast<float*>(smem) + wave * 32 * C_::EP;
-  const bool split = g.ksplit > 1;
-  float* W = split ? g.ws + (int64_t)blockIdx.y * g.M * g.N : nullptr;
-  OutT* C = (OutT*)g.C;
-  const bf16* R = (const bf16*)g.resid;
-  constexpr int VEC = sizeof(OutT) == 2 ? 8 : 4;  // elements per 16-byte store
-  static_for<FM>([&](auto I) {
-    constexpr int i = I;
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        stg[(8 * (e / 4) + 4 * (lane / 32) + (e % 4)) * C_::EP + j * 32 + lane % 32] = acc[i][j][e];
-    __syncthreads();
-    const int rbase = m0 + wm0 + i * 32;
-    if (split) {
-      for (int c = lane; c < 32 * WN / 4; c += 64) {
-        const int r = c / (WN / 4), cc = (c % (WN / 4)) * 4;
-        const int row = rbase + r, col = n0 + wn0 + cc;
-        if (!CHECK || (row < g.M && col < g.N))
-          *reinterpret_cast<float4*>(W + (int64_t)row * g.N + col) = *reinterpret_cast<const float4*>(stg + r * C_::EP + cc);
-      }
-    } else {
-      for (int c = lane; c < 32 * WN / VEC; c += 64) {
-        const int r = c / (WN / VEC), cc = (c % (WN / VEC)) * VEC;
-        const int row = rbase + r, col = n0 + wn0 + cc;
-        if (CHECK && (row >= g.M || col >= g.N)) continue;  // N is a multiple of 8
-        const int64_t o = (int64_t)row * g.ldc + col;
-        float v[VEC];
-#pragma unroll
-        for (int q = 0; q < VEC; ++q) v[q] = stg[r * C_::EP + cc + q];
-        if constexpr (sizeof(OutT) == 4) {
-          if (g.beta != 0.f) {
-            const float4 old = *reinterpret_cast<const float4*>((const float*)C + o);
-            v[0] += g.beta * old.x; v[1] += g.beta * old.y; v[2] += g.beta * old.z; v[3] += g.beta * old.w;
-          }
-          *reinterpret_cast<float4*>((float*)C + o) = make_float4(v[0], v[1], v[2], v[3]);
-        } else if (g.epi == 1) {  // SwiGLU backward from dz = v
-          const bf16* gu = (const bf16*)g.aux + (int64_t)row * g.ld_aux + col;
-          const bf16x8 av = *reinterpret_cast<const bf16x8*>(gu);
-          const bf16x8 bv = *reinterpret_cast<const bf16x8*>(gu + g.N);
-          bf16x8 da, db;
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const float a = (float)av[q], bb = (float)bv[q];
-            const float sg = 1.0f / (1.0f + __expf(-a));
-            da[q] = (bf16)(v[q] * bb * sg * (1.0f + a * (1.0f - sg)));
-            db[q] = (bf16)(v[q] * a * sg);
-          }
-          *reinterpret_cast<bf16x8*>((bf16*)C + o) = da;
-          *reinterpret_cast<bf16x8*>((bf16*)C + o + g.N) = db;
-        } else if (g.epi == 2 && col < g.rope_cols) {  // RoPE on the fp32 products
-          const int hd = g.rope_hd, hh = hd / 2;
-          const int c = col % hd, i0 = c % hh;
-          const bool first = c < hh;
-          const float* xp = stg + r * C_::EP + (first ? cc + hh : cc - hh);  // partner columns
-          const int64_t tb = (int64_t)(row % g.rope_S) * hh + i0;
-          bf16x8 ov;
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const float cs = g.rope_cos[tb + q], sn = g.rope_sin[tb + q];
-            ov[q] = (bf16)(first ? v[q] * cs - xp[q] * sn : v[q] * cs + xp[q] * sn);
-          }
-          *reinterpret_cast<bf16x8*>((bf16*)C + o) = ov;
-        } else {
-          if (R) {
-            const bf16x8 rr = *reinterpret_cast<const bf16x8*>(R + o);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) v[q] += (float)rr[q];
-          }
-          bf16x8 ov;
-#pragma unroll
-          for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
-          *reinterpret_cast<bf16x8*>((bf16*)C + o) = ov;
-        }
-      }
-    }
-    __syncthreads();
-  });
+  wait_vm_lds<0>();  // the tail's reloads too: the epilogue reuses the LDS
+  __syncthreads();
+  gemm_epilogue<BM, BN, WM, WN, OutT, false>(g, acc, smem, m0, n0, wm0, wn0);
 }
 
 // C = beta C + sum over splits of the partial tiles, in split order (fp32 output, ldc == N)
@@ -335,6 +578,30 @@ void launch_cfg(const GemmArgs& g, hipStream_t st) {
 #undef L
 }
 
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, int BKT, int NS>
+void launch_dma_one(const GemmArgs& g, int nblk, hipStream_t st) {
+  using C_ = DmaCfg<BM, BN, WM, WN, AK, BKM, BKT, NS>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)C_::lds);
+    attr_set = true;
+  }
+  gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS><<<dim3(nblk, g.ksplit), C_::NT, C_::lds, st>>>(g);
+}
+
+// Direct-to-LDS variant: full tiles and whole slices per split only; false if the shape is not.
+template <int BM, int BN, int WM, int WN, typename OutT, int BKT, int NS>
+bool launch_dma_cfg(const GemmArgs& g, hipStream_t st) {
+  if (g.M % BM || g.N % BN || g.K % BKT || g.K == 0 || (g.K / BKT) % g.ksplit) return false;
+  const int nblk = (g.M / BM) * (g.N / BN);
+  if (g.a_kmajor && g.b_kmajor) launch_dma_one<BM, BN, WM, WN, true, true, OutT, BKT, NS>(g, nblk, st);
+  else if (g.a_kmajor) launch_dma_one<BM, BN, WM, WN, true, false, OutT, BKT, NS>(g, nblk, st);
+  else if (g.b_kmajor) launch_dma_one<BM, BN, WM, WN, false, true, OutT, BKT, NS>(g, nblk, st);
+  else launch_dma_one<BM, BN, WM, WN, false, false, OutT, BKT, NS>(g, nblk, st);
+  return true;
+}
+
 }  // namespace
 
 bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
@@ -346,22 +613,34 @@ bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   g.ksplit = 1;
   const int64_t mn = (int64_t)g.M * g.N;
-  // 256x256 tiles when the product is deep enough to amortise them and still fills the chip
-  const bool big = g.K >= 2048 && cdiv(g.M, 256) * cdiv(g.N, 256) >= 256;
-  const int64_t tiles = big ? cdiv(g.M, 256) * cdiv(g.N, 256) : cdiv(g.M, 128) * cdiv(g.N, 128);
+  constexpr int DK = 32;  // k-slice of the direct-to-LDS kernels
+  // Full tiles go to the direct-to-LDS kernels: 256 x 256 (8 waves of 64 x 128) when the product
+  // has enough of them (or is deep enough to amortise them), else 128 x 128; ragged shapes to the
+  // register-staged kernel with bounds-checked loads.
+  const bool full128 = g.M % 128 == 0 && g.N % 128 == 0 && g.K % DK == 0;
+  const int64_t t256 = cdiv(g.M, 256) * cdiv(g.N, 256), t128 = cdiv(g.M, 128) * cdiv(g.N, 128);
+  const bool big = g.M % 256 == 0 && g.N % 256 == 0 && g.K % DK == 0 &&
+                   (t256 >= 512 || (t256 >= 256 && g.K >= 2048));
+  const int64_t tiles = big ? t256 : t128;
   if (g.out_f32 && g.ws && g.ldc == g.N && tiles < 512 && g.K >= 2048) {
+    // deterministic split-K for underfilled fp32-output products: whole slices per split
+    const int kq = full128 ? DK : BK;
     int s = (int)std::min<int64_t>(8, cdiv(512, tiles));
-    while (s > 1 && (s * mn > g.ws_elems || g.K / s < 512)) --s;
+    while (s > 1 && (s * mn > g.ws_elems || g.K / s < 512 || (g.K / kq) % s)) --s;
     g.ksplit = s;
   }
   // RoPE in the epilogue needs every head whole inside one wave's columns
   const int wn = big ? 128 : 64;
   const bool rope_after = g.epi == 2 && (g.out_f32 || wn % g.rope_hd != 0);
   if (rope_after) g.epi = 0;
-  if (big) {
-    if (g.out_f32) launch_cfg<256, 256, 128, 128, float>(g, st);
-    else launch_cfg<256, 256, 128, 128, bf16>(g, st);
-  } else {
+  bool done = false;  // the direct-to-LDS launchers decline shapes they do not take (K = 0)
+  if (big)
+    done = g.out_f32 ? launch_dma_cfg<256, 256, 64, 128, float, DK, 4>(g, st)
+                     : launch_dma_cfg<256, 256, 64, 128, bf16, DK, 4>(g, st);
+  else if (full128)
+    done = g.out_f32 ? launch_dma_cfg<128, 128, 64, 64, float, DK, 4>(g, st)
+                     : launch_dma_cfg<128, 128, 64, 64, bf16, DK, 4>(g, st);
+  if (!done) {
     if (g.out_f32) launch_cfg<128, 128, 64, 64, float>(g, st);
     else launch_cfg<128, 128, 64, 64, bf16>(g, st);
   }
