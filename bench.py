@@ -28,10 +28,46 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def kernel_sources_sha256():
+    """SHA-256 over the HIP sources of the library (file names and contents, in name order)."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2606_30634_amd", "csrc")
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, kernel_class):
+    """HBM bytes per launch of a kernel class from the committed rocprofv3 --pmc summary of this
+    workload (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy's counters), or None when there is
+    none or the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    start = text.find("```json")
+    if start < 0:
+        return None
+    end = text.find("```", start + 7)
+    try:
+        rec = json.loads(text[start + 7:end])
+    except ValueError:
+        return None
+    if rec.get("sources_sha256") != kernel_sources_sha256():
+        return None
+    v = rec.get("bytes_per_launch", {}).get(kernel_class)
+    return float(v) if v is not None else None
+
+
 def cpu_baseline(w):
-    """The oracle (float32, numpy) on one whole optimizer step of the workload (all sequences
-    forward+backward, then the full delayed update) when that is a bounded amount of CPU work;
-    otherwise on 2 of the step's sequences plus the full update, extrapolated linearly in tokens."""
+    """The oracle (float32, numpy) timed on whole optimizer steps of the workload -- all sequences
+    forward+backward, then the full delayed update -- repeated until at least 10 s of CPU work (at
+    most 4 steps) when one step is a bounded amount of work; otherwise on 2 of the step's sequences
+    plus the full update, extrapolated linearly in tokens."""
     import numpy as np
     import datagen
     import oracle
@@ -45,26 +81,32 @@ def cpu_baseline(w):
     n_seq = w.micro_batch if w.d_model <= 1024 else min(2, w.micro_batch)
     ws = w.with_(micro_batch=n_seq)
     p0 = datagen.init_params(ws)
+    hp = oracle.hparams_of(ws)
     st = OptState.create(p0, np.float32)
     inp = datagen.step_inputs(ws, 0)
-    t0 = time.perf_counter()
     g, _ = model.stage_step_grads(st.x, [inp], ws, np.float32)
-    t1 = time.perf_counter()
-    iteration_update(st, g, oracle.hparams_of(ws))   # t = 0: stashes g_0 (no arithmetic)
-    t2 = time.perf_counter()
-    iteration_update(st, g, oracle.hparams_of(ws))   # t = 1: the full AdamW + clip pass
-    t3 = time.perf_counter()
+    iteration_update(st, g, hp)   # t = 0: stashes g_0 (no arithmetic), untimed
+    fb_s, upd_s, reps = 0.0, 0.0, 0
+    while reps < 4 and (reps == 0 or fb_s + upd_s < 10.0):
+        t0 = time.perf_counter()
+        g, _ = model.stage_step_grads(st.x, [inp], ws, np.float32)
+        t1 = time.perf_counter()
+        iteration_update(st, g, hp)   # the full AdamW + clip + EF pass
+        t2 = time.perf_counter()
+        fb_s += t1 - t0
+        upd_s += t2 - t1
+        reps += 1
     tokens_step = w.tokens_per_micro * w.microbatches_per_step
-    fb_per_token = (t1 - t0) / (n_seq * w.seq_len)
-    step_s = fb_per_token * tokens_step + (t3 - t2)
+    fb_per_token = fb_s / reps / (n_seq * w.seq_len)
+    step_s = fb_per_token * tokens_step + upd_s / reps
     whole = n_seq * w.seq_len == tokens_step
-    how = ("one whole optimizer step" if whole else
-           f"step time extrapolated linearly in tokens to {tokens_step} tokens")
+    how = (f"{reps} whole optimizer steps" if whole else
+           f"{reps} steps, extrapolated linearly in tokens to {tokens_step} tokens per step")
     return {"value": tokens_step / step_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": f"float32 numpy oracle: {n_seq} of the step's {w.micro_batch * w.microbatches_per_step} "
-                      f"sequences forward+backward ({t1 - t0:.1f} s) plus one full delayed update over "
-                      f"{sum(v.size for v in p0.values())} parameters ({t3 - t2:.1f} s); {how}",
-            "measured_s": round(t3 - t0 + (t2 - t1), 2)}
+                      f"sequences forward+backward ({fb_s / reps:.1f} s per step) plus the full delayed update "
+                      f"over {sum(v.size for v in p0.values())} parameters ({upd_s / reps:.1f} s per step); {how}",
+            "measured_s": round(fb_s + upd_s, 2)}
 
 
 def update_workload(steps):
@@ -243,7 +285,8 @@ def main():
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
     kd = kern[dom]
     roofline = {"kernel": dom, "bound": kd["bound"], "achieved": kd["achieved"], "peak": kd["peak"],
-                "unit": kd["unit"], "frac": kd["frac"], "traffic": None}
+                "unit": kd["unit"], "frac": kd["frac"],
+                "traffic": measured_traffic(args.workload + ("-bf16" if bf else "-f32"), dom)}
     rc, skipped = B.stage_poll_nonfinite(st.handle)
     st.close()
 
