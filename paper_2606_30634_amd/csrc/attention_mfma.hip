@@ -1,7 +1,10 @@
 // Causal grouped-query flash attention on gfx950 matrix cores (bf16 in, fp32 accumulation).
 //
-// Every LDS tile holds rows of a head as they sit in memory ([row][d], 16-byte copies).  The MFMA
-// operand v_mfma_f32_32x32x16_bf16 wants 8 consecutive contraction values per lane:
+// Every LDS tile holds rows of a head as they sit in memory ([row][d], 16-byte copies), unpadded,
+// with the 16-byte chunks of row r permuted by an XOR with swz(r) so that both ways of reading a
+// tile are free of bank conflicts (64 banks; a 16-byte read is served 16 lanes, an 8-byte read half
+// a wave, per cycle).  The MFMA operand v_mfma_f32_32x32x16_bf16 wants 8 consecutive contraction
+// values per lane:
 //   - contraction over d (S = Q K^T, dP = dO V^T): 16-byte reads of a row;
 //   - contraction over rows (O^T += V^T P^T, dQ^T += K^T dS^T, dV^T += dO^T P, dK^T += Q^T dS):
 //     two ds_read_b64_tr_b16 transposing reads (each 16-lane group reads a 4 x 16 block whose
@@ -34,30 +37,78 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
   return (uint32_t)u | ((uint32_t)v << 16);
 }
 
+// Chunk permutation of tile row r (HD/8 chunks of 16 bytes per row):
+//   HD = 128 (a row spans the 64 banks): swz = 4 (r mod 4) + (r / 4 mod 4), a bijection on any 16
+//     consecutive rows (16-byte row reads) that sends 4 consecutive rows (k0 a multiple of 4) to 4
+//     different 4-chunk groups (transposing reads of 4 rows x 32 columns);
+//   HD = 64 (two rows per 64 banks): swz = 4 (r / 2 mod 2) + (r / 4 mod 4), the same two properties
+//     over the rows of one parity.
+template <int HD>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (HD == 128) return 4 * (r & 3) + ((r >> 2) & 3);
+  else return 4 * ((r >> 1) & 1) + ((r >> 2) & 3);
+}
+// element index of (row r, column c) in a swizzled [row][HD] tile
+template <int HD>
+__device__ __forceinline__ int tidx(int r, int c) {
+  return r * HD + ((((c >> 3) ^ swz<HD>(r))) << 3) + (c & 7);
+}
+
 // fragment of a [row][k] tile: row r0 + lane mod 32, k = k0 + 8 (lane / 32) .. +7
-__device__ __forceinline__ bf16x8 frag_rows(const bf16* T, int P, int r0, int k0) {
+template <int HD>
+__device__ __forceinline__ bf16x8 frag_rows(const bf16* T, int r0, int k0) {
   const int l = threadIdx.x % 64;
-  return *reinterpret_cast<const bf16x8*>(T + (r0 + l % 32) * P + k0 + 8 * (l / 32));
+  return *reinterpret_cast<const bf16x8*>(T + tidx<HD>(r0 + l % 32, k0 + 8 * (l / 32)));
+}
+
+// fragment of the transpose of a [k][col] tile: col c0 + lane mod 32, k = k0 + 8 (lane / 32) .. +7,
+// from two transposing reads (each 16-lane group reads 4 rows x 16 columns; lane j gets column j)
+template <int HD>
+__device__ __forceinline__ bf16x8 frag_cols(const bf16* T, int c0, int k0) {
+  const int l = threadIdx.x % 64, g = l / 16, i = l % 16;
+  const int c = c0 + 16 * (g & 1) + 4 * (i & 3);
+  const int k = k0 + 8 * (g >> 1) + (i >> 2);
+  typedef __attribute__((address_space(3))) v4i16_t lds_v4i16;
+  const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(T + tidx<HD>(k, c)));
+  const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(T + tidx<HD>(k + 4, c)));
+  bf16x8 f;
+  __builtin_memcpy(&f, &lo, 8);
+  __builtin_memcpy(reinterpret_cast<char*>(&f) + 8, &hi, 8);
+  return f;
+}
+
+// gfx950 v_permlane32_swap(X, Y) exchanges lanes 32..63 of X with lanes 0..31 of Y (no LDS trip).
+__device__ __forceinline__ void swap32(uint32_t& x, uint32_t& y) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, y, false, false);
+  x = r[0];
+  y = r[1];
+}
+// v combined with the value of lane l ^ 32: after swap32(a, a) the two results are v and the
+// partner's value in some order, so a commutative op of the two gives the same value on both lanes
+__device__ __forceinline__ float pair_max(float v) {
+  uint32_t a = __float_as_uint(v), b = a;
+  swap32(a, b);
+  return fmaxf(__uint_as_float(a), __uint_as_float(b));
+}
+__device__ __forceinline__ float pair_sum(float v) {
+  uint32_t a = __float_as_uint(v), b = a;
+  swap32(a, b);
+  return __uint_as_float(a) + __uint_as_float(b);
 }
 
 // B operand (8 consecutive k at column lane mod 32) from a 32x32 accumulator whose rows are the k
 // index, for the 16-row group starting at accumulator index ib (0 or 8).  Lane half h holds rows
-// ib+4h..ib+4h+3 of the group; the operand wants rows 8h..8h+7, so each half keeps its own four and
-// takes the other four from its partner lane (l ^ 32).  All accumulator indices are compile-time
-// constants; the half selects between two packed candidates.
+// ib+4h..ib+4h+3 of the group; the operand wants rows 8h..8h+7: half 0 needs its own rows ib..ib+3
+// then its partner's, half 1 its partner's rows ib+4..ib+7 then its own.  Swapping the packed lower
+// pair (lanes 32..63) with the packed upper pair (lanes 0..31) leaves exactly that in every lane:
+// the first word of each swap is the operand's first half, the second word its second half.
 template <int IB>
-__device__ __forceinline__ bf16x8 acc_rows_to_b(const f32x16& s, int half) {
-  const uint32_t lo0 = pack2(s[IB + 0], s[IB + 1]), lo1 = pack2(s[IB + 2], s[IB + 3]);
-  const uint32_t hi0 = pack2(s[IB + 4], s[IB + 5]), hi1 = pack2(s[IB + 6], s[IB + 7]);
-  const bool h = half != 0;
-  const uint32_t own0 = h ? hi0 : lo0, own1 = h ? hi1 : lo1;
-  const uint32_t rcv0 = __shfl_xor(h ? lo0 : hi0, 32, 64);
-  const uint32_t rcv1 = __shfl_xor(h ? lo1 : hi1, 32, 64);
-  uint32_t pw[4];
-  pw[0] = h ? rcv0 : own0;
-  pw[1] = h ? rcv1 : own1;
-  pw[2] = h ? own0 : rcv0;
-  pw[3] = h ? own1 : rcv1;
+__device__ __forceinline__ bf16x8 acc_rows_to_b(const f32x16& s) {
+  uint32_t lo0 = pack2(s[IB + 0], s[IB + 1]), lo1 = pack2(s[IB + 2], s[IB + 3]);
+  uint32_t hi0 = pack2(s[IB + 4], s[IB + 5]), hi1 = pack2(s[IB + 6], s[IB + 7]);
+  swap32(lo0, hi0);
+  swap32(lo1, hi1);
+  const uint32_t pw[4] = {lo0, lo1, hi0, hi1};
   bf16x8 r;
   __builtin_memcpy(&r, pw, 16);
   return r;
@@ -65,9 +116,9 @@ __device__ __forceinline__ bf16x8 acc_rows_to_b(const f32x16& s, int half) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// KB rows x HD of a head (row stride ld) through registers into an LDS tile of pitch P;
-// rows at or beyond S are zero.
-template <int HD, int P>
+// KB rows x HD of a head (row stride ld) through registers into a swizzled LDS tile; rows at or
+// beyond S are zero.
+template <int HD>
 struct RowTile {
   static constexpr int PER = KB * HD / 8 / NT;
   static constexpr int PERR = PER > 0 ? PER : 1;
@@ -86,7 +137,7 @@ struct RowTile {
     for (int p = 0; p < PERR; ++p) {
       const int c = threadIdx.x + p * NT;
       if (PER > 0 || c < KB * HD / 8)
-        *reinterpret_cast<u32x4*>(T + (c / (HD / 8)) * P + (c % (HD / 8)) * 8) = r[p];
+        *reinterpret_cast<u32x4*>(T + tidx<HD>(c / (HD / 8), (c % (HD / 8)) * 8)) = r[p];
     }
   }
 };
@@ -135,8 +186,7 @@ __device__ __forceinline__ void store_rows_from_t(float* __restrict__ stage, con
 
 template <int HD>
 struct Lds {
-  static constexpr int P = HD + 8;       // tile pitch (elements)
-  static constexpr int TSZ = KB * P;     // one [KB][HD] tile
+  static constexpr int TSZ = KB * HD;    // one [KB][HD] tile
   static constexpr size_t out_bytes = (size_t)QB * (HD + 4) * 4;  // fp32 output staging
   static constexpr size_t fwd_bytes() { const size_t t = (size_t)4 * TSZ * 2; return t > out_bytes ? t : out_bytes; }
   static constexpr size_t dq_bytes() { return fwd_bytes(); }
@@ -150,10 +200,10 @@ struct Lds {
 template <int HD>
 __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
   using L = Lds<HD>;
-  constexpr int P = L::P, KS = HD / 16, DT = HD / 32;
+  constexpr int KS = HD / 16, DT = HD / 32;
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16* Ks0 = reinterpret_cast<bf16*>(smem);   // [2][KB][P]
-  bf16* Vs0 = Ks0 + 2 * L::TSZ;                // [2][KB][P]
+  bf16* Ks0 = reinterpret_cast<bf16*>(smem);   // [2][KB][HD], swizzled
+  bf16* Vs0 = Ks0 + 2 * L::TSZ;                // [2][KB][HD], swizzled
 
   const int nqb = (a.S + QB - 1) / QB;
   const int qb = nqb - 1 - blockIdx.x;
@@ -181,7 +231,7 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
   float m = -INFINITY, lsum = 0.f;
 
   const int nkb = min(a.S - 1, qb * QB + QB - 1) / KB + 1;
-  RowTile<HD, P> tk, tv;
+  RowTile<HD> tk, tv;
   tk.load(kbase, ld, 0, a.S);
   tv.load(vbase, ld, 0, a.S);
   tk.store(Ks0);
@@ -204,7 +254,7 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
         for (int e = 0; e < 16; ++e) s[t][e] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows(Ks, P, t * 32, ks * 16), qf[ks], s[t], 0, 0, 0);
+          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s[t], 0, 0, 0);
       }
       float bm = -INFINITY;
       const bool diag = key0 + KB - 1 > q0;
@@ -217,7 +267,7 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
           s[t][e] = v;
           bm = fmaxf(bm, v);
         }
-      bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+      bm = pair_max(bm);
       const float mn = fmaxf(m, bm);  // every query of the wave sees key0 here, so mn is finite
       const float corr = (m == -INFINITY) ? 0.f : fast_exp2(m - mn);
       float rs = 0.f;
@@ -229,7 +279,7 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
           s[t][e] = p;
           rs += p;
         }
-      rs += __shfl_xor(rs, 32, 64);
+      rs = pair_sum(rs);
       lsum = lsum * corr + rs;
       m = mn;
       if (__any(corr != 1.0f)) {  // the running maximum moved for some query of the wave
@@ -240,10 +290,10 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
       }
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 pf = (kk % 2) ? acc_rows_to_b<8>(s[kk / 2], half) : acc_rows_to_b<0>(s[kk / 2], half);
+        const bf16x8 pf = (kk % 2) ? acc_rows_to_b<8>(s[kk / 2]) : acc_rows_to_b<0>(s[kk / 2]);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr(Vs, P, dt * 32, kk * 16), pf, o[dt], 0, 0, 0);
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Vs, dt * 32, kk * 16), pf, o[dt], 0, 0, 0);
       }
     }
     if (kb + 1 < nkb) {
@@ -263,7 +313,7 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
 template <int HD>
 __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
   using L = Lds<HD>;
-  constexpr int P = L::P, KS = HD / 16, DT = HD / 32;
+  constexpr int KS = HD / 16, DT = HD / 32;
   extern __shared__ __align__(16) unsigned char smem[];
   bf16* Ks0 = reinterpret_cast<bf16*>(smem);
   bf16* Vs0 = Ks0 + 2 * L::TSZ;
@@ -297,7 +347,7 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) dq[dt][e] = 0.f;
   const int nkb = min(a.S - 1, qb * QB + QB - 1) / KB + 1;
-  RowTile<HD, P> tk, tv;
+  RowTile<HD> tk, tv;
   tk.load(kbase, ld, 0, a.S);
   tv.load(vbase, ld, 0, a.S);
   tk.store(Ks0);
@@ -320,8 +370,8 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
         for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows(Ks, P, t * 32, ks * 16), qf[ks], s, 0, 0, 0);
-          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows(Vs, P, t * 32, ks * 16), df[ks], dp, 0, 0, 0);
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Vs, t * 32, ks * 16), df[ks], dp, 0, 0, 0);
         }
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
@@ -331,10 +381,10 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
         }
 #pragma unroll
         for (int g2 = 0; g2 < 2; ++g2) {
-          const bf16x8 bop = g2 ? acc_rows_to_b<8>(s, half) : acc_rows_to_b<0>(s, half);
+          const bf16x8 bop = g2 ? acc_rows_to_b<8>(s) : acc_rows_to_b<0>(s);
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
-            dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr(Ks, P, dt * 32, t * 32 + g2 * 16), bop, dq[dt], 0, 0, 0);
+            dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Ks, dt * 32, t * 32 + g2 * 16), bop, dq[dt], 0, 0, 0);
         }
       }
     }
@@ -352,10 +402,10 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
 template <int HD>
 __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
   using L = Lds<HD>;
-  constexpr int P = L::P, KS = HD / 16, DT = HD / 32;
+  constexpr int KS = HD / 16, DT = HD / 32;
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16* Qs0 = reinterpret_cast<bf16*>(smem);   // [2][KB][P]
-  bf16* Ds0 = Qs0 + 2 * L::TSZ;                // [2][KB][P]
+  bf16* Qs0 = reinterpret_cast<bf16*>(smem);   // [2][KB][HD], swizzled
+  bf16* Ds0 = Qs0 + 2 * L::TSZ;                // [2][KB][HD], swizzled
   float* Ls0 = reinterpret_cast<float*>(Ds0 + 2 * L::TSZ);  // [2][KB]
   float* Dl0 = Ls0 + 2 * KB;                                 // [2][KB]
   const int kbk = blockIdx.x;  // block of 128 keys; low blocks see the most queries and go first
@@ -387,7 +437,7 @@ __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
   const int nqblk = (a.S + KB - 1) / KB;
   const int per_head = nqblk - qblk0;
   const int nit = group * per_head;
-  RowTile<HD, P> tq, td;
+  RowTile<HD> tq, td;
   float lv = 0.f, dv1 = 0.f;
   auto fetch = [&](int it) {
     const int h = kvh * group + it / per_head, qs0 = (qblk0 + it % per_head) * KB;
@@ -426,8 +476,8 @@ __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
       for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows(Qs, P, t * 32, ks * 16), kf[ks], s, 0, 0, 0);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows(Ds, P, t * 32, ks * 16), vf[ks], dp, 0, 0, 0);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Qs, t * 32, ks * 16), kf[ks], s, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ds, t * 32, ks * 16), vf[ks], dp, 0, 0, 0);
       }
       // accumulator rows of this lane: t*32 + 8 (e/4) + 4 half + (e mod 4): four runs of 4
       // consecutive query rows, so lse and delta arrive as 16-byte reads
@@ -446,12 +496,12 @@ __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
       }
 #pragma unroll
       for (int g2 = 0; g2 < 2; ++g2) {
-        const bf16x8 pb = g2 ? acc_rows_to_b<8>(s, half) : acc_rows_to_b<0>(s, half);
-        const bf16x8 sb = g2 ? acc_rows_to_b<8>(dp, half) : acc_rows_to_b<0>(dp, half);
+        const bf16x8 pb = g2 ? acc_rows_to_b<8>(s) : acc_rows_to_b<0>(s);
+        const bf16x8 sb = g2 ? acc_rows_to_b<8>(dp) : acc_rows_to_b<0>(dp);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr(Ds, P, dt * 32, t * 32 + g2 * 16), pb, dv[dt], 0, 0, 0);
-          dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_tr(Qs, P, dt * 32, t * 32 + g2 * 16), sb, dk[dt], 0, 0, 0);
+          dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Ds, dt * 32, t * 32 + g2 * 16), pb, dv[dt], 0, 0, 0);
+          dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Qs, dt * 32, t * 32 + g2 * 16), sb, dk[dt], 0, 0, 0);
         }
       }
     }
