@@ -29,12 +29,14 @@ constexpr int NT = 256;   // 4 waves
 constexpr float LOG2E = 1.4426950408889634f;
 
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// two floats -> two RNE bf16 in one dword (a in the low half): one v_cvt_pk_bf16_f32
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-  bf16 x = (bf16)a, y = (bf16)b;
-  uint16_t u, v;
-  __builtin_memcpy(&u, &x, 2);
-  __builtin_memcpy(&v, &y, 2);
-  return (uint32_t)u | ((uint32_t)v << 16);
+  const bf16x2 v = __builtin_convertvector((f32x2){a, b}, bf16x2);
+  uint32_t u;
+  __builtin_memcpy(&u, &v, 4);
+  return u;
 }
 
 // Chunk permutation of tile row r (HD/8 chunks of 16 bytes per row):
@@ -256,33 +258,39 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
         for (int ks = 0; ks < KS; ++ks)
           s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s[t], 0, 0, 0);
       }
+      // row maximum of the raw scores (the scale is positive), masked on the diagonal block
       float bm = -INFINITY;
-      const bool diag = key0 + KB - 1 > q0;
+      if (key0 + KB - 1 > q0) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4) > myq) s[t][e] = -INFINITY;
+      }
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float v = s[t][e] * sl2;
-          if (diag && key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4) > myq) v = -INFINITY;
-          s[t][e] = v;
-          bm = fmaxf(bm, v);
-        }
-      bm = pair_max(bm);
-      const float mn = fmaxf(m, bm);  // every query of the wave sees key0 here, so mn is finite
-      const float corr = (m == -INFINITY) ? 0.f : fast_exp2(m - mn);
+        for (int e = 0; e < 16; ++e) bm = fmaxf(bm, s[t][e]);
+      bm = pair_max(bm) * sl2;  // every query of the wave sees key0 here, so bm is finite
+      // Lazy maximum: m (log2 units) moves only when a score exceeds it by more than 8, so
+      // p = 2^(s sl2 - m) <= 256 and O is rescaled only when some row's maximum jumps; O / l and
+      // lse = m + log2(l) do not depend on which m was used.
+      const bool move = bm > m + 8.0f;
+      const float mn = move ? bm : m;
+      const float corr = (m == -INFINITY) ? 0.f : fast_exp2(m - mn);  // 1 when m stays
       float rs = 0.f;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const float p = fast_exp2(s[t][e] - mn);
+          const float p = fast_exp2(__builtin_fmaf(s[t][e], sl2, -mn));
           s[t][e] = p;
           rs += p;
         }
       rs = pair_sum(rs);
       lsum = lsum * corr + rs;
       m = mn;
-      if (__any(corr != 1.0f)) {  // the running maximum moved for some query of the wave
+      if (__any(move)) {  // some query of the wave moved its maximum
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -373,11 +381,18 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
           s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s, 0, 0, 0);
           dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Vs, t * 32, ks * 16), df[ks], dp, 0, 0, 0);
         }
+        // every key of the sub-tile is visible to every query: no mask (head dim 64 only; at 128
+        // the second code path costs the kernel its spill-free register budget)
+        if (HD == 64 && key0 + t * 32 + 31 <= q0) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4);
-          const float p = key <= myq ? fast_exp2(s[e] * sl2 - lse2) : 0.f;
-          s[e] = p * (dp[e] - dl);
+          for (int e = 0; e < 16; ++e) s[e] = fast_exp2(__builtin_fmaf(s[e], sl2, -lse2)) * (dp[e] - dl);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int key = key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4);
+            const float p = key <= myq ? fast_exp2(__builtin_fmaf(s[e], sl2, -lse2)) : 0.f;
+            s[e] = p * (dp[e] - dl);
+          }
         }
 #pragma unroll
         for (int g2 = 0; g2 < 2; ++g2) {
@@ -481,17 +496,30 @@ __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
       }
       // accumulator rows of this lane: t*32 + 8 (e/4) + 4 half + (e mod 4): four runs of 4
       // consecutive query rows, so lse and delta arrive as 16-byte reads
+      // every query of the sub-tile sees every key of the wave and exists: no mask (head dim 64
+      // only, as in the dQ kernel)
+      const bool full = HD == 64 && q0t >= k0 + 31 && q0t + 31 < a.S;
 #pragma unroll
       for (int e4 = 0; e4 < 4; ++e4) {
         const int r0 = t * 32 + 8 * e4 + 4 * half;
         const f32x4 l4 = *reinterpret_cast<const f32x4*>(Ls + r0);
         const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + r0);
+        if (full) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int e = 4 * e4 + j, q = qs0 + r0 + j;
-          const float p = (q >= mykey && q < a.S) ? fast_exp2(s[e] * sl2 - l4[j]) : 0.f;
-          s[e] = p;
-          dp[e] = p * (dp[e] - d4[j]);
+          for (int j = 0; j < 4; ++j) {
+            const int e = 4 * e4 + j;
+            const float p = fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j]));
+            s[e] = p;
+            dp[e] = p * (dp[e] - d4[j]);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int e = 4 * e4 + j, q = qs0 + r0 + j;
+            const float p = (q >= mykey && q < a.S) ? fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j])) : 0.f;
+            s[e] = p;
+            dp[e] = p * (dp[e] - d4[j]);
+          }
         }
       }
 #pragma unroll
