@@ -66,6 +66,12 @@ struct stage {
   hipStream_t ust = nullptr;
   hipEvent_t ev_bwd[2] = {nullptr, nullptr}, ev_upd = nullptr, ev_now = nullptr;
   bool ev_bwd_set[2] = {false, false};
+  // The weight-gradient products (fp32 output) of a backward run on a second stream of their own,
+  // beside the activation-gradient chain: ev_m2s orders one after the stage stream's work so far,
+  // ev_wg[k] marks the end of the last product of kind k (the stage stream waits on it before it
+  // overwrites a buffer that product reads), ev_wjoin joins the stream back at the end.
+  hipStream_t wst = nullptr;
+  hipEvent_t ev_m2s = nullptr, ev_wjoin = nullptr, ev_wg[5] = {};
   bool bf;
   size_t esz;  // bytes per compute element
   int T, qkvw, hqd;
@@ -150,10 +156,34 @@ void timed(stage* S, int cls, double work, F&& launch, hipStream_t on = nullptr)
   }
 }
 
+// activation products on the stage stream (no split-K: the workspace belongs to the
+// weight-gradient stream)
 void run_gemm(stage* S, GemmArgs g) {
+  g.ws = nullptr;
+  g.ws_elems = 0;
+  timed(S, STAGE_PROF_GEMM, 2.0 * g.M * g.N * g.K, [&] { launch_gemm(S->bf, g, S->st); });
+}
+
+enum { WG_DOWN = 0, WG_GU = 1, WG_O = 2, WG_QKV = 3, WG_HEAD = 4 };
+
+// weight-gradient product of kind k on the weight-gradient stream, after everything enqueued on
+// the stage stream so far (its inputs)
+void run_wgrad(stage* S, GemmArgs g, int k) {
+  (void)hipEventRecord(S->ev_m2s, S->st);
+  (void)hipStreamWaitEvent(S->wst, S->ev_m2s, 0);
   g.ws = S->gemm_ws;
   g.ws_elems = S->gemm_ws ? GEMM_WS_ELEMS : 0;
-  timed(S, STAGE_PROF_GEMM, 2.0 * g.M * g.N * g.K, [&] { launch_gemm(S->bf, g, S->st); });
+  timed(S, STAGE_PROF_GEMM, 2.0 * g.M * g.N * g.K, [&] { launch_gemm(S->bf, g, S->wst); }, S->wst);
+  (void)hipEventRecord(S->ev_wg[k], S->wst);
+}
+
+// the stage stream waits for the last weight-gradient product of kind k (and, the stream being in
+// order, for every product issued before it)
+void after_wgrad(stage* S, int k) { (void)hipStreamWaitEvent(S->st, S->ev_wg[k], 0); }
+
+void join_wgrad(stage* S) {
+  (void)hipEventRecord(S->ev_wjoin, S->wst);
+  (void)hipStreamWaitEvent(S->st, S->ev_wjoin, 0);
 }
 
 double attn_fwd_flops(const stage* S) {  // QK^T and PV over the causal triangle
@@ -377,30 +407,36 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   const bool bf = S->bf;
   const float beta = first ? 0.f : 1.f;
   hipStream_t st = S->st;
+  // The weight gradients dW (+)= dY^T X run on the weight-gradient stream; before this stream
+  // overwrites dgu, dh, dqkv or the previous block's dy, it waits for the product that read it.
   // down projection: dz = dy Wd with the SwiGLU backward in its epilogue (-> dgate | dup);
   // dWd (+)= dy^T z
   GemmArgs gz = gemm(T, f, d, dy, d, true, S->wptr(vi, w.wdown), f, false, S->dgu, 2 * f);
   gz.epi = 1;
   gz.aux = b.gu;
   gz.ld_aux = 2 * f;
+  after_wgrad(S, WG_GU);
   run_gemm(S, gz);
-  run_gemm(S, gemm(d, f, T, dy, d, false, b.z, f, false, g + w.wdown, f, true, beta));
+  run_wgrad(S, gemm(d, f, T, dy, d, false, b.z, f, false, g + w.wdown, f, true, beta), WG_DOWN);
   // gate/up: dn2 = dgu Wgu ; dWgu (+)= dgu^T n2
   run_gemm(S, gemm(T, d, 2 * f, S->dgu, 2 * f, true, S->wptr(vi, w.wgu), d, false, S->dn, d));
-  run_gemm(S, gemm(2 * f, d, T, S->dgu, 2 * f, false, b.n2, d, false, g + w.wgu, d, true, beta));
+  run_wgrad(S, gemm(2 * f, d, T, S->dgu, 2 * f, false, b.n2, d, false, g + w.wgu, d, true, beta), WG_GU);
+  after_wgrad(S, WG_O);
   int np = launch_rmsnorm_bwd(bf, S->dn, b.h, b.rstd2, S->wptr(vi, w.ffn_norm), dy, S->dh, S->rms_part, T, d, st);
   launch_colsum_partials(S->rms_part, np, d, g + w.ffn_norm, !first, st);
   // output projection: do = dh Wo ; dWo (+)= dh^T o
   run_gemm(S, gemm(T, S->hqd, d, S->dh, d, true, S->wptr(vi, w.wo), S->hqd, false, S->do_, S->hqd));
-  run_gemm(S, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta));
+  run_wgrad(S, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta), WG_O);
   AttnArgs a = attn_args(S, b);
   a.dout = S->do_; a.dqkv = S->dqkv; a.delta = S->delta;
   a.rope_cos = S->cos_t;  // dq, dk come back w.r.t. the unrotated projections
   a.rope_sin = S->sin_t;
+  after_wgrad(S, WG_QKV);
   timed(S, STAGE_PROF_ATTN_BWD, 2.0 * attn_fwd_flops(S), [&] { launch_attention_bwd(bf, a, st); });
   // qkv projection: dn1 = dqkv Wqkv ; dWqkv (+)= dqkv^T n1
   run_gemm(S, gemm(T, d, S->qkvw, S->dqkv, S->qkvw, true, S->wptr(vi, w.wqkv), d, false, S->dn, d));
-  run_gemm(S, gemm(S->qkvw, d, T, S->dqkv, S->qkvw, false, b.n1, d, false, g + w.wqkv, d, true, beta));
+  run_wgrad(S, gemm(S->qkvw, d, T, S->dqkv, S->qkvw, false, b.n1, d, false, g + w.wqkv, d, true, beta), WG_QKV);
+  after_wgrad(S, WG_DOWN);  // dx is the buffer the next-higher block's down-projection product read
   np = launch_rmsnorm_bwd(bf, S->dn, b.x, b.rstd1, S->wptr(vi, w.attn_norm), S->dh, dx, S->rms_part, T, d, st);
   launch_colsum_partials(S->rms_part, np, d, g + w.attn_norm, !first, st);
 }
@@ -442,6 +478,10 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
   register_tensors(S);
   {
     hipError_t e = hipStreamCreateWithFlags(&S->ust, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&S->wst, hipStreamNonBlocking);
+    for (int k = 0; k < 5 && e == hipSuccess; ++k) e = hipEventCreateWithFlags(&S->ev_wg[k], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_m2s, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_wjoin, hipEventDisableTiming);
     for (int k = 0; k < 2 && e == hipSuccess; ++k) e = hipEventCreateWithFlags(&S->ev_bwd[k], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_upd, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_now, hipEventDisableTiming);
@@ -586,8 +626,8 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
     // dhf = dlogits E ; dE (+)= dlogits^T hf
     run_gemm(s, gemm(T, d, sh.vocab, s->dlog, sh.vocab, true, s->wptr(vi, s->off_embed), d, false,
                          s->dhf, d));
-    run_gemm(s, gemm(sh.vocab, d, T, s->dlog, sh.vocab, false, sl.hf, d, false, g + s->off_embed, d,
-                         true, first ? 0.f : 1.f));
+    run_wgrad(s, gemm(sh.vocab, d, T, s->dlog, sh.vocab, false, sl.hf, d, false, g + s->off_embed, d,
+                          true, first ? 0.f : 1.f), WG_HEAD);
     head_wrote_embed = true;
     const int np = launch_rmsnorm_bwd(bf, s->dhf, sl.y, sl.rstdf, s->wptr(vi, s->off_final), nullptr, s->dA,
                                        s->rms_part, T, d, st);
@@ -599,6 +639,7 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
     block_backward(s, vi, sl.blk[i], s->boff[i], cur, out, g, first);
     cur = out;
   }
+  join_wgrad(s);  // every weight gradient is in g (the scatter below may add to the tied head's)
   if (sh.first_stage) {
     const void* dx0 = cur;
     launch_token_sort(sl.tokens, T, sh.vocab, s->sorted, st);
@@ -775,11 +816,14 @@ void stage_destroy(stage_t* s) {
   if (!s) return;
   (void)hipStreamSynchronize(s->st);
   if (s->ust) (void)hipStreamSynchronize(s->ust);
+  if (s->wst) (void)hipStreamSynchronize(s->wst);
   for (auto& r : s->prof_pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
   for (auto e : s->prof_free) (void)hipEventDestroy(e);
-  for (hipEvent_t e : {s->ev_bwd[0], s->ev_bwd[1], s->ev_upd, s->ev_now})
+  for (hipEvent_t e : {s->ev_bwd[0], s->ev_bwd[1], s->ev_upd, s->ev_now, s->ev_m2s, s->ev_wjoin, s->ev_wg[0],
+                      s->ev_wg[1], s->ev_wg[2], s->ev_wg[3], s->ev_wg[4]})
     if (e) (void)hipEventDestroy(e);
   if (s->ust) (void)hipStreamDestroy(s->ust);
+  if (s->wst) (void)hipStreamDestroy(s->wst);
   delete s;
 }
 
