@@ -20,6 +20,7 @@
 // LDS as 16-byte rows.  Query blocks with the longest causal range are scheduled first.
 #include "common.h"
 #include "kernels.h"
+#include <algorithm>
 
 namespace {
 
@@ -319,15 +320,15 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
 
 // ------------------------------------------------------------------------------------------ dQ
 template <int HD>
-__global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
+__device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, int bz,
+    unsigned char* __restrict__ smem) {
   using L = Lds<HD>;
   constexpr int KS = HD / 16, DT = HD / 32;
-  extern __shared__ __align__(16) unsigned char smem[];
   bf16* Ks0 = reinterpret_cast<bf16*>(smem);
   bf16* Vs0 = Ks0 + 2 * L::TSZ;
   const int nqb = (a.S + QB - 1) / QB;
-  const int qb = nqb - 1 - blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  const int qb = nqb - 1 - bx;
+  const int h = by, b = bz;
   const int kvh = h / (a.Hq / a.Hkv);
   const int ld = (a.Hq + 2 * a.Hkv) * HD, hqd = a.Hq * HD;
   const bf16* base = (const bf16*)a.qkv + (int64_t)b * a.S * ld;
@@ -413,18 +414,24 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
                         (bf16*)a.dqkv + (int64_t)b * a.S * ld + h * HD, ld, qb * QB, a.S, a.rope_cos, a.rope_sin);
 }
 
+template <int HD>
+__global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  bwd_dq_block<HD>(a, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+}
+
 // ------------------------------------------------------------------------------------------ dK, dV
 template <int HD>
-__global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
+__device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by, int bz,
+    unsigned char* __restrict__ smem) {
   using L = Lds<HD>;
   constexpr int KS = HD / 16, DT = HD / 32;
-  extern __shared__ __align__(16) unsigned char smem[];
   bf16* Qs0 = reinterpret_cast<bf16*>(smem);   // [2][KB][HD], swizzled
   bf16* Ds0 = Qs0 + 2 * L::TSZ;                // [2][KB][HD], swizzled
   float* Ls0 = reinterpret_cast<float*>(Ds0 + 2 * L::TSZ);  // [2][KB]
   float* Dl0 = Ls0 + 2 * KB;                                 // [2][KB]
-  const int kbk = blockIdx.x;  // block of 128 keys; low blocks see the most queries and go first
-  const int kvh = blockIdx.y, b = blockIdx.z;
+  const int kbk = bx;  // block of 128 keys; low blocks see the most queries and go first
+  const int kvh = by, b = bz;
   const int group = a.Hq / a.Hkv;
   const int ld = (a.Hq + 2 * a.Hkv) * HD, hqd = a.Hq * HD;
   const bf16* base = (const bf16*)a.qkv + (int64_t)b * a.S * ld;
@@ -543,6 +550,29 @@ __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
                         a.S);
 }
 
+template <int HD>
+__global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  bwd_dkv_block<HD>(a, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+}
+
+// dQ and dK/dV work items in one launch (independent given delta): the dQ items (query blocks x
+// query heads x batch, heaviest first within each head) then the dK/dV items, so the two fill the
+// CUs together instead of each leaving a tail.
+template <int HD>
+__global__ void __launch_bounds__(NT) flash_bwd_fused(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int nb = (a.S + QB - 1) / QB;
+  const int n_dq = nb * a.Hq * a.B;
+  int i = blockIdx.x;
+  if (i < n_dq) {
+    bwd_dq_block<HD>(a, i % nb, (i / nb) % a.Hq, i / (nb * a.Hq), smem);
+  } else {
+    i -= n_dq;
+    bwd_dkv_block<HD>(a, i % nb, (i / nb) % a.Hkv, i / (nb * a.Hkv), smem);
+  }
+}
+
 // delta[b, h, i] = sum_d dO[b, i, h, d] O[b, i, h, d]; one thread per (token, head)
 template <int HD>
 __global__ void __launch_bounds__(256) flash_delta(AttnArgs a) {
@@ -585,8 +615,17 @@ void bwd_launch(const AttnArgs& a, hipStream_t st) {
     attr = true;
   }
   flash_delta<HD><<<(unsigned)cdiv((int64_t)a.B * a.S * a.Hq, 256), 256, 0, st>>>(a);
-  flash_bwd_dq<HD><<<dim3((unsigned)cdiv(a.S, QB), a.Hq, a.B), NT, Lds<HD>::dq_bytes(), st>>>(a);
-  flash_bwd_dkv<HD><<<dim3((unsigned)cdiv(a.S, QB), a.Hkv, a.B), NT, Lds<HD>::dkv_bytes(), st>>>(a);
+  if constexpr (HD == 64) {
+    // one launch for both (at head dim 128 the dK/dV register budget would halve dQ's occupancy)
+    static bool fattr = false;
+    const size_t bytes = std::max(Lds<HD>::dq_bytes(), Lds<HD>::dkv_bytes());
+    if (!fattr) { set_lds(flash_bwd_fused<HD>, bytes); fattr = true; }
+    const int nb = (int)cdiv(a.S, QB);
+    flash_bwd_fused<HD><<<(unsigned)(nb * (a.Hq + a.Hkv) * a.B), NT, bytes, st>>>(a);
+  } else {
+    flash_bwd_dq<HD><<<dim3((unsigned)cdiv(a.S, QB), a.Hq, a.B), NT, Lds<HD>::dq_bytes(), st>>>(a);
+    flash_bwd_dkv<HD><<<dim3((unsigned)cdiv(a.S, QB), a.Hkv, a.B), NT, Lds<HD>::dkv_bytes(), st>>>(a);
+  }
 }
 
 }  // namespace
