@@ -613,18 +613,19 @@ bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   GemmArgs g = g0;
   g.ksplit = 1;
   const int64_t mn = (int64_t)g.M * g.N;
-  constexpr int DK = 32;  // k-slice of the direct-to-LDS kernels
-  // Full tiles go to the direct-to-LDS kernels: 256 x 256 (8 waves of 64 x 128) when the product
-  // has enough of them (or is deep enough to amortise them), else 128 x 128; ragged shapes to the
-  // register-staged kernel with bounds-checked loads.
-  const bool full128 = g.M % 128 == 0 && g.N % 128 == 0 && g.K % DK == 0;
+  // Full tiles go to the direct-to-LDS kernels: 256 x 256 (8 waves of 64 x 128, 32-deep slices in
+  // 4 stages) when the product has enough of them (or is deep enough to amortise them), else
+  // 128 x 128 (4 waves, 64-deep slices in 2 stages: half the barriers per MFMA, two blocks per CU);
+  // ragged shapes to the register-staged kernel with bounds-checked loads.
+  constexpr int DKB = 32, DKS = 64;
+  const bool full128 = g.M % 128 == 0 && g.N % 128 == 0 && g.K % DKS == 0;
   const int64_t t256 = cdiv(g.M, 256) * cdiv(g.N, 256), t128 = cdiv(g.M, 128) * cdiv(g.N, 128);
-  const bool big = g.M % 256 == 0 && g.N % 256 == 0 && g.K % DK == 0 &&
+  const bool big = g.M % 256 == 0 && g.N % 256 == 0 && g.K % DKB == 0 &&
                    (t256 >= 512 || (t256 >= 256 && g.K >= 2048));
   const int64_t tiles = big ? t256 : t128;
   if (g.out_f32 && g.ws && g.ldc == g.N && tiles < 512 && g.K >= 2048) {
     // deterministic split-K for underfilled fp32-output products: whole slices per split
-    const int kq = full128 ? DK : BK;
+    const int kq = big ? DKB : (full128 ? DKS : BK);
     int s = (int)std::min<int64_t>(8, cdiv(512, tiles));
     while (s > 1 && (s * mn > g.ws_elems || g.K / s < 512 || (g.K / kq) % s)) --s;
     g.ksplit = s;
@@ -635,11 +636,11 @@ bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   if (rope_after) g.epi = 0;
   bool done = false;  // the direct-to-LDS launchers decline shapes they do not take (K = 0)
   if (big)
-    done = g.out_f32 ? launch_dma_cfg<256, 256, 64, 128, float, DK, 4>(g, st)
-                     : launch_dma_cfg<256, 256, 64, 128, bf16, DK, 4>(g, st);
+    done = g.out_f32 ? launch_dma_cfg<256, 256, 64, 128, float, DKB, 4>(g, st)
+                     : launch_dma_cfg<256, 256, 64, 128, bf16, DKB, 4>(g, st);
   else if (full128)
-    done = g.out_f32 ? launch_dma_cfg<128, 128, 64, 64, float, DK, 4>(g, st)
-                     : launch_dma_cfg<128, 128, 64, 64, bf16, DK, 4>(g, st);
+    done = g.out_f32 ? launch_dma_cfg<128, 128, 64, 64, float, DKS, 2>(g, st)
+                     : launch_dma_cfg<128, 128, 64, 64, bf16, DKS, 2>(g, st);
   if (!done) {
     if (g.out_f32) launch_cfg<128, 128, 64, 64, float>(g, st);
     else launch_cfg<128, 128, 64, 64, bf16>(g, st);
