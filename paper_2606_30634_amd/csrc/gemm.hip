@@ -109,6 +109,14 @@ void launch_gemm_tiled(bool bf, const GemmArgs& g, hipStream_t st) {
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st) {
   if (g.M == 0 || g.N == 0) return;
   if (bf && gemm_mfma_try(g, st)) return;
+  if (g.epi == 3) {  // the reference tiling writes gate|up, then the SwiGLU kernel makes z
+    GemmArgs p = g;
+    p.epi = 0;
+    p.glu = 0;
+    launch_gemm_tiled(bf, p, st);
+    launch_swiglu_fwd(bf, g.C, g.out2, g.M, g.glu, st);
+    return;
+  }
   if (g.epi == 2) {  // the reference tiling writes the products, then the rotation runs
     GemmArgs p = g;
     p.epi = 0;

@@ -202,6 +202,22 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[W
           }
           *reinterpret_cast<bf16x8*>((bf16*)C + o) = da;
           *reinterpret_cast<bf16x8*>((bf16*)C + o + g.N) = db;
+        } else if (g.epi == 3) {  // SwiGLU forward: panel column col is gate or up of z column zc
+          const int grp = col / 32, zc = (grp / 2) * 32 + col % 32;
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
+          bf16* Cb = (bf16*)C + (int64_t)row * g.ldc;
+          if ((grp & 1) == 0) {
+            *reinterpret_cast<bf16x8*>(Cb + zc) = ov;
+            const float* up = stg + r * EP + cc + 32;  // the up values of the same z columns
+            bf16x8 zv;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) zv[q] = (bf16)(v[q] / (1.0f + __expf(-v[q])) * up[q]);
+            *reinterpret_cast<bf16x8*>((bf16*)g.out2 + (int64_t)row * g.ld_out2 + zc) = zv;
+          } else {
+            *reinterpret_cast<bf16x8*>(Cb + g.glu + zc) = ov;
+          }
         } else if (g.epi == 2 && col < g.rope_cols) {  // RoPE on the fp32 products
           const int hd = g.rope_hd, hh = hd / 2;
           const int c = col % hd, i0 = c % hh;
@@ -353,6 +369,12 @@ struct DmaTile {
   static constexpr int ELEMS = ROWS * BKT;
   static_assert(CHUNKS % NT == 0, "tile does not split evenly over the threads");
   static_assert(KMAJ || ROWS >= 128, "row-contiguous swizzle needs 256-byte k-rows");
+  // k-contiguous tile: the row and the 8-element k chunk whose data LDS chunk p holds
+  __device__ static void row_chunk(int p, int& r, int& kc) {
+    constexpr int CPR = BKT / 8, RPB = 128 / BKT;
+    r = p / CPR;
+    kc = (p % CPR) ^ ((r / RPB) % CPR);
+  }
   // element offset, from the tile origin in global memory, of the data for LDS chunk p
   __device__ static int64_t src(int p, int ld) {
     if constexpr (KMAJ) {
@@ -467,8 +489,26 @@ gemm_dma_kernel(GemmArgs g) {
   const bf16* B = (const bf16*)g.B + (BKM ? (int64_t)n0 * g.ldb + (int64_t)s0 * BKT : (int64_t)s0 * BKT * g.ldb + n0);
 #pragma unroll
   for (int q = 0; q < PA; ++q) pa[q] = A + TA::src((q * NW + wave) * 64 + lane, g.lda);
+  if constexpr (BKM) {
+    if (g.glu > 0) {
+      // epilogue 3: panel row n0 + r is gate row (or, in odd 32-row groups, up row) n0/2 + ...
+      const bf16* Bg = (const bf16*)g.B + (int64_t)s0 * BKT;
 #pragma unroll
-  for (int q = 0; q < PB; ++q) pb[q] = B + TB::src((q * NW + wave) * 64 + lane, g.ldb);
+      for (int q = 0; q < PB; ++q) {
+        int r, kc;
+        TB::row_chunk((q * NW + wave) * 64 + lane, r, kc);
+        const int pc = n0 + r, grp = pc / 32;
+        const int brow = (grp & 1) * g.glu + (grp / 2) * 32 + pc % 32;
+        pb[q] = Bg + (int64_t)brow * g.ldb + kc * 8;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < PB; ++q) pb[q] = B + TB::src((q * NW + wave) * 64 + lane, g.ldb);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < PB; ++q) pb[q] = B + TB::src((q * NW + wave) * 64 + lane, g.ldb);
+  }
   const int64_t step_a = AK ? BKT : (int64_t)BKT * g.lda;
   const int64_t step_b = BKM ? BKT : (int64_t)BKT * g.ldb;
   // LDS byte addresses of this wave's first chunk in stage 0
@@ -607,6 +647,21 @@ bool launch_dma_cfg(const GemmArgs& g, hipStream_t st) {
 bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   // vector-load alignment: 8 elements along every contiguous dimension, rows in groups of 4
   if (g0.K % 8 || g0.M % 8 || g0.N % 8 || g0.lda % 8 || g0.ldb % 8 || g0.ldc % 8) return false;
+  if (g0.epi == 3) {
+    // the SwiGLU forward rides in the epilogue of the direct-to-LDS kernels only (their B loader
+    // gathers gate and up rows); any other shape runs the product, then the SwiGLU kernel
+    const bool fused = !g0.out_f32 && g0.b_kmajor && g0.K > 0 && g0.K % 64 == 0 && g0.M % 128 == 0 &&
+                       g0.N == 2 * g0.glu && g0.glu % 64 == 0 && g0.ld_out2 % 8 == 0 &&
+                       (uintptr_t)g0.out2 % 16 == 0;
+    if (!fused) {
+      GemmArgs p = g0;
+      p.epi = 0;
+      p.glu = 0;
+      if (!gemm_mfma_try(p, st)) return false;
+      launch_swiglu_fwd(true, g0.C, g0.out2, g0.M, g0.glu, st);
+      return true;
+    }
+  }
   if (g0.epi == 1 && (g0.out_f32 || g0.ld_aux % 8 || (uintptr_t)g0.aux % 16)) return false;
   if ((uintptr_t)g0.A % 16 || (uintptr_t)g0.B % 16 || (uintptr_t)g0.C % 16 || (uintptr_t)g0.resid % 16)
     return false;

@@ -75,10 +75,15 @@ struct GemmArgs {
   // [N, 2N) (row stride ldc): da = dz b s (1 + a (1 - s)), db = dz a s, s = sigmoid(a).
   // epilogue 2 (RoPE): columns [0, rope_cols) of the bf16 output are rotated in pairs
   // (i, i + hd/2) of each hd-wide head by angle(p, i), p = row mod rope_S (tables [rope_S][hd/2]).
+  // epilogue 3 (SwiGLU forward): B is [Wgate; Wup] ([2 glu, K], k-contiguous) and the product is
+  // the gate|up pre-activations [M, 2 glu] written to C (ldc = 2 glu) as usual, plus
+  // z = silu(gate) * up [M, glu] to out2 (row stride ld_out2).  Requires ldc = 2 glu and
+  // ld_out2 = glu (the layouts the SwiGLU kernel of the unfused paths assumes).
   int epi = 0;
   const void* aux = nullptr; int ld_aux = 0;
   const float* rope_cos = nullptr; const float* rope_sin = nullptr;
   int rope_cols = 0, rope_hd = 0, rope_S = 0;
+  int glu = 0; void* out2 = nullptr; int ld_out2 = 0;
 };
 constexpr int64_t GEMM_WS_ELEMS = 16 << 20;  // 64 MiB of fp32 split-K partials per stage
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st);

@@ -394,8 +394,13 @@ void block_forward(stage* S, int vi, BlockAct& b, const BlockOff& w, void* y) {
   run_gemm(S, gemm(T, d, S->hqd, b.o, S->hqd, true, S->wptr(vi, w.wo), S->hqd, true, b.h, d,
                        false, 0.f, b.x));
   launch_rmsnorm_fwd(bf, b.h, S->wptr(vi, w.ffn_norm), b.n2, b.rstd2, T, d, sh.rms_eps, st);
-  run_gemm(S, gemm(T, 2 * f, d, b.n2, d, true, S->wptr(vi, w.wgu), d, true, b.gu, 2 * f));
-  launch_swiglu_fwd(bf, b.gu, b.z, T, f, st);
+  // gate/up projection with the SwiGLU z = silu(gate) up in its epilogue
+  GemmArgs gg = gemm(T, 2 * f, d, b.n2, d, true, S->wptr(vi, w.wgu), d, true, b.gu, 2 * f);
+  gg.epi = 3;
+  gg.glu = f;
+  gg.out2 = b.z;
+  gg.ld_out2 = f;
+  run_gemm(S, gg);
   run_gemm(S, gemm(T, d, f, b.z, f, true, S->wptr(vi, w.wdown), f, true, y, d, false, 0.f, b.h));
 }
 

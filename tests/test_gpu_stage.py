@@ -79,9 +79,13 @@ MID_R = datagen.MID.with_(name="mid-reduced", n_blocks=2, d_model=256, n_heads=2
 LARGE_R = datagen.LARGE.with_(name="large-reduced", n_blocks=2, d_model=256, n_heads=4, n_kv_heads=2,
                               head_dim=64, d_ffn=384, seq_len=72, micro_batch=2,
                               microbatches_per_step=4, max_inflight=3)
+# whole 128-token tiles (256 tokens per microbatch): the full-tile GEMM kernels with their fused
+# epilogues (RoPE, SwiGLU forward and backward) at a size the oracle finishes in seconds
+TILED_R = datagen.SMALL.with_(name="small-full-tiles", n_blocks=2, d_model=256, n_heads=4, n_kv_heads=4,
+                              head_dim=64, d_ffn=512, vocab=1000, seq_len=128, micro_batch=2)
 
 
-@pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R], ids=lambda w: w.name)
+@pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, TILED_R], ids=lambda w: w.name)
 def test_reduced_bf16_stages(w):
     steps = 12
     p0 = datagen.init_params(w)
