@@ -244,38 +244,48 @@ __global__ void __launch_bounds__(256) swiglu_fwd(const T* __restrict__ gu, T* _
 // ------------------------------------------------------------------ token sort (rank sort)
 // Key of position i: (token << 14) | i, with tokens outside [0, vocab) given the token value
 // vocab so that they sort after every valid one and belong to no embedding row.  The keys are
-// distinct, so key i goes to out[#{j : key_j < key_i}].  A block ranks 64 keys; each of its four
-// waves counts over a quarter of every LDS-staged chunk of keys (all lanes read the same word, a
-// broadcast) and the four counts are added.
+// distinct, so key i goes to out[#{j : key_j < key_i}].  The count is split over SORT_PARTS ranges
+// of j (grid.y): a block counts, for 64 keys, the smaller keys of one range (its four waves each take
+// a quarter of the LDS-staged range; all lanes read the same word, a broadcast) and writes the
+// partial count; a second kernel adds the parts in order and scatters.
 constexpr int SORT_MAX = 16384;
-constexpr int SORT_CHUNK = 4096;
+constexpr int SORT_PARTS = SORT_RANK_PARTS;
+constexpr int SORT_CHUNK = 2048;  // keys of one range (SORT_MAX / SORT_PARTS)
 __device__ __forceinline__ uint32_t token_key(const int32_t* tok, int i, int vocab) {
   const int t = tok[i];
   return ((uint32_t)(t >= 0 && t < vocab ? t : vocab) << 14) | (uint32_t)i;
 }
-__global__ void __launch_bounds__(256) token_sort(const int32_t* __restrict__ tok, int n, int vocab,
-                                                  uint32_t* __restrict__ out) {
+__global__ void __launch_bounds__(256) token_rank_part(const int32_t* __restrict__ tok, int n, int vocab,
+                                                       int part_len, int32_t* __restrict__ part) {
   __shared__ u32x4 ks[SORT_CHUNK / 4];
   __shared__ int cnt4[4][64];
   const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
   const int i = blockIdx.x * 64 + lane;
   const uint32_t mine = i < n ? token_key(tok, i, vocab) : 0xFFFFFFFFu;
+  const int c0 = blockIdx.y * part_len, m = max(0, min(part_len, n - c0));
+  const int m16 = (m + 15) & ~15;  // padded with keys that no valid key exceeds
+  uint32_t* kw = reinterpret_cast<uint32_t*>(ks);
+  for (int e = threadIdx.x; e < m16; e += 256) kw[e] = e < m ? token_key(tok, c0 + e, vocab) : 0xFFFFFFFFu;
+  __syncthreads();
   int cnt = 0;
-  for (int c0 = 0; c0 < n; c0 += SORT_CHUNK) {
-    const int m = min(SORT_CHUNK, n - c0);
-    const int m16 = (m + 15) & ~15;  // padded with keys that no valid key exceeds
-    __syncthreads();
-    uint32_t* kw = reinterpret_cast<uint32_t*>(ks);
-    for (int e = threadIdx.x; e < m16; e += 256) kw[e] = e < m ? token_key(tok, c0 + e, vocab) : 0xFFFFFFFFu;
-    __syncthreads();
-    for (int q = wave; q < m16 / 4; q += 4) {
-      const u32x4 k = ks[q];
-      cnt += (k.x < mine) + (k.y < mine) + (k.z < mine) + (k.w < mine);
-    }
+  for (int q = wave; q < m16 / 4; q += 4) {
+    const u32x4 k = ks[q];
+    cnt += (k.x < mine) + (k.y < mine) + (k.z < mine) + (k.w < mine);
   }
   cnt4[wave][lane] = cnt;
   __syncthreads();
-  if (wave == 0 && i < n) out[cnt4[0][lane] + cnt4[1][lane] + cnt4[2][lane] + cnt4[3][lane]] = mine;
+  if (wave == 0 && i < n)
+    part[(int64_t)blockIdx.y * n + i] = cnt4[0][lane] + cnt4[1][lane] + cnt4[2][lane] + cnt4[3][lane];
+}
+__global__ void __launch_bounds__(256) token_rank_scatter(const int32_t* __restrict__ tok, int n, int vocab,
+                                                          const int32_t* __restrict__ part,
+                                                          uint32_t* __restrict__ out) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  int r = 0;
+#pragma unroll
+  for (int y = 0; y < SORT_PARTS; ++y) r += part[(int64_t)y * n + i];
+  out[r] = token_key(tok, i, vocab);
 }
 
 // row_start[v] = first sorted index with token >= v (binary search), v in [0, vocab]
@@ -472,8 +482,12 @@ static void swf_t(const void* gu, void* z, int rows, int f, hipStream_t st) {
 void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st) {
   DISPATCH(bf, swf_t, gu, z, rows, f, st);
 }
-void launch_token_sort(const int32_t* tok, int n, int vocab, uint32_t* sorted, hipStream_t st) {
-  if (n > 0) token_sort<<<(unsigned)cdiv(n, 64), 256, 0, st>>>(tok, n, vocab, sorted);
+void launch_token_sort(const int32_t* tok, int n, int vocab, int32_t* rank_part, uint32_t* sorted,
+                       hipStream_t st) {
+  if (n <= 0) return;
+  const int part_len = cdiv(cdiv(n, SORT_PARTS), 16) * 16;  // <= SORT_CHUNK for n <= SORT_MAX
+  token_rank_part<<<dim3((unsigned)cdiv(n, 64), SORT_PARTS), 256, 0, st>>>(tok, n, vocab, part_len, rank_part);
+  token_rank_scatter<<<(unsigned)cdiv(n, 256), 256, 0, st>>>(tok, n, vocab, rank_part, sorted);
 }
 void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_start, int32_t* ids,
                        int32_t* counts, int32_t* n_unique, hipStream_t st) {

@@ -44,7 +44,10 @@ void launch_rope(bool bf, void* qkv, int rows, int seq_len, int n_rot_heads, int
 void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st);
 // token sort for the embedding gradient: keys (tok << 14 | pos) ascending, tokens outside
 // [0, vocab) keyed as vocab; n <= 16384
-void launch_token_sort(const int32_t* tok, int n, int vocab, uint32_t* sorted, hipStream_t st);
+// rank_part: scratch of SORT_RANK_PARTS * n int32
+constexpr int SORT_RANK_PARTS = 8;
+void launch_token_sort(const int32_t* tok, int n, int vocab, int32_t* rank_part, uint32_t* sorted,
+                       hipStream_t st);
 void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_start,
                        int32_t* ids, int32_t* counts, int32_t* n_unique, hipStream_t st);
 void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted,

@@ -89,7 +89,7 @@ struct stage {
   int* flag;
   unsigned long long* skipped;
   uint32_t* sorted;
-  int32_t* row_start;
+  int32_t *row_start, *rank_part;
   std::vector<Slot> slots;
   // bookkeeping
   int64_t version_step[2] = {-1, -1};
@@ -291,6 +291,7 @@ size_t layout(stage* S, char* base) {
   S->cos_t = (float*)carve((int64_t)sh.seq_len * (hd / 2) * 4);
   S->sin_t = (float*)carve((int64_t)sh.seq_len * (hd / 2) * 4);
   S->sorted = sh.first_stage ? (uint32_t*)carve(T * 4) : nullptr;
+  S->rank_part = sh.first_stage ? (int32_t*)carve((int64_t)SORT_RANK_PARTS * T * 4) : nullptr;
   S->row_start = sh.first_stage ? (int32_t*)carve(((int64_t)sh.vocab + 1) * 4) : nullptr;
   S->dlog = sh.last_stage ? carve(T * (int64_t)sh.vocab * esz) : nullptr;
   S->dhf = sh.last_stage ? carve(T * d * esz) : nullptr;
@@ -647,7 +648,7 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   join_wgrad(s);  // every weight gradient is in g (the scatter below may add to the tied head's)
   if (sh.first_stage) {
     const void* dx0 = cur;
-    launch_token_sort(sl.tokens, T, sh.vocab, s->sorted, st);
+    launch_token_sort(sl.tokens, T, sh.vocab, s->rank_part, s->sorted, st);
     launch_token_runs(s->sorted, T, sh.vocab, s->row_start, nullptr, nullptr, nullptr, st);
     launch_embed_scatter(bf, dx0, s->sorted, s->row_start, sh.vocab, d, g + s->off_embed,
                          head_wrote_embed || !first, st);
@@ -772,7 +773,7 @@ int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts,
   if (slot < 0 || slot >= s->sh.max_inflight) return fail(STAGE_EINVAL, "slot out of range");
   const Slot& sl = s->slots[slot];
   if (sl.step < 0) return fail(STAGE_ESTATE, "slot has not run forward");
-  launch_token_sort(sl.tokens, s->T, s->sh.vocab, s->sorted, s->st);
+  launch_token_sort(sl.tokens, s->T, s->sh.vocab, s->rank_part, s->sorted, s->st);
   launch_token_runs(s->sorted, s->T, s->sh.vocab, s->row_start, ids, counts, n_unique, s->st);
   HIP_OK(hipGetLastError());
   return STAGE_OK;
