@@ -11,6 +11,7 @@
 
 bool attention_mfma_fwd_try(const AttnArgs& a, hipStream_t st);  // attention_mfma.hip
 bool attention_mfma_bwd_try(const AttnArgs& a, hipStream_t st);
+bool attention_mfma_delta_try(const AttnArgs& a, hipStream_t st);
 
 namespace {
 
@@ -211,8 +212,12 @@ void fwd_t(const AttnArgs& a, hipStream_t st) {
   attn_fwd<T, HD><<<dim3((unsigned)cdiv(a.S, TR), a.Hq, a.B), TR, 0, st>>>(a);
 }
 template <typename T, int HD>
-void bwd_t(const AttnArgs& a, hipStream_t st) {
+void delta_t(const AttnArgs& a, hipStream_t st) {
   attn_delta<T, HD><<<(unsigned)cdiv((int64_t)a.B * a.Hq * a.S, 256), 256, 0, st>>>(a);
+}
+template <typename T, int HD>
+void bwd_t(const AttnArgs& a, hipStream_t st) {
+  if (!a.delta_ready) delta_t<T, HD>(a, st);
   attn_bwd_dq<T, HD><<<dim3((unsigned)cdiv(a.S, TR), a.Hq, a.B), TR, 0, st>>>(a);
   attn_bwd_dkv<T, HD, false><<<dim3((unsigned)cdiv(a.S, TR), a.Hkv, a.B), TR, 0, st>>>(a);
   attn_bwd_dkv<T, HD, true><<<dim3((unsigned)cdiv(a.S, TR), a.Hkv, a.B), TR, 0, st>>>(a);
@@ -244,6 +249,17 @@ void launch_attention_fwd(bool bf, const AttnArgs& a, hipStream_t st) {
   if (bf && attention_mfma_fwd_try(a, st)) return;
   launch_attention_fwd_ref(bf, a, st);
 }
+void launch_attention_delta(bool bf, const AttnArgs& a, hipStream_t st) {
+  if (bf && attention_mfma_delta_try(a, st)) return;
+  auto run = [&](auto tag) {
+    using T = decltype(tag);
+    if (a.hd == 32) delta_t<T, 32>(a, st);
+    else if (a.hd == 64) delta_t<T, 64>(a, st);
+    else delta_t<T, 128>(a, st);
+  };
+  if (bf) run(bf16{}); else run(float{});
+}
+
 void launch_attention_bwd(bool bf, const AttnArgs& a, hipStream_t st) {
   if (bf && attention_mfma_bwd_try(a, st)) return;
   launch_attention_bwd_ref(bf, a, st);

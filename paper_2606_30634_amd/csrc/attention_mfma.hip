@@ -614,7 +614,7 @@ void bwd_launch(const AttnArgs& a, hipStream_t st) {
     set_lds(flash_bwd_dkv<HD>, Lds<HD>::dkv_bytes());
     attr = true;
   }
-  flash_delta<HD><<<(unsigned)cdiv((int64_t)a.B * a.S * a.Hq, 256), 256, 0, st>>>(a);
+  if (!a.delta_ready) flash_delta<HD><<<(unsigned)cdiv((int64_t)a.B * a.S * a.Hq, 256), 256, 0, st>>>(a);
   if constexpr (HD == 64) {
     // one launch for both (at head dim 128 the dK/dV register budget would halve dQ's occupancy)
     static bool fattr = false;
@@ -634,6 +634,14 @@ bool attention_mfma_fwd_try(const AttnArgs& a, hipStream_t st) {
   if ((uintptr_t)a.qkv % 16 || (uintptr_t)a.o % 16) return false;
   if (a.hd == 64) { fwd_launch<64>(a, st); return true; }
   if (a.hd == 128) { fwd_launch<128>(a, st); return true; }
+  return false;
+}
+
+bool attention_mfma_delta_try(const AttnArgs& a, hipStream_t st) {
+  if ((uintptr_t)a.o % 16 || (uintptr_t)a.dout % 16) return false;
+  const unsigned nb = (unsigned)cdiv((int64_t)a.B * a.S * a.Hq, 256);
+  if (a.hd == 64) { flash_delta<64><<<nb, 256, 0, st>>>(a); return true; }
+  if (a.hd == 128) { flash_delta<128><<<nb, 256, 0, st>>>(a); return true; }
   return false;
 }
 

@@ -109,6 +109,16 @@ void launch_gemm_tiled(bool bf, const GemmArgs& g, hipStream_t st) {
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st) {
   if (g.M == 0 || g.N == 0) return;
   if (bf && gemm_mfma_try(g, st)) return;
+  if (g.epi == 4) {  // the product, then delta = rowsum(dO O) by the attention's own kernel
+    GemmArgs p = g;
+    p.epi = 0;
+    launch_gemm(bf, p, st);
+    AttnArgs a{};
+    a.B = g.M / g.delta_S; a.S = g.delta_S; a.Hq = g.N / g.delta_hd; a.Hkv = a.Hq; a.hd = g.delta_hd;
+    a.o = const_cast<void*>(g.aux); a.dout = g.C; a.delta = g.delta;
+    launch_attention_delta(bf, a, st);
+    return;
+  }
   if (g.epi == 3) {  // the reference tiling writes gate|up, then the SwiGLU kernel makes z
     GemmArgs p = g;
     p.epi = 0;

@@ -202,6 +202,21 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[W
           }
           *reinterpret_cast<bf16x8*>((bf16*)C + o) = da;
           *reinterpret_cast<bf16x8*>((bf16*)C + o + g.N) = db;
+        } else if (g.epi == 4) {  // dO, plus delta = rowsum(dO O) over each head's columns
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
+          *reinterpret_cast<bf16x8*>((bf16*)C + o) = ov;
+          const bf16x8 ob = *reinterpret_cast<const bf16x8*>((const bf16*)g.aux + (int64_t)row * g.ld_aux + col);
+          float dot = 0.f;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) dot += (float)ov[q] * (float)ob[q];
+          // the head's delta_hd / 8 chunks sit in consecutive lanes (aligned groups)
+          for (int m = 1; m < g.delta_hd / 8; m <<= 1) dot += __shfl_xor(dot, m, 64);
+          if (col % g.delta_hd == 0) {
+            const int bb = row / g.delta_S, ii = row % g.delta_S, hh = col / g.delta_hd;
+            g.delta[((int64_t)bb * (g.N / g.delta_hd) + hh) * g.delta_S + ii] = dot;
+          }
         } else if (g.epi == 3) {  // SwiGLU forward: panel column col is gate or up of z column zc
           const int grp = col / 32, zc = (grp / 2) * 32 + col % 32;
           bf16x8 ov;
@@ -665,6 +680,16 @@ bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   if (g0.epi == 1 && (g0.out_f32 || g0.ld_aux % 8 || (uintptr_t)g0.aux % 16)) return false;
   if ((uintptr_t)g0.A % 16 || (uintptr_t)g0.B % 16 || (uintptr_t)g0.C % 16 || (uintptr_t)g0.resid % 16)
     return false;
+  if (g0.epi == 4) {
+    // delta rides in the epilogue of the direct-to-LDS kernels when a wave's columns hold whole
+    // heads (every lane of the epilogue active); otherwise the caller computes it separately
+    const bool full = !g0.out_f32 && g0.K > 0 && g0.K % 64 == 0 && g0.M % 128 == 0 && g0.N % 128 == 0;
+    const bool big = full && g0.M % 256 == 0 && g0.N % 256 == 0 &&
+                     (cdiv(g0.M, 256) * cdiv(g0.N, 256) >= 512 ||
+                      (cdiv(g0.M, 256) * cdiv(g0.N, 256) >= 256 && g0.K >= 2048));
+    const int wn = big ? 128 : 64;
+    if (!full || g0.delta_hd < 8 || wn % g0.delta_hd || g0.ld_aux % 8 || (uintptr_t)g0.aux % 16) return false;
+  }
   GemmArgs g = g0;
   g.ksplit = 1;
   const int64_t mn = (int64_t)g.M * g.N;

@@ -87,6 +87,10 @@ struct GemmArgs {
   const float* rope_cos = nullptr; const float* rope_sin = nullptr;
   int rope_cols = 0, rope_hd = 0, rope_S = 0;
   int glu = 0; void* out2 = nullptr; int ld_out2 = 0;
+  // epilogue 4 (attention delta): the product is dO [M, N] (bf16, heads of delta_hd columns, rows
+  // b * delta_S + i) and aux the attention output O of the same layout; besides C, writes
+  // delta[(b Hq + h) delta_S + i] = sum over head h's columns of dO O (bf16-rounded dO).
+  float* delta = nullptr; int delta_hd = 0, delta_S = 0;
 };
 constexpr int64_t GEMM_WS_ELEMS = 16 << 20;  // 64 MiB of fp32 split-K partials per stage
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st);
@@ -101,6 +105,9 @@ struct AttnArgs {
   const void* qkv; void* o; float* lse;
   const void* dout; void* dqkv; float* delta;  // backward only; delta fp32 [B, Hq, s]
   const float* rope_cos = nullptr; const float* rope_sin = nullptr;
+  bool delta_ready = false;  // backward: delta already holds rowsum(dO O)
 };
 void launch_attention_fwd(bool bf, const AttnArgs& a, hipStream_t st);
+// delta = rowsum(dO O) per (batch, head, query) alone
+void launch_attention_delta(bool bf, const AttnArgs& a, hipStream_t st);
 void launch_attention_bwd(bool bf, const AttnArgs& a, hipStream_t st);
