@@ -115,7 +115,7 @@ struct Cfg {
   static constexpr int SA = stage_elems<BM, AK>(), SB = stage_elems<BN, BKM>();
   static constexpr size_t main_lds = (size_t)2 * (SA + SB) * sizeof(bf16);
   static constexpr int EP = WN + 4;  // epilogue staging pitch (fp32 elements)
-  static constexpr size_t epi_lds = (size_t)NW * 32 * EP * sizeof(float);
+  static constexpr size_t epi_lds = (size_t)NW * 16 * EP * sizeof(float);
   static constexpr size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
 };
 
@@ -129,12 +129,11 @@ constexpr int tile_waves_per_simd() { return BM * BN >= 256 * 256 ? 1 : 2; }
 // the blocks resident on one XCD at a time cover a compact patch of C and share their A and B
 // slices in that XCD's L2.
 template <int BM, int BN>
-__device__ __forceinline__ void tile_origin(const GemmArgs& g, int& m0, int& n0) {
+__device__ __forceinline__ void tile_origin(const GemmArgs& g, int b, int& m0, int& n0) {
   constexpr int GM = 8;
   const int tiles_n = (g.N + BN - 1) / BN;
   const int tiles_m = (g.M + BM - 1) / BM;
   const int nblk = tiles_m * tiles_n;
-  int b = blockIdx.x;
   if ((nblk & 7) == 0) b = (b & 7) * (nblk >> 3) + (b >> 3);
   const int first_m = (b / (GM * tiles_n)) * GM;
   const int gsz = min(tiles_m - first_m, GM);
@@ -142,39 +141,44 @@ __device__ __forceinline__ void tile_origin(const GemmArgs& g, int& m0, int& n0)
   n0 = ((b % (GM * tiles_n)) / gsz) * BN;
 }
 
-// Epilogue: per 32-row slice of the wave tile, stage the fp32 accumulators through LDS and write
-// 16-byte rows: split-K partials to the workspace, or C with the beta / residual / SwiGLU-backward
-// / RoPE terms.  LDS must be free (every wave past its last read of the operand stages).
+// Epilogue: per 16-row half of each 32-row fragment row of the wave tile, stage the fp32
+// accumulators through the wave's own LDS area and write 16-byte rows: split-K partials to the
+// workspace, or C with the beta / residual / SwiGLU-backward / RoPE / delta / SwiGLU-forward terms.
+// A wave reads back only what it wrote, and one wave's LDS operations complete in issue order, so
+// no barrier is needed between the halves and the global stores are never waited for here.  The
+// staging area (NW x 16 x (WN + 4) floats) must be free: every wave past its last read of it.
 template <int BM, int BN, int WM, int WN, typename OutT, bool CHECK>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[WM / 32][WN / 32],
-                                              unsigned char* smem, int m0, int n0, int wm0, int wn0) {
+                                              float* stage, int m0, int n0, int wm0, int wn0) {
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int EP = WN + 4;  // staging pitch (fp32 elements)
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-  float* stg = reinterpret_cast<float*>(smem) + wave * 32 * EP;
+  float* stg = stage + wave * 16 * EP;
   const bool split = g.ksplit > 1;
   float* W = split ? g.ws + (int64_t)blockIdx.y * g.M * g.N : nullptr;
   OutT* C = (OutT*)g.C;
   const bf16* R = (const bf16*)g.resid;
   constexpr int VEC = sizeof(OutT) == 2 ? 8 : 4;  // elements per 16-byte store
-  static_for<FM>([&](auto I) {
-    constexpr int i = I;
+  static_for<FM * 2>([&](auto IH) {
+    constexpr int i = IH / 2, h = IH % 2;
+    // accumulator e of lane l holds fragment row 8 (e / 4) + 4 (l / 32) + e mod 4: rows 16h..16h+15
+    // are e = 8h..8h+7
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e)
-        stg[(8 * (e / 4) + 4 * (lane / 32) + (e % 4)) * EP + j * 32 + lane % 32] = acc[i][j][e];
-    __syncthreads();
-    const int rbase = m0 + wm0 + i * 32;
+      for (int e = 8 * h; e < 8 * h + 8; ++e)
+        stg[(8 * (e / 4 - 2 * h) + 4 * (lane / 32) + (e % 4)) * EP + j * 32 + lane % 32] = acc[i][j][e];
+    asm volatile("" ::: "memory");
+    const int rbase = m0 + wm0 + i * 32 + 16 * h;
     if (split) {
-      for (int c = lane; c < 32 * WN / 4; c += 64) {
+      for (int c = lane; c < 16 * WN / 4; c += 64) {
         const int r = c / (WN / 4), cc = (c % (WN / 4)) * 4;
         const int row = rbase + r, col = n0 + wn0 + cc;
         if (!CHECK || (row < g.M && col < g.N))
           *reinterpret_cast<float4*>(W + (int64_t)row * g.N + col) = *reinterpret_cast<const float4*>(stg + r * EP + cc);
       }
     } else {
-      for (int c = lane; c < 32 * WN / VEC; c += 64) {
+      for (int c = lane; c < 16 * WN / VEC; c += 64) {
         const int r = c / (WN / VEC), cc = (c % (WN / VEC)) * VEC;
         const int row = rbase + r, col = n0 + wn0 + cc;
         if (CHECK && (row >= g.M || col >= g.N)) continue;  // N is a multiple of 8
@@ -259,7 +263,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[W
         }
       }
     }
-    __syncthreads();
+    asm volatile("" ::: "memory");
   });
 }
 
@@ -275,7 +279,7 @@ gemm_mfma_kernel(GemmArgs g) {
   bf16* Bs = As + 2 * SA;                                   // [2][SB]
 
   int m0, n0;
-  tile_origin<BM, BN>(g, m0, n0);
+  tile_origin<BM, BN>(g, blockIdx.x, m0, n0);
 
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
@@ -362,7 +366,7 @@ gemm_mfma_kernel(GemmArgs g) {
     __syncthreads();
   }
 
-  gemm_epilogue<BM, BN, WM, WN, OutT, CHECK>(g, acc, smem, m0, n0, wm0, wn0);
+  gemm_epilogue<BM, BN, WM, WN, OutT, CHECK>(g, acc, reinterpret_cast<float*>(smem), m0, n0, wm0, wn0);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -431,8 +435,13 @@ struct DmaCfg {
   static constexpr int NT = NW * 64;
   using TA = DmaTile<BM, BKT, AK, NT>;
   using TB = DmaTile<BN, BKT, BKM, NT>;
-  static constexpr size_t main_lds = (size_t)NS * (TA::ELEMS + TB::ELEMS) * sizeof(bf16);
-  static constexpr size_t epi_lds = (size_t)NW * 32 * (WN + 4) * sizeof(float);
+  // one stage: the A tile, then the B tile (bf16 elements)
+  static constexpr int STAGE = TA::ELEMS + TB::ELEMS;
+  static constexpr size_t epi_lds = (size_t)NW * 16 * (WN + 4) * sizeof(float);
+  // A block walks several tiles when the epilogue's staging fits in one stage: the stage of a
+  // tile's last slice is then free for it while the next tile's first slices land in the others.
+  static constexpr bool persist = epi_lds <= (size_t)STAGE * sizeof(bf16);
+  static constexpr size_t main_lds = (size_t)NS * STAGE * sizeof(bf16);
   static constexpr size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
 };
 
@@ -443,11 +452,12 @@ __device__ __forceinline__ void wait_vm_lds() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
 }
 
-// One 16-byte global -> LDS load per lane (lane l writes lds + 16 l).  Issued as inline assembly so
-// that the compiler neither counts it in its own waits nor orders LDS reads after it: the kernel
-// waits for these loads itself (wait_vm_lds) before the barrier that publishes a stage.
-__device__ __forceinline__ void dma16(const void* src, uint32_t lds) {
-  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds) : "memory");
+// One 16-byte global -> LDS load per lane from base + voff bytes (base wave-uniform; lane l
+// writes lds + 16 l).  Issued as inline assembly so that the compiler neither counts it in its own
+// waits nor orders LDS reads after it: the kernel waits for these loads itself (wait_vm_lds)
+// before the barrier that publishes a stage.
+__device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(lds) : "memory");
 }
 
 __device__ __forceinline__ void block_barrier() {
@@ -465,6 +475,10 @@ constexpr int dma_waves_per_simd() {
   return w > 8 ? 8 : (w < 1 ? 1 : w);
 }
 
+// Block b takes tiles b, b + gridDim.x, ... (gridDim.x a multiple of 8 when it is below the tile
+// count, so that every tile of a block maps to the block's XCD).  The slices of all its tiles form
+// one sequence: the loads of slice G + NS - 1 of that sequence (the next tile's first slices near
+// the end of a tile) are issued while slice G is consumed, into stage (G + NS - 1) mod NS.
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, int BKT, int NS>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(dma_waves_per_simd<BM, BN, WM, WN, AK, BKM, BKT, NS>(),
@@ -473,109 +487,138 @@ gemm_dma_kernel(GemmArgs g) {
   using C_ = DmaCfg<BM, BN, WM, WN, AK, BKM, BKT, NS>;
   using TA = typename C_::TA;
   using TB = typename C_::TB;
-  constexpr int WAVES_N = BN / WN, NW = C_::NW;
+  constexpr int WAVES_N = BN / WN, NW = C_::NW, STAGE = C_::STAGE;
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int PA = TA::PER, PB = TB::PER;
+  // vector-memory operations one thread's epilogue issues at least: one per 16-byte output chunk
+  constexpr int EPI_OPS = FM * 2 * (16 * WN / (sizeof(OutT) == 2 ? 8 : 4) / 64);
+  static_assert((NS - 2) * (PA + PB) + EPI_OPS < 64, "vmcnt range");
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16* As = reinterpret_cast<bf16*>(smem);  // [NS][TA::ELEMS]
-  bf16* Bs = As + NS * TA::ELEMS;            // [NS][TB::ELEMS]
+  bf16* S = reinterpret_cast<bf16*>(smem);  // [NS][A tile | B tile]
 
-  int m0, n0;
-  tile_origin<BM, BN>(g, m0, n0);
-  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int tiles = (g.M / BM) * (g.N / BN);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64), lane = threadIdx.x % 64;
   const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
-
-  f32x16 acc[FM][FN];
+  // split-K: this block covers slices [s0, s0 + nk) of every tile
+  const int nk = g.K / BKT / g.ksplit, s0 = blockIdx.y * nk;
+  const bool glu = BKM && g.glu > 0;
+  // this thread's byte offsets from a tile's slice origin
+  uint32_t oa[PA], ob[PB];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int q = 0; q < PA; ++q) oa[q] = 2u * (uint32_t)TA::src((q * NW + wave) * 64 + lane, g.lda);
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  // split-K: this block covers slices [s0, s0 + nk)
-  const int nslices = g.K / BKT;
-  const int per_split = nslices / g.ksplit;
-  const int s0 = blockIdx.y * per_split, nk = per_split;
-  // this thread's source pointers for slice s0 and the step between slices
-  const bf16* pa[PA];
-  const bf16* pb[PB];
-  const bf16* A = (const bf16*)g.A + (AK ? (int64_t)m0 * g.lda + (int64_t)s0 * BKT : (int64_t)s0 * BKT * g.lda + m0);
-  const bf16* B = (const bf16*)g.B + (BKM ? (int64_t)n0 * g.ldb + (int64_t)s0 * BKT : (int64_t)s0 * BKT * g.ldb + n0);
-#pragma unroll
-  for (int q = 0; q < PA; ++q) pa[q] = A + TA::src((q * NW + wave) * 64 + lane, g.lda);
-  if constexpr (BKM) {
-    if (g.glu > 0) {
+  for (int q = 0; q < PB; ++q) {
+    const int p = (q * NW + wave) * 64 + lane;
+    if (glu) {
       // epilogue 3: panel row n0 + r is gate row (or, in odd 32-row groups, up row) n0/2 + ...
-      const bf16* Bg = (const bf16*)g.B + (int64_t)s0 * BKT;
-#pragma unroll
-      for (int q = 0; q < PB; ++q) {
-        int r, kc;
-        TB::row_chunk((q * NW + wave) * 64 + lane, r, kc);
-        const int pc = n0 + r, grp = pc / 32;
-        const int brow = (grp & 1) * g.glu + (grp / 2) * 32 + pc % 32;
-        pb[q] = Bg + (int64_t)brow * g.ldb + kc * 8;
-      }
+      int r, kc;
+      TB::row_chunk(p, r, kc);
+      ob[q] = 2u * (uint32_t)((((r / 32) & 1) * g.glu + (r / 64) * 32 + r % 32) * g.ldb + kc * 8);
     } else {
-#pragma unroll
-      for (int q = 0; q < PB; ++q) pb[q] = B + TB::src((q * NW + wave) * 64 + lane, g.ldb);
+      ob[q] = 2u * (uint32_t)TB::src(p, g.ldb);
     }
-  } else {
-#pragma unroll
-    for (int q = 0; q < PB; ++q) pb[q] = B + TB::src((q * NW + wave) * 64 + lane, g.ldb);
   }
+  // slice 0 (of this split) of the tiles at row m0 / column n0
+  auto a_tile = [&](int m0) {
+    return (const bf16*)g.A + (AK ? (int64_t)m0 * g.lda + (int64_t)s0 * BKT : (int64_t)s0 * BKT * g.lda + m0);
+  };
+  auto b_tile = [&](int n0) {
+    if (glu) return (const bf16*)g.B + (int64_t)(n0 / 2) * g.ldb + (int64_t)s0 * BKT;
+    return (const bf16*)g.B + (BKM ? (int64_t)n0 * g.ldb + (int64_t)s0 * BKT : (int64_t)s0 * BKT * g.ldb + n0);
+  };
   const int64_t step_a = AK ? BKT : (int64_t)BKT * g.lda;
   const int64_t step_b = BKM ? BKT : (int64_t)BKT * g.ldb;
-  // LDS byte addresses of this wave's first chunk in stage 0
+  // LDS byte addresses of this wave's first chunk of the A and B tiles of stage 0
   typedef __attribute__((address_space(3))) bf16 lds_bf16;
-  const uint32_t la0 = (uint32_t)(uintptr_t)(lds_bf16*)(As + wave * 512);
-  const uint32_t lb0 = (uint32_t)(uintptr_t)(lds_bf16*)(Bs + wave * 512);
-  // slice s (clamped to the last one: the tail reloads it into a stage nobody reads again, which
-  // keeps the count of outstanding loads per slice uniform) into stage `stage`
-  auto issue = [&](int s, int stage) {
-    s = min(s, nk - 1);
-    const uint32_t ta = la0 + stage * TA::ELEMS * 2, tb = lb0 + stage * TB::ELEMS * 2;
+  const uint32_t la0 = (uint32_t)(uintptr_t)(lds_bf16*)(S + wave * 512);
+  const uint32_t lb0 = la0 + TA::ELEMS * 2;
+  auto issue = [&](const bf16* at, const bf16* bt, int s, int stage) {
+    const bf16* as = at + s * step_a;
+    const bf16* bs = bt + s * step_b;
+    const uint32_t ta = la0 + stage * STAGE * 2, tb = lb0 + stage * STAGE * 2;
 #pragma unroll
-    for (int q = 0; q < PA; ++q) dma16(pa[q] + s * step_a, ta + q * NW * 1024);
+    for (int q = 0; q < PA; ++q) dma16(as, oa[q], ta + q * NW * 1024);
 #pragma unroll
-    for (int q = 0; q < PB; ++q) dma16(pb[q] + s * step_b, tb + q * NW * 1024);
+    for (int q = 0; q < PB; ++q) dma16(bs, ob[q], tb + q * NW * 1024);
   };
-  if (nk > 0) {
+
+  int t = blockIdx.x;
+  int m0, n0;
+  tile_origin<BM, BN>(g, t, m0, n0);
+  const bf16* at = a_tile(m0);
+  const bf16* bt = b_tile(n0);
+  // slices NS - 1 and later ahead come from the next tile only when a tile has that many
+  const bool chain = C_::persist && nk >= NS - 1;
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s) issue(s, s);
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    wait_vm_lds<(NS - 2) * (PA + PB)>();  // this thread's loads of slice kt are in LDS
-    block_barrier();                        // ... and every thread's; stage kt - 1 is free
-    issue(kt + NS - 1, (kt + NS - 1) % NS);
-    const int cur = kt % NS;
-    const bf16* as = As + cur * TA::ELEMS;
-    const bf16* bs = Bs + cur * TB::ELEMS;
-    bf16x8 af[2][FM], bfr[2][FN];
+  for (int s = 0; s < NS - 1; ++s) issue(at, bt, min(s, nk - 1), s);
+  int G = 0;  // position in the block's slice sequence
+  for (bool first = true;; first = false) {
+    const int tn = t + gridDim.x;
+    const bool next = chain && tn < tiles;
+    int m1 = m0, n1 = n0;
+    if (next) tile_origin<BM, BN>(g, tn, m1, n1);
+    const bf16* atn = a_tile(m1);
+    const bf16* btn = b_tile(n1);
+
+    f32x16 acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) af[0][i] = TA::frag(as, wm0 + i * 32, 0);
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) bfr[0][j] = TB::frag(bs, wn0 + j * 32, 0);
-    static_for<BKT / 16>([&](auto KS) {
-      constexpr int ks = KS, c = ks & 1;
-      if constexpr (ks + 1 < BKT / 16) {
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int i = 0; i < FM; ++i) af[c ^ 1][i] = TA::frag(as, wm0 + i * 32, (ks + 1) * 16);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) bfr[c ^ 1][j] = TB::frag(bs, wn0 + j * 32, (ks + 1) * 16);
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    for (int kt = 0; kt < nk; ++kt, ++G) {
+      // this thread's loads of slice G are in LDS: issued after them are the loads of the NS - 2
+      // following slices and, in a tile's first slices, the previous tile's epilogue
+      if (!first && kt < NS - 1) wait_vm_lds<(NS - 2) * (PA + PB) + EPI_OPS>();
+      else wait_vm_lds<(NS - 2) * (PA + PB)>();
+      block_barrier();  // ... and every thread's; the stage of slice G - 1 is free
+      {
+        const int x = kt + NS - 1, stage = (G + NS - 1) % NS;
+        if (x < nk) issue(at, bt, x, stage);
+        else if (next) issue(atn, btn, x - nk, stage);
+        else issue(at, bt, nk - 1, stage);  // a reload into a stage nobody reads again
       }
-      __builtin_amdgcn_sched_barrier(0);
+      const bf16* as = S + (G % NS) * STAGE;
+      const bf16* bs = as + TA::ELEMS;
+      bf16x8 af[2][FM], bfr[2][FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FM; ++i) af[0][i] = TA::frag(as, wm0 + i * 32, 0);
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    });
+      for (int j = 0; j < FN; ++j) bfr[0][j] = TB::frag(bs, wn0 + j * 32, 0);
+      static_for<BKT / 16>([&](auto KS) {
+        constexpr int ks = KS, c = ks & 1;
+        if constexpr (ks + 1 < BKT / 16) {
+#pragma unroll
+          for (int i = 0; i < FM; ++i) af[c ^ 1][i] = TA::frag(as, wm0 + i * 32, (ks + 1) * 16);
+#pragma unroll
+          for (int j = 0; j < FN; ++j) bfr[c ^ 1][j] = TB::frag(bs, wn0 + j * 32, (ks + 1) * 16);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
+    float* stg;
+    if constexpr (C_::persist) {
+      // the stage of the tile's last slice, once every wave is past its fragment reads
+      stg = reinterpret_cast<float*>(S + ((G - 1) % NS) * STAGE);
+    } else {
+      wait_vm_lds<0>();  // the whole LDS: the reloads too
+      stg = reinterpret_cast<float*>(smem);
+    }
+    wait_vm_lds<63>();
+    block_barrier();
+    gemm_epilogue<BM, BN, WM, WN, OutT, false>(g, acc, stg, m0, n0, wm0, wn0);
+    if (!next) break;
+    t = tn; m0 = m1; n0 = n1; at = atn; bt = btn;
   }
-  wait_vm_lds<0>();  // the tail's reloads too: the epilogue reuses the LDS
-  __syncthreads();
-  gemm_epilogue<BM, BN, WM, WN, OutT, false>(g, acc, smem, m0, n0, wm0, wn0);
+  wait_vm_lds<0>();  // no load may land in the LDS after the block ends
 }
 
 // C = beta C + sum over splits of the partial tiles, in split order (fp32 output, ldc == N)
@@ -642,7 +685,14 @@ void launch_dma_one(const GemmArgs& g, int nblk, hipStream_t st) {
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)C_::lds);
     attr_set = true;
   }
-  gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS><<<dim3(nblk, g.ksplit), C_::NT, C_::lds, st>>>(g);
+  // more tiles than the chip holds blocks at once: one block per slot, each walking its tiles
+  int grid = nblk;
+  if (C_::persist && g.K / BKT / g.ksplit >= NS - 1) {
+    const int per_cu = (int)(163840 / C_::lds);
+    const int slots = (per_cu * device_cu_count() / g.ksplit) / 8 * 8;
+    if (slots >= 8 && nblk > slots) grid = slots;
+  }
+  gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS><<<dim3(grid, g.ksplit), C_::NT, C_::lds, st>>>(g);
 }
 
 // Direct-to-LDS variant: full tiles and whole slices per split only; false if the shape is not.
@@ -658,6 +708,18 @@ bool launch_dma_cfg(const GemmArgs& g, hipStream_t st) {
 }
 
 }  // namespace
+
+int device_cu_count() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
 
 bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   // vector-load alignment: 8 elements along every contiguous dimension, rows in groups of 4

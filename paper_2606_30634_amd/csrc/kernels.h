@@ -10,13 +10,20 @@ struct UpdateScalars {
   int apply;  // 0: write the compute copy only (no pending gradient)
 };
 size_t norm_scratch_bytes();
+// blocks: partial sums (and blocks of the first pass), at most norm_scratch_bytes() / 8; <= 0
+// takes that maximum.
 void launch_grad_norm(const void* g, bool g_bf16, int64_t n, float clip, double* partial,
-                      float* out2, int* flag, unsigned long long* skipped, hipStream_t st);
+                      float* out2, int* flag, unsigned long long* skipped, int blocks, hipStream_t st);
+// blocks > 0: a resident grid of that many blocks walks the vector (for a pass that runs beside
+// the kernels of another stream); 0: one block per 1024 elements.
 void launch_fused_update(int64_t n, float* x, const void* g, bool g_bf16, float* m, float* v,
                          float* up, void* shadow, int shadow_kind, const UpdateScalars& hs,
-                         const float* clip, const int* flag, hipStream_t st);
+                         const float* clip, const int* flag, int blocks, hipStream_t st);
 void launch_cast_copy(int64_t n, const float* src, void* dst, bool dst_bf16, hipStream_t st);
 void launch_zero(void* p, int64_t bytes, hipStream_t st);
+
+// compute units of the current device (gemm_mfma.hip; cached per device)
+int device_cu_count();
 
 // ------------------------------------------------------------------ elementwise (elementwise.hip)
 // `bf` selects bf16 storage (else fp32) for every activation / weight pointer of the call.

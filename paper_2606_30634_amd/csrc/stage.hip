@@ -722,7 +722,7 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   if (apply && hp->clip_norm > 0.f) {
     timed(s, STAGE_PROF_NORM, 4.0 * s->n_flat, [&] {
       launch_grad_norm(s->grad[gb], false, s->n_flat, hp->clip_norm, s->upd_norm_part, s->upd_norm_out,
-                       s->flag, s->skipped, us);
+                       s->flag, s->skipped, device_cu_count(), us);
     }, us);
     clip = s->upd_norm_out + 1;
     flag = s->flag;
@@ -733,7 +733,7 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   timed(s, STAGE_PROF_UPDATE, ub * s->n_flat, [&] {
     launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v,
                         hp->ef_lambda != 0.f ? s->u_prev : nullptr, s->ver[vout], s->bf ? 2 : 1, hs,
-                        clip, flag, us);
+                        clip, flag, device_cu_count(), us);
   }, us);
   HIP_OK(hipGetLastError());
   // everything enqueued on the stage stream from here on runs after the update
@@ -770,7 +770,7 @@ int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf
   hs.ef = (hp->ef_lambda != 0.f && t >= 2) ? 1 : 0;
   hs.apply = t > 0 ? 1 : 0;
   launch_fused_update(n, x, g_prev, g_is_bf16 != 0, m, v, hp->ef_lambda != 0.f ? u_prev : nullptr,
-                      x_shadow, x_shadow ? (shadow_is_bf16 ? 2 : 1) : 0, hs, clip_scale_dev, nullptr,
+                      x_shadow, x_shadow ? (shadow_is_bf16 ? 2 : 1) : 0, hs, clip_scale_dev, nullptr, 0,
                       (hipStream_t)hip_stream);
   HIP_OK(hipGetLastError());
   return STAGE_OK;
@@ -802,7 +802,7 @@ int stage_poll_nonfinite(stage_t* s, int64_t* skipped) {
 int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev) {
   if (!s || !norm_dev || (which != 0 && which != 1)) return fail(STAGE_EINVAL, "bad argument");
   launch_grad_norm(s->grad[which], false, s->n_flat, 0.f, s->norm_part, s->norm_out, nullptr, nullptr,
-                   s->st);
+                   device_cu_count(), s->st);
   HIP_OK(hipMemcpyAsync(norm_dev, s->norm_out, 4, hipMemcpyDeviceToDevice, s->st));
   HIP_OK(hipGetLastError());
   return STAGE_OK;

@@ -60,6 +60,16 @@ __global__ void __launch_bounds__(NORM_THREADS) sumsq_partial(const G* __restric
   const int64_t hi = lo + per < n ? lo + per : n;
   double acc = 0.0;
   int64_t i = lo + 4 * threadIdx.x;
+  const int64_t B4 = 4 * (int64_t)blockDim.x;
+  for (; i + 3 * B4 + 3 < hi; i += 4 * B4) {  // four independent 16-byte loads in flight
+    float r[4][4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) load4<G>(g, i + k * B4, r[k]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      acc += (double)r[k][0] * r[k][0] + (double)r[k][1] * r[k][1] + (double)r[k][2] * r[k][2] +
+             (double)r[k][3] * r[k][3];
+  }
   for (; i + 3 < hi; i += 4 * blockDim.x) {
     float r[4];
     load4<G>(g, i, r);
@@ -164,6 +174,26 @@ __global__ void __launch_bounds__(256) fused_update(int64_t n, float* __restrict
     update_group<G, S, EF>(n, i0 + 4 * (int64_t)k * blockDim.x, x, g, m, v, up, shadow, hs, c, skip);
 }
 
+// Resident variant: a grid of a few blocks per CU walks the vector (V groups per thread and
+// pass), so that the pass shares the CUs with kernels of other streams instead of queueing a
+// block per 1024 elements in front of them.
+template <typename G, typename S, bool EF, int V>
+__global__ void __launch_bounds__(256) fused_update_resident(int64_t n, float* __restrict__ x,
+                                                             const G* __restrict__ g,
+                                                             float* __restrict__ m, float* __restrict__ v,
+                                                             float* __restrict__ up, S* __restrict__ shadow,
+                                                             UpdateScalars hs, const float* __restrict__ clip,
+                                                             const int* __restrict__ skip_flag) {
+  const bool skip = hs.apply == 0 || (skip_flag && skip_flag[0] != 0);
+  const float c = clip ? clip[0] : 1.0f;
+  const int64_t groups = (n + 3) / 4, stride = (int64_t)gridDim.x * blockDim.x * V;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x * V + threadIdx.x; q < groups; q += stride) {
+#pragma unroll
+    for (int k = 0; k < V; ++k)
+      update_group<G, S, EF>(n, 4 * (q + (int64_t)k * blockDim.x), x, g, m, v, up, shadow, hs, c, skip);
+  }
+}
+
 template <typename S>
 __global__ void __launch_bounds__(256) cast_copy(int64_t n, const float* __restrict__ src,
                                                  S* __restrict__ dst) {
@@ -185,8 +215,13 @@ __global__ void __launch_bounds__(256) zero_bytes(int64_t n16, int4* __restrict_
 template <typename G, typename S, bool EF, int V = 1>
 void launch_update_t(int64_t n, float* x, const void* g, float* m, float* v, float* up,
                      void* shadow, const UpdateScalars& hs, const float* clip, const int* flag,
-                     hipStream_t st) {
+                     int blocks, hipStream_t st) {
   const int64_t groups = cdiv(n, 4);
+  if (blocks > 0 && groups > (int64_t)blocks * 256 * 4) {
+    fused_update_resident<G, S, EF, 4><<<blocks, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow, hs,
+                                                               clip, flag);
+    return;
+  }
   const dim3 grid((unsigned)cdiv(groups, 256 * V));
   fused_update<G, S, EF, V><<<grid, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow, hs, clip,
                                                   flag);
@@ -197,20 +232,21 @@ void launch_update_t(int64_t n, float* x, const void* g, float* m, float* v, flo
 size_t norm_scratch_bytes() { return NORM_BLOCKS * sizeof(double); }
 
 void launch_grad_norm(const void* g, bool g_bf16, int64_t n, float clip, double* partial,
-                      float* out2, int* flag, unsigned long long* skipped, hipStream_t st) {
+                      float* out2, int* flag, unsigned long long* skipped, int blocks, hipStream_t st) {
+  const int nb = blocks > 0 && blocks < NORM_BLOCKS ? blocks : NORM_BLOCKS;
   if (g_bf16)
-    sumsq_partial<bf16><<<NORM_BLOCKS, NORM_THREADS, 0, st>>>((const bf16*)g, n, partial);
+    sumsq_partial<bf16><<<nb, NORM_THREADS, 0, st>>>((const bf16*)g, n, partial);
   else
-    sumsq_partial<float><<<NORM_BLOCKS, NORM_THREADS, 0, st>>>((const float*)g, n, partial);
-  norm_finish<<<1, 1024, 0, st>>>(partial, NORM_BLOCKS, clip, out2, flag, skipped);
+    sumsq_partial<float><<<nb, NORM_THREADS, 0, st>>>((const float*)g, n, partial);
+  norm_finish<<<1, 1024, 0, st>>>(partial, nb, clip, out2, flag, skipped);
 }
 
 void launch_fused_update(int64_t n, float* x, const void* g, bool g_bf16, float* m, float* v,
                          float* up, void* shadow, int shadow_kind, const UpdateScalars& hs,
-                         const float* clip, const int* flag, hipStream_t st) {
+                         const float* clip, const int* flag, int blocks, hipStream_t st) {
   // shadow_kind: 0 none, 1 fp32, 2 bf16.  EF instantiation whenever an EF buffer is present.
   const bool ef = up != nullptr;
-#define UPD(G, S, E) launch_update_t<G, S, E>(n, x, g, m, v, up, shadow, hs, clip, flag, st)
+#define UPD(G, S, E) launch_update_t<G, S, E>(n, x, g, m, v, up, shadow, hs, clip, flag, blocks, st)
   if (g_bf16) {
     if (shadow_kind == 2) { if (ef) UPD(bf16, bf16, true); else UPD(bf16, bf16, false); }
     else if (shadow_kind == 1) { if (ef) UPD(bf16, float, true); else UPD(bf16, float, false); }
