@@ -141,44 +141,47 @@ __device__ __forceinline__ void tile_origin(const GemmArgs& g, int b, int& m0, i
   n0 = ((b % (GM * tiles_n)) / gsz) * BN;
 }
 
-// Epilogue: per 16-row half of each 32-row fragment row of the wave tile, stage the fp32
-// accumulators through the wave's own LDS area and write 16-byte rows: split-K partials to the
-// workspace, or C with the beta / residual / SwiGLU-backward / RoPE / delta / SwiGLU-forward terms.
-// A wave reads back only what it wrote, and one wave's LDS operations complete in issue order, so
-// no barrier is needed between the halves and the global stores are never waited for here.  The
-// staging area (NW x 16 x (WN + 4) floats) must be free: every wave past its last read of it.
-template <int BM, int BN, int WM, int WN, typename OutT, bool CHECK>
+// Epilogue: per RP-row part (RP = 16 or 8) of each 32-row fragment row of the wave tile, stage
+// the fp32 accumulators through the wave's own LDS area and write 16-byte rows: split-K partials
+// to the workspace, or C with the beta / residual / SwiGLU-backward / RoPE / delta /
+// SwiGLU-forward terms.  A wave reads back only what it wrote, and one wave's LDS operations
+// complete in issue order, so no barrier is needed between the parts and the global stores are
+// never waited for here.  The staging area (NW x RP x (WN + 4) floats) must be free: every wave
+// past its last read of it.
+template <int BM, int BN, int WM, int WN, typename OutT, bool CHECK, int RP = 16>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[WM / 32][WN / 32],
                                               float* stage, int m0, int n0, int wm0, int wn0) {
+  static_assert(RP == 16 || RP == 8, "staging part of 8 or 16 rows");
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int EP = WN + 4;  // staging pitch (fp32 elements)
+  constexpr int NP = 32 / RP, EPP = 16 / NP;  // parts per fragment row, accumulators per part
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-  float* stg = stage + wave * 16 * EP;
+  float* stg = stage + wave * RP * EP;
   const bool split = g.ksplit > 1;
   float* W = split ? g.ws + (int64_t)blockIdx.y * g.M * g.N : nullptr;
   OutT* C = (OutT*)g.C;
   const bf16* R = (const bf16*)g.resid;
   constexpr int VEC = sizeof(OutT) == 2 ? 8 : 4;  // elements per 16-byte store
-  static_for<FM * 2>([&](auto IH) {
-    constexpr int i = IH / 2, h = IH % 2;
-    // accumulator e of lane l holds fragment row 8 (e / 4) + 4 (l / 32) + e mod 4: rows 16h..16h+15
-    // are e = 8h..8h+7
+  static_for<FM * NP>([&](auto IH) {
+    constexpr int i = IH / NP, h = IH % NP;
+    // accumulator e of lane l holds fragment row 8 (e / 4) + 4 (l / 32) + e mod 4: rows
+    // RP h .. RP h + RP - 1 are e = EPP h .. EPP h + EPP - 1
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int e = 8 * h; e < 8 * h + 8; ++e)
-        stg[(8 * (e / 4 - 2 * h) + 4 * (lane / 32) + (e % 4)) * EP + j * 32 + lane % 32] = acc[i][j][e];
+      for (int e = EPP * h; e < EPP * h + EPP; ++e)
+        stg[(8 * (e / 4) - RP * h + 4 * (lane / 32) + (e % 4)) * EP + j * 32 + lane % 32] = acc[i][j][e];
     asm volatile("" ::: "memory");
-    const int rbase = m0 + wm0 + i * 32 + 16 * h;
+    const int rbase = m0 + wm0 + i * 32 + RP * h;
     if (split) {
-      for (int c = lane; c < 16 * WN / 4; c += 64) {
+      for (int c = lane; c < RP * WN / 4; c += 64) {
         const int r = c / (WN / 4), cc = (c % (WN / 4)) * 4;
         const int row = rbase + r, col = n0 + wn0 + cc;
         if (!CHECK || (row < g.M && col < g.N))
           *reinterpret_cast<float4*>(W + (int64_t)row * g.N + col) = *reinterpret_cast<const float4*>(stg + r * EP + cc);
       }
     } else {
-      for (int c = lane; c < 16 * WN / VEC; c += 64) {
+      for (int c = lane; c < RP * WN / VEC; c += 64) {
         const int r = c / (WN / VEC), cc = (c % (WN / VEC)) * VEC;
         const int row = rbase + r, col = n0 + wn0 + cc;
         if (CHECK && (row >= g.M || col >= g.N)) continue;  // N is a multiple of 8
@@ -437,7 +440,9 @@ struct DmaCfg {
   using TB = DmaTile<BN, BKT, BKM, NT>;
   // one stage: the A tile, then the B tile (bf16 elements)
   static constexpr int STAGE = TA::ELEMS + TB::ELEMS;
-  static constexpr size_t epi_lds = (size_t)NW * 16 * (WN + 4) * sizeof(float);
+  // epilogue staging rows per part: 16 when that fits in one stage, else 8
+  static constexpr int RP = (size_t)NW * 16 * (WN + 4) * sizeof(float) <= (size_t)STAGE * sizeof(bf16) ? 16 : 8;
+  static constexpr size_t epi_lds = (size_t)NW * RP * (WN + 4) * sizeof(float);
   // A block walks several tiles when the epilogue's staging fits in one stage: the stage of a
   // tile's last slice is then free for it while the next tile's first slices land in the others.
   static constexpr bool persist = epi_lds <= (size_t)STAGE * sizeof(bf16);
@@ -491,7 +496,9 @@ gemm_dma_kernel(GemmArgs g) {
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int PA = TA::PER, PB = TB::PER;
   // vector-memory operations one thread's epilogue issues at least: one per 16-byte output chunk
-  constexpr int EPI_OPS = FM * 2 * (16 * WN / (sizeof(OutT) == 2 ? 8 : 4) / 64);
+  constexpr int RP = C_::RP, CPP = RP * WN / (sizeof(OutT) == 2 ? 8 : 4);  // 16-byte chunks per part
+  static_assert(CPP % 64 == 0, "every lane stores the same number of chunks per part");
+  constexpr int EPI_OPS = FM * (32 / RP) * (CPP / 64);
   static_assert((NS - 2) * (PA + PB) + EPI_OPS < 64, "vmcnt range");
   extern __shared__ __align__(16) unsigned char smem[];
   bf16* S = reinterpret_cast<bf16*>(smem);  // [NS][A tile | B tile]
@@ -614,7 +621,7 @@ gemm_dma_kernel(GemmArgs g) {
     }
     wait_vm_lds<63>();
     block_barrier();
-    gemm_epilogue<BM, BN, WM, WN, OutT, false>(g, acc, stg, m0, n0, wm0, wn0);
+    gemm_epilogue<BM, BN, WM, WN, OutT, false, C_::RP>(g, acc, stg, m0, n0, wm0, wn0);
     if (!next) break;
     t = tn; m0 = m1; n0 = n1; at = atn; bt = btn;
   }
@@ -709,6 +716,18 @@ bool launch_dma_cfg(const GemmArgs& g, hipStream_t st) {
 
 }  // namespace
 
+namespace {
+// Tile choice for full tiles: 256 x 256 (8 waves of 64 x 128, 64-deep slices in 2 stages) when the
+// product has enough of them and is deep enough for the larger tile to pay (at K = 768 the
+// persistent 128 x 128 kernel is faster, from K = 1536 on the 256 x 256 one), else 128 x 128.
+constexpr int BIG_K = 1536;
+bool use_big(const GemmArgs& g) {
+  const int64_t t256 = cdiv(g.M, 256) * cdiv(g.N, 256);
+  return g.M % 256 == 0 && g.N % 256 == 0 && g.K % 64 == 0 && g.K >= BIG_K &&
+         (t256 >= 512 || (t256 >= 256 && g.K >= 2048));
+}
+}  // namespace
+
 int device_cu_count() {
   static int cus[64] = {};
   int dev = 0;
@@ -746,24 +765,19 @@ bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
     // delta rides in the epilogue of the direct-to-LDS kernels when a wave's columns hold whole
     // heads (every lane of the epilogue active); otherwise the caller computes it separately
     const bool full = !g0.out_f32 && g0.K > 0 && g0.K % 64 == 0 && g0.M % 128 == 0 && g0.N % 128 == 0;
-    const bool big = full && g0.M % 256 == 0 && g0.N % 256 == 0 &&
-                     (cdiv(g0.M, 256) * cdiv(g0.N, 256) >= 512 ||
-                      (cdiv(g0.M, 256) * cdiv(g0.N, 256) >= 256 && g0.K >= 2048));
-    const int wn = big ? 128 : 64;
+    const int wn = full && use_big(g0) ? 128 : 64;
     if (!full || g0.delta_hd < 8 || wn % g0.delta_hd || g0.ld_aux % 8 || (uintptr_t)g0.aux % 16) return false;
   }
   GemmArgs g = g0;
   g.ksplit = 1;
   const int64_t mn = (int64_t)g.M * g.N;
-  // Full tiles go to the direct-to-LDS kernels: 256 x 256 (8 waves of 64 x 128, 32-deep slices in
-  // 4 stages) when the product has enough of them (or is deep enough to amortise them), else
-  // 128 x 128 (4 waves, 64-deep slices in 2 stages: half the barriers per MFMA, two blocks per CU);
-  // ragged shapes to the register-staged kernel with bounds-checked loads.
-  constexpr int DKB = 32, DKS = 64;
+  // Full tiles go to the direct-to-LDS kernels (use_big picks 256 x 256 or 128 x 128: 4 waves,
+  // 64-deep slices in 2 stages, two blocks per CU, persistent when the tiles outnumber the
+  // blocks the chip holds); ragged shapes to the register-staged kernel with bounds-checked loads.
+  constexpr int DKB = 64, DKS = 64;
   const bool full128 = g.M % 128 == 0 && g.N % 128 == 0 && g.K % DKS == 0;
   const int64_t t256 = cdiv(g.M, 256) * cdiv(g.N, 256), t128 = cdiv(g.M, 128) * cdiv(g.N, 128);
-  const bool big = g.M % 256 == 0 && g.N % 256 == 0 && g.K % DKB == 0 &&
-                   (t256 >= 512 || (t256 >= 256 && g.K >= 2048));
+  const bool big = use_big(g);
   const int64_t tiles = big ? t256 : t128;
   if (g.out_f32 && g.ws && g.ldc == g.N && tiles < 512 && g.K >= 2048) {
     // deterministic split-K for underfilled fp32-output products: whole slices per split
@@ -778,8 +792,8 @@ bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   if (rope_after) g.epi = 0;
   bool done = false;  // the direct-to-LDS launchers decline shapes they do not take (K = 0)
   if (big)
-    done = g.out_f32 ? launch_dma_cfg<256, 256, 64, 128, float, DKB, 4>(g, st)
-                     : launch_dma_cfg<256, 256, 64, 128, bf16, DKB, 4>(g, st);
+    done = g.out_f32 ? launch_dma_cfg<256, 256, 64, 128, float, DKB, 2>(g, st)
+                     : launch_dma_cfg<256, 256, 64, 128, bf16, DKB, 2>(g, st);
   else if (full128)
     done = g.out_f32 ? launch_dma_cfg<128, 128, 64, 64, float, DKS, 2>(g, st)
                      : launch_dma_cfg<128, 128, 64, 64, bf16, DKS, 2>(g, st);
