@@ -119,31 +119,46 @@ __device__ __forceinline__ bf16x8 acc_rows_to_b(const f32x16& s) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// KB rows x HD of a head (row stride ld) through registers into a swizzled LDS tile; rows at or
-// beyond S are zero.
+// Streamed tiles: KB rows x HD of a head (row stride ld) land in a swizzled [KB][HD] LDS tile by
+// direct-to-LDS loads.  Load q of a wave writes 1 KB (16 bytes per lane, in lane order), so LDS
+// chunk p = (q * 4 + wave) * 64 + lane of the tile holds row p / (HD/8), data chunk
+// (p mod HD/8) ^ swz(row): the layout tidx reads.  Rows at or beyond the tile's valid rows repeat
+// its last valid row (finite data whose probabilities the causal mask makes exactly zero).
 template <int HD>
-struct RowTile {
-  static constexpr int PER = KB * HD / 8 / NT;
-  static constexpr int PERR = PER > 0 ? PER : 1;
-  u32x4 r[PERR];
-  __device__ __forceinline__ void load(const bf16* __restrict__ g, int ld, int row0, int S) {
-#pragma unroll
-    for (int p = 0; p < PERR; ++p) {
-      const int c = threadIdx.x + p * NT;
-      const int row = row0 + c / (HD / 8), d = (c % (HD / 8)) * 8;
-      const bool ok = (PER > 0 || c < KB * HD / 8) && row < S;
-      r[p] = ok ? *reinterpret_cast<const u32x4*>(g + (int64_t)row * ld + d) : u32x4{0u, 0u, 0u, 0u};
-    }
+struct DmaRowTile {
+  static constexpr int CPR = HD / 8;
+  static constexpr int PER = KB * CPR / NT;  // loads per thread and tile
+  static_assert(PER * NT == KB * CPR, "tile does not split evenly over the threads");
+  // byte offset, from the tile's first row in global memory, of this thread's q-th load
+  __device__ static uint32_t voff(int q, int ld, int rows) {
+    const int p = (q * (NT / 64) + (int)threadIdx.x / 64) * 64 + (int)threadIdx.x % 64;
+    const int r = p / CPR, kc = (p % CPR) ^ swz<HD>(r);
+    return 2u * (uint32_t)(min(r, rows - 1) * ld + kc * 8);
   }
-  __device__ __forceinline__ void store(bf16* __restrict__ T) const {
+  // the tile's rows [row0, row0 + KB) of g (rows below S valid) into the LDS tile at lds
+  __device__ static void issue(const bf16* g, int ld, int row0, int S, uint32_t lds) {
+    const bf16* t = g + (int64_t)row0 * ld;
+    const uint32_t w = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x / 64) * 1024u;
 #pragma unroll
-    for (int p = 0; p < PERR; ++p) {
-      const int c = threadIdx.x + p * NT;
-      if (PER > 0 || c < KB * HD / 8)
-        *reinterpret_cast<u32x4*>(T + tidx<HD>(c / (HD / 8), (c % (HD / 8)) * 8)) = r[p];
-    }
+    for (int q = 0; q < PER; ++q) dma16(t, voff(q, ld, S - row0), lds + w + (uint32_t)q * (NT / 64) * 1024u);
   }
 };
+
+// stages of the streamed-tile ring: a tile's loads are issued NS - 1 iterations before it is used
+template <int HD>
+constexpr int ring_stages() { return HD == 64 ? 3 : 2; }
+
+// Waits until this thread's loads of the current iteration's stage are in LDS: issued after them
+// are the loads of the next NS - 2 iterations, those that exist (`more` = the next iteration does)
+template <int NS, int PER_STAGE>
+__device__ __forceinline__ void ring_wait(bool more) {
+  if constexpr (NS >= 3) {
+    if (more) wait_vm_lds<(NS - 2) * PER_STAGE>();
+    else wait_vm_lds<0>();
+  } else {
+    wait_vm_lds<0>();
+  }
+}
 
 // Writes a wave's 32 columns of X^T (accumulators: rows d, column = the wave's 32 rows) as rows of
 // out (row stride ldo) through the LDS staging area, scaled.  Ends with all staging reads done.
@@ -187,30 +202,45 @@ __device__ __forceinline__ void store_rows_from_t(float* __restrict__ stage, con
   __syncthreads();
 }
 
+// Work item of block L in a 1-D grid of N blocks made of units of per_unit items (a unit: the
+// blocks of one head, which stream the same K/V or Q/dO rows).  The hardware places block L on XCD
+// L mod 8; when N is a multiple of 8, XCD x gets the contiguous run [x N/8, (x+1) N/8) of items, so
+// a unit's blocks share that XCD's L2 instead of each XCD fetching every head.
+__device__ __forceinline__ void xcd_item(int L, int N, int per_unit, int& unit, int& idx) {
+  const int r = (N % 8 == 0) ? (L % 8) * (N / 8) + L / 8 : L;
+  unit = r / per_unit;
+  idx = r % per_unit;
+}
+
 template <int HD>
 struct Lds {
-  static constexpr int TSZ = KB * HD;    // one [KB][HD] tile
+  static constexpr int NS = ring_stages<HD>();
+  static constexpr int TSZ = KB * HD;  // elements of one [KB][HD] tile
   static constexpr size_t out_bytes = (size_t)QB * (HD + 4) * 4;  // fp32 output staging
-  static constexpr size_t fwd_bytes() { const size_t t = (size_t)4 * TSZ * 2; return t > out_bytes ? t : out_bytes; }
+  // forward and dQ: a stage holds a K and a V tile; dK/dV: a Q and a dO tile, then the lse and
+  // delta values of the tile's rows
+  static constexpr size_t kv_stage = (size_t)2 * TSZ * 2;
+  static constexpr size_t qd_stage = (size_t)2 * TSZ * 2 + 2 * KB * 4;
+  static constexpr size_t mx(size_t x, size_t y) { return x > y ? x : y; }
+  static constexpr size_t fwd_bytes() { return mx(NS * kv_stage, out_bytes); }
   static constexpr size_t dq_bytes() { return fwd_bytes(); }
-  static constexpr size_t dkv_bytes() {
-    const size_t t = (size_t)4 * TSZ * 2 + 4 * KB * 4;
-    return t > out_bytes ? t : out_bytes;
-  }
+  static constexpr size_t dkv_bytes() { return mx(NS * qd_stage, out_bytes); }
 };
 
 // ------------------------------------------------------------------------------------------ forward
 template <int HD>
 __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
   using L = Lds<HD>;
-  constexpr int KS = HD / 16, DT = HD / 32;
+  using TT = DmaRowTile<HD>;
+  constexpr int KS = HD / 16, DT = HD / 32, NS = L::NS;
   extern __shared__ __align__(16) unsigned char smem[];
-  bf16* Ks0 = reinterpret_cast<bf16*>(smem);   // [2][KB][HD], swizzled
-  bf16* Vs0 = Ks0 + 2 * L::TSZ;                // [2][KB][HD], swizzled
+  bf16* ring = reinterpret_cast<bf16*>(smem);  // [NS][K tile | V tile], swizzled
 
   const int nqb = (a.S + QB - 1) / QB;
-  const int qb = nqb - 1 - blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  int unit, idx;  // unit: (batch, query head); heaviest query blocks first
+  xcd_item(blockIdx.x, nqb * a.Hq * a.B, nqb, unit, idx);
+  const int qb = nqb - 1 - idx;
+  const int h = unit % a.Hq, b = unit / a.Hq;
   const int kvh = h / (a.Hq / a.Hkv);
   const int ld = (a.Hq + 2 * a.Hkv) * HD;
   const bf16* base = (const bf16*)a.qkv + (int64_t)b * a.S * ld;
@@ -218,13 +248,24 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
   const bf16* vbase = base + (a.Hq + a.Hkv + kvh) * HD;
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64, half = lane / 32, col = lane % 32;
   const int q0 = qb * QB + wave * 32, myq = q0 + col;
-
+  const int nkb = min(a.S - 1, qb * QB + QB - 1) / KB + 1;
+  auto issue = [&](int kb) {
+    bf16* st = ring + (kb % NS) * 2 * L::TSZ;
+    TT::issue(kbase, ld, kb * KB, a.S, lds_addr(st));
+    TT::issue(vbase, ld, kb * KB, a.S, lds_addr(st + L::TSZ));
+  };
   bf16x8 qf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     if (myq < a.S) qf[ks] = *reinterpret_cast<const bf16x8*>(base + (int64_t)myq * ld + h * HD + ks * 16 + 8 * half);
     else for (int j = 0; j < 8; ++j) qf[ks][j] = (bf16)0.f;
   }
+  // The register loads complete here, so that no wait the compiler places for them lands inside
+  // the loop (a vmcnt wait there would also drain the ring's loads in flight).
+  wait_vm_lds<0>();
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nkb) issue(s);
   const float sl2 = LOG2E / sqrtf((float)HD);
   f32x16 o[DT];
 #pragma unroll
@@ -233,21 +274,12 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
     for (int e = 0; e < 16; ++e) o[dt][e] = 0.f;
   float m = -INFINITY, lsum = 0.f;
 
-  const int nkb = min(a.S - 1, qb * QB + QB - 1) / KB + 1;
-  RowTile<HD> tk, tv;
-  tk.load(kbase, ld, 0, a.S);
-  tv.load(vbase, ld, 0, a.S);
-  tk.store(Ks0);
-  tv.store(Vs0);
-  __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
-    const int cur = kb & 1;
-    if (kb + 1 < nkb) {
-      tk.load(kbase, ld, (kb + 1) * KB, a.S);
-      tv.load(vbase, ld, (kb + 1) * KB, a.S);
-    }
-    const bf16* Ks = Ks0 + cur * L::TSZ;
-    const bf16* Vs = Vs0 + cur * L::TSZ;
+    ring_wait<NS, 2 * TT::PER>(kb + 1 < nkb);
+    block_barrier();  // every thread's loads of tile kb are in; every wave is done with tile kb - 1
+    if (kb + NS - 1 < nkb) issue(kb + NS - 1);  // into the stage tile kb - 1 occupied
+    const bf16* Ks = ring + (kb % NS) * 2 * L::TSZ;
+    const bf16* Vs = Ks + L::TSZ;
     const int key0 = kb * KB;
     if (key0 <= q0 + 31) {  // some key of this block is visible to some query of this wave
       f32x16 s[2];
@@ -305,12 +337,8 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Vs, dt * 32, kk * 16), pf, o[dt], 0, 0, 0);
       }
     }
-    if (kb + 1 < nkb) {
-      tk.store(Ks0 + (cur ^ 1) * L::TSZ);
-      tv.store(Vs0 + (cur ^ 1) * L::TSZ);
-    }
-    __syncthreads();
   }
+  block_barrier();  // every wave is done with the last tile: the ring becomes the output staging
   if (half == 0 && myq < a.S)
     a.lse[((int64_t)b * a.Hq + h) * a.S + myq] = (m + log2f(lsum)) * 0.6931471805599453f;
   const float inv = lsum > 0.f ? 1.0f / lsum : 0.f;
@@ -323,9 +351,9 @@ template <int HD>
 __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, int bz,
     unsigned char* __restrict__ smem) {
   using L = Lds<HD>;
-  constexpr int KS = HD / 16, DT = HD / 32;
-  bf16* Ks0 = reinterpret_cast<bf16*>(smem);
-  bf16* Vs0 = Ks0 + 2 * L::TSZ;
+  using TT = DmaRowTile<HD>;
+  constexpr int KS = HD / 16, DT = HD / 32, NS = L::NS;
+  bf16* ring = reinterpret_cast<bf16*>(smem);  // [NS][K tile | V tile], swizzled
   const int nqb = (a.S + QB - 1) / QB;
   const int qb = nqb - 1 - bx;
   const int h = by, b = bz;
@@ -337,6 +365,12 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
   const bf16* dob = (const bf16*)a.dout + (int64_t)b * a.S * hqd + h * HD;
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64, half = lane / 32, col = lane % 32;
   const int q0 = qb * QB + wave * 32, myq = q0 + col;
+  const int nkb = min(a.S - 1, qb * QB + QB - 1) / KB + 1;
+  auto issue = [&](int kb) {
+    bf16* st = ring + (kb % NS) * 2 * L::TSZ;
+    TT::issue(kbase, ld, kb * KB, a.S, lds_addr(st));
+    TT::issue(vbase, ld, kb * KB, a.S, lds_addr(st + L::TSZ));
+  };
   bf16x8 qf[KS], df[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
@@ -349,27 +383,22 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
   }
   const int64_t sidx = ((int64_t)b * a.Hq + h) * a.S + min(myq, a.S - 1);
   const float lse2 = a.lse[sidx] * LOG2E, dl = a.delta[sidx];
+  wait_vm_lds<0>();  // register loads done before the ring starts (as in the forward)
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nkb) issue(s);
   const float sl2 = LOG2E / sqrtf((float)HD);
   f32x16 dq[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) dq[dt][e] = 0.f;
-  const int nkb = min(a.S - 1, qb * QB + QB - 1) / KB + 1;
-  RowTile<HD> tk, tv;
-  tk.load(kbase, ld, 0, a.S);
-  tv.load(vbase, ld, 0, a.S);
-  tk.store(Ks0);
-  tv.store(Vs0);
-  __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
-    const int cur = kb & 1;
-    if (kb + 1 < nkb) {
-      tk.load(kbase, ld, (kb + 1) * KB, a.S);
-      tv.load(vbase, ld, (kb + 1) * KB, a.S);
-    }
-    const bf16* Ks = Ks0 + cur * L::TSZ;
-    const bf16* Vs = Vs0 + cur * L::TSZ;
+    ring_wait<NS, 2 * TT::PER>(kb + 1 < nkb);
+    block_barrier();  // every thread's loads of tile kb are in; every wave is done with tile kb - 1
+    if (kb + NS - 1 < nkb) issue(kb + NS - 1);
+    const bf16* Ks = ring + (kb % NS) * 2 * L::TSZ;
+    const bf16* Vs = Ks + L::TSZ;
     const int key0 = kb * KB;
     if (key0 <= q0 + 31) {
 #pragma unroll
@@ -404,12 +433,8 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
         }
       }
     }
-    if (kb + 1 < nkb) {
-      tk.store(Ks0 + (cur ^ 1) * L::TSZ);
-      tv.store(Vs0 + (cur ^ 1) * L::TSZ);
-    }
-    __syncthreads();
   }
+  block_barrier();  // every wave is done with the last tile: the ring becomes the output staging
   store_rows_from_t<HD>(reinterpret_cast<float*>(smem), dq, 1.0f / sqrtf((float)HD),
                         (bf16*)a.dqkv + (int64_t)b * a.S * ld + h * HD, ld, qb * QB, a.S, a.rope_cos, a.rope_sin);
 }
@@ -417,7 +442,10 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
 template <int HD>
 __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  bwd_dq_block<HD>(a, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+  const int nqb = (a.S + QB - 1) / QB;
+  int unit, idx;  // unit: (batch, query head)
+  xcd_item(blockIdx.x, nqb * a.Hq * a.B, nqb, unit, idx);
+  bwd_dq_block<HD>(a, idx, unit % a.Hq, unit / a.Hq, smem);
 }
 
 // ------------------------------------------------------------------------------------------ dK, dV
@@ -425,11 +453,11 @@ template <int HD>
 __device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by, int bz,
     unsigned char* __restrict__ smem) {
   using L = Lds<HD>;
-  constexpr int KS = HD / 16, DT = HD / 32;
-  bf16* Qs0 = reinterpret_cast<bf16*>(smem);   // [2][KB][HD], swizzled
-  bf16* Ds0 = Qs0 + 2 * L::TSZ;                // [2][KB][HD], swizzled
-  float* Ls0 = reinterpret_cast<float*>(Ds0 + 2 * L::TSZ);  // [2][KB]
-  float* Dl0 = Ls0 + 2 * KB;                                 // [2][KB]
+  using TT = DmaRowTile<HD>;
+  constexpr int KS = HD / 16, DT = HD / 32, NS = L::NS;
+  // stage: Q tile, dO tile (swizzled [KB][HD] each), lse[KB], delta[KB]
+  constexpr int SSZ = (int)(L::qd_stage / 2);  // stage size in bf16 elements
+  bf16* ring = reinterpret_cast<bf16*>(smem);
   const int kbk = bx;  // block of 128 keys; low blocks see the most queries and go first
   const int kvh = by, b = bz;
   const int group = a.Hq / a.Hkv;
@@ -438,6 +466,23 @@ __device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by,
   const bf16* dbase = (const bf16*)a.dout + (int64_t)b * a.S * hqd;
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64, half = lane / 32, col = lane % 32;
   const int k0 = kbk * QB + wave * 32, mykey = k0 + col;
+  // iterations: every (query head of the group, query block at or after this key block)
+  const int qblk0 = (kbk * QB) / KB;
+  const int nqblk = (a.S + KB - 1) / KB;
+  const int per_head = nqblk - qblk0;
+  const int nit = group * per_head;
+  // each wave loads one row vector per stage: waves 0 and 2 the lse values, 1 and 3 the deltas
+  // (the same data twice, so that every thread has the same number of loads in flight)
+  const float* rowv = (__builtin_amdgcn_readfirstlane(wave) & 1) ? a.delta : a.lse;
+  auto issue = [&](int it) {
+    const int h = kvh * group + it / per_head, qs0 = (qblk0 + it % per_head) * KB;
+    bf16* st = ring + (it % NS) * SSZ;
+    TT::issue(base + h * HD, ld, qs0, a.S, lds_addr(st));
+    TT::issue(dbase + h * HD, hqd, qs0, a.S, lds_addr(st + L::TSZ));
+    const float* rv = rowv + ((int64_t)b * a.Hq + h) * a.S;
+    dma4(rv, 4u * (uint32_t)min(qs0 + lane, a.S - 1),
+         lds_addr(reinterpret_cast<float*>(st + 2 * L::TSZ) + (__builtin_amdgcn_readfirstlane(wave) & 1) * KB));
+  };
   bf16x8 kf[KS], vf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
@@ -448,46 +493,24 @@ __device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by,
       for (int j = 0; j < 8; ++j) { kf[ks][j] = (bf16)0.f; vf[ks][j] = (bf16)0.f; }
     }
   }
+  wait_vm_lds<0>();  // register loads done before the ring starts (as in the forward)
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nit) issue(s);
   const float sl2 = LOG2E / sqrtf((float)HD);
   f32x16 dk[DT], dv[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
     for (int e = 0; e < 16; ++e) { dk[dt][e] = 0.f; dv[dt][e] = 0.f; }
-  // iterations: every (query head of the group, query block at or after this key block)
-  const int qblk0 = (kbk * QB) / KB;
-  const int nqblk = (a.S + KB - 1) / KB;
-  const int per_head = nqblk - qblk0;
-  const int nit = group * per_head;
-  RowTile<HD> tq, td;
-  float lv = 0.f, dv1 = 0.f;
-  auto fetch = [&](int it) {
-    const int h = kvh * group + it / per_head, qs0 = (qblk0 + it % per_head) * KB;
-    tq.load(base + h * HD, ld, qs0, a.S);
-    td.load(dbase + h * HD, hqd, qs0, a.S);
-    if (threadIdx.x < KB) {
-      const int64_t srow = ((int64_t)b * a.Hq + h) * a.S + min(qs0 + (int)threadIdx.x, a.S - 1);
-      lv = a.lse[srow] * LOG2E;
-      dv1 = a.delta[srow];
-    }
-  };
-  auto commit = [&](int buf) {
-    tq.store(Qs0 + buf * L::TSZ);
-    td.store(Ds0 + buf * L::TSZ);
-    if (threadIdx.x < KB) { Ls0[buf * KB + threadIdx.x] = lv; Dl0[buf * KB + threadIdx.x] = dv1; }
-  };
-  if (nit > 0) {
-    fetch(0);
-    commit(0);
-  }
-  __syncthreads();
   for (int it = 0; it < nit; ++it) {
-    const int cur = it & 1;
-    if (it + 1 < nit) fetch(it + 1);
-    const bf16* Qs = Qs0 + cur * L::TSZ;
-    const bf16* Ds = Ds0 + cur * L::TSZ;
-    const float* Ls = Ls0 + cur * KB;
-    const float* Dl = Dl0 + cur * KB;
+    ring_wait<NS, 2 * TT::PER + 1>(it + 1 < nit);
+    block_barrier();  // every thread's loads of iteration it are in; every wave is done with it - 1
+    if (it + NS - 1 < nit) issue(it + NS - 1);
+    const bf16* Qs = ring + (it % NS) * SSZ;
+    const bf16* Ds = Qs + L::TSZ;
+    const float* Ls = reinterpret_cast<const float*>(Qs + 2 * L::TSZ);
+    const float* Dl = Ls + KB;
     const int qs0 = (qblk0 + it % per_head) * KB;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -515,7 +538,7 @@ __device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by,
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int e = 4 * e4 + j;
-            const float p = fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j]));
+            const float p = fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j] * LOG2E));
             s[e] = p;
             dp[e] = p * (dp[e] - d4[j]);
           }
@@ -523,7 +546,7 @@ __device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by,
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int e = 4 * e4 + j, q = qs0 + r0 + j;
-            const float p = (q >= mykey && q < a.S) ? fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j])) : 0.f;
+            const float p = (q >= mykey && q < a.S) ? fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j] * LOG2E)) : 0.f;
             s[e] = p;
             dp[e] = p * (dp[e] - d4[j]);
           }
@@ -540,9 +563,8 @@ __device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by,
         }
       }
     }
-    if (it + 1 < nit) commit(cur ^ 1);
-    __syncthreads();
   }
+  block_barrier();  // every wave is done with the last stage: the ring becomes the output staging
   bf16* outb = (bf16*)a.dqkv + (int64_t)b * a.S * ld;
   store_rows_from_t<HD>(reinterpret_cast<float*>(smem), dk, 1.0f / sqrtf((float)HD), outb + (a.Hq + kvh) * HD, ld,
                         kbk * QB, a.S, a.rope_cos, a.rope_sin);
@@ -553,24 +575,28 @@ __device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by,
 template <int HD>
 __global__ void __launch_bounds__(NT) flash_bwd_dkv(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  bwd_dkv_block<HD>(a, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+  const int nkb = (a.S + QB - 1) / QB;
+  int unit, idx;  // unit: (batch, key/value head); low key blocks (the most queries) first
+  xcd_item(blockIdx.x, nkb * a.Hkv * a.B, nkb, unit, idx);
+  bwd_dkv_block<HD>(a, idx, unit % a.Hkv, unit / a.Hkv, smem);
 }
 
-// dQ and dK/dV work items in one launch (independent given delta): the dQ items (query blocks x
-// query heads x batch, heaviest first within each head) then the dK/dV items, so the two fill the
-// CUs together instead of each leaving a tail.
+// dQ and dK/dV work items in one launch (independent given delta), so the two fill the CUs
+// together instead of each leaving a tail.  A unit is one (batch, key/value head): its dK/dV items
+// and the dQ items of its query heads, which all stream that head group's rows, on one XCD.
+// Within a unit, level k holds dK/dV block k and query block nb - 1 - k of each query head: the
+// items of one level have the same causal extent, and heavier levels come first.
 template <int HD>
 __global__ void __launch_bounds__(NT) flash_bwd_fused(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int nb = (a.S + QB - 1) / QB;
-  const int n_dq = nb * a.Hq * a.B;
-  int i = blockIdx.x;
-  if (i < n_dq) {
-    bwd_dq_block<HD>(a, i % nb, (i / nb) % a.Hq, i / (nb * a.Hq), smem);
-  } else {
-    i -= n_dq;
-    bwd_dkv_block<HD>(a, i % nb, (i / nb) % a.Hkv, i / (nb * a.Hkv), smem);
-  }
+  const int group = a.Hq / a.Hkv, per_unit = nb * (group + 1);
+  int unit, idx;
+  xcd_item(blockIdx.x, per_unit * a.Hkv * a.B, per_unit, unit, idx);
+  const int kvh = unit % a.Hkv, b = unit / a.Hkv;
+  const int level = idx / (group + 1), j = idx % (group + 1);
+  if (j == 0) bwd_dkv_block<HD>(a, level, kvh, b, smem);
+  else bwd_dq_block<HD>(a, level, kvh * group + j - 1, b, smem);
 }
 
 // delta[b, h, i] = sum_d dO[b, i, h, d] O[b, i, h, d]; one thread per (token, head)
@@ -603,7 +629,7 @@ template <int HD>
 void fwd_launch(const AttnArgs& a, hipStream_t st) {
   static bool attr = false;
   if (!attr) { set_lds(flash_fwd<HD>, Lds<HD>::fwd_bytes()); attr = true; }
-  flash_fwd<HD><<<dim3((unsigned)cdiv(a.S, QB), a.Hq, a.B), NT, Lds<HD>::fwd_bytes(), st>>>(a);
+  flash_fwd<HD><<<(unsigned)(cdiv(a.S, QB) * a.Hq * a.B), NT, Lds<HD>::fwd_bytes(), st>>>(a);
 }
 
 template <int HD>
@@ -623,8 +649,8 @@ void bwd_launch(const AttnArgs& a, hipStream_t st) {
     const int nb = (int)cdiv(a.S, QB);
     flash_bwd_fused<HD><<<(unsigned)(nb * (a.Hq + a.Hkv) * a.B), NT, bytes, st>>>(a);
   } else {
-    flash_bwd_dq<HD><<<dim3((unsigned)cdiv(a.S, QB), a.Hq, a.B), NT, Lds<HD>::dq_bytes(), st>>>(a);
-    flash_bwd_dkv<HD><<<dim3((unsigned)cdiv(a.S, QB), a.Hkv, a.B), NT, Lds<HD>::dkv_bytes(), st>>>(a);
+    flash_bwd_dq<HD><<<(unsigned)(cdiv(a.S, QB) * a.Hq * a.B), NT, Lds<HD>::dq_bytes(), st>>>(a);
+    flash_bwd_dkv<HD><<<(unsigned)(cdiv(a.S, QB) * a.Hkv * a.B), NT, Lds<HD>::dkv_bytes(), st>>>(a);
   }
 }
 

@@ -82,3 +82,36 @@ template <int N, typename F>
 __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
+
+// ------------------------------------------------------------------ direct-to-LDS loads (gfx950)
+// s_waitcnt: at most N vector-memory operations and no LDS operation outstanding
+template <int N>
+__device__ __forceinline__ void wait_vm_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+}
+
+// One 16-byte global -> LDS load per lane from base + voff bytes (base wave-uniform; lane l
+// writes lds + 16 l).  Issued as inline assembly so that the compiler neither counts it in its own
+// waits nor orders LDS reads after it: a kernel waits for these loads itself (wait_vm_lds)
+// before the barrier that publishes the LDS they fill.
+__device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(lds) : "memory");
+}
+// The same with 4 bytes per lane (lane l writes lds + 4 l).
+__device__ __forceinline__ void dma4(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("global_load_lds_dword %0, %1" ::"v"(voff), "s"(base), "{m0}"(lds) : "memory");
+}
+
+__device__ __forceinline__ void block_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// LDS byte address of a pointer into __shared__ memory (the m0 operand of dma16 / dma4)
+template <typename T>
+__device__ __forceinline__ uint32_t lds_addr(const T* p) {
+  typedef __attribute__((address_space(3))) const T lds_t;
+  return (uint32_t)(uintptr_t)(lds_t*)p;
+}

@@ -270,6 +270,220 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[W
   });
 }
 
+// Epilogue kinds of the direct-to-LDS kernels (compile-time; the numbers of the first five are
+// GemmArgs::epi): bf16 output as is, SwiGLU backward, RoPE, SwiGLU forward, attention delta, plus
+// a residual row added.
+enum { EPI_PLAIN = 0, EPI_SWIGLU_BWD = 1, EPI_ROPE = 2, EPI_SWIGLU_FWD = 3, EPI_DELTA = 4, EPI_RESID = 5 };
+
+// Global operands of one 16-byte output chunk (8 bf16 columns) that an epilogue reads.
+template <int EPI> struct EpiIn { static constexpr bool loads = false; };
+template <> struct EpiIn<EPI_RESID> { static constexpr bool loads = true; bf16x8 r; };
+template <> struct EpiIn<EPI_SWIGLU_BWD> { static constexpr bool loads = true; bf16x8 a, b; };
+template <> struct EpiIn<EPI_DELTA> { static constexpr bool loads = true; bf16x8 o; };
+template <> struct EpiIn<EPI_ROPE> { static constexpr bool loads = true; f32x4 c0, c1, s0, s1; };
+
+template <int EPI>
+__device__ __forceinline__ void epi_load(EpiIn<EPI>& in, const GemmArgs& g, int row, int col) {
+  if constexpr (EPI == EPI_RESID) {
+    in.r = ld_nt<bf16x8>((const bf16*)g.resid + (int64_t)row * g.ldc + col);
+  } else if constexpr (EPI == EPI_SWIGLU_BWD) {
+    const bf16* gu = (const bf16*)g.aux + (int64_t)row * g.ld_aux + col;
+    in.a = ld_nt<bf16x8>(gu);
+    in.b = ld_nt<bf16x8>(gu + g.N);
+  } else if constexpr (EPI == EPI_DELTA) {
+    in.o = ld_nt<bf16x8>((const bf16*)g.aux + (int64_t)row * g.ld_aux + col);
+  } else if constexpr (EPI == EPI_ROPE) {
+    if (col < g.rope_cols) {
+      const int hh = g.rope_hd / 2, i0 = (col % g.rope_hd) % hh;
+      const int64_t tb = (int64_t)(row % g.rope_S) * hh + i0;
+      in.c0 = *reinterpret_cast<const f32x4*>(g.rope_cos + tb);
+      in.c1 = *reinterpret_cast<const f32x4*>(g.rope_cos + tb + 4);
+      in.s0 = *reinterpret_cast<const f32x4*>(g.rope_sin + tb);
+      in.s1 = *reinterpret_cast<const f32x4*>(g.rope_sin + tb + 4);
+    }
+  }
+}
+
+// Output chunks leave with non-temporal stores and read-once epilogue operands arrive with
+// non-temporal loads: a product streams 10-150 MB of them through the 4 MB L2 of each XCD, which
+// would otherwise evict the operand panels that the tiles resident on the XCD share.
+template <typename V>
+__device__ __forceinline__ void st_nt(void* p, const V& v) {
+  static_assert(sizeof(V) == 16, "16-byte chunk");
+  u32x4 u;
+  __builtin_memcpy(&u, &v, 16);
+  __builtin_nontemporal_store(u, reinterpret_cast<u32x4*>(p));
+}
+template <typename V>
+__device__ __forceinline__ V ld_nt(const void* p) {
+  static_assert(sizeof(V) == 16, "16-byte chunk");
+  const u32x4 u = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  V v;
+  __builtin_memcpy(&v, &u, 16);
+  return v;
+}
+
+__device__ __forceinline__ float sigmoid_fast(float a) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * a));
+}
+
+// Epilogue of the direct-to-LDS kernels (full tiles).  Per RP-row part of each 32-row fragment
+// row of the wave tile: the accumulators go through the wave's own LDS staging area and leave as
+// 16-byte rows.  The global operands the epilogue kind reads are all requested before the first
+// part is written (or one part ahead, where the registers for all of them would not fit), so their
+// latency is paid about once per tile instead of once per part.  A wave reads back only what it wrote and
+// its LDS operations complete in issue order: no barrier between parts, and the stores are never
+// waited for here.  The staging area (waves x RP x (WN + 4) floats) must be free.
+template <int BM, int BN, int WM, int WN, typename OutT, int EPI, int RP>
+__device__ __forceinline__ void dma_epilogue(const GemmArgs& g, f32x16 (&acc)[WM / 32][WN / 32],
+                                             float* stage, int m0, int n0, int wm0, int wn0) {
+  static_assert(RP == 16 || RP == 8, "staging part of 8 or 16 rows");
+  static_assert(sizeof(OutT) == 2 || EPI == EPI_PLAIN, "fp32 output has no fused epilogue");
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int EP = WN + 4;  // staging pitch (fp32 elements)
+  constexpr int NP = 32 / RP, EPP = 16 / NP;  // parts per fragment row, accumulators per part
+  constexpr int VEC = sizeof(OutT) == 2 ? 8 : 4;  // elements per 16-byte chunk
+  constexpr int CPR = WN / VEC;                   // chunks per staged row
+  constexpr int CPL = RP * CPR / 64;              // chunks per lane and part
+  constexpr int NPART = FM * NP;
+  static_assert(CPL * 64 == RP * CPR, "every lane writes the same number of chunks per part");
+  // Parts requested ahead of the one being written, within a per-lane register budget for the
+  // requested operands (the wider wave tile holds more accumulators): all of them, one, or none.
+  constexpr int PART_BYTES = EpiIn<EPI>::loads ? CPL * (int)sizeof(EpiIn<EPI>) : 0;
+  constexpr int BUDGET = WN <= 64 ? 256 : 128;
+  constexpr int PD = PART_BYTES == 0 ? 0
+                     : PART_BYTES * NPART <= BUDGET ? NPART
+                     : 2 * PART_BYTES <= BUDGET ? 1 : 0;
+  constexpr int RS = PD >= NPART ? NPART : PD + 1;  // ring of requested parts
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  float* stg = stage + wave * RP * EP;
+  const bool split = sizeof(OutT) == 4 && g.ksplit > 1;
+  float* W = split ? g.ws + (int64_t)blockIdx.y * g.M * g.N : nullptr;
+  // output chunk j of part p of this lane: staged row r, column cc; C row, column
+  auto chunk = [&](int p, int j, int& r, int& cc, int& row, int& col) {
+    const int c = lane + 64 * j;
+    r = c / CPR;
+    cc = (c % CPR) * VEC;
+    row = m0 + wm0 + (p / NP) * 32 + RP * (p % NP) + r;
+    col = n0 + wn0 + cc;
+  };
+  EpiIn<EPI> in[RS][CPL];
+  auto request = [&](auto P) {
+    constexpr int p = P;
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      int r, cc, row, col;
+      chunk(p, j, r, cc, row, col);
+      epi_load<EPI>(in[p % RS][j], g, row, col);
+    }
+  };
+  if constexpr (PD > 0) static_for<(PD < NPART ? PD : NPART)>(request);
+  static_for<NPART>([&](auto P) {
+    constexpr int p = P, i = p / NP, h = p % NP;
+    if constexpr (EpiIn<EPI>::loads && p + PD < NPART) request(std::integral_constant<int, p + PD>{});
+    // accumulator e of lane l holds fragment row 8 (e / 4) + 4 (l / 32) + e mod 4: rows
+    // RP h .. RP h + RP - 1 are e = EPP h .. EPP h + EPP - 1
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = EPP * h; e < EPP * h + EPP; ++e)
+        stg[(8 * (e / 4) - RP * h + 4 * (lane / 32) + (e % 4)) * EP + j * 32 + lane % 32] = acc[i][j][e];
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      int r, cc, row, col;
+      chunk(p, j, r, cc, row, col);
+      const EpiIn<EPI>& x = in[p % RS][j];
+      float v[VEC];
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) v[q] = stg[r * EP + cc + q];
+      if constexpr (sizeof(OutT) == 4) {
+        if (split) {
+          st_nt(W + (int64_t)row * g.N + col, make_float4(v[0], v[1], v[2], v[3]));
+        } else {
+          float* Cf = (float*)g.C + (int64_t)row * g.ldc + col;
+          if (g.beta != 0.f) {
+            const float4 old = *reinterpret_cast<const float4*>(Cf);
+            v[0] += g.beta * old.x; v[1] += g.beta * old.y; v[2] += g.beta * old.z; v[3] += g.beta * old.w;
+          }
+          st_nt(Cf, make_float4(v[0], v[1], v[2], v[3]));
+        }
+      } else {
+        bf16* Cb = (bf16*)g.C;
+        const int64_t o = (int64_t)row * g.ldc + col;
+        if constexpr (EPI == EPI_SWIGLU_BWD) {  // dz = v -> dgate | dup
+          bf16x8 da, db;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float a = (float)x.a[q], bb = (float)x.b[q];
+            const float sg = sigmoid_fast(a);
+            da[q] = (bf16)(v[q] * bb * sg * (1.0f + a * (1.0f - sg)));
+            db[q] = (bf16)(v[q] * a * sg);
+          }
+          st_nt(Cb + o, da);
+          st_nt(Cb + o + g.N, db);
+        } else if constexpr (EPI == EPI_DELTA) {  // dO, plus delta = rowsum(dO O) per head
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
+          st_nt(Cb + o, ov);
+          float dot = 0.f;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) dot += (float)ov[q] * (float)x.o[q];
+          // the head's delta_hd / 8 chunks sit in consecutive lanes (aligned groups)
+          for (int m = 1; m < g.delta_hd / 8; m <<= 1) dot += __shfl_xor(dot, m, 64);
+          if (col % g.delta_hd == 0) {
+            const int bb = row / g.delta_S, ii = row % g.delta_S, hh = col / g.delta_hd;
+            g.delta[((int64_t)bb * (g.N / g.delta_hd) + hh) * g.delta_S + ii] = dot;
+          }
+        } else if constexpr (EPI == EPI_SWIGLU_FWD) {  // panel column col: gate or up of z column zc
+          const int grp = col / 32, zc = (grp / 2) * 32 + col % 32;
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
+          bf16* Crow = Cb + (int64_t)row * g.ldc;
+          if ((grp & 1) == 0) {
+            st_nt(Crow + zc, ov);
+            const float* up = stg + r * EP + cc + 32;  // the up values of the same z columns
+            bf16x8 zv;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) zv[q] = (bf16)(v[q] * sigmoid_fast(v[q]) * up[q]);
+            st_nt((bf16*)g.out2 + (int64_t)row * g.ld_out2 + zc, zv);
+          } else {
+            st_nt(Crow + g.glu + zc, ov);
+          }
+        } else if constexpr (EPI == EPI_ROPE) {  // rotate pairs (i, i + hd/2) of each head
+          bf16x8 ov;
+          if (col < g.rope_cols) {
+            const int hh = g.rope_hd / 2;
+            const bool first = (col % g.rope_hd) < hh;
+            const float* xp = stg + r * EP + (first ? cc + hh : cc - hh);  // partner columns
+            const float cs[8] = {x.c0[0], x.c0[1], x.c0[2], x.c0[3], x.c1[0], x.c1[1], x.c1[2], x.c1[3]};
+            const float sn[8] = {x.s0[0], x.s0[1], x.s0[2], x.s0[3], x.s1[0], x.s1[1], x.s1[2], x.s1[3]};
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+              ov[q] = (bf16)(first ? v[q] * cs[q] - xp[q] * sn[q] : v[q] * cs[q] + xp[q] * sn[q]);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
+          }
+          st_nt(Cb + o, ov);
+        } else {
+          if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] += (float)x.r[q];
+          }
+          bf16x8 ov;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
+          st_nt(Cb + o, ov);
+        }
+      }
+    }
+    asm volatile("" ::: "memory");
+  });
+}
+
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, bool CHECK>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(tile_waves_per_simd<BM, BN>(), tile_waves_per_simd<BM, BN>())))
@@ -450,27 +664,6 @@ struct DmaCfg {
   static constexpr size_t lds = main_lds > epi_lds ? main_lds : epi_lds;
 };
 
-// s_waitcnt: at most N vector-memory operations and no LDS operation outstanding
-template <int N>
-__device__ __forceinline__ void wait_vm_lds() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
-}
-
-// One 16-byte global -> LDS load per lane from base + voff bytes (base wave-uniform; lane l
-// writes lds + 16 l).  Issued as inline assembly so that the compiler neither counts it in its own
-// waits nor orders LDS reads after it: the kernel waits for these loads itself (wait_vm_lds)
-// before the barrier that publishes a stage.
-__device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
-  asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(lds) : "memory");
-}
-
-__device__ __forceinline__ void block_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
 // waves per SIMD: the block's waves over the 4 SIMDs times the blocks the LDS lets a CU hold
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, int BKT, int NS>
 constexpr int dma_waves_per_simd() {
@@ -484,7 +677,7 @@ constexpr int dma_waves_per_simd() {
 // count, so that every tile of a block maps to the block's XCD).  The slices of all its tiles form
 // one sequence: the loads of slice G + NS - 1 of that sequence (the next tile's first slices near
 // the end of a tile) are issued while slice G is consumed, into stage (G + NS - 1) mod NS.
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, int BKT, int NS>
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, int BKT, int NS, int EPI>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(dma_waves_per_simd<BM, BN, WM, WN, AK, BKM, BKT, NS>(),
                                    dma_waves_per_simd<BM, BN, WM, WN, AK, BKM, BKT, NS>())))
@@ -508,7 +701,7 @@ gemm_dma_kernel(GemmArgs g) {
   const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
   // split-K: this block covers slices [s0, s0 + nk) of every tile
   const int nk = g.K / BKT / g.ksplit, s0 = blockIdx.y * nk;
-  const bool glu = BKM && g.glu > 0;
+  const bool glu = BKM && EPI == EPI_SWIGLU_FWD;
   // this thread's byte offsets from a tile's slice origin
   uint32_t oa[PA], ob[PB];
 #pragma unroll
@@ -621,7 +814,7 @@ gemm_dma_kernel(GemmArgs g) {
     }
     wait_vm_lds<63>();
     block_barrier();
-    gemm_epilogue<BM, BN, WM, WN, OutT, false, C_::RP>(g, acc, stg, m0, n0, wm0, wn0);
+    dma_epilogue<BM, BN, WM, WN, OutT, EPI, C_::RP>(g, acc, stg, m0, n0, wm0, wn0);
     if (!next) break;
     t = tn; m0 = m1; n0 = n1; at = atn; bt = btn;
   }
@@ -634,9 +827,9 @@ __global__ void __launch_bounds__(256) splitk_reduce(const float* __restrict__ w
   const int64_t i = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
   if (i >= mn) return;
   if (i + 3 < mn) {
-    float4 acc = *reinterpret_cast<const float4*>(ws + i);
+    float4 acc = ld_nt<float4>(ws + i);
     for (int s = 1; s < splits; ++s) {
-      const float4 v = *reinterpret_cast<const float4*>(ws + (int64_t)s * mn + i);
+      const float4 v = ld_nt<float4>(ws + (int64_t)s * mn + i);
       acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
     }
     if (beta != 0.f) {
@@ -683,12 +876,12 @@ void launch_cfg(const GemmArgs& g, hipStream_t st) {
 #undef L
 }
 
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, int BKT, int NS>
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename OutT, int BKT, int NS, int EPI>
 void launch_dma_one(const GemmArgs& g, int nblk, hipStream_t st) {
   using C_ = DmaCfg<BM, BN, WM, WN, AK, BKM, BKT, NS>;
   static bool attr_set = false;
   if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS>,
+    (void)hipFuncSetAttribute((const void*)gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS, EPI>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)C_::lds);
     attr_set = true;
   }
@@ -699,18 +892,35 @@ void launch_dma_one(const GemmArgs& g, int nblk, hipStream_t st) {
     const int slots = (per_cu * device_cu_count() / g.ksplit) / 8 * 8;
     if (slots >= 8 && nblk > slots) grid = slots;
   }
-  gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS><<<dim3(grid, g.ksplit), C_::NT, C_::lds, st>>>(g);
+  gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS, EPI><<<dim3(grid, g.ksplit), C_::NT, C_::lds, st>>>(g);
 }
 
 // Direct-to-LDS variant: full tiles and whole slices per split only; false if the shape is not.
+// fp32 output: every operand layout, no fused epilogue; bf16 output: a k-contiguous A (every
+// bf16-output product of the stage has one) with each epilogue kind.
 template <int BM, int BN, int WM, int WN, typename OutT, int BKT, int NS>
 bool launch_dma_cfg(const GemmArgs& g, hipStream_t st) {
   if (g.M % BM || g.N % BN || g.K % BKT || g.K == 0 || (g.K / BKT) % g.ksplit) return false;
   const int nblk = (g.M / BM) * (g.N / BN);
-  if (g.a_kmajor && g.b_kmajor) launch_dma_one<BM, BN, WM, WN, true, true, OutT, BKT, NS>(g, nblk, st);
-  else if (g.a_kmajor) launch_dma_one<BM, BN, WM, WN, true, false, OutT, BKT, NS>(g, nblk, st);
-  else if (g.b_kmajor) launch_dma_one<BM, BN, WM, WN, false, true, OutT, BKT, NS>(g, nblk, st);
-  else launch_dma_one<BM, BN, WM, WN, false, false, OutT, BKT, NS>(g, nblk, st);
+  if constexpr (sizeof(OutT) == 4) {
+    if (g.a_kmajor && g.b_kmajor) launch_dma_one<BM, BN, WM, WN, true, true, OutT, BKT, NS, EPI_PLAIN>(g, nblk, st);
+    else if (g.a_kmajor) launch_dma_one<BM, BN, WM, WN, true, false, OutT, BKT, NS, EPI_PLAIN>(g, nblk, st);
+    else if (g.b_kmajor) launch_dma_one<BM, BN, WM, WN, false, true, OutT, BKT, NS, EPI_PLAIN>(g, nblk, st);
+    else launch_dma_one<BM, BN, WM, WN, false, false, OutT, BKT, NS, EPI_PLAIN>(g, nblk, st);
+  } else {
+    if (!g.a_kmajor) return false;
+    const int kind = g.epi != 0 ? g.epi : (g.resid ? EPI_RESID : EPI_PLAIN);
+#define K_(E)                                                                                     \
+  case E:                                                                                         \
+    if (g.b_kmajor) launch_dma_one<BM, BN, WM, WN, true, true, OutT, BKT, NS, E>(g, nblk, st);     \
+    else launch_dma_one<BM, BN, WM, WN, true, false, OutT, BKT, NS, E>(g, nblk, st);              \
+    break;
+    switch (kind) {
+      K_(EPI_PLAIN) K_(EPI_SWIGLU_BWD) K_(EPI_ROPE) K_(EPI_SWIGLU_FWD) K_(EPI_DELTA) K_(EPI_RESID)
+      default: return false;
+    }
+#undef K_
+  }
   return true;
 }
 
