@@ -401,32 +401,38 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
     const bf16* Vs = Ks + L::TSZ;
     const int key0 = kb * KB;
     if (key0 <= q0 + 31) {
+      // S and dP of both 32-key sub-tiles first, so that the softmax of the first runs on the
+      // vector ALUs while the matrix cores work on the second, and the dQ products of the first
+      // while the softmax of the second runs
+      f32x16 s[2], dp[2];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        f32x16 s, dp;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
+        for (int e = 0; e < 16; ++e) { s[t][e] = 0.f; dp[t][e] = 0.f; }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s, 0, 0, 0);
-          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Vs, t * 32, ks * 16), df[ks], dp, 0, 0, 0);
+          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s[t], 0, 0, 0);
+          dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Vs, t * 32, ks * 16), df[ks], dp[t], 0, 0, 0);
         }
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
         // every key of the sub-tile is visible to every query: no mask (head dim 64 only; at 128
         // the second code path costs the kernel its spill-free register budget)
         if (HD == 64 && key0 + t * 32 + 31 <= q0) {
 #pragma unroll
-          for (int e = 0; e < 16; ++e) s[e] = fast_exp2(__builtin_fmaf(s[e], sl2, -lse2)) * (dp[e] - dl);
+          for (int e = 0; e < 16; ++e) s[t][e] = fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) * (dp[t][e] - dl);
         } else {
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             const int key = key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4);
-            const float p = key <= myq ? fast_exp2(__builtin_fmaf(s[e], sl2, -lse2)) : 0.f;
-            s[e] = p * (dp[e] - dl);
+            const float p = key <= myq ? fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) : 0.f;
+            s[t][e] = p * (dp[t][e] - dl);
           }
         }
 #pragma unroll
         for (int g2 = 0; g2 < 2; ++g2) {
-          const bf16x8 bop = g2 ? acc_rows_to_b<8>(s) : acc_rows_to_b<0>(s);
+          const bf16x8 bop = g2 ? acc_rows_to_b<8>(s[t]) : acc_rows_to_b<0>(s[t]);
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
             dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Ks, dt * 32, t * 32 + g2 * 16), bop, dq[dt], 0, 0, 0);

@@ -275,6 +275,25 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[W
 // a residual row added.
 enum { EPI_PLAIN = 0, EPI_SWIGLU_BWD = 1, EPI_ROPE = 2, EPI_SWIGLU_FWD = 3, EPI_DELTA = 4, EPI_RESID = 5 };
 
+// Output chunks leave with non-temporal stores and read-once epilogue operands arrive with
+// non-temporal loads: a product streams 10-150 MB of them through the 4 MB L2 of each XCD, which
+// would otherwise evict the operand panels that the tiles resident on the XCD share.
+template <typename V>
+__device__ __forceinline__ void st_nt(void* p, const V& v) {
+  static_assert(sizeof(V) == 16, "16-byte chunk");
+  u32x4 u;
+  __builtin_memcpy(&u, &v, 16);
+  __builtin_nontemporal_store(u, reinterpret_cast<u32x4*>(p));
+}
+template <typename V>
+__device__ __forceinline__ V ld_nt(const void* p) {
+  static_assert(sizeof(V) == 16, "16-byte chunk");
+  const u32x4 u = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  V v;
+  __builtin_memcpy(&v, &u, 16);
+  return v;
+}
+
 // Global operands of one 16-byte output chunk (8 bf16 columns) that an epilogue reads.
 template <int EPI> struct EpiIn { static constexpr bool loads = false; };
 template <> struct EpiIn<EPI_RESID> { static constexpr bool loads = true; bf16x8 r; };
@@ -302,25 +321,6 @@ __device__ __forceinline__ void epi_load(EpiIn<EPI>& in, const GemmArgs& g, int 
       in.s1 = *reinterpret_cast<const f32x4*>(g.rope_sin + tb + 4);
     }
   }
-}
-
-// Output chunks leave with non-temporal stores and read-once epilogue operands arrive with
-// non-temporal loads: a product streams 10-150 MB of them through the 4 MB L2 of each XCD, which
-// would otherwise evict the operand panels that the tiles resident on the XCD share.
-template <typename V>
-__device__ __forceinline__ void st_nt(void* p, const V& v) {
-  static_assert(sizeof(V) == 16, "16-byte chunk");
-  u32x4 u;
-  __builtin_memcpy(&u, &v, 16);
-  __builtin_nontemporal_store(u, reinterpret_cast<u32x4*>(p));
-}
-template <typename V>
-__device__ __forceinline__ V ld_nt(const void* p) {
-  static_assert(sizeof(V) == 16, "16-byte chunk");
-  const u32x4 u = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-  V v;
-  __builtin_memcpy(&v, &u, 16);
-  return v;
 }
 
 __device__ __forceinline__ float sigmoid_fast(float a) {
