@@ -113,6 +113,67 @@ struct Vec {
   typedef T type __attribute__((ext_vector_type(V)));
 };
 
+// RMSNorm forward, one wave per row and two rows in flight per wave: lane l owns the V-element
+// vectors at columns (l + 64 k) V, k < NI, keeps gamma of those columns in registers for all its
+// rows, and the row's sum of squares is a wave reduction.  A block covers RMS_ROWS_VEC
+// consecutive rows (rows wave, wave + 4, ... of the block).
+template <typename T, int V, int NI>
+__global__ void __launch_bounds__(256) rmsnorm_fwd_vec(const T* __restrict__ x, const T* __restrict__ gamma,
+                                                       T* __restrict__ y, float* __restrict__ rstd,
+                                                       int rows, float eps) {
+  constexpr int d = 64 * V * NI;
+  using VT = typename Vec<T, V>::type;
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  float gm[NI][V];
+#pragma unroll
+  for (int k = 0; k < NI; ++k) {
+    const VT gv = *reinterpret_cast<const VT*>(gamma + (lane + 64 * k) * V);
+#pragma unroll
+    for (int q = 0; q < V; ++q) gm[k][q] = to_f32(gv[q]);
+  }
+  const int r0 = blockIdx.x * RMS_ROWS_VEC + wave;
+#pragma unroll 1
+  for (int it = 0; it < RMS_ROWS_VEC / 8; ++it) {
+    int r[2];
+    VT xv[2][NI];
+    float ss[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      r[u] = r0 + 4 * (2 * it + u);
+      const int64_t base = (int64_t)(r[u] < rows ? r[u] : 0) * d;
+#pragma unroll
+      for (int k = 0; k < NI; ++k) xv[u][k] = *reinterpret_cast<const VT*>(x + base + (lane + 64 * k) * V);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      ss[u] = 0.f;
+#pragma unroll
+      for (int k = 0; k < NI; ++k)
+#pragma unroll
+        for (int q = 0; q < V; ++q) {
+          const float v = to_f32(xv[u][k][q]);
+          ss[u] += v * v;
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) ss[u] = wave_sum(ss[u]);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (r[u] >= rows) continue;
+      const float rs = 1.0f / sqrtf(ss[u] / (float)d + eps);
+      const int64_t base = (int64_t)r[u] * d;
+#pragma unroll
+      for (int k = 0; k < NI; ++k) {
+        VT ov;
+#pragma unroll
+        for (int q = 0; q < V; ++q) ov[q] = from_f32<T>(to_f32(xv[u][k][q]) * rs * gm[k][q]);
+        *reinterpret_cast<VT*>(y + base + (lane + 64 * k) * V) = ov;
+      }
+      if (lane == 0) rstd[r[u]] = rs;
+    }
+  }
+}
+
 // RMSNorm backward, one wave per row and U rows in flight per wave: lane l owns the V-element
 // vectors at columns (l + 64 k) V, k < NI, so every load and store is V elements wide; gamma and
 // the dgamma partial sums of those columns stay in registers and the row dot product is a wave
@@ -404,6 +465,28 @@ void launch_embed_gather(bool bf, const int32_t* tok, const void* table, void* x
 template <typename T>
 static void rmsf_t(const void* x, const void* g, void* y, float* r, int rows, int d, float eps,
                    hipStream_t st) {
+  const unsigned nv = (unsigned)cdiv(rows, RMS_ROWS_VEC);
+  const uintptr_t align = (uintptr_t)x | (uintptr_t)g | (uintptr_t)y;
+#define RF(V, NI)                                                                                   \
+  if (align % (V * sizeof(T)) == 0) {                                                               \
+    rmsnorm_fwd_vec<T, V, NI><<<nv, 256, 0, st>>>((const T*)x, (const T*)g, (T*)y, r, rows, eps);   \
+    return;                                                                                         \
+  }
+  // the row widths of the vectorised backward, plus 4096; any other width, or rows not aligned to
+  // the vector, take the block-per-row kernel
+  constexpr bool B = sizeof(T) == 2;
+  switch (d) {
+    case 128: RF(2, 1) break;
+    case 256: RF(4, 1) break;
+    case 512: if (B) { RF(8, 1) } else { RF(4, 2) } break;
+    case 768: RF(4, 3) break;
+    case 1024: if (B) { RF(8, 2) } else { RF(4, 4) } break;
+    case 1536: if (B) { RF(8, 3) } else { RF(4, 6) } break;
+    case 2048: if (B) { RF(8, 4) } else { RF(4, 8) } break;
+    case 4096: if (B) { RF(8, 8) } else { RF(4, 16) } break;
+    default: break;
+  }
+#undef RF
   rmsnorm_fwd<T><<<rows, 256, 0, st>>>((const T*)x, (const T*)g, (T*)y, r, d, eps);
 }
 void launch_rmsnorm_fwd(bool bf, const void* x, const void* gamma, void* y, float* rstd, int rows,
@@ -434,6 +517,7 @@ static int rmsb_t(const void* dn, const void* x, const float* r, const void* g, 
     case 1024: if (B) { RB(8, 2) } else { RB(4, 4) } break;
     case 1536: if (B) { RB(8, 3) } else { RB(4, 6) } break;
     case 2048: if (B) { RB(8, 4) } else { RB(4, 8) } break;
+    case 4096: if (B) { RB(8, 8) } break;
     default: break;
   }
 #undef RB
