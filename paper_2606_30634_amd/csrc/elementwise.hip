@@ -113,6 +113,12 @@ struct Vec {
   typedef T type __attribute__((ext_vector_type(V)));
 };
 
+// RMSNorm backward, one wave per row and U rows in flight per wave: lane l owns the V-element
+// vectors at columns (l + 64 k) V, k < NI, so every load and store is V elements wide; gamma and
+// the dgamma partial sums of those columns stay in registers and the row dot product is a wave
+// reduction.  A block covers RMS_ROWS_VEC consecutive rows (4 per wave) and writes one dgamma
+// partial row, the sum of its waves' rows in wave order.
+constexpr int RMS_ROWS_VEC = 16;
 // RMSNorm forward, one wave per row and two rows in flight per wave: lane l owns the V-element
 // vectors at columns (l + 64 k) V, k < NI, keeps gamma of those columns in registers for all its
 // rows, and the row's sum of squares is a wave reduction.  A block covers RMS_ROWS_VEC
@@ -174,12 +180,6 @@ __global__ void __launch_bounds__(256) rmsnorm_fwd_vec(const T* __restrict__ x, 
   }
 }
 
-// RMSNorm backward, one wave per row and U rows in flight per wave: lane l owns the V-element
-// vectors at columns (l + 64 k) V, k < NI, so every load and store is V elements wide; gamma and
-// the dgamma partial sums of those columns stay in registers and the row dot product is a wave
-// reduction.  A block covers RMS_ROWS_VEC consecutive rows (4 per wave) and writes one dgamma
-// partial row, the sum of its waves' rows in wave order.
-constexpr int RMS_ROWS_VEC = 16;
 template <typename T, int V, int NI>
 __global__ void __launch_bounds__(256) rmsnorm_bwd_vec(const T* __restrict__ dn, const T* __restrict__ x,
                                                        const float* __restrict__ rstd,
