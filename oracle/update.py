@@ -22,6 +22,19 @@ where the paper is silent: eps = 1e-8; the clip epsilon 1e-6; weight decay on ev
 step t = 0 changes nothing (the zero gradient g_{-1} is not fed to the statistics, so the first
 real update has k = 1); the EF buffer holds the whole previous update u_{t-2}, learning rate and
 weight decay included.
+
+With optimizer "muon", u of every 2-D weight matrix of a decoder block is the one of Alg. 2
+(Delayed Muon, §4); the embedding and the RMSNorm gains keep AdamW:
+    M <- mu M + (1 - mu) g              momentum (the EMA form §3 uses for mu = 0.95)
+    O  = Newton-Schulz(M)                approximate orthogonalisation of M
+    u  = lr ( s O + wd x_t )             s = rms sqrt(max(rows, cols)), rms = 0.2 (§3)
+then the same standard or Error-Feedback step.  Readings where the paper is silent: Newton-Schulz
+is the quintic iteration of the Muon write-up (Jordan et al., 2024) - X <- X / (||X||_F + 1e-7),
+then 5 times X <- a X + (b A + c A A) X with A = X X^T on the wide orientation (rows <= cols) and
+(a, b, c) = (3.4445, -4.7750, 2.0315); every matrix of the block (wq, wk, wv, wo, wgate, wup,
+wdown) separately; the momentum takes the clipped gradient and has no bias correction (Newton-
+Schulz is invariant to the scale of M); the "update RMS 0.2" scales O to RMS 0.2, the RMS of an
+exactly orthogonal m x n matrix being 1 / sqrt(max(m, n)).
 """
 from __future__ import annotations
 
@@ -42,6 +55,48 @@ class HParams:
     clip_norm: float = 1.0       # <= 0 disables clipping
     ef_lambda: float = 0.0       # 0: standard async; 1: Error Feedback of §3.2
     delay: int = 1               # 1: Alg. 1; 0: synchronous
+    optimizer: str = "adamw"     # "adamw", or "muon": Alg. 2 on the blocks' weight matrices
+    momentum: float = 0.95       # Muon momentum mu
+    update_rms: float = 0.2      # Muon update RMS
+    ns_steps: int = 5            # Newton-Schulz iterations
+
+
+# quintic Newton-Schulz coefficients of the Muon write-up (Jordan et al., 2024)
+NS_COEFFS = (3.4445, -4.7750, 2.0315)
+NS_EPS = 1e-7
+MUON_MATRICES = ("wq", "wk", "wv", "wo", "wgate", "wup", "wdown")
+
+
+def is_muon_matrix(name: str) -> bool:
+    """The 2-D weight matrices of a decoder block (names blk<i>.<matrix>)."""
+    return name.startswith("blk") and name.split(".")[-1] in MUON_MATRICES
+
+
+def newton_schulz(M: np.ndarray, steps: int = 5) -> np.ndarray:
+    """O ~ U V^T for M = U S V^T (Alg. 2's Newton-Schulz step): normalise by the Frobenius norm,
+    then iterate X <- a X + (b A + c A^2) X, A = X X^T, on the orientation with rows <= cols."""
+    a, b, c = NS_COEFFS
+    X = M / (np.linalg.norm(M) + NS_EPS)
+    tall = X.shape[0] > X.shape[1]
+    if tall:
+        X = X.T
+    for _ in range(steps):
+        A = X @ X.T
+        X = a * X + (b * A + c * (A @ A)) @ X
+    return X.T if tall else X
+
+
+def muon_scale(shape, rms: float) -> float:
+    """s with RMS(s O) = rms for an exactly orthogonal O of this shape."""
+    return rms * math.sqrt(max(shape))
+
+
+def muon_u(x, g, M, hp: "HParams"):
+    """One Muon evaluation (Alg. 2) on already-clipped g.  Returns (u, M_new)."""
+    M1 = hp.momentum * M + (1.0 - hp.momentum) * g
+    O = newton_schulz(M1, hp.ns_steps)
+    u = hp.lr * (muon_scale(x.shape, hp.update_rms) * O + hp.weight_decay * x)
+    return u, M1
 
 
 class NonFiniteGradient(Exception):
@@ -109,6 +164,8 @@ def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> d
         raise ValueError("delay must be 0 or 1")
     if hp.delay == 0 and hp.ef_lambda != 0.0:
         raise ValueError("Error Feedback needs a delayed gradient (delay 1)")
+    if hp.optimizer not in ("adamw", "muon"):
+        raise ValueError("optimizer must be adamw or muon")
     if hp.delay == 1:
         g_use = st.pending
     else:
@@ -123,7 +180,10 @@ def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> d
         ef = hp.ef_lambda != 0.0 and st.n_updates >= 1   # "t <= 1": the first update is standard
         for name in st.x:
             g = g_use[name] * c
-            u, st.m[name], st.v[name] = adamw_u(st.x[name], g, st.m[name], st.v[name], k, hp)
+            if hp.optimizer == "muon" and is_muon_matrix(name):
+                u, st.m[name] = muon_u(st.x[name], g, st.m[name], hp)   # m holds Muon's momentum
+            else:
+                u, st.m[name], st.v[name] = adamw_u(st.x[name], g, st.m[name], st.v[name], k, hp)
             st.x[name] = apply_update(st.x[name], u, st.u_prev[name], ef, hp.ef_lambda)
             st.u_prev[name] = u
         st.n_updates = k
