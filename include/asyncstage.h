@@ -64,21 +64,35 @@ typedef enum { STAGE_DT_F32 = 0, STAGE_DT_BF16 = 1, STAGE_DT_I32 = 2 } stage_dty
  * vocab > 0 requires first_stage (token embedding [vocab, d_model]); last_stage requires
  * tie_embedding and vocab > 0 (logits = RMSNorm(x) E^T).  head_dim in {32, 64, 128};
  * n_heads a multiple of n_kv_heads; d_model a multiple of 64.  max_inflight >= 1 is the number
- * of activation slots (microbatches whose backward is pending). */
+ * of activation slots (microbatches whose backward is pending).  optimizer 0: AdamW only;
+ * 1: the arena also holds the Newton-Schulz workspace of delayed Muon (Alg. 2 of §4), about two
+ * bf16 (fp32) copies of the blocks' weight matrices plus their Gram matrices, so that
+ * delayed_update accepts update_hparams_t.optimizer = 1. */
 typedef struct {
   int32_t n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ffn;
   int32_t vocab, first_stage, last_stage, tie_embedding;
   int32_t seq_len, micro_batch, max_inflight;
   int32_t dtype;
   float rms_eps, rope_theta;
+  int32_t optimizer;
 } stage_shape_t;
 
 /* Hyper-parameters of one update.  clip_norm <= 0 disables clipping.  ef_lambda = 0 is standard
- * delayed training, 1 the Error-Feedback equation of §3.2.  delay 1 is Alg. 1; delay 0 is
- * synchronous AdamW (requires ef_lambda = 0). */
+ * delayed training, 1 the Error-Feedback equation of §3.2.  delay 1 is Alg. 1; delay 0 is the
+ * synchronous optimizer (requires ef_lambda = 0).
+ * optimizer 0: AdamW (beta1, beta2, eps) on every parameter.  optimizer 1: delayed Muon (Alg. 2
+ * of §4) on every 2-D weight matrix of a block (wq, wk, wv, wo, wgate, wup, wdown, each on its
+ * own) and AdamW on the embedding and the gains: M <- momentum M + (1 - momentum) c g;
+ * O = Newton-Schulz(M) (ns_steps >= 1 quintic iterations on M / ||M||_F in the orientation with
+ * rows <= cols, coefficients (3.4445, -4.7750, 2.0315), in the stage's compute type);
+ * u = lr (update_rms sqrt(max(rows, cols)) O + weight_decay x_t); then the same standard or
+ * Error-Feedback step as AdamW.  Needs a stage shaped with optimizer 1. */
 typedef struct {
   float lr, beta1, beta2, eps, weight_decay, clip_norm, ef_lambda;
   int32_t delay;
+  int32_t optimizer;
+  float momentum, update_rms;
+  int32_t ns_steps;
 } update_hparams_t;
 
 /* Bytes of device memory the stage needs (weights, optimizer state, two gradient buffers, two
@@ -144,7 +158,7 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out,
  * device; see stage_poll_nonfinite.  STAGE_ESTATE on out-of-order t or an incomplete gradient. */
 int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp);
 
-/* Stateless fused update over flat device vectors of n elements (the update kernel alone):
+/* Stateless fused AdamW update (hp->optimizer must be 0) over flat device vectors of n elements:
  * iteration t of a delay-1 run consumes g_prev (= g_{t-1}; fp32, or bf16 when g_is_bf16), with
  * k = t the AdamW bias-correction index and EF from t >= 2; t = 0 only writes x_shadow.
  * x, m, v, u_prev fp32 (read and written; u_prev may be NULL when ef_lambda = 0); x_shadow
@@ -172,11 +186,11 @@ int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev);
  * stream around every launch of a class and, when read, adds up the elapsed times and the algorithmic work of
  * those launches: GEMM and attention in flops (2 M N K per product; causal attention forward
  * 4 B Hq hd s(s+1)/2, backward twice that), the delayed update and the gradient norm in bytes of
- * HBM traffic.  Reading synchronises the stream and resets the counters.  Meant for measurement
+ * HBM traffic, the Newton-Schulz products of Muon (STAGE_PROF_NS) in flops.  Reading synchronises the stream and resets the counters.  Meant for measurement
  * passes; it adds two event records per launch. */
 typedef enum {
   STAGE_PROF_GEMM = 0, STAGE_PROF_ATTN_FWD = 1, STAGE_PROF_ATTN_BWD = 2, STAGE_PROF_UPDATE = 3,
-  STAGE_PROF_NORM = 4, STAGE_PROF_OTHER = 5, STAGE_PROF_NCLASS = 6
+  STAGE_PROF_NORM = 4, STAGE_PROF_OTHER = 5, STAGE_PROF_NS = 6, STAGE_PROF_NCLASS = 7
 } stage_prof_class;
 int stage_profile_enable(stage_t* s, int32_t on);
 int stage_profile_read(stage_t* s, int32_t cls, double* ms, int64_t* launches, double* work);

@@ -18,19 +18,22 @@ EXPORTS = ["stage_required_bytes", "stage_init", "stage_num_tensors", "stage_ten
            "delayed_update", "delayed_update_flat", "stage_embed_indices", "stage_poll_nonfinite",
            "stage_grad_norm", "stage_profile_enable", "stage_profile_read", "stage_last_error",
            "stage_destroy"]
-PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_UPDATE, PROF_NORM, PROF_OTHER = range(6)
+PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_UPDATE, PROF_NORM, PROF_OTHER, PROF_NS = range(7)
 
 
 class StageShape(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("n_blocks", "d_model", "n_heads", "n_kv_heads", "head_dim",
                                          "d_ffn", "vocab", "first_stage", "last_stage",
                                          "tie_embedding", "seq_len", "micro_batch", "max_inflight",
-                                         "dtype")] + [("rms_eps", C.c_float), ("rope_theta", C.c_float)]
+                                         "dtype")] + [("rms_eps", C.c_float), ("rope_theta", C.c_float),
+                                                      ("optimizer", C.c_int32)]
 
 
 class UpdateHParams(C.Structure):
     _fields_ = [(n, C.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay", "clip_norm",
-                                         "ef_lambda")] + [("delay", C.c_int32)]
+                                         "ef_lambda")] + [("delay", C.c_int32), ("optimizer", C.c_int32),
+                                                          ("momentum", C.c_float), ("update_rms", C.c_float),
+                                                          ("ns_steps", C.c_int32)]
 
 
 class StageError(RuntimeError):

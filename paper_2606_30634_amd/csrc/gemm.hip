@@ -106,9 +106,46 @@ void launch_gemm_tiled(bool bf, const GemmArgs& g, hipStream_t st) {
   }
 }
 
+// y = alpha y + beta x, one thread per element of a rows x cols block of row stride ld
+template <typename T>
+__global__ void __launch_bounds__(256) axpby_kernel(T* __restrict__ y, const T* __restrict__ x, float alpha,
+                                                    float beta, int rows, int cols, int ld) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)rows * cols) return;
+  const int64_t o = (i / cols) * ld + i % cols;
+  y[o] = from_f32<T>(alpha * to_f32(y[o]) + beta * to_f32(x[o]));
+}
+
+void launch_axpby(bool bf, void* y, const void* x, float alpha, float beta, int rows, int cols, int ld,
+                  hipStream_t st) {
+  const unsigned nb = (unsigned)cdiv((int64_t)rows * cols, 256);
+  if (bf) axpby_kernel<bf16><<<nb, 256, 0, st>>>((bf16*)y, (const bf16*)x, alpha, beta, rows, cols, ld);
+  else axpby_kernel<float><<<nb, 256, 0, st>>>((float*)y, (const float*)x, alpha, beta, rows, cols, ld);
+}
+
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st) {
   if (g.M == 0 || g.N == 0) return;
   if (bf && gemm_mfma_try(g, st)) return;
+  if (g.batch > 1 || g.epi == GEMM_EPI_AXPBY) {
+    // one product at a time, then the AXPBY pass
+    const size_t es = bf ? 2 : 4, cs = g.out_f32 ? 4 : es;
+    for (int b = 0; b < g.batch; ++b) {
+      GemmArgs p = g;
+      p.batch = 1;
+      p.A = (const char*)g.A + b * g.sA * es;
+      p.B = (const char*)g.B + b * g.sB * es;
+      p.C = (char*)g.C + b * g.sC * cs;
+      p.D = g.D ? (const char*)g.D + b * g.sD * cs : nullptr;
+      if (g.epi == GEMM_EPI_AXPBY) {
+        p.epi = 0;
+        launch_gemm(bf, p, st);
+        launch_axpby(bf && !g.out_f32, p.C, p.D, g.alpha, g.beta_d, g.M, g.N, g.ldc, st);
+      } else {
+        launch_gemm(bf, p, st);
+      }
+    }
+    return;
+  }
   if (g.epi == 4) {  // the product, then delta = rowsum(dO O) by the attention's own kernel
     GemmArgs p = g;
     p.epi = 0;

@@ -272,8 +272,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[W
 
 // Epilogue kinds of the direct-to-LDS kernels (compile-time; the numbers of the first five are
 // GemmArgs::epi): bf16 output as is, SwiGLU backward, RoPE, SwiGLU forward, attention delta, plus
-// a residual row added.
-enum { EPI_PLAIN = 0, EPI_SWIGLU_BWD = 1, EPI_ROPE = 2, EPI_SWIGLU_FWD = 3, EPI_DELTA = 4, EPI_RESID = 5 };
+// a residual row added, alpha (A B) + beta D.
+enum { EPI_PLAIN = 0, EPI_SWIGLU_BWD = 1, EPI_ROPE = 2, EPI_SWIGLU_FWD = 3, EPI_DELTA = 4, EPI_RESID = 5,
+       EPI_AXPBY = GEMM_EPI_AXPBY };
 
 // Output chunks leave with non-temporal stores and read-once epilogue operands arrive with
 // non-temporal loads: a product streams 10-150 MB of them through the 4 MB L2 of each XCD, which
@@ -297,6 +298,7 @@ __device__ __forceinline__ V ld_nt(const void* p) {
 // Global operands of one 16-byte output chunk (8 bf16 columns) that an epilogue reads.
 template <int EPI> struct EpiIn { static constexpr bool loads = false; };
 template <> struct EpiIn<EPI_RESID> { static constexpr bool loads = true; bf16x8 r; };
+template <> struct EpiIn<EPI_AXPBY> { static constexpr bool loads = true; bf16x8 r; };
 template <> struct EpiIn<EPI_SWIGLU_BWD> { static constexpr bool loads = true; bf16x8 a, b; };
 template <> struct EpiIn<EPI_DELTA> { static constexpr bool loads = true; bf16x8 o; };
 template <> struct EpiIn<EPI_ROPE> { static constexpr bool loads = true; f32x4 c0, c1, s0, s1; };
@@ -305,6 +307,8 @@ template <int EPI>
 __device__ __forceinline__ void epi_load(EpiIn<EPI>& in, const GemmArgs& g, int row, int col) {
   if constexpr (EPI == EPI_RESID) {
     in.r = ld_nt<bf16x8>((const bf16*)g.resid + (int64_t)row * g.ldc + col);
+  } else if constexpr (EPI == EPI_AXPBY) {
+    in.r = ld_nt<bf16x8>((const bf16*)g.D + (int64_t)row * g.ldc + col);
   } else if constexpr (EPI == EPI_SWIGLU_BWD) {
     const bf16* gu = (const bf16*)g.aux + (int64_t)row * g.ld_aux + col;
     in.a = ld_nt<bf16x8>(gu);
@@ -472,6 +476,9 @@ __device__ __forceinline__ void dma_epilogue(const GemmArgs& g, f32x16 (&acc)[WM
           if constexpr (EPI == EPI_RESID) {
 #pragma unroll
             for (int q = 0; q < 8; ++q) v[q] += (float)x.r[q];
+          } else if constexpr (EPI == EPI_AXPBY) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] = g.alpha * v[q] + g.beta_d * (float)x.r[q];
           }
           bf16x8 ov;
 #pragma unroll
@@ -682,6 +689,13 @@ __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(dma_waves_per_simd<BM, BN, WM, WN, AK, BKM, BKT, NS>(),
                                    dma_waves_per_simd<BM, BN, WM, WN, AK, BKM, BKT, NS>())))
 gemm_dma_kernel(GemmArgs g) {
+  if (g.batch > 1) {  // product blockIdx.z of a batch
+    const int64_t z = blockIdx.z;
+    g.A = (const bf16*)g.A + z * g.sA;
+    g.B = (const bf16*)g.B + z * g.sB;
+    g.C = (char*)g.C + z * g.sC * (int64_t)sizeof(OutT);
+    if (g.D) g.D = (const OutT*)g.D + z * g.sD;
+  }
   using C_ = DmaCfg<BM, BN, WM, WN, AK, BKM, BKT, NS>;
   using TA = typename C_::TA;
   using TB = typename C_::TB;
@@ -887,12 +901,12 @@ void launch_dma_one(const GemmArgs& g, int nblk, hipStream_t st) {
   }
   // more tiles than the chip holds blocks at once: one block per slot, each walking its tiles
   int grid = nblk;
-  if (C_::persist && g.K / BKT / g.ksplit >= NS - 1) {
+  if (C_::persist && g.batch == 1 && g.K / BKT / g.ksplit >= NS - 1) {
     const int per_cu = (int)(163840 / C_::lds);
     const int slots = (per_cu * device_cu_count() / g.ksplit) / 8 * 8;
     if (slots >= 8 && nblk > slots) grid = slots;
   }
-  gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS, EPI><<<dim3(grid, g.ksplit), C_::NT, C_::lds, st>>>(g);
+  gemm_dma_kernel<BM, BN, WM, WN, AK, BKM, OutT, BKT, NS, EPI><<<dim3(grid, g.ksplit, g.batch), C_::NT, C_::lds, st>>>(g);
 }
 
 // Direct-to-LDS variant: full tiles and whole slices per split only; false if the shape is not.
@@ -917,6 +931,7 @@ bool launch_dma_cfg(const GemmArgs& g, hipStream_t st) {
     break;
     switch (kind) {
       K_(EPI_PLAIN) K_(EPI_SWIGLU_BWD) K_(EPI_ROPE) K_(EPI_SWIGLU_FWD) K_(EPI_DELTA) K_(EPI_RESID)
+      K_(EPI_AXPBY)
       default: return false;
     }
 #undef K_
@@ -953,6 +968,20 @@ int device_cu_count() {
 bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   // vector-load alignment: 8 elements along every contiguous dimension, rows in groups of 4
   if (g0.K % 8 || g0.M % 8 || g0.N % 8 || g0.lda % 8 || g0.ldb % 8 || g0.ldc % 8) return false;
+  if (g0.batch > 1 || g0.epi == EPI_AXPBY) {
+    // batched and AXPBY products run on the direct-to-LDS kernels only (full tiles, 16-byte
+    // aligned operands and batch strides; AXPBY with bf16 output, fp32 output plain or
+    // accumulating beta C); the caller loops over the others
+    const bool ok = g0.a_kmajor && g0.M % 128 == 0 && g0.N % 128 == 0 && g0.K % 64 == 0 &&
+                    (g0.epi == 0 || (g0.epi == EPI_AXPBY && !g0.out_f32)) && !g0.resid &&
+                    ((uintptr_t)g0.A | (uintptr_t)g0.B | (uintptr_t)g0.C | (uintptr_t)g0.D) % 16 == 0 &&
+                    (g0.sA | g0.sB | g0.sC | g0.sD) % 8 == 0;
+    if (!ok) return false;
+    GemmArgs g = g0;
+    g.ksplit = 1;
+    return g.out_f32 ? launch_dma_cfg<128, 128, 64, 64, float, 64, 2>(g, st)
+                     : launch_dma_cfg<128, 128, 64, 64, bf16, 64, 2>(g, st);
+  }
   if (g0.epi == 3) {
     // the SwiGLU forward rides in the epilogue of the direct-to-LDS kernels only (their B loader
     // gathers gate and up rows); any other shape runs the product, then the SwiGLU kernel

@@ -98,7 +98,18 @@ struct GemmArgs {
   // b * delta_S + i) and aux the attention output O of the same layout; besides C, writes
   // delta[(b Hq + h) delta_S + i] = sum over head h's columns of dO O (bf16-rounded dO).
   float* delta = nullptr; int delta_hd = 0, delta_S = 0;
+  // epilogue 6 (AXPBY): C = alpha (A B) + beta_d D, D of C's type and layout (leading dim ldc).
+  float alpha = 1.f, beta_d = 0.f;
+  const void* D = nullptr;
+  // batch > 1: `batch` independent products of this shape; operand b starts at A + b sA, B + b sB,
+  // C + b sC, D + b sD (elements)
+  int batch = 1;
+  int64_t sA = 0, sB = 0, sC = 0, sD = 0;
 };
+constexpr int GEMM_EPI_AXPBY = 6;
+// y = alpha y + beta x over rows x cols (row stride ld), in place, bf16 or fp32 storage
+void launch_axpby(bool bf, void* y, const void* x, float alpha, float beta, int rows, int cols, int ld,
+                  hipStream_t st);
 constexpr int64_t GEMM_WS_ELEMS = 16 << 20;  // 64 MiB of fp32 split-K partials per stage
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st);
 
@@ -118,3 +129,35 @@ void launch_attention_fwd(bool bf, const AttnArgs& a, hipStream_t st);
 // delta = rowsum(dO O) per (batch, head, query) alone
 void launch_attention_delta(bool bf, const AttnArgs& a, hipStream_t st);
 void launch_attention_bwd(bool bf, const AttnArgs& a, hipStream_t st);
+
+// ------------------------------------------------------------------ Muon (muon.hip)
+// One weight matrix of delayed Muon: W [rows, cols] row-major at element offset `off` of the flat
+// parameter vectors; x[0], x[1] its fp32 Newton-Schulz iterates in wide orientation (the
+// transpose, [cols, rows], when trans): ping-pong buffers of the fp32 stage, x[0] alone (updated
+// in place) on the bf16 stage; blk0 / tile0 its first block in the element-chunk grid of the
+// momentum pass and in the 64 x 64 tile grid of the prep and apply passes.
+constexpr int MUON_CHUNK = 4096;
+struct MuonMat {
+  int64_t off;
+  int rows, cols, trans;
+  int blk0, tile0;
+  float sqrt_max;  // sqrt(max(rows, cols)): the update is scaled to RMS rms with s = rms sqrt_max
+  float* x[2];
+};
+int64_t muon_chunks(int64_t numel);
+int64_t muon_tiles(int rows, int cols);
+// M <- mu M + (1 - mu) c g on every matrix, then norm[i] = ||M_i||_F (partial: nblk doubles)
+void launch_muon_momentum(const MuonMat* mats, int nmat, int nblk, const float* g, float* M, const float* clip,
+                          const int* flag, float mu, double* partial, float* norm, hipStream_t st);
+// x[0] = M / (||M|| + 1e-7) in wide orientation (fp32)
+void launch_muon_prep(const MuonMat* mats, int nmat, int ntile, const float* M, const float* norm, hipStream_t st);
+// The bf16 operand form of fp32 iterates X [rows, n] (row stride n): S [rows, 4n] holds, per row,
+// [hi | hi | lo | hi] with hi = bf16(x) and lo = bf16(x - hi), so that the Gram product over
+// K = 3n of S[:, 0:3n] and S[:, n:4n] is hi hi^T + hi lo^T + lo hi^T, and a product L X is
+// L S[:, 0:n] + L S[:, 2n:3n] (row stride 4n)
+void launch_muon_split(const float* X, bf16* S, int64_t rows, int n, hipStream_t st);
+// W, u_prev and the compute copy (bf16 when bf) from O = x[fin]
+void launch_muon_apply(bool bf, const MuonMat* mats, int nmat, int ntile, int fin, float* W, float* up,
+                       void* shadow, const int* flag, float lr, float wd, float rms, bool ef, float lam,
+                       hipStream_t st);
+

@@ -8,6 +8,7 @@
 // no pending microbatch reads any more.
 #include <cmath>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -106,6 +107,17 @@ struct stage {
   std::vector<hipEvent_t> prof_free;
   double prof_ms[STAGE_PROF_NCLASS] = {}, prof_work[STAGE_PROF_NCLASS] = {};
   int64_t prof_n[STAGE_PROF_NCLASS] = {};
+  // Muon (shapes with optimizer 1): the blocks' weight matrices, grouped by their wide-orientation
+  // shape for the batched Newton-Schulz products, and the ranges of the flat vector outside them
+  // (AdamW: embedding, gains, padding)
+  struct MuonGroup { int m, n, nb; float* X[2]; bf16* S; void* A; void* P; };
+  std::vector<MuonMat> muon;
+  std::vector<MuonGroup> mgroups;
+  std::vector<std::pair<int64_t, int64_t>> adamw_ranges;  // (offset, count)
+  MuonMat* muon_tab = nullptr;
+  double* muon_part = nullptr;
+  float* muon_norm = nullptr;
+  int muon_nblk = 0, muon_ntile = 0;
   // named tensors
   struct Named { std::string name; void* ptr; int64_t numel; int32_t dtype; };
   std::vector<Named> named;
@@ -202,6 +214,7 @@ int validate(const stage_shape_t* s) {
   if (s->d_model % 64 || s->d_ffn % 64) return fail(STAGE_EINVAL, "d_model, d_ffn must be multiples of 64");
   if (s->d_model > 4096) return fail(STAGE_EINVAL, "d_model > 4096 not supported");
   if (s->dtype != 0 && s->dtype != 1) return fail(STAGE_EINVAL, "dtype must be 0 (fp32) or 1 (bf16)");
+  if (s->optimizer != 0 && s->optimizer != 1) return fail(STAGE_EINVAL, "optimizer must be 0 or 1");
   if (s->vocab < 0 || s->vocab >= (1 << 17)) return fail(STAGE_EINVAL, "vocab out of range");
   if (s->vocab > 0 && !s->first_stage) return fail(STAGE_EINVAL, "embedding requires first_stage");
   if (s->first_stage && s->vocab == 0) return fail(STAGE_EINVAL, "first_stage requires vocab > 0");
@@ -296,6 +309,77 @@ size_t layout(stage* S, char* base) {
   S->dlog = sh.last_stage ? carve(T * (int64_t)sh.vocab * esz) : nullptr;
   S->dhf = sh.last_stage ? carve(T * d * esz) : nullptr;
   S->row_loss = sh.last_stage ? (float*)carve(T * 4) : nullptr;
+  // Muon: every block's wq, wk, wv, wo, wgate, wup, wdown; a group per wide-orientation shape
+  // (m = min(rows, cols) <= n) holds the matrices' fp32 Newton-Schulz iterates [m, n] (ping-pong
+  // on the fp32 stage; one, updated in place, plus its bf16 hi/lo operand form [m, 4n] on the bf16
+  // stage), and their Gram products A = X X^T and P = b A + c A A [m, m] in the compute type,
+  // each kind contiguous over the group for the batched GEMMs
+  S->muon.clear();
+  S->mgroups.clear();
+  S->adamw_ranges.clear();
+  S->muon_tab = nullptr;
+  if (sh.optimizer == 1) {
+    const int64_t dkv = (int64_t)sh.n_kv_heads * hd;
+    struct Mx { int64_t off; int rows, cols; };
+    std::vector<Mx> mx;
+    for (const BlockOff& b : S->boff) {
+      mx.push_back({b.wqkv, (int)hqd, (int)d});
+      mx.push_back({b.wqkv + hqd * d, (int)dkv, (int)d});
+      mx.push_back({b.wqkv + hqd * d + dkv * d, (int)dkv, (int)d});
+      mx.push_back({b.wo, (int)d, (int)hqd});
+      mx.push_back({b.wgu, (int)f, (int)d});
+      mx.push_back({b.wgu + f * d, (int)f, (int)d});
+      mx.push_back({b.wdown, (int)d, (int)f});
+    }
+    std::vector<int> gidx(mx.size()), slot(mx.size());
+    for (size_t k = 0; k < mx.size(); ++k) {
+      const int m = std::min(mx[k].rows, mx[k].cols), nn = std::max(mx[k].rows, mx[k].cols);
+      size_t gi = 0;
+      while (gi < S->mgroups.size() && (S->mgroups[gi].m != m || S->mgroups[gi].n != nn)) ++gi;
+      if (gi == S->mgroups.size()) S->mgroups.push_back({m, nn, 0, {nullptr, nullptr}, nullptr, nullptr, nullptr});
+      gidx[k] = (int)gi;
+      slot[k] = S->mgroups[gi].nb++;
+    }
+    for (auto& gr : S->mgroups) {
+      gr.X[0] = (float*)carve((size_t)gr.nb * gr.m * gr.n * 4);
+      gr.X[1] = sh.dtype == 1 ? nullptr : (float*)carve((size_t)gr.nb * gr.m * gr.n * 4);
+      gr.S = sh.dtype == 1 ? (bf16*)carve((size_t)gr.nb * gr.m * gr.n * 4 * 2) : nullptr;
+      gr.A = carve((size_t)gr.nb * gr.m * gr.m * esz);
+      gr.P = carve((size_t)gr.nb * gr.m * gr.m * esz);
+    }
+    int blk = 0, tile = 0;
+    for (size_t k = 0; k < mx.size(); ++k) {
+      const auto& gr = S->mgroups[gidx[k]];
+      MuonMat mm{};
+      mm.off = mx[k].off;
+      mm.rows = mx[k].rows;
+      mm.cols = mx[k].cols;
+      mm.trans = mx[k].rows > mx[k].cols ? 1 : 0;
+      mm.blk0 = blk;
+      mm.tile0 = tile;
+      mm.sqrt_max = (float)std::sqrt((double)std::max(mm.rows, mm.cols));
+      for (int q = 0; q < 2; ++q)
+        mm.x[q] = gr.X[q] ? gr.X[q] + (size_t)slot[k] * gr.m * gr.n : nullptr;
+      blk += (int)muon_chunks((int64_t)mm.rows * mm.cols);
+      tile += (int)muon_tiles(mm.rows, mm.cols);
+      S->muon.push_back(mm);
+    }
+    S->muon_nblk = blk;
+    S->muon_ntile = tile;
+    S->muon_tab = (MuonMat*)carve(S->muon.size() * sizeof(MuonMat));
+    S->muon_part = (double*)carve((size_t)blk * 8);
+    S->muon_norm = (float*)carve(S->muon.size() * 4);
+    // the flat vector outside the matrices (every matrix starts and ends on a 64-element boundary)
+    std::vector<std::pair<int64_t, int64_t>> iv;
+    for (const auto& mm : S->muon) iv.push_back({mm.off, mm.off + (int64_t)mm.rows * mm.cols});
+    std::sort(iv.begin(), iv.end());
+    int64_t at = 0;
+    for (const auto& r : iv) {
+      if (r.first > at) S->adamw_ranges.push_back({at, r.first - at});
+      at = std::max(at, r.second);
+    }
+    if (n > at) S->adamw_ranges.push_back({at, n - at});
+  }
   return off;
 }
 
@@ -517,6 +601,8 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
     }
   hipError_t e = hipMemcpyAsync(S->cos_t, c.data(), c.size() * 4, hipMemcpyHostToDevice, S->st);
   if (e == hipSuccess) e = hipMemcpyAsync(S->sin_t, s.data(), s.size() * 4, hipMemcpyHostToDevice, S->st);
+  if (e == hipSuccess && S->muon_tab)
+    e = hipMemcpyAsync(S->muon_tab, S->muon.data(), S->muon.size() * sizeof(MuonMat), hipMemcpyHostToDevice, S->st);
   if (e == hipSuccess) e = hipStreamSynchronize(S->st);
   if (e == hipSuccess) e = hipGetLastError();
   if (e != hipSuccess) {
@@ -676,6 +762,11 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   if (!s || !hp) return fail(STAGE_EINVAL, "null argument");
   if (hp->delay != 0 && hp->delay != 1) return fail(STAGE_EINVAL, "delay must be 0 or 1");
   if (hp->delay == 0 && hp->ef_lambda != 0.f) return fail(STAGE_EINVAL, "Error Feedback needs delay 1");
+  if (hp->optimizer != 0 && hp->optimizer != 1) return fail(STAGE_EINVAL, "optimizer must be 0 (AdamW) or 1 (Muon)");
+  if (hp->optimizer == 1 && s->sh.optimizer != 1)
+    return fail(STAGE_EINVAL, "Muon needs a stage shaped with optimizer = 1 (its Newton-Schulz workspace)");
+  if (hp->optimizer == 1 && (hp->ns_steps < 1 || hp->ns_steps > 32))
+    return fail(STAGE_EINVAL, "ns_steps must be in [1, 32]");
   if (t != s->next_t) return fail(STAGE_ESTATE, "delayed_update: expected t = " + std::to_string(s->next_t));
   const int64_t gstep = hp->delay == 1 ? t - 1 : t;  // the gradient this iteration consumes
   bool apply = gstep >= 0;
@@ -730,11 +821,93 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   // bytes: x, m, v r+w; g read; shadow write; u_prev r+w with EF (no-op pass: x read, shadow write)
   const double ub = apply ? (24.0 + 4.0 + (s->bf ? 2.0 : 4.0) + (hp->ef_lambda != 0.f ? 8.0 : 0.0))
                           : (4.0 + (s->bf ? 2.0 : 4.0));
-  timed(s, STAGE_PROF_UPDATE, ub * s->n_flat, [&] {
-    launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v,
-                        hp->ef_lambda != 0.f ? s->u_prev : nullptr, s->ver[vout], s->bf ? 2 : 1, hs,
-                        clip, flag, device_cu_count(), us);
-  }, us);
+  float* up = hp->ef_lambda != 0.f ? s->u_prev : nullptr;
+  if (apply && hp->optimizer == 1) {
+    // AdamW on the embedding, the gains and the padding ...
+    for (const auto& r : s->adamw_ranges) {
+      const int64_t o = r.first;
+      timed(s, STAGE_PROF_UPDATE, ub * r.second, [&] {
+        launch_fused_update(r.second, s->master + o, s->grad[gb] + o, false, s->m + o, s->v + o,
+                            up ? up + o : nullptr, (char*)s->ver[vout] + o * s->esz, s->bf ? 2 : 1, hs, clip,
+                            flag, r.second > (1 << 22) ? device_cu_count() : 0, us);
+      }, us);
+    }
+    // ... and Muon on the blocks' weight matrices (Alg. 2): momentum and norms, the normalised
+    // wide-orientation copy, Newton-Schulz, the update
+    int64_t nm = 0;
+    for (const auto& mm : s->muon) nm += (int64_t)mm.rows * mm.cols;
+    const int nmat = (int)s->muon.size();
+    timed(s, STAGE_PROF_UPDATE, (12.0 + 4.0 + 4.0) * nm, [&] {
+      launch_muon_momentum(s->muon_tab, nmat, s->muon_nblk, s->grad[gb], s->m, clip, flag, hp->momentum,
+                           s->muon_part, s->muon_norm, us);
+      launch_muon_prep(s->muon_tab, nmat, s->muon_ntile, s->m, s->muon_norm, us);
+    }, us);
+    // quintic Newton-Schulz coefficients of the Muon write-up (Jordan et al., 2024)
+    const float ca = 3.4445f, cb = -4.7750f, cc = 2.0315f;
+    for (const auto& gr : s->mgroups) {
+      const int m = gr.m, n = gr.n;
+      const int64_t mn = (int64_t)m * n, mm2 = (int64_t)m * m;
+      if (s->bf) {
+        // X in fp32, its products from the hi/lo form S = [hi | hi | lo | hi]:
+        //   A  = S[:, 0:3n] S[:, n:4n]^T = hi hi^T + hi lo^T + lo hi^T     (bf16)
+        //   P  = c A A + b A                                                 (bf16)
+        //   X <- P lo + a X, then X <- P hi + X                              (fp32, in place)
+        const double fl = 2.0 * gr.nb * (5.0 * mm2 * n + (double)mm2 * m);
+        timed(s, STAGE_PROF_UPDATE, 12.0 * gr.nb * mn, [&] {
+          launch_muon_split(gr.X[0], gr.S, (int64_t)gr.nb * m, n, us);
+        }, us);
+        for (int it = 0; it < hp->ns_steps; ++it) {
+          GemmArgs g1 = gemm(m, m, 3 * n, gr.S, 4 * n, true, gr.S + n, 4 * n, true, gr.A, m);
+          g1.batch = gr.nb; g1.sA = g1.sB = 4 * mn; g1.sC = mm2;
+          GemmArgs g2 = gemm(m, m, m, gr.A, m, true, gr.A, m, true, gr.P, m);
+          g2.epi = GEMM_EPI_AXPBY; g2.alpha = cc; g2.beta_d = cb; g2.D = gr.A;
+          g2.batch = gr.nb; g2.sA = g2.sB = g2.sC = g2.sD = mm2;
+          GemmArgs g3 = gemm(m, n, m, gr.P, m, true, gr.S + 2 * n, 4 * n, false, gr.X[0], n, true, ca);
+          g3.batch = gr.nb; g3.sA = mm2; g3.sB = 4 * mn; g3.sC = mn;
+          GemmArgs g4 = g3;
+          g4.B = gr.S;
+          g4.beta = 1.f;
+          timed(s, STAGE_PROF_NS, fl, [&] {
+            launch_gemm(true, g1, us);
+            launch_gemm(true, g2, us);
+            launch_gemm(true, g3, us);
+            launch_gemm(true, g4, us);
+            launch_muon_split(gr.X[0], gr.S, (int64_t)gr.nb * m, n, us);
+          }, us);
+        }
+      } else {
+        const double fl = 2.0 * gr.nb * (2.0 * mm2 * n + (double)mm2 * m);
+        for (int it = 0; it < hp->ns_steps; ++it) {
+          float* X = gr.X[it % 2];
+          float* Xn = gr.X[(it + 1) % 2];
+          // A = X X^T;  P = c A A + b A;  X' = P X + a X
+          GemmArgs g1 = gemm(m, m, n, X, n, true, X, n, true, gr.A, m);
+          g1.batch = gr.nb; g1.sA = g1.sB = mn; g1.sC = mm2;
+          GemmArgs g2 = gemm(m, m, m, gr.A, m, true, gr.A, m, true, gr.P, m);
+          g2.epi = GEMM_EPI_AXPBY; g2.alpha = cc; g2.beta_d = cb; g2.D = gr.A;
+          g2.batch = gr.nb; g2.sA = g2.sB = g2.sC = g2.sD = mm2;
+          GemmArgs g3 = gemm(m, n, m, gr.P, m, true, X, n, false, Xn, n);
+          g3.epi = GEMM_EPI_AXPBY; g3.alpha = 1.f; g3.beta_d = ca; g3.D = X;
+          g3.batch = gr.nb; g3.sA = mm2; g3.sB = g3.sC = g3.sD = mn;
+          timed(s, STAGE_PROF_NS, fl, [&] {
+            launch_gemm(false, g1, us);
+            launch_gemm(false, g2, us);
+            launch_gemm(false, g3, us);
+          }, us);
+        }
+      }
+    }
+    const bool ef = hs.ef != 0;
+    timed(s, STAGE_PROF_UPDATE, (s->esz + 8.0 + 4.0 + s->esz + (up ? 8.0 : 0.0)) * nm, [&] {
+      launch_muon_apply(s->bf, s->muon_tab, nmat, s->muon_ntile, s->bf ? 0 : hp->ns_steps % 2, s->master, up, s->ver[vout],
+                        flag, hp->lr, hp->weight_decay, hp->update_rms, ef, hp->ef_lambda, us);
+    }, us);
+  } else {
+    timed(s, STAGE_PROF_UPDATE, ub * s->n_flat, [&] {
+      launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v, up, s->ver[vout],
+                          s->bf ? 2 : 1, hs, clip, flag, device_cu_count(), us);
+    }, us);
+  }
   HIP_OK(hipGetLastError());
   // everything enqueued on the stage stream from here on runs after the update
   HIP_OK(hipEventRecord(s->ev_upd, us));
@@ -753,6 +926,7 @@ int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf
                         const update_hparams_t* hp, const float* clip_scale_dev, void* hip_stream) {
   if (!hp || n < 0 || t < 0) return fail(STAGE_EINVAL, "bad argument");
   if (hp->delay != 1) return fail(STAGE_EINVAL, "delayed_update_flat implements delay 1");
+  if (hp->optimizer != 0) return fail(STAGE_EINVAL, "delayed_update_flat implements AdamW (optimizer 0)");
   if (n == 0) return STAGE_OK;
   if (!x || !g_prev || !m || !v) return fail(STAGE_EINVAL, "null vector");
   if (hp->ef_lambda != 0.f && !u_prev) return fail(STAGE_EINVAL, "Error Feedback needs u_prev");

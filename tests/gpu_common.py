@@ -23,12 +23,12 @@ def rel(a, b) -> float:
     return float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-30))
 
 
-def shape_of(w):
+def shape_of(w, muon=False):
     from paper_2606_30634_amd.stage import make_shape
     return make_shape(w.n_blocks, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ffn, w.vocab,
                       w.first_stage, w.last_stage, w.tie_embedding, w.seq_len, w.micro_batch,
                       w.max_inflight, bf16=(w.dtype == "bf16"), rms_eps=w.rms_eps,
-                      rope_theta=w.rope_theta)
+                      rope_theta=w.rope_theta, muon=muon)
 
 
 def hp_of(w, **kw):
@@ -66,7 +66,7 @@ def schedule_1f1b(M: int, warm: int):
 
 
 def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps: Iterable[int] = (),
-            device: str = "cuda:0", upd_steps: Iterable[int] = ()):
+            device: str = "cuda:0", upd_steps: Iterable[int] = (), muon: bool = False):
     """T iterations of Alg. 1 on the GPU stage.  Returns losses (per step, per microbatch), outputs
     at y_steps, and at grad_steps the gradient g_t together with the master weights x_t it was taken
     at, at upd_steps the whole optimizer state before and after delayed_update(t) with the gradient
@@ -74,7 +74,7 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     import torch
     from paper_2606_30634_amd.stage import Stage
     dev = torch.device(device)
-    st = Stage(shape_of(w), device)
+    st = Stage(shape_of(w, muon=muon or hp.optimizer == 1), device)
     st.load_master(params0)
     names = list(params0)
     grad_steps, y_steps = set(grad_steps), set(y_steps)
