@@ -7,6 +7,11 @@ d_model 768, 12 heads, SwiGLU 3072, seq 1024, microbatch 8, vocab-32000 embeddin
 stage), synthetic seeded inputs already resident in HBM.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload small|mid|large|tiny] [--no-cpu-baseline]
+                  [--optimizer adamw|muon]
+
+With --optimizer muon the blocks' weight matrices take delayed Muon (Alg. 2: momentum 0.95, five
+quintic Newton-Schulz steps, update RMS 0.2) with Error Feedback lambda = 1, the embedding and gains
+AdamW; the line then also reports the Newton-Schulz GEMMs as their own kernel class.
 """
 from __future__ import annotations
 
@@ -63,7 +68,7 @@ def measured_traffic(workload, kernel_class):
     return float(v) if v is not None else None
 
 
-def cpu_baseline(w):
+def cpu_baseline(w, optimizer="adamw"):
     """The oracle (float32, numpy) timed on whole optimizer steps of the workload -- all sequences
     forward+backward, then the full delayed update -- repeated until at least 10 s of CPU work (at
     most 4 steps) when one step is a bounded amount of work; otherwise on 2 of the step's sequences
@@ -81,7 +86,7 @@ def cpu_baseline(w):
     n_seq = w.micro_batch if w.d_model <= 1024 else min(2, w.micro_batch)
     ws = w.with_(micro_batch=n_seq)
     p0 = datagen.init_params(ws)
-    hp = oracle.hparams_of(ws)
+    hp = oracle.hparams_of(ws, optimizer=optimizer)
     st = OptState.create(p0, np.float32)
     inp = datagen.step_inputs(ws, 0)
     g, _ = model.stage_step_grads(st.x, [inp], ws, np.float32)
@@ -91,7 +96,7 @@ def cpu_baseline(w):
         t0 = time.perf_counter()
         g, _ = model.stage_step_grads(st.x, [inp], ws, np.float32)
         t1 = time.perf_counter()
-        iteration_update(st, g, hp)   # the full AdamW + clip + EF pass
+        iteration_update(st, g, hp)   # the full optimizer + clip + EF pass
         t2 = time.perf_counter()
         fb_s += t1 - t0
         upd_s += t2 - t1
@@ -164,6 +169,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="small")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--optimizer", choices=("adamw", "muon"), default="adamw")
     ap.add_argument("--update-steps", type=int, default=50,
                     help="iterations of the update-only workload (1.0e9 fp32 elements); 0 skips it")
     ap.add_argument("--calib-copy", action="store_true",
@@ -182,14 +188,16 @@ def main():
     from paper_2606_30634_amd.stage import Stage, hparams, make_shape
 
     w = datagen.WORKLOADS[args.workload]
+    muon = args.optimizer == "muon"
     dev = torch.device("cuda:0")
     bf = w.dtype == "bf16"
     st = Stage(make_shape(w.n_blocks, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ffn, w.vocab,
                           w.first_stage, w.last_stage, w.tie_embedding, w.seq_len, w.micro_batch,
-                          w.max_inflight, bf16=bf, rms_eps=w.rms_eps, rope_theta=w.rope_theta), "cuda:0")
+                          w.max_inflight, bf16=bf, rms_eps=w.rms_eps, rope_theta=w.rope_theta,
+                          muon=muon), "cuda:0")
     st.load_master(datagen.init_params(w))
     hp = hparams(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay,
-                 clip_norm=w.clip_norm, ef_lambda=1.0, delay=1)
+                 clip_norm=w.clip_norm, ef_lambda=1.0, delay=1, optimizer=args.optimizer)
     M = w.microbatches_per_step
     cdt = torch.bfloat16 if bf else torch.float32
     # two distinct input sets per microbatch, resident in HBM, alternated across steps
@@ -261,7 +269,7 @@ def main():
     for _ in range(args.steps):
         step(t); t += 1
     classes = {"gemm": B.PROF_GEMM, "attention_fwd": B.PROF_ATTN_FWD, "attention_bwd": B.PROF_ATTN_BWD,
-               "delayed_update": B.PROF_UPDATE, "grad_norm": B.PROF_NORM}
+               "delayed_update": B.PROF_UPDATE, "grad_norm": B.PROF_NORM, "newton_schulz": B.PROF_NS}
     kern = {}
     for name, c in classes.items():
         kms, n, work = B.stage_profile_read(st.handle, c)
@@ -290,12 +298,12 @@ def main():
     rc, skipped = B.stage_poll_nonfinite(st.handle)
     st.close()
 
-    upd = update_workload(args.update_steps) if args.update_steps > 0 else None
+    upd = update_workload(args.update_steps) if args.update_steps > 0 and not muon else None
 
     cpu = None
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline")
-        cpu = cpu_baseline(w)
+        cpu = cpu_baseline(w, args.optimizer)
 
     out = {
         "metric": "stage tokens/sec (fwd+bwd+delayed update)",
@@ -311,7 +319,10 @@ def main():
         "dtype": "bf16" if bf else "f32",
         "data": "synthetic (seeded: uniform tokens / N(0,1) activations, N(0,1e-3) upstream gradients, N(0,0.02) weights)",
         "config": {"workload": w.name, "tokens_per_step": tokens, "microbatches_per_step": M,
-                   "optimizer": "AdamW, delay 1, Error Feedback lambda 1, clip 1.0", "parallelism": "1 GPU, one stage"},
+                   "optimizer": ("Muon (momentum 0.95, 5 Newton-Schulz steps, update RMS 0.2) on the block "
+                                 "matrices, AdamW elsewhere" if muon else "AdamW") +
+                                ", delay 1, Error Feedback lambda 1, clip 1.0",
+                   "parallelism": "1 GPU, one stage"},
         "roofline": roofline,
         "kernels": kern,
         "update_workload": upd,

@@ -842,59 +842,57 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
                            s->muon_part, s->muon_norm, us);
       launch_muon_prep(s->muon_tab, nmat, s->muon_ntile, s->m, s->muon_norm, us);
     }, us);
-    // quintic Newton-Schulz coefficients of the Muon write-up (Jordan et al., 2024)
+    // quintic Newton-Schulz coefficients of the Muon write-up (Jordan et al., 2024); one timed
+    // launch per group, its work the method's flops: ns_steps x 2 nb (2 m^2 n + m^3)
     const float ca = 3.4445f, cb = -4.7750f, cc = 2.0315f;
     for (const auto& gr : s->mgroups) {
       const int m = gr.m, n = gr.n;
       const int64_t mn = (int64_t)m * n, mm2 = (int64_t)m * m;
+      const double fl = hp->ns_steps * 2.0 * gr.nb * (2.0 * mm2 * n + (double)mm2 * m);
       if (s->bf) {
         // X in fp32, its products from the hi/lo form S = [hi | hi | lo | hi]:
         //   A  = S[:, 0:3n] S[:, n:4n]^T = hi hi^T + hi lo^T + lo hi^T     (bf16)
         //   P  = c A A + b A                                                 (bf16)
         //   X <- P lo + a X, then X <- P hi + X                              (fp32, in place)
-        const double fl = 2.0 * gr.nb * (5.0 * mm2 * n + (double)mm2 * m);
-        timed(s, STAGE_PROF_UPDATE, 12.0 * gr.nb * mn, [&] {
+        GemmArgs g1 = gemm(m, m, 3 * n, gr.S, 4 * n, true, gr.S + n, 4 * n, true, gr.A, m);
+        g1.batch = gr.nb; g1.sA = g1.sB = 4 * mn; g1.sC = mm2;
+        GemmArgs g2 = gemm(m, m, m, gr.A, m, true, gr.A, m, true, gr.P, m);
+        g2.epi = GEMM_EPI_AXPBY; g2.alpha = cc; g2.beta_d = cb; g2.D = gr.A;
+        g2.batch = gr.nb; g2.sA = g2.sB = g2.sC = g2.sD = mm2;
+        GemmArgs g3 = gemm(m, n, m, gr.P, m, true, gr.S + 2 * n, 4 * n, false, gr.X[0], n, true, ca);
+        g3.batch = gr.nb; g3.sA = mm2; g3.sB = 4 * mn; g3.sC = mn;
+        GemmArgs g4 = g3;
+        g4.B = gr.S;
+        g4.beta = 1.f;
+        timed(s, STAGE_PROF_NS, fl, [&] {
           launch_muon_split(gr.X[0], gr.S, (int64_t)gr.nb * m, n, us);
-        }, us);
-        for (int it = 0; it < hp->ns_steps; ++it) {
-          GemmArgs g1 = gemm(m, m, 3 * n, gr.S, 4 * n, true, gr.S + n, 4 * n, true, gr.A, m);
-          g1.batch = gr.nb; g1.sA = g1.sB = 4 * mn; g1.sC = mm2;
-          GemmArgs g2 = gemm(m, m, m, gr.A, m, true, gr.A, m, true, gr.P, m);
-          g2.epi = GEMM_EPI_AXPBY; g2.alpha = cc; g2.beta_d = cb; g2.D = gr.A;
-          g2.batch = gr.nb; g2.sA = g2.sB = g2.sC = g2.sD = mm2;
-          GemmArgs g3 = gemm(m, n, m, gr.P, m, true, gr.S + 2 * n, 4 * n, false, gr.X[0], n, true, ca);
-          g3.batch = gr.nb; g3.sA = mm2; g3.sB = 4 * mn; g3.sC = mn;
-          GemmArgs g4 = g3;
-          g4.B = gr.S;
-          g4.beta = 1.f;
-          timed(s, STAGE_PROF_NS, fl, [&] {
+          for (int it = 0; it < hp->ns_steps; ++it) {
             launch_gemm(true, g1, us);
             launch_gemm(true, g2, us);
             launch_gemm(true, g3, us);
             launch_gemm(true, g4, us);
-            launch_muon_split(gr.X[0], gr.S, (int64_t)gr.nb * m, n, us);
-          }, us);
-        }
+            if (it + 1 < hp->ns_steps) launch_muon_split(gr.X[0], gr.S, (int64_t)gr.nb * m, n, us);
+          }
+        }, us);
       } else {
-        const double fl = 2.0 * gr.nb * (2.0 * mm2 * n + (double)mm2 * m);
-        for (int it = 0; it < hp->ns_steps; ++it) {
-          float* X = gr.X[it % 2];
-          float* Xn = gr.X[(it + 1) % 2];
-          // A = X X^T;  P = c A A + b A;  X' = P X + a X
-          GemmArgs g1 = gemm(m, m, n, X, n, true, X, n, true, gr.A, m);
-          g1.batch = gr.nb; g1.sA = g1.sB = mn; g1.sC = mm2;
-          GemmArgs g2 = gemm(m, m, m, gr.A, m, true, gr.A, m, true, gr.P, m);
-          g2.epi = GEMM_EPI_AXPBY; g2.alpha = cc; g2.beta_d = cb; g2.D = gr.A;
-          g2.batch = gr.nb; g2.sA = g2.sB = g2.sC = g2.sD = mm2;
-          GemmArgs g3 = gemm(m, n, m, gr.P, m, true, X, n, false, Xn, n);
-          g3.epi = GEMM_EPI_AXPBY; g3.alpha = 1.f; g3.beta_d = ca; g3.D = X;
-          g3.batch = gr.nb; g3.sA = mm2; g3.sB = g3.sC = g3.sD = mn;
-          timed(s, STAGE_PROF_NS, fl, [&] {
+        timed(s, STAGE_PROF_NS, fl, [&] {
+          for (int it = 0; it < hp->ns_steps; ++it) {
+            float* X = gr.X[it % 2];
+            float* Xn = gr.X[(it + 1) % 2];
+            // A = X X^T;  P = c A A + b A;  X' = P X + a X
+            GemmArgs g1 = gemm(m, m, n, X, n, true, X, n, true, gr.A, m);
+            g1.batch = gr.nb; g1.sA = g1.sB = mn; g1.sC = mm2;
+            GemmArgs g2 = gemm(m, m, m, gr.A, m, true, gr.A, m, true, gr.P, m);
+            g2.epi = GEMM_EPI_AXPBY; g2.alpha = cc; g2.beta_d = cb; g2.D = gr.A;
+            g2.batch = gr.nb; g2.sA = g2.sB = g2.sC = g2.sD = mm2;
+            GemmArgs g3 = gemm(m, n, m, gr.P, m, true, X, n, false, Xn, n);
+            g3.epi = GEMM_EPI_AXPBY; g3.alpha = 1.f; g3.beta_d = ca; g3.D = X;
+            g3.batch = gr.nb; g3.sA = mm2; g3.sB = g3.sC = g3.sD = mn;
             launch_gemm(false, g1, us);
             launch_gemm(false, g2, us);
             launch_gemm(false, g3, us);
-          }, us);
-        }
+          }
+        }, us);
       }
     }
     const bool ef = hs.ef != 0;
