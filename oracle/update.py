@@ -12,6 +12,14 @@ Alg. 1, one iteration t (g_{-1} = 0, u_{-1} = 0):
 (lambda = 1 is the equation of §3.2; lambda = 0 is standard async.)  With delay 0 the same
 update consumes g_t instead, which is plain synchronous AdamW.
 
+Delay tau >= 2 (the delayed-gradient method of App. C with prev(k) = k - tau): iteration t consumes
+g_{t-tau} (iterations t < tau change nothing), and Error Feedback takes the update formed tau
+iterations earlier,
+    x_{t+1} = x_t - u - lambda (u - u_{t-tau})
+which is the appendix's x_{k+1} = x_k - (tau + 1) u_k + tau u_{k-tau} at lambda = tau (the
+coefficients its convergence proof uses) and the printed algorithm's 2 / 1 at lambda = 1.  The step
+is standard until tau earlier updates exist (the "t <= 1" rule of Alg. 1 for tau = 1).
+
 u is decoupled AdamW (§2: beta = (0.9, 0.95); App. E.1: weight decay 0.1, clipping at 1.0):
     g <- c g,  c = min(1, clip / (||g||_2 + 1e-6))        (global norm over the stage)
     m <- b1 m + (1 - b1) g;   v <- b2 v + (1 - b2) g^2
@@ -40,7 +48,7 @@ from __future__ import annotations
 
 import math
 from dataclasses import dataclass, field
-from typing import Dict, Optional
+from typing import Dict, List, Optional
 
 import numpy as np
 
@@ -54,7 +62,7 @@ class HParams:
     weight_decay: float = 0.1
     clip_norm: float = 1.0       # <= 0 disables clipping
     ef_lambda: float = 0.0       # 0: standard async; 1: Error Feedback of §3.2
-    delay: int = 1               # 1: Alg. 1; 0: synchronous
+    delay: int = 1               # 1: Alg. 1; 0: synchronous; tau >= 2: g_{t-tau} with tau-step EF
     optimizer: str = "adamw"     # "adamw", or "muon": Alg. 2 on the blocks' weight matrices
     momentum: float = 0.95       # Muon momentum mu
     update_rms: float = 0.2      # Muon update RMS
@@ -142,6 +150,8 @@ class OptState:
     pending: Optional[Dict[str, np.ndarray]] = None  # g_{t-1}, not yet consumed
     n_updates: int = 0                      # updates applied so far
     t: int = 0                              # next iteration index
+    queue: List[Dict[str, np.ndarray]] = field(default_factory=list)   # delay >= 2: g_{t-tau} .. g_{t-1}
+    u_ring: List[Dict[str, np.ndarray]] = field(default_factory=list)  # delay >= 2: the last tau updates, oldest first
 
     @staticmethod
     def create(x: Dict[str, np.ndarray], dt=np.float64) -> "OptState":
@@ -153,19 +163,21 @@ class OptState:
     def copy(self) -> "OptState":
         cp = lambda d: None if d is None else {k: v.copy() for k, v in d.items()}
         return OptState(cp(self.x), cp(self.m), cp(self.v), cp(self.u_prev), cp(self.pending),
-                        self.n_updates, self.t)
+                        self.n_updates, self.t, [cp(g) for g in self.queue], [cp(u) for u in self.u_ring])
 
 
 def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> dict:
     """Second half of iteration t of Alg. 1, after g_t has been computed at x_t.
 
     Mutates st into the state at iteration t+1 and returns diagnostics (applied, norm, clip)."""
-    if hp.delay not in (0, 1):
-        raise ValueError("delay must be 0 or 1")
+    if hp.delay < 0:
+        raise ValueError("delay must be >= 0")
     if hp.delay == 0 and hp.ef_lambda != 0.0:
-        raise ValueError("Error Feedback needs a delayed gradient (delay 1)")
+        raise ValueError("Error Feedback needs a delayed gradient (delay >= 1)")
     if hp.optimizer not in ("adamw", "muon"):
         raise ValueError("optimizer must be adamw or muon")
+    if hp.delay >= 2:
+        return _iteration_update_tau(st, g_t, hp)
     if hp.delay == 1:
         g_use = st.pending
     else:
@@ -179,11 +191,7 @@ def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> d
         k = st.n_updates + 1
         ef = hp.ef_lambda != 0.0 and st.n_updates >= 1   # "t <= 1": the first update is standard
         for name in st.x:
-            g = g_use[name] * c
-            if hp.optimizer == "muon" and is_muon_matrix(name):
-                u, st.m[name] = muon_u(st.x[name], g, st.m[name], hp)   # m holds Muon's momentum
-            else:
-                u, st.m[name], st.v[name] = adamw_u(st.x[name], g, st.m[name], st.v[name], k, hp)
+            u = _u_of(st, name, g_use[name] * c, k, hp)
             st.x[name] = apply_update(st.x[name], u, st.u_prev[name], ef, hp.ef_lambda)
             st.u_prev[name] = u
         st.n_updates = k
@@ -193,13 +201,54 @@ def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> d
     return info
 
 
-def flat_update(x, g, m, v, u_prev, t: int, hp: HParams, clip_scale: float = 1.0):
-    """Elementwise form on flat arrays for a fixed delay-1 run: iteration t consumes g (= g_{t-1}).
+def _u_of(st: OptState, name: str, g, k: int, hp: HParams):
+    """u of one parameter from its clipped gradient; updates the optimizer statistics in st."""
+    if hp.optimizer == "muon" and is_muon_matrix(name):
+        u, st.m[name] = muon_u(st.x[name], g, st.m[name], hp)   # m holds Muon's momentum
+    else:
+        u, st.m[name], st.v[name] = adamw_u(st.x[name], g, st.m[name], st.v[name], k, hp)
+    return u
 
-    t = 0 is a no-op; the update is the k = t-th; EF applies from t = 2 on.  Returns the new
-    (x, m, v, u_prev)."""
-    if t == 0:
+
+def _iteration_update_tau(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> dict:
+    """Iteration t with delay tau = hp.delay >= 2: consume g_{t-tau} once tau gradients wait, EF
+    against the update formed tau iterations earlier once tau updates exist."""
+    tau = hp.delay
+    info = dict(applied=False, norm=0.0, clip=1.0)
+    if len(st.queue) == tau:
+        g_use = st.queue.pop(0)
+        norm = global_norm(g_use)
+        if not math.isfinite(norm):
+            raise NonFiniteGradient(f"non-finite gradient norm at iteration {st.t}")
+        c = clip_coefficient(norm, hp.clip_norm)
+        k = st.n_updates + 1
+        ef = hp.ef_lambda != 0.0 and len(st.u_ring) == tau
+        new_u = {}
+        for name in st.x:
+            u = _u_of(st, name, g_use[name] * c, k, hp)
+            old = st.u_ring[0][name] if ef else None
+            st.x[name] = apply_update(st.x[name], u, old, ef, hp.ef_lambda)
+            new_u[name] = u
+        st.u_ring.append(new_u)
+        if len(st.u_ring) > tau:
+            st.u_ring.pop(0)
+        st.n_updates = k
+        info.update(applied=True, norm=norm, clip=c)
+    st.queue.append({k: v.copy() for k, v in g_t.items()})
+    st.t += 1
+    return info
+
+
+def flat_update(x, g, m, v, u_prev, t: int, hp: HParams, clip_scale: float = 1.0):
+    """Elementwise form on flat arrays for a fixed-delay run (tau = hp.delay, at least 1): iteration
+    t consumes g (= g_{t-tau}) and u_prev holds the update formed tau iterations earlier.
+
+    t < tau is a no-op; the update is the k = (t - tau + 1)-th; EF applies once tau earlier updates
+    exist (k > tau, i.e. t >= 2 tau).  Returns the new (x, m, v, u_prev)."""
+    tau = max(hp.delay, 1)
+    if t < tau:
         return x, m, v, u_prev
-    u, m1, v1 = adamw_u(x, g * clip_scale, m, v, t, hp)
-    ef = hp.ef_lambda != 0.0 and t >= 2
+    k = t - tau + 1
+    u, m1, v1 = adamw_u(x, g * clip_scale, m, v, k, hp)
+    ef = hp.ef_lambda != 0.0 and k > tau
     return apply_update(x, u, u_prev, ef, hp.ef_lambda), m1, v1, u
