@@ -13,6 +13,10 @@
  *   - §2 / App. F.1: PipeDream-2BW keeps one stashed weight version, so a stage holds two compute
  *     copies of its weights (versions t mod 2) and two gradient buffers (g_t being accumulated,
  *     g_{t-1} being consumed).
+ *   - App. C (delayed method with prev(k) = k - tau): a fixed delay tau >= 2 consumes g_{t-tau},
+ *     with Error Feedback against the update formed tau iterations earlier, x_{t+1} = x_t - u -
+ *     lambda (u - u_{t-tau}) (lambda = tau: the coefficients tau + 1 and tau of its proof); the
+ *     stage then holds tau + 1 gradient buffers and tau EF buffers.
  *   - App. E.2: the stage is a stack of Llama-style decoder blocks (pre-norm RMSNorm, grouped-query
  *     causal attention with RoPE, SwiGLU feed-forward, no biases); a first stage owns the token
  *     embedding, a last stage the tied LM head with next-token cross-entropy (App. E).
@@ -59,15 +63,20 @@ typedef enum {
 
 typedef enum { STAGE_DT_F32 = 0, STAGE_DT_BF16 = 1, STAGE_DT_I32 = 2 } stage_dtype;
 
+/* Largest delay a stage can be shaped for (stage_shape_t.max_delay). */
+enum { STAGE_MAX_DELAY = 8 };
+
 /* Shape of one stage.  dtype 0: fp32 compute and storage; 1: bf16 compute copies, bf16
  * activations, fp32 accumulation, fp32 master weights / optimizer state / gradients.
  * vocab > 0 requires first_stage (token embedding [vocab, d_model]); last_stage requires
  * tie_embedding and vocab > 0 (logits = RMSNorm(x) E^T).  head_dim in {32, 64, 128};
  * n_heads a multiple of n_kv_heads; d_model a multiple of 64.  max_inflight >= 1 is the number
  * of activation slots (microbatches whose backward is pending).  optimizer 0: AdamW only;
- * 1: the arena also holds the Newton-Schulz workspace of delayed Muon (Alg. 2 of §4), about two
- * bf16 (fp32) copies of the blocks' weight matrices plus their Gram matrices, so that
- * delayed_update accepts update_hparams_t.optimizer = 1. */
+ * 1: the arena also holds the Newton-Schulz workspace of delayed Muon (Alg. 2 of §4), about 12 (fp32
+ * stage: 8) bytes per element of the blocks' weight matrices plus their Gram matrices, so that
+ * delayed_update accepts update_hparams_t.optimizer = 1.  max_delay in [0, 8] (0 is read as 1):
+ * the largest delay delayed_update accepts; the arena holds max_delay + 1 gradient buffers and
+ * max_delay EF buffers. */
 typedef struct {
   int32_t n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ffn;
   int32_t vocab, first_stage, last_stage, tie_embedding;
@@ -75,16 +84,20 @@ typedef struct {
   int32_t dtype;
   float rms_eps, rope_theta;
   int32_t optimizer;
+  int32_t max_delay;
 } stage_shape_t;
 
 /* Hyper-parameters of one update.  clip_norm <= 0 disables clipping.  ef_lambda = 0 is standard
  * delayed training, 1 the Error-Feedback equation of §3.2.  delay 1 is Alg. 1; delay 0 is the
- * synchronous optimizer (requires ef_lambda = 0).
+ * synchronous optimizer (requires ef_lambda = 0); delay tau in [2, max_delay] consumes g_{t-tau}
+ * with EF against the update formed tau iterations earlier (ef_lambda = tau reproduces the
+ * appendix's x_k - (tau + 1) u_k + tau u_{k-tau}).  The delay of a stage stays fixed over a run.
  * optimizer 0: AdamW (beta1, beta2, eps) on every parameter.  optimizer 1: delayed Muon (Alg. 2
  * of §4) on every 2-D weight matrix of a block (wq, wk, wv, wo, wgate, wup, wdown, each on its
  * own) and AdamW on the embedding and the gains: M <- momentum M + (1 - momentum) c g;
  * O = Newton-Schulz(M) (ns_steps >= 1 quintic iterations on M / ||M||_F in the orientation with
- * rows <= cols, coefficients (3.4445, -4.7750, 2.0315), in the stage's compute type);
+ * rows <= cols, coefficients (3.4445, -4.7750, 2.0315); on a bf16 stage the iterate stays fp32
+ * and enters the bf16 products as a hi + lo pair, A = X X^T and b A + c A A are bf16);
  * u = lr (update_rms sqrt(max(rows, cols)) O + weight_decay x_t); then the same standard or
  * Error-Feedback step as AdamW.  Needs a stage shaped with optimizer 1. */
 typedef struct {
@@ -95,8 +108,9 @@ typedef struct {
   int32_t ns_steps;
 } update_hparams_t;
 
-/* Bytes of device memory the stage needs (weights, optimizer state, two gradient buffers, two
- * compute versions, the activation ring and scratch).  0 on an invalid shape. */
+/* Bytes of device memory the stage needs (weights, optimizer state, max_delay + 1 gradient
+ * buffers, max_delay EF buffers, two compute versions, the activation ring and scratch).  0 on an
+ * invalid shape. */
 size_t stage_required_bytes(const stage_shape_t* shape);
 
 /* Carve the arena (device memory, >= stage_required_bytes, 256-byte aligned) and zero the
@@ -110,10 +124,12 @@ int stage_num_tensors(const stage_t* s, int32_t* count);
 
 /* Tensor idx: name, device pointer, element count and dtype (stage_dtype).  Names:
  *   "embed", "blk{i}.attn_norm|wq|wk|wv|wo|ffn_norm|wgate|wup|wdown", "final_norm"  - fp32
- *   master weights [out, in]; the same names prefixed "m.", "v.", "u_prev.", "grad0.", "grad1."
- *   (fp32 optimizer state, EF buffer, the two gradient buffers) and "w0.", "w1." (the two
- *   compute versions, bf16 or fp32); "flat.master|m|v|u_prev|grad0|grad1|w0|w1" for the whole
- *   flat vectors (padding between tensors is zero and stays zero);
+ *   master weights [out, in]; the same names prefixed "m.", "v.", "u_prev." (fp32 optimizer
+ *   state, EF buffer), "u_prev{j}." for j in [1, max_delay) (the further EF buffers: iteration t
+ *   of a delay-tau run uses buffer t mod tau, "u_prev." being buffer 0), "grad{j}." for j in
+ *   [0, max_delay] (gradient buffers: step s accumulates into buffer s mod (max_delay + 1)) and
+ *   "w0.", "w1." (the two compute versions, bf16 or fp32); "flat.master|m|v|u_prev|u_prev{j}|
+ *   grad{j}|w0|w1" for the whole flat vectors (padding between tensors is zero and stays zero);
  *   "act{slot}.blk{i}.{x|rstd1|n1|qkv|o|lse|h|rstd2|n2|gu|z}" and "act{slot}.{x0|y|logits}"
  *   for the saved activations of an activation slot. */
 int stage_tensor(const stage_t* s, int32_t idx, const char** name, void** dev_ptr,
@@ -142,28 +158,31 @@ int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens,
                   const int32_t* targets, void* y_out, float* loss_dev);
 
 /* Backward of the microbatch saved in `slot`; its parameter gradient is added to gradient buffer
- * (step mod 2) - the first backward of a step overwrites it.  dy: upstream gradient
+ * (step mod (max_delay + 1)) - the first backward of a step overwrites it; STAGE_ESTATE if that
+ * buffer still holds a gradient no update has consumed.  dy: upstream gradient
  * [micro_batch, seq_len, d_model] (non-last stage; NULL on a last stage, whose loss is the mean
  * cross-entropy divided by microbatches_per_step).  dx_out: gradient w.r.t. x_in (non-first
  * stage; may be NULL).  STAGE_ESTATE if the slot holds no pending forward. */
 int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out,
                    int32_t microbatches_per_step);
 
-/* Second half of iteration t of Alg. 1: with delay 1 consume g_{t-1} (the gradient of step t-1,
- * complete), with delay 0 consume g_t; clip by the global norm; AdamW; standard or lambda-EF
- * update of the master weights (EF from the second applied update on, the "t <= 1" rule); write
- * x_{t+1} to compute version (t+1) mod 2.  Must be called once per t in increasing order; with
- * delay 1 and t = 0 (no pending gradient) the weights are unchanged (u_{-1} = 0).  A non-finite
+/* Second half of iteration t of Alg. 1: with delay tau >= 1 consume g_{t-tau} (the gradient of
+ * step t-tau, complete), with delay 0 consume g_t; clip by the global norm; AdamW (or Muon);
+ * standard or lambda-EF update of the master weights (EF once tau earlier updates exist: the
+ * "t <= 1" rule for tau = 1; the EF buffer of iteration t is t mod tau); write x_{t+1} to compute
+ * version (t+1) mod 2.  Must be called once per t in increasing order; for t < tau (no pending
+ * gradient) the weights are unchanged (u_{-1} = 0).  A non-finite
  * gradient norm leaves x, m, v and the EF buffer untouched (x_{t+1} = x_t) and is counted on the
  * device; see stage_poll_nonfinite.  STAGE_ESTATE on out-of-order t or an incomplete gradient. */
 int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp);
 
 /* Stateless fused AdamW update (hp->optimizer must be 0) over flat device vectors of n elements:
- * iteration t of a delay-1 run consumes g_prev (= g_{t-1}; fp32, or bf16 when g_is_bf16), with
- * k = t the AdamW bias-correction index and EF from t >= 2; t = 0 only writes x_shadow.
- * x, m, v, u_prev fp32 (read and written; u_prev may be NULL when ef_lambda = 0); x_shadow
- * (written, bf16 when shadow_is_bf16 else fp32; may be NULL).  clip_scale_dev: device float
- * multiplying g_prev, or NULL for 1.  hp->delay must be 1. */
+ * iteration t of a delay-tau run (tau = hp->delay >= 1) consumes g_prev (= g_{t-tau}; fp32, or
+ * bf16 when g_is_bf16), with k = t - tau + 1 the AdamW bias-correction index and EF from
+ * t >= 2 tau; t < tau only writes x_shadow.  x, m, v, u_prev fp32 (read and written; u_prev holds
+ * the update formed tau iterations earlier - the caller keeps a ring of tau buffers, slot t mod
+ * tau - and may be NULL when ef_lambda = 0); x_shadow (written, bf16 when shadow_is_bf16 else
+ * fp32; may be NULL).  clip_scale_dev: device float multiplying g_prev, or NULL for 1. */
 int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf16, float* m,
                         float* v, float* u_prev, void* x_shadow, int32_t shadow_is_bf16,
                         int64_t t, const update_hparams_t* hp, const float* clip_scale_dev,
@@ -179,7 +198,8 @@ int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts,
  * norm since the last poll (STAGE_ENONFINITE if any). */
 int stage_poll_nonfinite(stage_t* s, int64_t* skipped);
 
-/* Global L2 norm of gradient buffer `which` (0/1), computed on device into norm_dev (float). */
+/* Global L2 norm of gradient buffer `which` (0 <= which <= max_delay), computed on device into
+ * norm_dev (float). */
 int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev);
 
 /* Kernel-class timing.  While enabled, the stage records a HIP event pair on the launching

@@ -26,7 +26,7 @@ class StageShape(C.Structure):
                                          "d_ffn", "vocab", "first_stage", "last_stage",
                                          "tie_embedding", "seq_len", "micro_batch", "max_inflight",
                                          "dtype")] + [("rms_eps", C.c_float), ("rope_theta", C.c_float),
-                                                      ("optimizer", C.c_int32)]
+                                                      ("optimizer", C.c_int32), ("max_delay", C.c_int32)]
 
 
 class UpdateHParams(C.Structure):

@@ -3,9 +3,11 @@
 // backward and update.  Every device operation is a kernel of this library on the stage's stream.
 //
 // Bookkeeping (PipeDream-2BW, §2; Alg. 1): compute version v = step mod 2 holds x_step while the
-// microbatches of that step run forward and backward; gradient buffer step mod 2 accumulates g_step;
-// delayed_update(t) reads g_{t-1} (delay 1) and writes x_{t+1} into version (t+1) mod 2, which
-// no pending microbatch reads any more.
+// microbatches of that step run forward and backward; gradient buffer step mod (max_delay + 1)
+// accumulates g_step; delayed_update(t) reads g_{t-tau} (delay tau, 1 in Alg. 1; App. C for a
+// larger fixed delay) and writes x_{t+1} into version (t+1) mod 2, which no pending microbatch
+// reads any more.  Error Feedback of iteration t uses EF buffer t mod tau, which holds the update
+// formed tau iterations earlier and receives this one.
 #include <cmath>
 #include <cstdio>
 #include <algorithm>
@@ -67,6 +69,10 @@ struct stage {
   hipStream_t ust = nullptr;
   hipEvent_t ev_bwd[2] = {nullptr, nullptr}, ev_upd = nullptr, ev_now = nullptr;
   bool ev_bwd_set[2] = {false, false};
+  // ev_grad[j]: the end of the last backward that wrote gradient buffer j (one per buffer of the
+  // delay ring; with max_delay 1 the same points as ev_bwd)
+  hipEvent_t ev_grad[STAGE_MAX_DELAY + 1] = {};
+  bool ev_grad_set[STAGE_MAX_DELAY + 1] = {};
   // The weight-gradient products (fp32 output) of a backward run on a second stream of their own,
   // beside the activation-gradient chain: ev_m2s orders one after the stage stream's work so far,
   // ev_wg[k] marks the end of the last product of kind k (the stage stream waits on it before it
@@ -80,7 +86,10 @@ struct stage {
   int64_t n_flat = 0, off_embed = -1, off_final = -1;
   std::vector<BlockOff> boff;
   // flat vectors
-  float *master, *m, *v, *u_prev, *grad[2];
+  // ng = max_delay + 1 gradient buffers (step s accumulates into s mod ng) and max_delay EF
+  // buffers (iteration t of a delay-tau run uses u_ring[t mod tau]; u_prev = u_ring[0])
+  int ndelay = 1, ng = 2;
+  float *master, *m, *v, *u_prev, *grad[STAGE_MAX_DELAY + 1], *u_ring[STAGE_MAX_DELAY];
   void* ver[2];
   // scratch
   void *dA, *dB, *dh, *dn, *dgu, *do_, *dqkv, *dlog, *dhf;
@@ -94,9 +103,9 @@ struct stage {
   std::vector<Slot> slots;
   // bookkeeping
   int64_t version_step[2] = {-1, -1};
-  int64_t grad_step[2] = {-1, -1};
-  int grad_count[2] = {0, 0};
-  bool grad_consumed[2] = {true, true};
+  int64_t grad_step[STAGE_MAX_DELAY + 1];
+  int grad_count[STAGE_MAX_DELAY + 1];
+  bool grad_consumed[STAGE_MAX_DELAY + 1];
   int64_t next_t = 0;
   int64_t n_updates = 0;
   unsigned long long skipped_seen = 0;
@@ -215,6 +224,8 @@ int validate(const stage_shape_t* s) {
   if (s->d_model > 4096) return fail(STAGE_EINVAL, "d_model > 4096 not supported");
   if (s->dtype != 0 && s->dtype != 1) return fail(STAGE_EINVAL, "dtype must be 0 (fp32) or 1 (bf16)");
   if (s->optimizer != 0 && s->optimizer != 1) return fail(STAGE_EINVAL, "optimizer must be 0 or 1");
+  if (s->max_delay < 0 || s->max_delay > STAGE_MAX_DELAY)
+    return fail(STAGE_EINVAL, "max_delay must be in [0, " + std::to_string(STAGE_MAX_DELAY) + "]");
   if (s->vocab < 0 || s->vocab >= (1 << 17)) return fail(STAGE_EINVAL, "vocab out of range");
   if (s->vocab > 0 && !s->first_stage) return fail(STAGE_EINVAL, "embedding requires first_stage");
   if (s->first_stage && s->vocab == 0) return fail(STAGE_EINVAL, "first_stage requires vocab > 0");
@@ -255,9 +266,11 @@ size_t layout(stage* S, char* base) {
   S->master = (float*)carve(n * 4);
   S->m = (float*)carve(n * 4);
   S->v = (float*)carve(n * 4);
-  S->u_prev = (float*)carve(n * 4);
-  S->grad[0] = (float*)carve(n * 4);
-  S->grad[1] = (float*)carve(n * 4);
+  S->ndelay = sh.max_delay > 1 ? sh.max_delay : 1;
+  S->ng = S->ndelay + 1;
+  for (int j = 0; j < S->ndelay; ++j) S->u_ring[j] = (float*)carve(n * 4);
+  S->u_prev = S->u_ring[0];
+  for (int j = 0; j < S->ng; ++j) S->grad[j] = (float*)carve(n * 4);
   S->ver[0] = carve(n * esz);
   S->ver[1] = carve(n * esz);
   // activation slots
@@ -407,16 +420,19 @@ void register_tensors(stage* S) {
   }
   if (S->off_final >= 0) ps.push_back({"final_norm", S->off_final, d});
   struct V { std::string pre; void* base; size_t es; int32_t dt; };
-  const std::vector<V> vs = {{"", S->master, 4, STAGE_DT_F32},     {"m.", S->m, 4, STAGE_DT_F32},
-                             {"v.", S->v, 4, STAGE_DT_F32},        {"u_prev.", S->u_prev, 4, STAGE_DT_F32},
-                             {"grad0.", S->grad[0], 4, STAGE_DT_F32}, {"grad1.", S->grad[1], 4, STAGE_DT_F32},
-                             {"w0.", S->ver[0], S->esz, cdt},      {"w1.", S->ver[1], S->esz, cdt}};
+  std::vector<V> vs = {{"", S->master, 4, STAGE_DT_F32}, {"m.", S->m, 4, STAGE_DT_F32},
+                       {"v.", S->v, 4, STAGE_DT_F32},    {"u_prev.", S->u_prev, 4, STAGE_DT_F32}};
+  for (int j = 1; j < S->ndelay; ++j) vs.push_back({"u_prev" + std::to_string(j) + ".", S->u_ring[j], 4, STAGE_DT_F32});
+  for (int j = 0; j < S->ng; ++j) vs.push_back({"grad" + std::to_string(j) + ".", S->grad[j], 4, STAGE_DT_F32});
+  vs.push_back({"w0.", S->ver[0], S->esz, cdt});
+  vs.push_back({"w1.", S->ver[1], S->esz, cdt});
   for (const auto& vv : vs)
     for (const auto& p : ps)
       S->named.push_back({vv.pre + p.name, (char*)vv.base + p.off * vv.es, p.numel, vv.dt});
-  const char* flat_names[] = {"flat.master", "flat.m", "flat.v", "flat.u_prev", "flat.grad0", "flat.grad1", "flat.w0", "flat.w1"};
-  for (size_t k = 0; k < vs.size(); ++k)
-    S->named.push_back({flat_names[k], vs[k].base, S->n_flat, vs[k].dt});
+  for (const auto& vv : vs) {  // "flat.master", "flat.m", ..., "flat.grad0", ..., "flat.w1"
+    const std::string pre = vv.pre.empty() ? "master" : vv.pre.substr(0, vv.pre.size() - 1);
+    S->named.push_back({"flat." + pre, vv.base, S->n_flat, vv.dt});
+  }
   const int64_t lse_n = (int64_t)sh.micro_batch * sh.n_heads * sh.seq_len;
   for (size_t si = 0; si < S->slots.size(); ++si) {
     const Slot& sl = S->slots[si];
@@ -562,6 +578,11 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
   if (!arena || ((uintptr_t)arena % ALIGN)) return fail(STAGE_EINVAL, "arena must be 256-byte aligned");
   stage* S = new stage();
   S->sh = *shape;
+  for (int j = 0; j <= STAGE_MAX_DELAY; ++j) {
+    S->grad_step[j] = -1;
+    S->grad_count[j] = 0;
+    S->grad_consumed[j] = true;
+  }
   S->st = (hipStream_t)hip_stream;
   S->bf = shape->dtype == 1;
   S->esz = S->bf ? 2 : 4;
@@ -582,6 +603,8 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_m2s, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_wjoin, hipEventDisableTiming);
     for (int k = 0; k < 2 && e == hipSuccess; ++k) e = hipEventCreateWithFlags(&S->ev_bwd[k], hipEventDisableTiming);
+    for (int k = 0; k < S->ng && e == hipSuccess; ++k)
+      e = hipEventCreateWithFlags(&S->ev_grad[k], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_upd, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_now, hipEventDisableTiming);
     if (e != hipSuccess) {
@@ -649,6 +672,7 @@ int stage_sync_weights(stage_t* s) {
   HIP_OK(hipGetLastError());
   // the caller may have written the optimizer state: the next update waits for the whole stream
   s->ev_bwd_set[0] = s->ev_bwd_set[1] = false;
+  for (int j = 0; j < s->ng; ++j) s->ev_grad_set[j] = false;
   s->version_step[s->next_t % 2] = s->next_t;
   s->version_step[(s->next_t + 1) % 2] = -1;
   return STAGE_OK;
@@ -705,7 +729,7 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   if (!sh.last_stage && !dy) return fail(STAGE_EINVAL, "non-last stage needs dy");
   if (microbatches_per_step <= 0) return fail(STAGE_EINVAL, "microbatches_per_step must be positive");
   const int64_t step = sl.step;
-  const int gb = (int)(step % 2), vi = gb;
+  const int gb = (int)(step % s->ng), vi = (int)(step % 2);
   if (s->grad_step[gb] != step) {
     if (s->grad_step[gb] >= 0 && !s->grad_consumed[gb])
       return fail(STAGE_ESTATE, "gradient buffer still holds the unconsumed gradient of step " +
@@ -750,8 +774,10 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   } else if (dx_out) {
     HIP_OK(hipMemcpyAsync(dx_out, cur, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
   }
-  HIP_OK(hipEventRecord(s->ev_bwd[gb], st));
-  s->ev_bwd_set[gb] = true;
+  HIP_OK(hipEventRecord(s->ev_bwd[vi], st));
+  s->ev_bwd_set[vi] = true;
+  HIP_OK(hipEventRecord(s->ev_grad[gb], st));
+  s->ev_grad_set[gb] = true;
   HIP_OK(hipGetLastError());
   s->grad_count[gb] += 1;
   sl.pending = false;
@@ -760,19 +786,21 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
 
 int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   if (!s || !hp) return fail(STAGE_EINVAL, "null argument");
-  if (hp->delay != 0 && hp->delay != 1) return fail(STAGE_EINVAL, "delay must be 0 or 1");
-  if (hp->delay == 0 && hp->ef_lambda != 0.f) return fail(STAGE_EINVAL, "Error Feedback needs delay 1");
+  if (hp->delay < 0 || hp->delay > s->ndelay)
+    return fail(STAGE_EINVAL, "delay must be in [0, " + std::to_string(s->ndelay) + "] (the stage's max_delay)");
+  if (hp->delay == 0 && hp->ef_lambda != 0.f) return fail(STAGE_EINVAL, "Error Feedback needs a delay >= 1");
   if (hp->optimizer != 0 && hp->optimizer != 1) return fail(STAGE_EINVAL, "optimizer must be 0 (AdamW) or 1 (Muon)");
   if (hp->optimizer == 1 && s->sh.optimizer != 1)
     return fail(STAGE_EINVAL, "Muon needs a stage shaped with optimizer = 1 (its Newton-Schulz workspace)");
   if (hp->optimizer == 1 && (hp->ns_steps < 1 || hp->ns_steps > 32))
     return fail(STAGE_EINVAL, "ns_steps must be in [1, 32]");
   if (t != s->next_t) return fail(STAGE_ESTATE, "delayed_update: expected t = " + std::to_string(s->next_t));
-  const int64_t gstep = hp->delay == 1 ? t - 1 : t;  // the gradient this iteration consumes
+  const int tau = hp->delay;
+  const int64_t gstep = t - tau;  // the gradient this iteration consumes
   bool apply = gstep >= 0;
   int gb = 0;
   if (apply) {
-    gb = (int)(gstep % 2);
+    gb = (int)(gstep % s->ng);
     if (s->grad_step[gb] != gstep || s->grad_count[gb] == 0 || s->grad_consumed[gb])
       return fail(STAGE_ESTATE, "gradient of step " + std::to_string(gstep) + " is not available");
     for (const auto& sl : s->slots)
@@ -791,22 +819,22 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   hs.bc2 = (float)(1.0 - std::pow((double)hp->beta2, (double)k));
   hs.eps = hp->eps; hs.wd = hp->weight_decay; hs.lam = hp->ef_lambda;
   hs.one_plus_lam = 1.0f + hp->ef_lambda;
-  hs.ef = (apply && hp->ef_lambda != 0.f && s->n_updates >= 1) ? 1 : 0;
+  hs.ef = (apply && hp->ef_lambda != 0.f && s->n_updates >= tau) ? 1 : 0;  // u_{t-tau} exists
   hs.apply = apply ? 1 : 0;
-  // Order the update after the backwards whose gradient it reads (parity gb) and after the last
+  // Order the update after the backwards whose gradient it reads (buffer gb) and after the last
   // use of the version it overwrites (parity vout); with no such backward on record, after
   // everything on the stage stream.
   hipStream_t us = s->ust;
-  const int need[2] = {vout, apply ? gb : vout};
-  for (int k = 0; k < 2; ++k) {
-    if (k == 1 && need[1] == need[0]) break;
-    const int p = need[k];
-    if (s->ev_bwd_set[p]) {
-      HIP_OK(hipStreamWaitEvent(us, s->ev_bwd[p], 0));
-    } else {
-      HIP_OK(hipEventRecord(s->ev_now, s->st));
-      HIP_OK(hipStreamWaitEvent(us, s->ev_now, 0));
-    }
+  bool after_all = false;
+  if (s->ev_bwd_set[vout]) HIP_OK(hipStreamWaitEvent(us, s->ev_bwd[vout], 0));
+  else after_all = true;
+  if (apply) {
+    if (s->ev_grad_set[gb]) HIP_OK(hipStreamWaitEvent(us, s->ev_grad[gb], 0));
+    else after_all = true;
+  }
+  if (after_all) {
+    HIP_OK(hipEventRecord(s->ev_now, s->st));
+    HIP_OK(hipStreamWaitEvent(us, s->ev_now, 0));
   }
   const float* clip = nullptr;
   const int* flag = nullptr;
@@ -821,7 +849,7 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   // bytes: x, m, v r+w; g read; shadow write; u_prev r+w with EF (no-op pass: x read, shadow write)
   const double ub = apply ? (24.0 + 4.0 + (s->bf ? 2.0 : 4.0) + (hp->ef_lambda != 0.f ? 8.0 : 0.0))
                           : (4.0 + (s->bf ? 2.0 : 4.0));
-  float* up = hp->ef_lambda != 0.f ? s->u_prev : nullptr;
+  float* up = hp->ef_lambda != 0.f ? s->u_ring[t % tau] : nullptr;  // tau >= 1 whenever lambda != 0
   if (apply && hp->optimizer == 1) {
     // AdamW on the embedding, the gains and the padding ...
     for (const auto& r : s->adamw_ranges) {
@@ -923,7 +951,7 @@ int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf
                         float* u_prev, void* x_shadow, int32_t shadow_is_bf16, int64_t t,
                         const update_hparams_t* hp, const float* clip_scale_dev, void* hip_stream) {
   if (!hp || n < 0 || t < 0) return fail(STAGE_EINVAL, "bad argument");
-  if (hp->delay != 1) return fail(STAGE_EINVAL, "delayed_update_flat implements delay 1");
+  if (hp->delay < 1) return fail(STAGE_EINVAL, "delayed_update_flat implements a delay >= 1");
   if (hp->optimizer != 0) return fail(STAGE_EINVAL, "delayed_update_flat implements AdamW (optimizer 0)");
   if (n == 0) return STAGE_OK;
   if (!x || !g_prev || !m || !v) return fail(STAGE_EINVAL, "null vector");
@@ -932,15 +960,17 @@ int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf
       (uintptr_t)g_prev % 8)
     return fail(STAGE_EINVAL, "vectors must be 16-byte aligned (g_prev 8-byte)");
   UpdateScalars hs{};
-  const double k = (double)t;
+  const int64_t tau = hp->delay;
+  const bool apply = t >= tau;
+  const double k = (double)(t - tau + 1);  // the update's index when applied
   hs.lr = hp->lr; hs.b1 = hp->beta1; hs.b2 = hp->beta2;
   hs.omb1 = 1.0f - hp->beta1; hs.omb2 = 1.0f - hp->beta2;
-  hs.bc1 = t > 0 ? (float)(1.0 - std::pow((double)hp->beta1, k)) : 1.f;
-  hs.bc2 = t > 0 ? (float)(1.0 - std::pow((double)hp->beta2, k)) : 1.f;
+  hs.bc1 = apply ? (float)(1.0 - std::pow((double)hp->beta1, k)) : 1.f;
+  hs.bc2 = apply ? (float)(1.0 - std::pow((double)hp->beta2, k)) : 1.f;
   hs.eps = hp->eps; hs.wd = hp->weight_decay; hs.lam = hp->ef_lambda;
   hs.one_plus_lam = 1.0f + hp->ef_lambda;
-  hs.ef = (hp->ef_lambda != 0.f && t >= 2) ? 1 : 0;
-  hs.apply = t > 0 ? 1 : 0;
+  hs.ef = (hp->ef_lambda != 0.f && t >= 2 * tau) ? 1 : 0;
+  hs.apply = apply ? 1 : 0;
   launch_fused_update(n, x, g_prev, g_is_bf16 != 0, m, v, hp->ef_lambda != 0.f ? u_prev : nullptr,
                       x_shadow, x_shadow ? (shadow_is_bf16 ? 2 : 1) : 0, hs, clip_scale_dev, nullptr, 0,
                       (hipStream_t)hip_stream);
@@ -972,7 +1002,7 @@ int stage_poll_nonfinite(stage_t* s, int64_t* skipped) {
 }
 
 int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev) {
-  if (!s || !norm_dev || (which != 0 && which != 1)) return fail(STAGE_EINVAL, "bad argument");
+  if (!s || !norm_dev || which < 0 || which >= s->ng) return fail(STAGE_EINVAL, "bad argument");
   launch_grad_norm(s->grad[which], false, s->n_flat, 0.f, s->norm_part, s->norm_out, nullptr, nullptr,
                    device_cu_count(), s->st);
   HIP_OK(hipMemcpyAsync(norm_dev, s->norm_out, 4, hipMemcpyDeviceToDevice, s->st));
@@ -1006,6 +1036,8 @@ void stage_destroy(stage_t* s) {
   if (s->wst) (void)hipStreamSynchronize(s->wst);
   for (auto& r : s->prof_pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
   for (auto e : s->prof_free) (void)hipEventDestroy(e);
+  for (hipEvent_t e : s->ev_grad)
+    if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : {s->ev_bwd[0], s->ev_bwd[1], s->ev_upd, s->ev_now, s->ev_m2s, s->ev_wjoin, s->ev_wg[0],
                       s->ev_wg[1], s->ev_wg[2], s->ev_wg[3], s->ev_wg[4]})
     if (e) (void)hipEventDestroy(e);

@@ -16,10 +16,10 @@ _ESZ = {B.DT_F32: 4, B.DT_BF16: 2, B.DT_I32: 4}
 
 def make_shape(n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab, first_stage,
                last_stage, tie_embedding, seq_len, micro_batch, max_inflight=1, bf16=True,
-               rms_eps=1e-5, rope_theta=10000.0, muon=False) -> B.StageShape:
+               rms_eps=1e-5, rope_theta=10000.0, muon=False, max_delay=1) -> B.StageShape:
     return B.StageShape(n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab,
                         int(first_stage), int(last_stage), int(tie_embedding), seq_len, micro_batch,
-                        max_inflight, 1 if bf16 else 0, rms_eps, rope_theta, 1 if muon else 0)
+                        max_inflight, 1 if bf16 else 0, rms_eps, rope_theta, 1 if muon else 0, max_delay)
 
 
 def hparams(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1, clip_norm=1.0,

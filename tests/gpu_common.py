@@ -23,12 +23,12 @@ def rel(a, b) -> float:
     return float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-30))
 
 
-def shape_of(w, muon=False):
+def shape_of(w, muon=False, max_delay=1):
     from paper_2606_30634_amd.stage import make_shape
     return make_shape(w.n_blocks, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ffn, w.vocab,
                       w.first_stage, w.last_stage, w.tie_embedding, w.seq_len, w.micro_batch,
                       w.max_inflight, bf16=(w.dtype == "bf16"), rms_eps=w.rms_eps,
-                      rope_theta=w.rope_theta, muon=muon)
+                      rope_theta=w.rope_theta, muon=muon, max_delay=max_delay)
 
 
 def hp_of(w, **kw):
@@ -70,11 +70,14 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     """T iterations of Alg. 1 on the GPU stage.  Returns losses (per step, per microbatch), outputs
     at y_steps, and at grad_steps the gradient g_t together with the master weights x_t it was taken
     at, at upd_steps the whole optimizer state before and after delayed_update(t) with the gradient
-    it consumed, plus the final master / m / v / u_prev."""
+    it consumed (and, under "u_slot", the EF buffer iteration t uses), plus the final master / m / v /
+    u_prev and every EF buffer ("u_ring", buffer j = iterations j mod tau)."""
     import torch
     from paper_2606_30634_amd.stage import Stage
     dev = torch.device(device)
-    st = Stage(shape_of(w, muon=muon or hp.optimizer == 1), device)
+    tau = max(hp.delay, 1)
+    ng = tau + 1
+    st = Stage(shape_of(w, muon=muon or hp.optimizer == 1, max_delay=tau), device)
     st.load_master(params0)
     names = list(params0)
     grad_steps, y_steps = set(grad_steps), set(y_steps)
@@ -82,12 +85,18 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     upd_steps = set(upd_steps)
     res = dict(losses=[], ys={}, grads={}, x_at={}, upd={})
 
-    def state(g_idx=None):
-        d = {pre: {n: st.view(pre + n).float().cpu().numpy().reshape(params0[n].shape).copy() for n in names}
-             for pre in ("", "m.", "v.", "u_prev.")}
+    def ef_name(j):
+        return "u_prev." if j == 0 else f"u_prev{j}."
+
+    def grab(pre):
+        return {n: st.view(pre + n).float().cpu().numpy().reshape(params0[n].shape).copy() for n in names}
+
+    def state(g_idx=None, u_slot=None):
+        d = {pre: grab(pre) for pre in ("", "m.", "v.", "u_prev.")}
         if g_idx is not None:
-            d["g"] = {n: st.view(f"grad{g_idx}.{n}").float().cpu().numpy().reshape(params0[n].shape).copy()
-                      for n in names}
+            d["g"] = grab(f"grad{g_idx}.")
+        if u_slot is not None:
+            d["u_slot"] = grab(ef_name(u_slot))
         return d
 
     for t in range(steps):
@@ -111,8 +120,7 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
             else:
                 st.backward(slot, dy=inp.get("dy"), microbatches_per_step=M)
         if t in grad_steps:
-            res["grads"][t] = {n: st.view(f"grad{t % 2}.{n}").float().cpu().numpy().reshape(params0[n].shape)
-                               for n in names}
+            res["grads"][t] = grab(f"grad{t % ng}.")
         for i in range(M):
             if w.last_stage:
                 losses[i] = float(loss_t[i].item())
@@ -125,14 +133,15 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
             res["ys"][t] = ys
         res["losses"].append(losses)
         if t in upd_steps:
-            pre = state((t - 1) % 2 if hp.delay == 1 else t % 2)
+            pre = state((t - hp.delay) % ng, t % tau)
         st.update(t, hp)
         if t in upd_steps:
-            res["upd"][t] = (pre, state())
+            res["upd"][t] = (pre, state(None, t % tau))
     torch.cuda.synchronize(dev)
     final = {}
     for pre in ("", "m.", "v.", "u_prev."):
         final[pre] = {n: st.view(pre + n).float().cpu().numpy().reshape(params0[n].shape) for n in names}
+    final["u_ring"] = [grab(ef_name(j)) for j in range(tau)]
     res["final"] = final
     rc, skipped = __import__("paper_2606_30634_amd.binding", fromlist=["x"]).stage_poll_nonfinite(st.handle)
     res["skipped"] = skipped
@@ -160,5 +169,5 @@ def run_oracle(w, steps: int, hp_oracle, params0, grad_steps=(), y_steps=(), dt=
             res["ys"][t] = [o.get("y") for o in info["outs"]]
 
     st = oracle.run(w, steps, hp_oracle, params0, lambda t, i: datagen.step_inputs(w, t, i), dt, rec)
-    res["final"] = {"": st.x, "m.": st.m, "v.": st.v, "u_prev.": st.u_prev}
+    res["final"] = {"": st.x, "m.": st.m, "v.": st.v, "u_prev.": st.u_prev, "u_ring": st.u_ring}
     return res
