@@ -7,11 +7,13 @@ d_model 768, 12 heads, SwiGLU 3072, seq 1024, microbatch 8, vocab-32000 embeddin
 stage), synthetic seeded inputs already resident in HBM.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload small|mid|large|tiny] [--no-cpu-baseline]
-                  [--optimizer adamw|muon]
+                  [--optimizer adamw|muon] [--delay TAU]
 
 With --optimizer muon the blocks' weight matrices take delayed Muon (Alg. 2: momentum 0.95, five
 quintic Newton-Schulz steps, update RMS 0.2) with Error Feedback lambda = 1, the embedding and gains
-AdamW; the line then also reports the Newton-Schulz GEMMs as their own kernel class.
+AdamW; the line then also reports the Newton-Schulz GEMMs as their own kernel class.  --delay TAU
+(default 1) runs the fixed delay TAU of App. C (g_{t-TAU} consumed, Error Feedback lambda = TAU
+against the update formed TAU iterations earlier).
 """
 from __future__ import annotations
 
@@ -170,6 +172,7 @@ def main():
     ap.add_argument("--workload", default="small")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--optimizer", choices=("adamw", "muon"), default="adamw")
+    ap.add_argument("--delay", type=int, default=1)
     ap.add_argument("--update-steps", type=int, default=50,
                     help="iterations of the update-only workload (1.0e9 fp32 elements); 0 skips it")
     ap.add_argument("--calib-copy", action="store_true",
@@ -194,10 +197,10 @@ def main():
     st = Stage(make_shape(w.n_blocks, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ffn, w.vocab,
                           w.first_stage, w.last_stage, w.tie_embedding, w.seq_len, w.micro_batch,
                           w.max_inflight, bf16=bf, rms_eps=w.rms_eps, rope_theta=w.rope_theta,
-                          muon=muon), "cuda:0")
+                          muon=muon, max_delay=args.delay), "cuda:0")
     st.load_master(datagen.init_params(w))
     hp = hparams(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay,
-                 clip_norm=w.clip_norm, ef_lambda=1.0, delay=1, optimizer=args.optimizer)
+                 clip_norm=w.clip_norm, ef_lambda=float(args.delay), delay=args.delay, optimizer=args.optimizer)
     M = w.microbatches_per_step
     cdt = torch.bfloat16 if bf else torch.float32
     # two distinct input sets per microbatch, resident in HBM, alternated across steps
@@ -321,7 +324,7 @@ def main():
         "config": {"workload": w.name, "tokens_per_step": tokens, "microbatches_per_step": M,
                    "optimizer": ("Muon (momentum 0.95, 5 Newton-Schulz steps, update RMS 0.2) on the block "
                                  "matrices, AdamW elsewhere" if muon else "AdamW") +
-                                ", delay 1, Error Feedback lambda 1, clip 1.0",
+                                f", delay {args.delay}, Error Feedback lambda {args.delay}, clip 1.0",
                    "parallelism": "1 GPU, one stage"},
         "roofline": roofline,
         "kernels": kern,

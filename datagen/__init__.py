@@ -111,7 +111,7 @@ class Workload:
     n_kv_heads: int
     head_dim: int
     d_ffn: int
-    vocab: int            # 0: no embedding on this stage
+    vocab: int            # 0: no embedding and no head on this stage
     first_stage: bool
     last_stage: bool
     tie_embedding: bool
@@ -153,7 +153,10 @@ UPDATE_N = 1_000_000_000
 UPDATE_SEED = 5
 UPDATE_STEPS = 50
 
-WORKLOADS = {"tiny": TINY, "small": SMALL, "mid": MID, "large": LARGE}
+LAST = Workload("last-bf16: 3 blocks d768 h12 ffn3072 seq1024 mb8 vocab49152 last stage, untied head",
+                3, 768, 12, 12, 64, 3072, 49152, False, True, False, 1024, 8, 1, "bf16", 100, 6)
+
+WORKLOADS = {"tiny": TINY, "small": SMALL, "mid": MID, "large": LARGE, "last": LAST}
 
 
 # --------------------------------------------------------------------------------------------
@@ -165,7 +168,7 @@ def param_specs(w: Workload) -> List[Tuple[str, Tuple[int, ...], str]]:
     init is "normal" (N(0, 0.02)) or "ones" (RMSNorm gains)."""
     d, hd, f = w.d_model, w.head_dim, w.d_ffn
     out: List[Tuple[str, Tuple[int, ...], str]] = []
-    if w.vocab > 0:
+    if w.vocab > 0 and w.first_stage:
         out.append(("embed", (w.vocab, d), "normal"))
     for i in range(w.n_blocks):
         p = f"blk{i}."
@@ -182,6 +185,8 @@ def param_specs(w: Workload) -> List[Tuple[str, Tuple[int, ...], str]]:
         ]
     if w.last_stage:
         out.append(("final_norm", (d,), "ones"))
+        if not w.tie_embedding:
+            out.append(("head", (w.vocab, d), "normal"))
     return out
 
 
@@ -200,8 +205,9 @@ def step_inputs(w: Workload, step: int, micro: int = 0) -> Dict[str, np.ndarray]
     """Inputs of one microbatch of one step, as float32 values / int32 ids.
 
     First stage: tokens [B, s] (and, on a last stage, next-token targets [B, s], drawn as s+1
-    tokens per row).  Middle stage: x_in [B, s, d] ~ N(0, 1).  Any stage without a head:
-    dy [B, s, d] ~ N(0, 1e-3).  bf16 workloads get bf16-representable values."""
+    tokens per row).  Other stages: x_in [B, s, d] ~ N(0, 1); a last stage among them gets
+    targets [B, s] uniform over the vocabulary.  Any stage without a head: dy [B, s, d] ~
+    N(0, 1e-3).  bf16 workloads get bf16-representable values."""
     B, s, d = w.micro_batch, w.seq_len, w.d_model
     out: Dict[str, np.ndarray] = {}
     if w.first_stage:
@@ -212,6 +218,8 @@ def step_inputs(w: Workload, step: int, micro: int = 0) -> Dict[str, np.ndarray]
     else:
         x = normal(w.seed, "x_in", (B, s, d), 1.0, step, micro)
         out["x_in"] = bf16_values(x) if w.dtype == "bf16" else x
+        if w.last_stage:
+            out["targets"] = uniform_tokens(w.seed, "targets", (B, s), w.vocab, step, micro)
     if not w.last_stage:
         dy = normal(w.seed, "dy", (B, s, d), 1e-3, step, micro)
         out["dy"] = bf16_values(dy) if w.dtype == "bf16" else dy

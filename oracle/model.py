@@ -1,5 +1,6 @@
 """Oracle forward and backward of one pipeline stage: a stack of decoder blocks, with the token
-embedding on a first stage and the tied LM head with next-token cross-entropy on a last stage.
+embedding on a first stage and the LM head with next-token cross-entropy on a last stage (tied to
+the embedding when the stage holds both ends, its own matrix otherwise).
 
 TEST INFRASTRUCTURE: only the tests, the smoke check and the bench's CPU-baseline leg may use this
 package.  It shares no code with the HIP path.
@@ -7,7 +8,8 @@ package.  It shares no code with the HIP path.
 Block (App. E.2, Llama-style, pre-norm):
     h = x + Attn(RoPE(n1 Wq^T), RoPE(n1 Wk^T), n1 Wv^T) Wo^T,   n1 = RMSNorm(x; attn_norm)
     y = h + (silu(n2 Wg^T) * (n2 Wu^T)) Wd^T,                   n2 = RMSNorm(h; ffn_norm)
-Head (last stage, tied): logits = RMSNorm(x_L; final_norm) E^T, loss = mean next-token CE.
+Head (last stage): logits = RMSNorm(x_L; final_norm) W^T with W the embedding E (tied) or the
+stage's head matrix [vocab, d], loss = mean CE against the given next-token targets.
 A stage without a head reports the surrogate loss sum(Y * dY) for the upstream gradient dY it is
 handed, so that its backward is the gradient of that scalar.
 """
@@ -97,7 +99,7 @@ def stage_forward(params: Dict[str, np.ndarray], inp: Dict[str, np.ndarray], w, 
         B, s, d = x.shape
         xf = x.reshape(B * s, d)
         hf, rf = ops.rmsnorm_fwd(xf, P["final_norm"], dt(w.rms_eps))
-        logits = ops.linear_fwd(hf, P["embed"])
+        logits = ops.linear_fwd(hf, P["head"] if "head" in P else P["embed"])
         loss, lse = ops.ce_fwd(logits, inp["targets"].reshape(-1))
         saves.update(xL=xf, hf=hf, rf=rf, logits=logits, lse_ce=lse)
         out["logits"] = logits
@@ -122,7 +124,12 @@ def stage_backward(params, inp, saves, w, dt=np.float64, loss_scale: float = 1.0
         logits, tg = saves["logits"], inp["targets"].reshape(-1)
         n = logits.shape[0]
         dlog = ops.ce_bwd(logits, tg, saves["lse_ce"], dt(loss_scale / n))
-        dhf, de_head = ops.linear_bwd(dlog, saves["hf"], P["embed"])
+        untied = "head" in P
+        dhf, dw = ops.linear_bwd(dlog, saves["hf"], P["head"] if untied else P["embed"])
+        if untied:
+            grads["head"], de_head = dw, None
+        else:
+            de_head = dw
         dxl, grads["final_norm"] = ops.rmsnorm_bwd(dhf, saves["xL"], saves["rf"], P["final_norm"])
         B, s = inp["targets"].shape
         dx = dxl.reshape(B, s, w.d_model)

@@ -13,6 +13,7 @@ R = np.random.default_rng(99)
 HEAD = Workload("test-head", 2, 8, 4, 2, 4, 12, 11, True, True, True, 5, 2, 1, "f32", 3, 7)
 MIDDLE = Workload("test-mid", 2, 8, 4, 2, 4, 12, 0, False, False, False, 5, 2, 1, "f32", 3, 8)
 FIRST = Workload("test-first", 1, 8, 2, 2, 4, 12, 11, True, False, False, 5, 2, 1, "f32", 3, 9)
+LAST = Workload("test-last", 2, 8, 4, 2, 4, 12, 11, False, True, False, 5, 2, 1, "f32", 3, 10)
 
 
 def _params(w, scale=0.5):
@@ -28,7 +29,7 @@ def _loss(w, p, inp):
     return float(out["loss"])
 
 
-@pytest.mark.parametrize("w", [HEAD, MIDDLE, FIRST], ids=["head", "middle", "first"])
+@pytest.mark.parametrize("w", [HEAD, MIDDLE, FIRST, LAST], ids=["head", "middle", "first", "last-untied"])
 def test_stage_gradients_finite_differences(w):
     p = _params(w)
     inp = {k: (v.astype(np.float64) if v.dtype != np.int32 else v) for k, v in step_inputs(w, 0).items()}
@@ -120,6 +121,31 @@ def test_zero_embedding_gives_uniform_loss_log_vocab():
     p["embed"][:] = 0.0
     out, _ = model.stage_forward(p, step_inputs(w, 0), w)
     assert abs(float(out["loss"]) - math.log(w.vocab)) < 1e-14
+
+
+def test_zero_untied_head_gives_uniform_loss_log_vocab():
+    w = LAST
+    p = _params(w)
+    p["head"][:] = 0.0
+    out, _ = model.stage_forward(p, step_inputs(w, 0), w)
+    assert abs(float(out["loss"]) - math.log(w.vocab)) < 1e-14
+
+
+def test_untied_head_equal_to_embedding_matches_tied():
+    # a stage holding both ends with a separate head matrix equal to the embedding computes the
+    # tied stage's logits, and its two matrix gradients sum to the tied embedding gradient
+    wt = HEAD
+    wu = HEAD.with_(tie_embedding=False)
+    p = _params(wt)
+    pu = dict(p, head=p["embed"].copy())
+    inp = step_inputs(wt, 0)
+    ot, st = model.stage_forward(p, inp, wt)
+    ou, su = model.stage_forward(pu, inp, wu)
+    np.testing.assert_array_equal(ot["logits"], ou["logits"])
+    gt, _ = model.stage_backward(p, inp, st, wt)
+    gu, _ = model.stage_backward(pu, inp, su, wu)
+    np.testing.assert_allclose(gu["embed"] + gu["head"], gt["embed"], rtol=1e-12, atol=1e-15)
+    assert np.abs(gu["head"]).max() > 0 and np.abs(gu["embed"]).max() > 0
 
 
 def test_tiny_workload_initial_loss_near_log_vocab():
