@@ -19,7 +19,8 @@
  *     stage then holds tau + 1 gradient buffers and tau EF buffers.
  *   - App. E.2: the stage is a stack of Llama-style decoder blocks (pre-norm RMSNorm, grouped-query
  *     causal attention with RoPE, SwiGLU feed-forward, no biases); a first stage owns the token
- *     embedding, a last stage the tied LM head with next-token cross-entropy (App. E).
+ *     embedding, a last stage the LM head with next-token cross-entropy (App. E) - tied to the
+ *     embedding when one stage holds both ends, else its own matrix.
  *
  * Conventions
  *   - Every function returns a stage_status; no C++ exception crosses the ABI.  On error,
@@ -68,8 +69,10 @@ enum { STAGE_MAX_DELAY = 8 };
 
 /* Shape of one stage.  dtype 0: fp32 compute and storage; 1: bf16 compute copies, bf16
  * activations, fp32 accumulation, fp32 master weights / optimizer state / gradients.
- * vocab > 0 requires first_stage (token embedding [vocab, d_model]); last_stage requires
- * tie_embedding and vocab > 0 (logits = RMSNorm(x) E^T).  head_dim in {32, 64, 128};
+ * vocab > 0 sizes the token embedding [vocab, d_model] of a first stage (vocab < 2^17) and the
+ * head of a last stage (vocab < 2^20): logits = RMSNorm(x) W^T with W the embedding when
+ * tie_embedding (which needs first_stage and last_stage), else the stage's "head" matrix
+ * [vocab, d_model].  The head keeps fp32 logits [tokens, vocab] per activation slot.  head_dim in {32, 64, 128};
  * n_heads a multiple of n_kv_heads; d_model a multiple of 64.  max_inflight >= 1 is the number
  * of activation slots (microbatches whose backward is pending).  optimizer 0: AdamW only;
  * 1: the arena also holds the Newton-Schulz workspace of delayed Muon (Alg. 2 of §4), about 12 (fp32
@@ -123,7 +126,7 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
 int stage_num_tensors(const stage_t* s, int32_t* count);
 
 /* Tensor idx: name, device pointer, element count and dtype (stage_dtype).  Names:
- *   "embed", "blk{i}.attn_norm|wq|wk|wv|wo|ffn_norm|wgate|wup|wdown", "final_norm"  - fp32
+ *   "embed", "blk{i}.attn_norm|wq|wk|wv|wo|ffn_norm|wgate|wup|wdown", "final_norm", "head" - fp32
  *   master weights [out, in]; the same names prefixed "m.", "v.", "u_prev." (fp32 optimizer
  *   state, EF buffer), "u_prev{j}." for j in [1, max_delay) (the further EF buffers: iteration t
  *   of a delay-tau run uses buffer t mod tau, "u_prev." being buffer 0), "grad{j}." for j in

@@ -406,36 +406,85 @@ __global__ void __launch_bounds__(256) embed_scatter(const T* __restrict__ dx0,
 }
 
 // ------------------------------------------------------------------ cross-entropy rows
+// Cross-entropy of one row of logits z [V] (one block per row), in two passes over the fp32
+// logits: the forward keeps a running (max m, sum s of exp(z - m)) per thread over 16-byte
+// chunks, merges the pairs across the block in a fixed order and writes lse = m + log s and the
+// row's loss lse - z[target]; the backward writes (exp(z - lse) - onehot) scale.  A target outside
+// [0, V) is ignored: zero loss and zero gradient.
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  const float mm = fmaxf(m, m2);
+  if (mm == -INFINITY) return;  // both empty
+  s = s * __expf(m - mm) + s2 * __expf(m2 - mm);
+  m = mm;
+}
+
+__global__ void __launch_bounds__(256) ce_fwd_rows(const float* __restrict__ logits,
+                                                   const int32_t* __restrict__ tg, int V,
+                                                   float* __restrict__ lse_out, float* __restrict__ row_loss) {
+  __shared__ float sm_m[4], sm_s[4];
+  const float* z = logits + (int64_t)blockIdx.x * V;
+  float m = -INFINITY, s = 0.f;
+  if ((V & 3) == 0) {
+    const f32x4* z4 = reinterpret_cast<const f32x4*>(z);
+    for (int j = threadIdx.x; j < V / 4; j += 256) {
+      const f32x4 v = z4[j];
+      const float mm = fmaxf(m, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+      s = s * __expf(m - mm) + (__expf(v[0] - mm) + __expf(v[1] - mm)) + (__expf(v[2] - mm) + __expf(v[3] - mm));
+      m = mm;
+    }
+  } else {
+    for (int j = threadIdx.x; j < V; j += 256) lse_merge(m, s, z[j], 1.f);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, WAVE), s2 = __shfl_xor(s, o, WAVE);
+    lse_merge(m, s, m2, s2);
+  }
+  if (threadIdx.x % WAVE == 0) {
+    sm_m[threadIdx.x / WAVE] = m;
+    sm_s[threadIdx.x / WAVE] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float M = sm_m[0], S = sm_s[0];
+    for (int w = 1; w < 4; ++w) lse_merge(M, S, sm_m[w], sm_s[w]);
+    const float l = M + __logf(S);
+    lse_out[blockIdx.x] = l;
+    const int t = tg[blockIdx.x];
+    row_loss[blockIdx.x] = (t >= 0 && t < V) ? l - z[t] : 0.f;
+  }
+}
+
 template <typename T>
-__global__ void __launch_bounds__(256) ce_rows(const float* __restrict__ logits,
-                                               const int32_t* __restrict__ tg, int V, float scale,
-                                               T* __restrict__ dlog, float* __restrict__ row_loss) {
-  __shared__ float sm[16];
-  __shared__ float smx[16];
+__global__ void __launch_bounds__(256) ce_bwd_rows(const float* __restrict__ logits,
+                                                   const int32_t* __restrict__ tg,
+                                                   const float* __restrict__ lse, int V, float scale,
+                                                   T* __restrict__ dlog) {
   const int64_t base = (int64_t)blockIdx.x * V;
   const int t = tg[blockIdx.x];
-  if (t < 0 || t >= V) {  // a target outside [0, V) is ignored: zero loss, zero gradient
-    for (int j = threadIdx.x; j < V; j += blockDim.x) dlog[base + j] = from_f32<T>(0.f);
-    if (threadIdx.x == 0) row_loss[blockIdx.x] = 0.f;
-    return;
+  const bool valid = t >= 0 && t < V;
+  const float l = lse[blockIdx.x];
+  const float sc = valid ? scale : 0.f;
+  if ((V & 3) == 0) {
+    const f32x4* z4 = reinterpret_cast<const f32x4*>(logits + base);
+    for (int j = threadIdx.x; j < V / 4; j += 256) {
+      const f32x4 v = z4[j];
+      float p[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) p[q] = __expf(v[q] - l) * sc - (4 * j + q == t ? sc : 0.f);
+      if constexpr (sizeof(T) == 2) {
+        bf16x4 o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = (bf16)p[q];
+        *reinterpret_cast<bf16x4*>(dlog + base + 4 * j) = o;
+      } else {
+        *reinterpret_cast<f32x4*>(dlog + base + 4 * j) = f32x4{p[0], p[1], p[2], p[3]};
+      }
+    }
+  } else {
+    for (int j = threadIdx.x; j < V; j += 256)
+      dlog[base + j] = from_f32<T>(__expf(logits[base + j] - l) * sc - (j == t ? sc : 0.f));
   }
-  float mx = -INFINITY;
-  for (int j = threadIdx.x; j < V; j += blockDim.x) mx = fmaxf(mx, logits[base + j]);
-  mx = wave_max(mx);
-  if (threadIdx.x % WAVE == 0) smx[threadIdx.x / WAVE] = mx;
-  __syncthreads();
-  mx = -INFINITY;
-  for (int i = 0; i < (int)blockDim.x / WAVE; ++i) mx = fmaxf(mx, smx[i]);
-  float se = 0.f;
-  for (int j = threadIdx.x; j < V; j += blockDim.x) se += expf(logits[base + j] - mx);
-  se = block_sum<float>(se, sm);
-  const float lse = mx + logf(se);
-  for (int j = threadIdx.x; j < V; j += blockDim.x) {
-    float p = expf(logits[base + j] - lse);
-    if (j == t) p -= 1.0f;
-    dlog[base + j] = from_f32<T>(p * scale);
-  }
-  if (threadIdx.x == 0) row_loss[blockIdx.x] = lse - logits[base + t];
 }
 
 __global__ void __launch_bounds__(1024) mean_kernel(const float* __restrict__ v, int n,
@@ -589,14 +638,18 @@ void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted,
   DISPATCH(bf, scat_t, dx0, sorted, row_start, vocab, d, de, accumulate, st);
 }
 
-template <typename T>
-static void ce_t(const float* logits, const int32_t* tg, int rows, int V, float scale, void* dl,
-                 float* rl, hipStream_t st) {
-  ce_rows<T><<<rows, 256, 0, st>>>(logits, tg, V, scale, (T*)dl, rl);
+void launch_ce_fwd(const float* logits, const int32_t* targets, int rows, int vocab, float* lse,
+                   float* row_loss, hipStream_t st) {
+  if (rows > 0) ce_fwd_rows<<<rows, 256, 0, st>>>(logits, targets, vocab, lse, row_loss);
 }
-void launch_ce_rows(bool bf, const float* logits, const int32_t* targets, int rows, int vocab,
-                    float scale, void* dlogits, float* row_loss, hipStream_t st) {
-  DISPATCH(bf, ce_t, logits, targets, rows, vocab, scale, dlogits, row_loss, st);
+template <typename T>
+static void ce_bwd_t(const float* logits, const int32_t* tg, const float* lse, int rows, int V, float scale,
+                     void* dl, hipStream_t st) {
+  if (rows > 0) ce_bwd_rows<T><<<rows, 256, 0, st>>>(logits, tg, lse, V, scale, (T*)dl);
+}
+void launch_ce_bwd(bool bf, const float* logits, const int32_t* targets, const float* lse, int rows, int vocab,
+                   float scale, void* dlogits, hipStream_t st) {
+  DISPATCH(bf, ce_bwd_t, logits, targets, lse, rows, vocab, scale, dlogits, st);
 }
 void launch_mean(const float* v, int n, float* out, hipStream_t st) {
   mean_kernel<<<1, 1024, 0, st>>>(v, n, out);

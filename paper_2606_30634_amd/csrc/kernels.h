@@ -60,9 +60,13 @@ void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_st
 void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted,
                           const int32_t* row_start, int vocab, int d, float* de, bool accumulate,
                           hipStream_t st);
-// cross-entropy rows: dlogits = (softmax - onehot) * scale (stored bf16/fp32), row_loss fp32
-void launch_ce_rows(bool bf, const float* logits, const int32_t* targets, int rows, int vocab,
-                    float scale, void* dlogits, float* row_loss, hipStream_t st);
+// cross-entropy rows of fp32 logits [rows, vocab]: the forward writes lse and the row loss
+// lse - z[target]; the backward dlogits = (exp(z - lse) - onehot) * scale (bf16/fp32).  Targets
+// outside [0, vocab) give zero loss and zero gradient.
+void launch_ce_fwd(const float* logits, const int32_t* targets, int rows, int vocab, float* lse,
+                   float* row_loss, hipStream_t st);
+void launch_ce_bwd(bool bf, const float* logits, const int32_t* targets, const float* lse, int rows, int vocab,
+                   float scale, void* dlogits, hipStream_t st);
 void launch_mean(const float* v, int n, float* out, hipStream_t st);
 
 // ------------------------------------------------------------------ GEMM (gemm.hip)

@@ -50,7 +50,7 @@ struct Slot {
   std::vector<BlockAct> blk;
   void* y;          // output of the last block [T, d]
   void *hf;         // final norm output (last stage)
-  float *rstdf, *logits;
+  float *rstdf, *logits, *lse_ce;  // head: final-norm statistics, fp32 logits, their row lse
   int32_t *tokens, *targets;
   int64_t step = -1;
   bool pending = false;
@@ -83,7 +83,7 @@ struct stage {
   size_t esz;  // bytes per compute element
   int T, qkvw, hqd;
   // flat parameter layout
-  int64_t n_flat = 0, off_embed = -1, off_final = -1;
+  int64_t n_flat = 0, off_embed = -1, off_final = -1, off_head = -1;  // off_head = off_embed when tied
   std::vector<BlockOff> boff;
   // flat vectors
   // ng = max_delay + 1 gradient buffers (step s accumulates into s mod ng) and max_delay EF
@@ -226,11 +226,15 @@ int validate(const stage_shape_t* s) {
   if (s->optimizer != 0 && s->optimizer != 1) return fail(STAGE_EINVAL, "optimizer must be 0 or 1");
   if (s->max_delay < 0 || s->max_delay > STAGE_MAX_DELAY)
     return fail(STAGE_EINVAL, "max_delay must be in [0, " + std::to_string(STAGE_MAX_DELAY) + "]");
-  if (s->vocab < 0 || s->vocab >= (1 << 17)) return fail(STAGE_EINVAL, "vocab out of range");
-  if (s->vocab > 0 && !s->first_stage) return fail(STAGE_EINVAL, "embedding requires first_stage");
+  if (s->vocab < 0 || s->vocab >= (1 << 20)) return fail(STAGE_EINVAL, "vocab out of range [0, 2^20)");
+  if (s->first_stage && s->vocab >= (1 << 17))
+    return fail(STAGE_EINVAL, "a first stage's vocab must be below 2^17 (embedding-gradient sort keys)");
+  if (s->vocab > 0 && !s->first_stage && !s->last_stage)
+    return fail(STAGE_EINVAL, "vocab > 0 needs an embedding (first_stage) or a head (last_stage)");
   if (s->first_stage && s->vocab == 0) return fail(STAGE_EINVAL, "first_stage requires vocab > 0");
-  if (s->last_stage && (!s->tie_embedding || !s->first_stage))
-    return fail(STAGE_EINVAL, "a last stage needs the tied embedding (first_stage, tie_embedding)");
+  if (s->last_stage && s->vocab == 0) return fail(STAGE_EINVAL, "last_stage requires vocab > 0");
+  if (s->tie_embedding && !(s->first_stage && s->last_stage))
+    return fail(STAGE_EINVAL, "tie_embedding needs a stage with both the embedding and the head");
   const int64_t T = (int64_t)s->seq_len * s->micro_batch;
   if (T > (1 << 24)) return fail(STAGE_EINVAL, "too many tokens per microbatch");
   if (s->first_stage && T > 16384) return fail(STAGE_EINVAL, "first stage: at most 16384 tokens per microbatch");
@@ -248,7 +252,7 @@ size_t layout(stage* S, char* base) {
   int64_t n = 0;
   auto take = [&](int64_t cnt) { int64_t o = n; n += (cnt + 63) / 64 * 64; return o; };
   S->boff.clear();
-  S->off_embed = sh.vocab > 0 ? take((int64_t)sh.vocab * d) : -1;
+  S->off_embed = sh.first_stage ? take((int64_t)sh.vocab * d) : -1;
   for (int i = 0; i < sh.n_blocks; ++i) {
     BlockOff b;
     b.attn_norm = take(d);
@@ -260,6 +264,7 @@ size_t layout(stage* S, char* base) {
     S->boff.push_back(b);
   }
   S->off_final = sh.last_stage ? take(d) : -1;
+  S->off_head = !sh.last_stage ? -1 : sh.tie_embedding ? S->off_embed : take((int64_t)sh.vocab * d);
   S->n_flat = n;
   size_t off = 0;
   auto carve = [&](size_t bytes) -> void* { void* p = base ? base + off : nullptr; off += up(bytes); return p; };
@@ -296,6 +301,7 @@ size_t layout(stage* S, char* base) {
     sl.hf = sh.last_stage ? carve(T * d * esz) : nullptr;
     sl.rstdf = sh.last_stage ? (float*)carve(T * 4) : nullptr;
     sl.logits = sh.last_stage ? (float*)carve(T * (int64_t)sh.vocab * 4) : nullptr;
+    sl.lse_ce = sh.last_stage ? (float*)carve(T * 4) : nullptr;
   }
   // scratch shared by all calls
   S->dA = carve(T * d * esz);
@@ -419,6 +425,7 @@ void register_tensors(stage* S) {
     ps.push_back({p + "wdown", b.wdown, d * f});
   }
   if (S->off_final >= 0) ps.push_back({"final_norm", S->off_final, d});
+  if (S->off_head >= 0 && S->off_head != S->off_embed) ps.push_back({"head", S->off_head, (int64_t)sh.vocab * d});
   struct V { std::string pre; void* base; size_t es; int32_t dt; };
   std::vector<V> vs = {{"", S->master, 4, STAGE_DT_F32}, {"m.", S->m, 4, STAGE_DT_F32},
                        {"v.", S->v, 4, STAGE_DT_F32},    {"u_prev.", S->u_prev, 4, STAGE_DT_F32}};
@@ -707,9 +714,9 @@ int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens,
   if (sh.last_stage) {
     HIP_OK(hipMemcpyAsync(sl.targets, targets, (size_t)T * 4, hipMemcpyDeviceToDevice, st));
     launch_rmsnorm_fwd(s->bf, sl.y, s->wptr(vi, s->off_final), sl.hf, sl.rstdf, T, d, sh.rms_eps, st);
-    run_gemm(s, gemm(T, sh.vocab, d, sl.hf, d, true, s->wptr(vi, s->off_embed), d, true,
+    run_gemm(s, gemm(T, sh.vocab, d, sl.hf, d, true, s->wptr(vi, s->off_head), d, true,
                             sl.logits, sh.vocab, true, 0.f));
-    launch_ce_rows(s->bf, sl.logits, sl.targets, T, sh.vocab, 1.0f / T, s->dlog, s->row_loss, st);
+    launch_ce_fwd(sl.logits, sl.targets, T, sh.vocab, sl.lse_ce, s->row_loss, st);
     launch_mean(s->row_loss, T, loss_dev, st);
   }
   if (y_out && !sh.last_stage)
@@ -746,14 +753,14 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   const void* cur = dy;
   bool head_wrote_embed = false;
   if (sh.last_stage) {
-    launch_ce_rows(bf, sl.logits, sl.targets, T, sh.vocab, 1.0f / ((float)T * microbatches_per_step),
-                   s->dlog, s->row_loss, st);
-    // dhf = dlogits E ; dE (+)= dlogits^T hf
-    run_gemm(s, gemm(T, d, sh.vocab, s->dlog, sh.vocab, true, s->wptr(vi, s->off_embed), d, false,
+    launch_ce_bwd(bf, sl.logits, sl.targets, sl.lse_ce, T, sh.vocab, 1.0f / ((float)T * microbatches_per_step),
+                  s->dlog, st);
+    // dhf = dlogits W ; dW (+)= dlogits^T hf   (W the head matrix, or the tied embedding)
+    run_gemm(s, gemm(T, d, sh.vocab, s->dlog, sh.vocab, true, s->wptr(vi, s->off_head), d, false,
                          s->dhf, d));
-    run_wgrad(s, gemm(sh.vocab, d, T, s->dlog, sh.vocab, false, sl.hf, d, false, g + s->off_embed, d,
+    run_wgrad(s, gemm(sh.vocab, d, T, s->dlog, sh.vocab, false, sl.hf, d, false, g + s->off_head, d,
                           true, first ? 0.f : 1.f), WG_HEAD);
-    head_wrote_embed = true;
+    head_wrote_embed = s->off_head == s->off_embed;
     const int np = launch_rmsnorm_bwd(bf, s->dhf, sl.y, sl.rstdf, s->wptr(vi, s->off_final), nullptr, s->dA,
                                        s->rms_part, T, d, st);
     launch_colsum_partials(s->rms_part, np, d, g + s->off_final, !first, st);

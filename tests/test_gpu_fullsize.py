@@ -3,6 +3,9 @@
 * small workload (first stage, 3 blocks, d 768, seq 1024 x 8, vocab 32000): the whole step -
   output, every parameter gradient (float64 oracle at the same x_0), then the delayed update in
   place over the whole flat parameter vector.
+* last-stage workload (3 blocks, d 768, seq 1024 x 8, untied head over vocab 49152): the whole
+  step - loss, every parameter gradient (float64 oracle at the same x_0) - then the update in
+  place over the whole flat vector.
 * mid and large workloads: the last block's forward and backward recomputed by the oracle from the
   GPU's saved input of that block and the given upstream gradient (its output, all its weight
   gradients), and the update in place on sampled slices of the flat vector."""
@@ -80,6 +83,42 @@ def test_small_workload_full_step():
     st.backward(0, dy=d1["dy"])
     e = _update_in_place(st, w, hp_of(w), 1)
     log(f"fullsize small: update in place, worst rel {e:.3e}")
+    assert e < 1e-5
+    st.close()
+
+
+def test_last_stage_full_step():
+    import torch
+    from paper_2606_30634_amd.stage import Stage
+    w = datagen.LAST
+    dev = torch.device("cuda:0")
+    log("fullsize last: GPU step 0")
+    st = Stage(shape_of(w), "cuda:0")
+    p0 = datagen.init_params(w)
+    st.load_master(p0)
+    inp = datagen.step_inputs(w, 0)
+    d = to_device(inp, w, dev)
+    loss = torch.zeros(1, device=dev)
+    st.forward(0, 0, x_in=d["x_in"], targets=d["targets"], loss=loss)
+    st.backward(0)
+    torch.cuda.synchronize()
+    g = {n: _host(st.view(f"grad0.{n}"), p0[n].shape) for n in p0}
+    lg = float(loss.item())
+    log("fullsize last: oracle step 0 (float64)")
+    ref, outs = model.stage_step_grads(p0, [inp], w, np.float64)
+    errs = {"loss": abs(lg - float(outs[0]["loss"])) / abs(float(outs[0]["loss"]))}
+    for n in p0:
+        errs[f"grad.{n}"] = rel(g[n], ref[n])
+    worst = max(errs, key=errs.get)
+    log(f"fullsize last: {len(errs)} comparisons, loss {lg:.6f}, worst {worst} = {errs[worst]:.3e}")
+    bad = {k: v for k, v in errs.items() if not v <= 2e-2}
+    assert not bad, bad
+    st.update(0, hp_of(w))
+    d1 = to_device(datagen.step_inputs(w, 1), w, dev)
+    st.forward(0, 1, x_in=d1["x_in"], targets=d1["targets"], loss=loss)
+    st.backward(0)
+    e = _update_in_place(st, w, hp_of(w), 1)
+    log(f"fullsize last: update in place, worst rel {e:.3e}")
     assert e < 1e-5
     st.close()
 

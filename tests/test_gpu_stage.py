@@ -70,6 +70,19 @@ def test_tiny_fp32_20_steps(lam):
     _compare(w, g, o, 1e-4, (0, 1, 19), f"tiny lambda={lam}", lam)
 
 
+@pytest.mark.parametrize("lam", [0.0, 1.0])
+def test_tiny_fp32_untied_last_stage(lam):
+    # a last stage that is not the first: input activations, given targets, its own head matrix
+    w = TINY_LAST
+    p0 = datagen.init_params(w)
+    log(f"{w.name} 12 steps lambda={lam}")
+    g = run_gpu(w, 12, hp_of(w, ef_lambda=lam), p0, grad_steps=(0, 1, 11), upd_steps=(1, 2, 11))
+    o = run_oracle(w, 12, oracle.hparams_of(w, ef_lambda=lam), p0, grad_steps=(0, 1, 11))
+    _compare(w, g, o, 1e-4, (0, 1, 11), f"{w.name} lambda={lam}", lam)
+
+
+TINY_LAST = datagen.TINY.with_(name="tiny-last-untied", first_stage=False, tie_embedding=False, seed=21)
+
 # Reduced bf16 stages: the shapes of the bf16 workloads at sizes the oracle finishes in seconds,
 # with ragged sequence lengths (not multiples of 64) and GQA.
 SMALL_R = datagen.SMALL.with_(name="small-reduced", n_blocks=2, d_model=256, n_heads=4, n_kv_heads=4,
@@ -85,7 +98,15 @@ TILED_R = datagen.SMALL.with_(name="small-full-tiles", n_blocks=2, d_model=256, 
                               head_dim=64, d_ffn=512, vocab=1000, seq_len=128, micro_batch=2)
 
 
-@pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, TILED_R], ids=lambda w: w.name)
+# the last stage with its own head: an odd vocabulary (scalar cross-entropy path, ragged head
+# products), and whole tiles (vocab 4096, 256 tokens)
+LAST_R = datagen.LAST.with_(name="last-reduced", n_blocks=2, d_model=256, n_heads=4, n_kv_heads=2,
+                            head_dim=64, d_ffn=512, vocab=4001, seq_len=96, micro_batch=2)
+LAST_TILED_R = datagen.LAST.with_(name="last-full-tiles", n_blocks=1, d_model=256, n_heads=4, n_kv_heads=4,
+                                  head_dim=64, d_ffn=512, vocab=4096, seq_len=128, micro_batch=2)
+
+
+@pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, TILED_R, LAST_R, LAST_TILED_R], ids=lambda w: w.name)
 def test_reduced_bf16_stages(w):
     steps = 12
     p0 = datagen.init_params(w)
