@@ -6,14 +6,15 @@ lambda = 1, global-norm clipping at 1.0).  Default workload: the small bf16 stag
 d_model 768, 12 heads, SwiGLU 3072, seq 1024, microbatch 8, vocab-32000 embedding on the first
 stage), synthetic seeded inputs already resident in HBM.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload small|mid|large|tiny] [--no-cpu-baseline]
-                  [--optimizer adamw|muon] [--delay TAU]
+  python bench.py [--steps K] [--warmup W] [--workload small|mid|large|tiny|last] [--no-cpu-baseline]
+                  [--optimizer adamw|muon] [--delay TAU] [--vocab V]
 
 With --optimizer muon the blocks' weight matrices take delayed Muon (Alg. 2: momentum 0.95, five
 quintic Newton-Schulz steps, update RMS 0.2) with Error Feedback lambda = 1, the embedding and gains
 AdamW; the line then also reports the Newton-Schulz GEMMs as their own kernel class.  --delay TAU
 (default 1) runs the fixed delay TAU of App. C (g_{t-TAU} consumed, Error Feedback lambda = TAU
-against the update formed TAU iterations earlier).
+against the update formed TAU iterations earlier).  --workload last is the last stage of the small
+model's shape with its own LM head (vocab 49152; --vocab V sets another, e.g. 128256).
 """
 from __future__ import annotations
 
@@ -173,6 +174,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--optimizer", choices=("adamw", "muon"), default="adamw")
     ap.add_argument("--delay", type=int, default=1)
+    ap.add_argument("--vocab", type=int, default=0, help="head vocabulary of a last-stage workload")
     ap.add_argument("--update-steps", type=int, default=50,
                     help="iterations of the update-only workload (1.0e9 fp32 elements); 0 skips it")
     ap.add_argument("--calib-copy", action="store_true",
@@ -191,6 +193,11 @@ def main():
     from paper_2606_30634_amd.stage import Stage, hparams, make_shape
 
     w = datagen.WORKLOADS[args.workload]
+    if args.vocab:
+        if not w.last_stage or w.first_stage:
+            print("--vocab applies to a last-stage workload", file=sys.stderr)
+            sys.exit(2)
+        w = w.with_(vocab=args.vocab, name=w.name.replace(f"vocab{w.vocab}", f"vocab{args.vocab}"))
     muon = args.optimizer == "muon"
     dev = torch.device("cuda:0")
     bf = w.dtype == "bf16"
@@ -297,7 +304,7 @@ def main():
     kd = kern[dom]
     roofline = {"kernel": dom, "bound": kd["bound"], "achieved": kd["achieved"], "peak": kd["peak"],
                 "unit": kd["unit"], "frac": kd["frac"],
-                "traffic": measured_traffic(args.workload + ("-bf16" if bf else "-f32"), dom)}
+                "traffic": None if args.vocab else measured_traffic(args.workload + ("-bf16" if bf else "-f32"), dom)}
     rc, skipped = B.stage_poll_nonfinite(st.handle)
     st.close()
 
