@@ -42,7 +42,7 @@ def run(w, steps: int, hp: HParams, params0: Dict[str, np.ndarray],
     st = OptState.create(params0, dt)
     M = w.microbatches_per_step
     for t in range(steps):
-        x_t = st.x
+        x_t = st.x if st.x_compute is None else st.x_compute   # the compute weights of step t
         grads, outs = model.stage_step_grads(x_t, [inputs(t, i) for i in range(M)], w, dt)
         info = iteration_update(st, grads, hp)
         if record is not None:

@@ -12,6 +12,17 @@ Alg. 1, one iteration t (g_{-1} = 0, u_{-1} = 0):
 (lambda = 1 is the equation of §3.2; lambda = 0 is standard async.)  With delay 0 the same
 update consumes g_t instead, which is plain synchronous AdamW.
 
+Elementwise variants of u (the optimizer list of §3.3, on every parameter; same delay and EF):
+    "lion"  (Chen et al., 2023):  u = lr (sign(b1 m + (1 - b1) g) + wd x_t),  m <- b2 m + (1 - b2) g
+    "nadam" (Dozat, 2016, the momentum-decay schedule of torch.optim.NAdam): mu_k = b1 (1 - 0.5 0.96^(k psi)),
+            m, v as AdamW, u = lr ((1 - mu_k) / (1 - P_k) g + mu_{k+1} / (1 - P_k mu_{k+1}) m) /
+            (sqrt(v / (1 - b2^k)) + eps) + lr wd x_t,   P_k = mu_1 ... mu_k
+and SAPipe weight prediction with the updated optimizer state (App. B.1, predict = "updated", AdamW):
+the master follows the standard delayed update x_{t+1} = x_t - u_{t-1}(g_{t-1}), while the next
+forward/backward runs at x~_{t+1} = x_{t+1} - u_t(g_{t-1}), the AdamW step from the state after the
+real update fed g_{t-1} once more (bias correction k + 1, decay on x_{t+1}); the predicted state is
+not kept.
+
 Delay tau >= 2 (the delayed-gradient method of App. C with prev(k) = k - tau): iteration t consumes
 g_{t-tau} (iterations t < tau change nothing), and Error Feedback takes the update formed tau
 iterations earlier,
@@ -67,6 +78,8 @@ class HParams:
     momentum: float = 0.95       # Muon momentum mu
     update_rms: float = 0.2      # Muon update RMS
     ns_steps: int = 5            # Newton-Schulz iterations
+    nadam_psi: float = 0.004     # NAdam momentum decay
+    predict: str = "none"        # "updated": SAPipe-WP with the updated optimizer state (AdamW)
 
 
 # quintic Newton-Schulz coefficients of the Muon write-up (Jordan et al., 2024)
@@ -105,6 +118,31 @@ def muon_u(x, g, M, hp: "HParams"):
     O = newton_schulz(M1, hp.ns_steps)
     u = hp.lr * (muon_scale(x.shape, hp.update_rms) * O + hp.weight_decay * x)
     return u, M1
+
+
+def lion_u(x, g, m, hp: "HParams"):
+    """One Lion evaluation on already-clipped g.  Returns (u, m_new)."""
+    c = hp.beta1 * m + (1.0 - hp.beta1) * g
+    u = hp.lr * (np.sign(c) + hp.weight_decay * x)
+    return u, hp.beta2 * m + (1.0 - hp.beta2) * g
+
+
+def nadam_mu(k: int, hp: "HParams") -> float:
+    return hp.beta1 * (1.0 - 0.5 * 0.96 ** (k * hp.nadam_psi))
+
+
+def nadam_u(x, g, m, v, k: int, hp: "HParams"):
+    """One NAdam evaluation (k-th update) on already-clipped g.  Returns (u, m_new, v_new)."""
+    prod = 1.0
+    for j in range(1, k + 1):
+        prod *= nadam_mu(j, hp)
+    mu, mu_next = nadam_mu(k, hp), nadam_mu(k + 1, hp)
+    m1 = hp.beta1 * m + (1.0 - hp.beta1) * g
+    v1 = hp.beta2 * v + (1.0 - hp.beta2) * g * g
+    denom = np.sqrt(v1 / (1.0 - hp.beta2 ** k)) + hp.eps
+    u = hp.lr * ((1.0 - mu) / (1.0 - prod) * g + mu_next / (1.0 - prod * mu_next) * m1) / denom \
+        + hp.lr * hp.weight_decay * x
+    return u, m1, v1
 
 
 class NonFiniteGradient(Exception):
@@ -151,6 +189,7 @@ class OptState:
     n_updates: int = 0                      # updates applied so far
     t: int = 0                              # next iteration index
     queue: List[Dict[str, np.ndarray]] = field(default_factory=list)   # delay >= 2: g_{t-tau} .. g_{t-1}
+    x_compute: Optional[Dict[str, np.ndarray]] = None  # predict: the weights the next forward uses
     u_ring: List[Dict[str, np.ndarray]] = field(default_factory=list)  # delay >= 2: the last tau updates, oldest first
 
     @staticmethod
@@ -163,7 +202,8 @@ class OptState:
     def copy(self) -> "OptState":
         cp = lambda d: None if d is None else {k: v.copy() for k, v in d.items()}
         return OptState(cp(self.x), cp(self.m), cp(self.v), cp(self.u_prev), cp(self.pending),
-                        self.n_updates, self.t, [cp(g) for g in self.queue], [cp(u) for u in self.u_ring])
+                        self.n_updates, self.t, [cp(g) for g in self.queue], [cp(u) for u in self.u_ring],
+                        cp(self.x_compute))
 
 
 def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> dict:
@@ -174,8 +214,12 @@ def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> d
         raise ValueError("delay must be >= 0")
     if hp.delay == 0 and hp.ef_lambda != 0.0:
         raise ValueError("Error Feedback needs a delayed gradient (delay >= 1)")
-    if hp.optimizer not in ("adamw", "muon"):
-        raise ValueError("optimizer must be adamw or muon")
+    if hp.optimizer not in ("adamw", "muon", "lion", "nadam"):
+        raise ValueError("optimizer must be adamw, muon, lion or nadam")
+    if hp.predict not in ("none", "updated"):
+        raise ValueError("predict must be none or updated")
+    if hp.predict == "updated" and (hp.optimizer != "adamw" or hp.ef_lambda != 0.0 or hp.delay != 1):
+        raise ValueError("weight prediction is defined here for delay-1 AdamW without Error Feedback")
     if hp.delay >= 2:
         return _iteration_update_tau(st, g_t, hp)
     if hp.delay == 1:
@@ -190,10 +234,15 @@ def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> d
         c = clip_coefficient(norm, hp.clip_norm)
         k = st.n_updates + 1
         ef = hp.ef_lambda != 0.0 and st.n_updates >= 1   # "t <= 1": the first update is standard
+        pred = {} if hp.predict == "updated" else None
         for name in st.x:
             u = _u_of(st, name, g_use[name] * c, k, hp)
             st.x[name] = apply_update(st.x[name], u, st.u_prev[name], ef, hp.ef_lambda)
             st.u_prev[name] = u
+            if pred is not None:   # the step from the updated state, not kept
+                up, _, _ = adamw_u(st.x[name], g_use[name] * c, st.m[name], st.v[name], k + 1, hp)
+                pred[name] = st.x[name] - up
+        st.x_compute = pred
         st.n_updates = k
         info.update(applied=True, norm=norm, clip=c)
     st.pending = {k: v.copy() for k, v in g_t.items()} if hp.delay == 1 else None
@@ -205,6 +254,10 @@ def _u_of(st: OptState, name: str, g, k: int, hp: HParams):
     """u of one parameter from its clipped gradient; updates the optimizer statistics in st."""
     if hp.optimizer == "muon" and is_muon_matrix(name):
         u, st.m[name] = muon_u(st.x[name], g, st.m[name], hp)   # m holds Muon's momentum
+    elif hp.optimizer == "lion":
+        u, st.m[name] = lion_u(st.x[name], g, st.m[name], hp)
+    elif hp.optimizer == "nadam":
+        u, st.m[name], st.v[name] = nadam_u(st.x[name], g, st.m[name], st.v[name], k, hp)
     else:
         u, st.m[name], st.v[name] = adamw_u(st.x[name], g, st.m[name], st.v[name], k, hp)
     return u
