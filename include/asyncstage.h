@@ -102,13 +102,24 @@ typedef struct {
  * rows <= cols, coefficients (3.4445, -4.7750, 2.0315); on a bf16 stage the iterate stays fp32
  * and enters the bf16 products as a hi + lo pair, A = X X^T and b A + c A A are bf16);
  * u = lr (update_rms sqrt(max(rows, cols)) O + weight_decay x_t); then the same standard or
- * Error-Feedback step as AdamW.  Needs a stage shaped with optimizer 1. */
+ * Error-Feedback step as AdamW.  Needs a stage shaped with optimizer 1.
+ * optimizer 2: Lion (§3.3's optimizer list) on every parameter, u = lr (sign(beta1 m + (1 - beta1)
+ * c g) + weight_decay x_t), m <- beta2 m + (1 - beta2) c g (v unused).  optimizer 3: NAdam with the
+ * momentum-decay schedule mu_k = beta1 (1 - 0.5 0.96^(k nadam_psi)): m, v as AdamW and u = lr
+ * ((1 - mu_k) / (1 - P_k) c g + mu_{k+1} / (1 - P_k mu_{k+1}) m) / (sqrt(v / (1 - beta2^k)) + eps)
+ * + lr weight_decay x_t, P_k = mu_1 ... mu_k.
+ * predict 1 (AdamW, delay 1, ef_lambda 0 only): SAPipe weight prediction with the updated
+ * optimizer state (App. B.1) - the master takes the standard delayed step x_{t+1} = x_t -
+ * u_{t-1}(g_{t-1}) while the compute copy receives x_{t+1} - u_t(g_{t-1}), AdamW fed g_{t-1} once
+ * more from the updated state (bias correction k + 1; the predicted state is not kept). */
 typedef struct {
   float lr, beta1, beta2, eps, weight_decay, clip_norm, ef_lambda;
   int32_t delay;
   int32_t optimizer;
   float momentum, update_rms;
   int32_t ns_steps;
+  int32_t predict;
+  float nadam_psi;
 } update_hparams_t;
 
 /* Bytes of device memory the stage needs (weights, optimizer state, max_delay + 1 gradient
@@ -179,13 +190,15 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out,
  * device; see stage_poll_nonfinite.  STAGE_ESTATE on out-of-order t or an incomplete gradient. */
 int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp);
 
-/* Stateless fused AdamW update (hp->optimizer must be 0) over flat device vectors of n elements:
+/* Stateless fused update (AdamW, Lion, NAdam or the AdamW weight prediction of hp; not Muon) over
+ * flat device vectors of n elements:
  * iteration t of a delay-tau run (tau = hp->delay >= 1) consumes g_prev (= g_{t-tau}; fp32, or
  * bf16 when g_is_bf16), with k = t - tau + 1 the AdamW bias-correction index and EF from
  * t >= 2 tau; t < tau only writes x_shadow.  x, m, v, u_prev fp32 (read and written; u_prev holds
  * the update formed tau iterations earlier - the caller keeps a ring of tau buffers, slot t mod
  * tau - and may be NULL when ef_lambda = 0); x_shadow (written, bf16 when shadow_is_bf16 else
- * fp32; may be NULL).  clip_scale_dev: device float multiplying g_prev, or NULL for 1. */
+ * fp32; may be NULL; required with predict, which writes the predicted point there).
+ * clip_scale_dev: device float multiplying g_prev, or NULL for 1. */
 int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf16, float* m,
                         float* v, float* u_prev, void* x_shadow, int32_t shadow_is_bf16,
                         int64_t t, const update_hparams_t* hp, const float* clip_scale_dev,

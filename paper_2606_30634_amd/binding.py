@@ -33,7 +33,8 @@ class UpdateHParams(C.Structure):
     _fields_ = [(n, C.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay", "clip_norm",
                                          "ef_lambda")] + [("delay", C.c_int32), ("optimizer", C.c_int32),
                                                           ("momentum", C.c_float), ("update_rms", C.c_float),
-                                                          ("ns_steps", C.c_int32)]
+                                                          ("ns_steps", C.c_int32), ("predict", C.c_int32),
+                                                          ("nadam_psi", C.c_float)]
 
 
 class StageError(RuntimeError):

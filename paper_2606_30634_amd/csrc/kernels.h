@@ -4,10 +4,15 @@
 #include <cstdint>
 
 // ------------------------------------------------------------------ update (update.hip)
+// Elementwise update rules of the fused pass (UpdateScalars::opt)
+enum { UPD_ADAMW = 0, UPD_LION = 2, UPD_NADAM = 3, UPD_ADAMW_PREDICT = 4 };
 struct UpdateScalars {
   float lr, b1, b2, omb1, omb2, bc1, bc2, eps, wd, lam, one_plus_lam;
   int ef;     // 1: Error-Feedback form this call
   int apply;  // 0: write the compute copy only (no pending gradient)
+  int opt = UPD_ADAMW;
+  float cg = 0.f, cm = 0.f;      // NAdam: lr (1 - mu_k) / (1 - P_k), lr mu_{k+1} / (1 - P_k mu_{k+1})
+  float bc1n = 1.f, bc2n = 1.f;  // prediction: bias corrections of update k + 1
 };
 size_t norm_scratch_bytes();
 // blocks: partial sums (and blocks of the first pass), at most norm_scratch_bytes() / 8; <= 0

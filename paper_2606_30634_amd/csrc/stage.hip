@@ -791,12 +791,54 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   return STAGE_OK;
 }
 
+// Scalars of the fused elementwise pass for the k-th applied update (k >= 1 when apply): the
+// AdamW bias corrections, Lion's betas, NAdam's momentum-schedule coefficients (mu_j = b1 (1 -
+// 0.5 0.96^(j psi)), P_k = mu_1 ... mu_k, in double), and the bias corrections of update k + 1 for
+// the weight prediction with the updated state.
+UpdateScalars update_scalars(const update_hparams_t* hp, int64_t k, bool apply, bool ef) {
+  UpdateScalars hs{};
+  const double kk = apply ? (double)k : 0.0;
+  hs.lr = hp->lr; hs.b1 = hp->beta1; hs.b2 = hp->beta2;
+  hs.omb1 = 1.0f - hp->beta1; hs.omb2 = 1.0f - hp->beta2;
+  hs.bc1 = apply ? (float)(1.0 - std::pow((double)hp->beta1, kk)) : 1.f;
+  hs.bc2 = apply ? (float)(1.0 - std::pow((double)hp->beta2, kk)) : 1.f;
+  hs.eps = hp->eps; hs.wd = hp->weight_decay; hs.lam = hp->ef_lambda;
+  hs.one_plus_lam = 1.0f + hp->ef_lambda;
+  hs.ef = ef ? 1 : 0;
+  hs.apply = apply ? 1 : 0;
+  hs.opt = hp->optimizer == 2 ? UPD_LION : hp->optimizer == 3 ? UPD_NADAM
+           : hp->predict ? UPD_ADAMW_PREDICT : UPD_ADAMW;
+  if (apply && hs.opt == UPD_NADAM) {
+    auto mu = [&](int64_t j) { return (double)hp->beta1 * (1.0 - 0.5 * std::pow(0.96, (double)j * hp->nadam_psi)); };
+    double prod = 1.0;
+    for (int64_t j = 1; j <= k; ++j) prod *= mu(j);
+    const double mk = mu(k), mn = mu(k + 1);
+    hs.cg = (float)(hp->lr * (1.0 - mk) / (1.0 - prod));
+    hs.cm = (float)(hp->lr * mn / (1.0 - prod * mn));
+  }
+  if (apply && hs.opt == UPD_ADAMW_PREDICT) {
+    hs.bc1n = (float)(1.0 - std::pow((double)hp->beta1, kk + 1.0));
+    hs.bc2n = (float)(1.0 - std::pow((double)hp->beta2, kk + 1.0));
+  }
+  return hs;
+}
+
+// Hyper-parameter checks shared by the stage and the flat update.
+int check_update_hparams(const update_hparams_t* hp) {
+  if (hp->optimizer < 0 || hp->optimizer > 3)
+    return fail(STAGE_EINVAL, "optimizer must be 0 (AdamW), 1 (Muon), 2 (Lion) or 3 (NAdam)");
+  if (hp->predict != 0 && hp->predict != 1) return fail(STAGE_EINVAL, "predict must be 0 or 1");
+  if (hp->predict && (hp->optimizer != 0 || hp->ef_lambda != 0.f || hp->delay != 1))
+    return fail(STAGE_EINVAL, "weight prediction (predict 1) needs AdamW, delay 1 and ef_lambda 0");
+  return STAGE_OK;
+}
+
 int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   if (!s || !hp) return fail(STAGE_EINVAL, "null argument");
   if (hp->delay < 0 || hp->delay > s->ndelay)
     return fail(STAGE_EINVAL, "delay must be in [0, " + std::to_string(s->ndelay) + "] (the stage's max_delay)");
   if (hp->delay == 0 && hp->ef_lambda != 0.f) return fail(STAGE_EINVAL, "Error Feedback needs a delay >= 1");
-  if (hp->optimizer != 0 && hp->optimizer != 1) return fail(STAGE_EINVAL, "optimizer must be 0 (AdamW) or 1 (Muon)");
+  if (int rc = check_update_hparams(hp)) return rc;
   if (hp->optimizer == 1 && s->sh.optimizer != 1)
     return fail(STAGE_EINVAL, "Muon needs a stage shaped with optimizer = 1 (its Newton-Schulz workspace)");
   if (hp->optimizer == 1 && (hp->ns_steps < 1 || hp->ns_steps > 32))
@@ -818,16 +860,9 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   for (const auto& sl : s->slots)
     if (sl.pending && sl.step % 2 == vout)
       return fail(STAGE_ESTATE, "a pending microbatch still reads the version being overwritten");
-  UpdateScalars hs{};
   const int64_t k = s->n_updates + 1;
-  hs.lr = hp->lr; hs.b1 = hp->beta1; hs.b2 = hp->beta2;
-  hs.omb1 = 1.0f - hp->beta1; hs.omb2 = 1.0f - hp->beta2;
-  hs.bc1 = (float)(1.0 - std::pow((double)hp->beta1, (double)k));
-  hs.bc2 = (float)(1.0 - std::pow((double)hp->beta2, (double)k));
-  hs.eps = hp->eps; hs.wd = hp->weight_decay; hs.lam = hp->ef_lambda;
-  hs.one_plus_lam = 1.0f + hp->ef_lambda;
-  hs.ef = (apply && hp->ef_lambda != 0.f && s->n_updates >= tau) ? 1 : 0;  // u_{t-tau} exists
-  hs.apply = apply ? 1 : 0;
+  // EF once u_{t-tau} exists
+  const UpdateScalars hs = update_scalars(hp, k, apply, apply && hp->ef_lambda != 0.f && s->n_updates >= tau);
   // Order the update after the backwards whose gradient it reads (buffer gb) and after the last
   // use of the version it overwrites (parity vout); with no such backward on record, after
   // everything on the stage stream.
@@ -853,8 +888,10 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
     clip = s->upd_norm_out + 1;
     flag = s->flag;
   }
-  // bytes: x, m, v r+w; g read; shadow write; u_prev r+w with EF (no-op pass: x read, shadow write)
-  const double ub = apply ? (24.0 + 4.0 + (s->bf ? 2.0 : 4.0) + (hp->ef_lambda != 0.f ? 8.0 : 0.0))
+  // bytes: x, m, v r+w (Lion: no v); g read; shadow write; u_prev r+w with EF (no-op pass: x
+  // read, shadow write)
+  const double ub = apply ? ((hs.opt == UPD_LION ? 16.0 : 24.0) + 4.0 + (s->bf ? 2.0 : 4.0) +
+                             (hp->ef_lambda != 0.f ? 8.0 : 0.0))
                           : (4.0 + (s->bf ? 2.0 : 4.0));
   float* up = hp->ef_lambda != 0.f ? s->u_ring[t % tau] : nullptr;  // tau >= 1 whenever lambda != 0
   if (apply && hp->optimizer == 1) {
@@ -959,25 +996,18 @@ int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf
                         const update_hparams_t* hp, const float* clip_scale_dev, void* hip_stream) {
   if (!hp || n < 0 || t < 0) return fail(STAGE_EINVAL, "bad argument");
   if (hp->delay < 1) return fail(STAGE_EINVAL, "delayed_update_flat implements a delay >= 1");
-  if (hp->optimizer != 0) return fail(STAGE_EINVAL, "delayed_update_flat implements AdamW (optimizer 0)");
+  if (int rc = check_update_hparams(hp)) return rc;
+  if (hp->optimizer == 1) return fail(STAGE_EINVAL, "delayed_update_flat implements the elementwise rules (not Muon)");
+  if (hp->predict && !x_shadow) return fail(STAGE_EINVAL, "weight prediction writes the compute copy: x_shadow needed");
   if (n == 0) return STAGE_OK;
   if (!x || !g_prev || !m || !v) return fail(STAGE_EINVAL, "null vector");
   if (hp->ef_lambda != 0.f && !u_prev) return fail(STAGE_EINVAL, "Error Feedback needs u_prev");
   if (((uintptr_t)x | (uintptr_t)m | (uintptr_t)v | (uintptr_t)u_prev | (uintptr_t)x_shadow) % 16 ||
       (uintptr_t)g_prev % 8)
     return fail(STAGE_EINVAL, "vectors must be 16-byte aligned (g_prev 8-byte)");
-  UpdateScalars hs{};
   const int64_t tau = hp->delay;
   const bool apply = t >= tau;
-  const double k = (double)(t - tau + 1);  // the update's index when applied
-  hs.lr = hp->lr; hs.b1 = hp->beta1; hs.b2 = hp->beta2;
-  hs.omb1 = 1.0f - hp->beta1; hs.omb2 = 1.0f - hp->beta2;
-  hs.bc1 = apply ? (float)(1.0 - std::pow((double)hp->beta1, k)) : 1.f;
-  hs.bc2 = apply ? (float)(1.0 - std::pow((double)hp->beta2, k)) : 1.f;
-  hs.eps = hp->eps; hs.wd = hp->weight_decay; hs.lam = hp->ef_lambda;
-  hs.one_plus_lam = 1.0f + hp->ef_lambda;
-  hs.ef = (hp->ef_lambda != 0.f && t >= 2 * tau) ? 1 : 0;
-  hs.apply = apply ? 1 : 0;
+  const UpdateScalars hs = update_scalars(hp, t - tau + 1, apply, hp->ef_lambda != 0.f && t >= 2 * tau);
   launch_fused_update(n, x, g_prev, g_is_bf16 != 0, m, v, hp->ef_lambda != 0.f ? u_prev : nullptr,
                       x_shadow, x_shadow ? (shadow_is_bf16 ? 2 : 1) : 0, hs, clip_scale_dev, nullptr, 0,
                       (hipStream_t)hip_stream);

@@ -103,63 +103,87 @@ __global__ void __launch_bounds__(1024) norm_finish(const double* __restrict__ p
   }
 }
 
-template <typename G, typename S, bool EF>
+// One element of the fused pass: the optimizer rule OPT on the clipped gradient gg, then the
+// standard or Error-Feedback step.  x, m, v are updated in place; u is the update, xc the value
+// the compute copy receives (x, or the predicted point of UPD_ADAMW_PREDICT).
+template <int OPT>
+__device__ __forceinline__ void step_elem(float gg, float& x, float& m, float& v, float up, bool ef,
+                                          const UpdateScalars& hs, float& u, float& xc) {
+  if constexpr (OPT == UPD_LION) {
+    const float c = hs.b1 * m + hs.omb1 * gg;
+    const float sg = (c > 0.f) ? 1.f : (c < 0.f ? -1.f : 0.f);
+    u = hs.lr * (sg + hs.wd * x);
+    m = hs.b2 * m + hs.omb2 * gg;
+  } else if constexpr (OPT == UPD_NADAM) {
+    m = hs.b1 * m + hs.omb1 * gg;
+    v = hs.b2 * v + hs.omb2 * (gg * gg);
+    const float denom = sqrtf(v / hs.bc2) + hs.eps;
+    u = (hs.cg * gg + hs.cm * m) / denom + hs.lr * hs.wd * x;
+  } else {
+    m = hs.b1 * m + hs.omb1 * gg;
+    v = hs.b2 * v + hs.omb2 * (gg * gg);
+    u = hs.lr * ((m / hs.bc1) / (sqrtf(v / hs.bc2) + hs.eps) + hs.wd * x);
+  }
+  x = ef ? x - hs.one_plus_lam * u + hs.lam * up : x - u;
+  xc = x;
+  if constexpr (OPT == UPD_ADAMW_PREDICT) {  // AdamW once more from the updated state, not kept
+    const float m2 = hs.b1 * m + hs.omb1 * gg;
+    const float v2 = hs.b2 * v + hs.omb2 * (gg * gg);
+    xc = x - hs.lr * ((m2 / hs.bc1n) / (sqrtf(v2 / hs.bc2n) + hs.eps) + hs.wd * x);
+  }
+}
+
+template <typename G, typename S, bool EF, int OPT>
 __device__ __forceinline__ void update_group(int64_t n, int64_t i, float* __restrict__ x,
                                              const G* __restrict__ g, float* __restrict__ m,
                                              float* __restrict__ v, float* __restrict__ up,
                                              S* __restrict__ shadow, const UpdateScalars& hs, float c,
                                              bool skip) {
+  constexpr bool USES_V = OPT != UPD_LION;
   if (i >= n) return;
   if (i + 3 < n) {
-    float xr[4];
+    float xr[4], xc[4];
     load4<float>(x, i, xr);
     if (!skip) {
-      float gr[4], mr[4], vr[4], ur[4];
+      float gr[4], mr[4], vr[4] = {0.f, 0.f, 0.f, 0.f}, ur[4] = {0.f, 0.f, 0.f, 0.f};
       load4<G>(g, i, gr);
       load4<float>(m, i, mr);
-      load4<float>(v, i, vr);
+      if (USES_V) load4<float>(v, i, vr);
       if (EF) load4<float>(up, i, ur);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float gg = gr[j] * c;
-        mr[j] = hs.b1 * mr[j] + hs.omb1 * gg;
-        vr[j] = hs.b2 * vr[j] + hs.omb2 * (gg * gg);
-        const float mhat = mr[j] / hs.bc1;
-        const float vhat = vr[j] / hs.bc2;
-        const float u = hs.lr * (mhat / (sqrtf(vhat) + hs.eps) + hs.wd * xr[j]);
-        if (EF && hs.ef) xr[j] = xr[j] - hs.one_plus_lam * u + hs.lam * ur[j];
-        else xr[j] = xr[j] - u;
+        float u;
+        step_elem<OPT>(gr[j] * c, xr[j], mr[j], vr[j], ur[j], EF && hs.ef, hs, u, xc[j]);
         ur[j] = u;
       }
       store4<float>(x, i, xr);
       store4<float>(m, i, mr);
-      store4<float>(v, i, vr);
+      if (USES_V) store4<float>(v, i, vr);
       if (EF) store4<float>(up, i, ur);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) xc[j] = xr[j];
     }
-    if (shadow) store4<S>(shadow, i, xr);
+    if (shadow) store4<S>(shadow, i, xc);
   } else {
     for (int64_t k = i; k < n; ++k) {  // ragged tail of a flat vector whose length is not 4k
-      float xv = x[k];
+      float xv = x[k], xcv = xv;
       if (!skip) {
-        const float gg = to_f32(g[k]) * c;
-        const float mm = hs.b1 * m[k] + hs.omb1 * gg;
-        const float vv = hs.b2 * v[k] + hs.omb2 * (gg * gg);
-        const float u = hs.lr * ((mm / hs.bc1) / (sqrtf(vv / hs.bc2) + hs.eps) + hs.wd * xv);
-        if (EF && hs.ef) xv = xv - hs.one_plus_lam * u + hs.lam * up[k];
-        else xv = xv - u;
+        float mm = m[k], vv = USES_V ? v[k] : 0.f, u;
+        step_elem<OPT>(to_f32(g[k]) * c, xv, mm, vv, EF ? up[k] : 0.f, EF && hs.ef, hs, u, xcv);
         m[k] = mm;
-        v[k] = vv;
+        if (USES_V) v[k] = vv;
         if (EF) up[k] = u;
         x[k] = xv;
       }
-      if (shadow) shadow[k] = from_f32<S>(xv);
+      if (shadow) shadow[k] = from_f32<S>(xcv);
     }
   }
 }
 
 // Each thread owns V groups of 4 consecutive elements, the groups one block-width apart so that
 // every load instruction of a wave covers contiguous memory.
-template <typename G, typename S, bool EF, int V>
+template <typename G, typename S, bool EF, int V, int OPT>
 __global__ void __launch_bounds__(256) fused_update(int64_t n, float* __restrict__ x,
                                                     const G* __restrict__ g,
                                                     float* __restrict__ m, float* __restrict__ v,
@@ -171,13 +195,13 @@ __global__ void __launch_bounds__(256) fused_update(int64_t n, float* __restrict
   const int64_t i0 = 4 * ((int64_t)blockIdx.x * blockDim.x * V + threadIdx.x);
 #pragma unroll
   for (int k = 0; k < V; ++k)
-    update_group<G, S, EF>(n, i0 + 4 * (int64_t)k * blockDim.x, x, g, m, v, up, shadow, hs, c, skip);
+    update_group<G, S, EF, OPT>(n, i0 + 4 * (int64_t)k * blockDim.x, x, g, m, v, up, shadow, hs, c, skip);
 }
 
 // Resident variant: a grid of a few blocks per CU walks the vector (V groups per thread and
 // pass), so that the pass shares the CUs with kernels of other streams instead of queueing a
 // block per 1024 elements in front of them.
-template <typename G, typename S, bool EF, int V>
+template <typename G, typename S, bool EF, int V, int OPT>
 __global__ void __launch_bounds__(256) fused_update_resident(int64_t n, float* __restrict__ x,
                                                              const G* __restrict__ g,
                                                              float* __restrict__ m, float* __restrict__ v,
@@ -190,7 +214,7 @@ __global__ void __launch_bounds__(256) fused_update_resident(int64_t n, float* _
   for (int64_t q = (int64_t)blockIdx.x * blockDim.x * V + threadIdx.x; q < groups; q += stride) {
 #pragma unroll
     for (int k = 0; k < V; ++k)
-      update_group<G, S, EF>(n, 4 * (q + (int64_t)k * blockDim.x), x, g, m, v, up, shadow, hs, c, skip);
+      update_group<G, S, EF, OPT>(n, 4 * (q + (int64_t)k * blockDim.x), x, g, m, v, up, shadow, hs, c, skip);
   }
 }
 
@@ -212,19 +236,34 @@ __global__ void __launch_bounds__(256) zero_bytes(int64_t n16, int4* __restrict_
   if (i < n16) p[i] = make_int4(0, 0, 0, 0);
 }
 
-template <typename G, typename S, bool EF, int V = 1>
-void launch_update_t(int64_t n, float* x, const void* g, float* m, float* v, float* up,
+template <typename G, typename S, bool EF, int OPT>
+void launch_update_o(int64_t n, float* x, const void* g, float* m, float* v, float* up,
                      void* shadow, const UpdateScalars& hs, const float* clip, const int* flag,
                      int blocks, hipStream_t st) {
+  constexpr int V = 1;
   const int64_t groups = cdiv(n, 4);
   if (blocks > 0 && groups > (int64_t)blocks * 256 * 4) {
-    fused_update_resident<G, S, EF, 4><<<blocks, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow, hs,
-                                                               clip, flag);
+    fused_update_resident<G, S, EF, 4, OPT><<<blocks, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow,
+                                                                    hs, clip, flag);
     return;
   }
   const dim3 grid((unsigned)cdiv(groups, 256 * V));
-  fused_update<G, S, EF, V><<<grid, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow, hs, clip,
-                                                  flag);
+  fused_update<G, S, EF, V, OPT><<<grid, 256, 0, st>>>(n, x, (const G*)g, m, v, up, (S*)shadow, hs, clip,
+                                                       flag);
+}
+
+template <typename G, typename S, bool EF>
+void launch_update_t(int64_t n, float* x, const void* g, float* m, float* v, float* up,
+                     void* shadow, const UpdateScalars& hs, const float* clip, const int* flag,
+                     int blocks, hipStream_t st) {
+  switch (hs.opt) {
+    case UPD_LION: launch_update_o<G, S, EF, UPD_LION>(n, x, g, m, v, up, shadow, hs, clip, flag, blocks, st); break;
+    case UPD_NADAM: launch_update_o<G, S, EF, UPD_NADAM>(n, x, g, m, v, up, shadow, hs, clip, flag, blocks, st); break;
+    case UPD_ADAMW_PREDICT:
+      launch_update_o<G, S, EF, UPD_ADAMW_PREDICT>(n, x, g, m, v, up, shadow, hs, clip, flag, blocks, st);
+      break;
+    default: launch_update_o<G, S, EF, UPD_ADAMW>(n, x, g, m, v, up, shadow, hs, clip, flag, blocks, st);
+  }
 }
 
 }  // namespace

@@ -24,10 +24,11 @@ def make_shape(n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab, f
 
 def hparams(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1, clip_norm=1.0,
             ef_lambda=1.0, delay=1, optimizer="adamw", momentum=0.95, update_rms=0.2,
-            ns_steps=5) -> B.UpdateHParams:
-    opt = {"adamw": 0, "muon": 1}[optimizer]
+            ns_steps=5, predict="none", nadam_psi=0.004) -> B.UpdateHParams:
+    opt = {"adamw": 0, "muon": 1, "lion": 2, "nadam": 3}[optimizer]
+    pred = {"none": 0, "updated": 1}[predict]
     return B.UpdateHParams(lr, beta1, beta2, eps, weight_decay, clip_norm, ef_lambda, delay, opt,
-                           momentum, update_rms, ns_steps)
+                           momentum, update_rms, ns_steps, pred, nadam_psi)
 
 
 class Stage:
