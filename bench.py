@@ -7,14 +7,16 @@ d_model 768, 12 heads, SwiGLU 3072, seq 1024, microbatch 8, vocab-32000 embeddin
 stage), synthetic seeded inputs already resident in HBM.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload small|mid|large|tiny|last] [--no-cpu-baseline]
-                  [--optimizer adamw|muon] [--delay TAU] [--vocab V]
+                  [--optimizer adamw|muon|lion|nadam] [--predict] [--delay TAU] [--vocab V]
 
 With --optimizer muon the blocks' weight matrices take delayed Muon (Alg. 2: momentum 0.95, five
 quintic Newton-Schulz steps, update RMS 0.2) with Error Feedback lambda = 1, the embedding and gains
 AdamW; the line then also reports the Newton-Schulz GEMMs as their own kernel class.  --delay TAU
 (default 1) runs the fixed delay TAU of App. C (g_{t-TAU} consumed, Error Feedback lambda = TAU
 against the update formed TAU iterations earlier).  --workload last is the last stage of the small
-model's shape with its own LM head (vocab 49152; --vocab V sets another, e.g. 128256).
+model's shape with its own LM head (vocab 49152; --vocab V sets another, e.g. 128256).  --optimizer
+lion|nadam and --predict (AdamW with SAPipe weight prediction from the updated state) select the
+elementwise variants of the update, also for the update-only workload.
 """
 from __future__ import annotations
 
@@ -71,7 +73,7 @@ def measured_traffic(workload, kernel_class):
     return float(v) if v is not None else None
 
 
-def cpu_baseline(w, optimizer="adamw"):
+def cpu_baseline(w, optimizer="adamw", predict=False):
     """The oracle (float32, numpy) timed on whole optimizer steps of the workload -- all sequences
     forward+backward, then the full delayed update -- repeated until at least 10 s of CPU work (at
     most 4 steps) when one step is a bounded amount of work; otherwise on 2 of the step's sequences
@@ -89,7 +91,8 @@ def cpu_baseline(w, optimizer="adamw"):
     n_seq = w.micro_batch if w.d_model <= 1024 else min(2, w.micro_batch)
     ws = w.with_(micro_batch=n_seq)
     p0 = datagen.init_params(ws)
-    hp = oracle.hparams_of(ws, optimizer=optimizer)
+    kw = update_rule(optimizer, predict)
+    hp = oracle.hparams_of(ws, **(dict(kw, ef_lambda=0.0) if predict else kw))
     st = OptState.create(p0, np.float32)
     inp = datagen.step_inputs(ws, 0)
     g, _ = model.stage_step_grads(st.x, [inp], ws, np.float32)
@@ -117,11 +120,21 @@ def cpu_baseline(w, optimizer="adamw"):
             "measured_s": round(fb_s + upd_s, 2)}
 
 
-def update_workload(steps):
+def update_rule(optimizer, predict):
+    """Keyword arguments of the update rule (hparams) for the optimizer options of this script."""
+    kw = {"lion": dict(optimizer="lion", beta1=0.9, beta2=0.99, weight_decay=0.5),
+          "nadam": dict(optimizer="nadam", beta2=0.999)}.get(optimizer, dict(optimizer=optimizer))
+    if predict:
+        kw.update(predict="updated")
+    return kw
+
+
+def update_workload(steps, optimizer="adamw", predict=False):
     """The update-only workload: delayed_update_flat over a flat 1.0e9-element fp32 vector (x, m, v,
     EF buffer), one bf16 gradient N(0, 1e-3), bf16 compute copy; `steps` iterations timed with HIP
-    events on the stream.  36 algorithmic bytes per element.  A plain device copy of 4 GiB is timed
-    in the same process as the practical HBM ceiling."""
+    events on the stream.  36 algorithmic bytes per element (Lion, which keeps no v: 28; the
+    weight prediction, which has no EF buffer: 28).  A plain device copy of 4 GiB is timed in the
+    same process as the practical HBM ceiling."""
     import torch
     from paper_2606_30634_amd import binding as B
     from paper_2606_30634_amd.stage import hparams
@@ -135,7 +148,10 @@ def update_workload(steps):
     v = torch.zeros(n, device=dev)
     up = torch.zeros(n, device=dev)
     sh = torch.empty(n, device=dev, dtype=torch.bfloat16)
-    hp = hparams(lr=1e-3, ef_lambda=1.0, clip_norm=0.0)
+    kw = update_rule(optimizer, predict)
+    lam = 0.0 if predict else 1.0
+    hp = hparams(lr=1e-3, ef_lambda=lam, clip_norm=0.0, **kw)
+    bpe = 2 + 2 + 8 + 8 + (0 if optimizer == "lion" else 8) + (8 if lam else 0)
     stream = torch.cuda.current_stream(dev)
     call = lambda t: B.delayed_update_flat(n, x.data_ptr(), g.data_ptr(), True, m.data_ptr(), v.data_ptr(),
                                            up.data_ptr(), sh.data_ptr(), True, t, hp, None, stream.cuda_stream)
@@ -148,7 +164,7 @@ def update_workload(steps):
     e1.record(stream)
     torch.cuda.synchronize(dev)
     ms = e0.elapsed_time(e1) / steps
-    gbs = 36.0 * n / (ms * 1e-3) / 1e9
+    gbs = bpe * n / (ms * 1e-3) / 1e9
     del g, m, v, up, sh
     src = x[: 1 << 30]  # 4 GiB
     dst = torch.empty_like(src)
@@ -160,7 +176,8 @@ def update_workload(steps):
     e1.record(stream)
     torch.cuda.synchronize(dev)
     copy_gbs = 2.0 * src.numel() * 4 / (e0.elapsed_time(e1) / 5 * 1e-3) / 1e9
-    return {"elements": n, "steps": steps, "bytes_per_element": 36, "ms_per_step": round(ms, 4),
+    return {"elements": n, "steps": steps, "rule": kw, "ef_lambda": lam, "bytes_per_element": bpe,
+            "ms_per_step": round(ms, 4),
             "achieved_GBs": round(gbs, 1), "peak_GBs": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
             "plain_copy_GBs": round(copy_gbs, 1), "frac_of_copy": round(gbs / copy_gbs, 4)}
 
@@ -172,7 +189,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="small")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--optimizer", choices=("adamw", "muon"), default="adamw")
+    ap.add_argument("--optimizer", choices=("adamw", "muon", "lion", "nadam"), default="adamw")
+    ap.add_argument("--predict", action="store_true",
+                    help="AdamW with SAPipe weight prediction from the updated state (no Error Feedback)")
     ap.add_argument("--delay", type=int, default=1)
     ap.add_argument("--vocab", type=int, default=0, help="head vocabulary of a last-stage workload")
     ap.add_argument("--update-steps", type=int, default=50,
@@ -206,8 +225,13 @@ def main():
                           w.max_inflight, bf16=bf, rms_eps=w.rms_eps, rope_theta=w.rope_theta,
                           muon=muon, max_delay=args.delay), "cuda:0")
     st.load_master(datagen.init_params(w))
-    hp = hparams(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay,
-                 clip_norm=w.clip_norm, ef_lambda=float(args.delay), delay=args.delay, optimizer=args.optimizer)
+    if args.predict and (args.optimizer != "adamw" or args.delay != 1):
+        print("--predict applies to AdamW at delay 1", file=sys.stderr)
+        sys.exit(2)
+    lam = 0.0 if args.predict else float(args.delay)
+    hp = hparams(**dict(dict(lr=w.lr, beta1=w.beta1, beta2=w.beta2, eps=w.eps, weight_decay=w.weight_decay,
+                             clip_norm=w.clip_norm, ef_lambda=lam, delay=args.delay),
+                        **update_rule(args.optimizer, args.predict)))
     M = w.microbatches_per_step
     cdt = torch.bfloat16 if bf else torch.float32
     # two distinct input sets per microbatch, resident in HBM, alternated across steps
@@ -308,12 +332,13 @@ def main():
     rc, skipped = B.stage_poll_nonfinite(st.handle)
     st.close()
 
-    upd = update_workload(args.update_steps) if args.update_steps > 0 and not muon else None
+    upd = (update_workload(args.update_steps, args.optimizer, args.predict)
+           if args.update_steps > 0 and not muon else None)
 
     cpu = None
     if not args.no_cpu_baseline:
         log("bench: CPU oracle baseline")
-        cpu = cpu_baseline(w, args.optimizer)
+        cpu = cpu_baseline(w, args.optimizer, args.predict)
 
     out = {
         "metric": "stage tokens/sec (fwd+bwd+delayed update)",
@@ -330,8 +355,11 @@ def main():
         "data": "synthetic (seeded: uniform tokens / N(0,1) activations, N(0,1e-3) upstream gradients, N(0,0.02) weights)",
         "config": {"workload": w.name, "tokens_per_step": tokens, "microbatches_per_step": M,
                    "optimizer": ("Muon (momentum 0.95, 5 Newton-Schulz steps, update RMS 0.2) on the block "
-                                 "matrices, AdamW elsewhere" if muon else "AdamW") +
-                                f", delay {args.delay}, Error Feedback lambda {args.delay}, clip 1.0",
+                                 "matrices, AdamW elsewhere" if muon else
+                                 {"adamw": "AdamW", "lion": "Lion (betas 0.9, 0.99; wd 0.5)",
+                                  "nadam": "NAdam (betas 0.9, 0.999)"}[args.optimizer]) +
+                                (" with SAPipe weight prediction (updated state)" if args.predict else "") +
+                                f", delay {args.delay}, Error Feedback lambda {lam:g}, clip 1.0",
                    "parallelism": "1 GPU, one stage"},
         "roofline": roofline,
         "kernels": kern,
