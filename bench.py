@@ -1,8 +1,9 @@
 """Stage throughput of the delay-1 training step on one MI355X.
 
-One step = one pass of the whole hot path over one optimizer step's input: stage_forward and
-stage_backward of every microbatch, then delayed_update (Alg. 1 with AdamW, Error Feedback
-lambda = 1, global-norm clipping at 1.0).  Default workload: the small bf16 stage (3 decoder blocks,
+One step = one pass of the whole hot path over one optimizer step's input: delayed_update(t)
+(Alg. 1 with AdamW, Error Feedback lambda = 1, global-norm clipping at 1.0; it consumes g_{t-1}
+and is issued first, in the stage's overlap mode, so that it runs beside the step's work), then
+stage_forward and stage_backward of every microbatch of step t.  Default workload: the small bf16 stage (3 decoder blocks,
 d_model 768, 12 heads, SwiGLU 3072, seq 1024, microbatch 8, vocab-32000 embedding on the first
 stage), synthetic seeded inputs already resident in HBM.  Prints one JSON line.
 
@@ -251,7 +252,12 @@ def main():
         sets.append(per)
     warm = max(0, min(w.max_inflight - 1, M))
 
+    # overlap mode: delayed_update(t) - it reads x_t and g_{t-1} only - is issued before step t's
+    # forwards and backwards and runs beside them on the stage's update stream
+    st.set_update_overlap(True)
+
     def step(t):
+        st.update(t, hp)
         per = sets[t % 2]
         order, f, b = [], 0, 0
         for _ in range(warm):
@@ -268,7 +274,6 @@ def main():
                            y_out=d.get("y"), loss=d["loss"] if w.last_stage else None)
             else:
                 st.backward(slot, dy=d.get("dy"), microbatches_per_step=M)
-        st.update(t, hp)
 
     if args.calib_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
@@ -290,6 +295,7 @@ def main():
     e0.record(stream)
     for _ in range(args.steps):
         step(t); t += 1
+    st.join_update()   # the last update is part of the timed work
     e1.record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - wall0

@@ -214,6 +214,20 @@ int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts,
  * norm since the last poll (STAGE_ENONFINITE if any). */
 int stage_poll_nonfinite(stage_t* s, int64_t* skipped);
 
+/* Overlap mode (off by default).  Off: everything enqueued on the stage stream after
+ * delayed_update(t) returns runs after that update.  On: the stage stream waits for update t only
+ * where the one-step delay needs it - the first stage_forward of step t+1 (it reads compute
+ * version (t+1) mod 2, which the update writes) and the first stage_backward that overwrites the
+ * gradient buffer the update read (stage_sync_weights and stage_join_update wait for every
+ * update).  A caller may then issue delayed_update(t) before step t's forwards and backwards, and
+ * the update runs beside them on the stage's own stream (Alg. 1: x_{t+1} depends only on x_t and
+ * g_{t-1}).  Reads of the master weights or optimizer state through stage_tensor() views must
+ * follow stage_join_update() or a device synchronisation.  Turning it off joins. */
+int stage_set_update_overlap(stage_t* s, int32_t on);
+
+/* The stage stream waits for every delayed_update issued so far (no-op when none is owed). */
+int stage_join_update(stage_t* s);
+
 /* Global L2 norm of gradient buffer `which` (0 <= which <= max_delay), computed on device into
  * norm_dev (float). */
 int stage_grad_norm(stage_t* s, int32_t which, float* norm_dev);

@@ -17,7 +17,7 @@ EXPORTS = ["stage_required_bytes", "stage_init", "stage_num_tensors", "stage_ten
            "stage_tensor_by_name", "stage_sync_weights", "stage_forward", "stage_backward",
            "delayed_update", "delayed_update_flat", "stage_embed_indices", "stage_poll_nonfinite",
            "stage_grad_norm", "stage_profile_enable", "stage_profile_read", "stage_last_error",
-           "stage_destroy"]
+           "stage_destroy", "stage_set_update_overlap", "stage_join_update"]
 PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_UPDATE, PROF_NORM, PROF_OTHER, PROF_NS = range(7)
 
 
@@ -68,6 +68,8 @@ def _load():
         "stage_poll_nonfinite": (C.c_int, [vp, C.POINTER(i64)]),
         "stage_grad_norm": (C.c_int, [vp, i32, vp]),
         "stage_profile_enable": (C.c_int, [vp, i32]),
+        "stage_set_update_overlap": (C.c_int, [vp, i32]),
+        "stage_join_update": (C.c_int, [vp]),
         "stage_profile_read": (C.c_int, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
         "stage_last_error": (C.c_char_p, []),
         "stage_destroy": (None, [vp]),
@@ -161,6 +163,14 @@ def stage_poll_nonfinite(s: int):
 
 def stage_grad_norm(s: int, which: int, norm_dev) -> None:
     _call("stage_grad_norm", s, which, norm_dev)
+
+
+def stage_set_update_overlap(s: int, on: bool) -> None:
+    _call("stage_set_update_overlap", s, int(on))
+
+
+def stage_join_update(s: int) -> None:
+    _call("stage_join_update", s)
 
 
 def stage_profile_enable(s: int, on: bool) -> None:

@@ -73,6 +73,13 @@ struct stage {
   // delay ring; with max_delay 1 the same points as ev_bwd)
   hipEvent_t ev_grad[STAGE_MAX_DELAY + 1] = {};
   bool ev_grad_set[STAGE_MAX_DELAY + 1] = {};
+  // Overlap mode (stage_set_update_overlap): the stage stream does not wait for an update as a
+  // whole; ev_upd_v[v] marks the end of the update that wrote compute version v, ev_upd_g[j] of the
+  // one that read gradient buffer j, and the first stage-stream call that reads that version or
+  // overwrites that buffer waits on it (the flags say a wait is still owed).
+  bool overlap = false;
+  hipEvent_t ev_upd_v[2] = {}, ev_upd_g[STAGE_MAX_DELAY + 1] = {};
+  bool upd_owed_v[2] = {}, upd_owed_g[STAGE_MAX_DELAY + 1] = {}, upd_owed_all = false;
   // The weight-gradient products (fp32 output) of a backward run on a second stream of their own,
   // beside the activation-gradient chain: ev_m2s orders one after the stage stream's work so far,
   // ev_wg[k] marks the end of the last product of kind k (the stage stream waits on it before it
@@ -613,6 +620,9 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
     for (int k = 0; k < S->ng && e == hipSuccess; ++k)
       e = hipEventCreateWithFlags(&S->ev_grad[k], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_upd, hipEventDisableTiming);
+    for (int k = 0; k < 2 && e == hipSuccess; ++k) e = hipEventCreateWithFlags(&S->ev_upd_v[k], hipEventDisableTiming);
+    for (int k = 0; k < S->ng && e == hipSuccess; ++k)
+      e = hipEventCreateWithFlags(&S->ev_upd_g[k], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_now, hipEventDisableTiming);
     if (e != hipSuccess) {
       stage_destroy(S);
@@ -673,8 +683,27 @@ int stage_tensor_by_name(const stage_t* s, const char* name, void** dev_ptr, int
   return fail(STAGE_EINVAL, std::string("no tensor named ") + name);
 }
 
+int stage_join_update(stage_t* s) {
+  if (!s) return fail(STAGE_EINVAL, "null stage");
+  if (s->upd_owed_all) {
+    HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd, 0));
+    s->upd_owed_all = false;
+    for (int v = 0; v < 2; ++v) s->upd_owed_v[v] = false;
+    for (int j = 0; j < s->ng; ++j) s->upd_owed_g[j] = false;
+  }
+  return STAGE_OK;
+}
+
+int stage_set_update_overlap(stage_t* s, int32_t on) {
+  if (!s) return fail(STAGE_EINVAL, "null stage");
+  if (!on) stage_join_update(s);
+  s->overlap = on != 0;
+  return STAGE_OK;
+}
+
 int stage_sync_weights(stage_t* s) {
   if (!s) return fail(STAGE_EINVAL, "null stage");
+  stage_join_update(s);
   for (int k = 0; k < 2; ++k) launch_cast_copy(s->n_flat, s->master, s->ver[k], s->bf, s->st);
   HIP_OK(hipGetLastError());
   // the caller may have written the optimizer state: the next update waits for the whole stream
@@ -698,6 +727,10 @@ int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens,
   Slot& sl = s->slots[slot];
   if (sl.pending) return fail(STAGE_ESTATE, "slot holds a microbatch whose backward is pending");
   const int vi = (int)(step % 2);
+  if (s->upd_owed_v[vi]) {
+    HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd_v[vi], 0));
+    s->upd_owed_v[vi] = false;
+  }
   const int T = s->T, d = sh.d_model;
   hipStream_t st = s->st;
   void* x0 = sh.n_blocks > 0 ? sl.blk[0].x : sl.y;
@@ -737,6 +770,10 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   if (microbatches_per_step <= 0) return fail(STAGE_EINVAL, "microbatches_per_step must be positive");
   const int64_t step = sl.step;
   const int gb = (int)(step % s->ng), vi = (int)(step % 2);
+  if (s->upd_owed_g[gb]) {
+    HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd_g[gb], 0));
+    s->upd_owed_g[gb] = false;
+  }
   if (s->grad_step[gb] != step) {
     if (s->grad_step[gb] >= 0 && !s->grad_consumed[gb])
       return fail(STAGE_ESTATE, "gradient buffer still holds the unconsumed gradient of step " +
@@ -981,7 +1018,18 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   HIP_OK(hipGetLastError());
   // everything enqueued on the stage stream from here on runs after the update
   HIP_OK(hipEventRecord(s->ev_upd, us));
-  HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd, 0));
+  if (s->overlap) {
+    // only the calls that read what this update wrote, or overwrite what it read, wait for it
+    HIP_OK(hipEventRecord(s->ev_upd_v[vout], us));
+    s->upd_owed_v[vout] = true;
+    if (apply) {
+      HIP_OK(hipEventRecord(s->ev_upd_g[gb], us));
+      s->upd_owed_g[gb] = true;
+    }
+    s->upd_owed_all = true;
+  } else {
+    HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd, 0));
+  }
   if (apply) {
     s->grad_consumed[gb] = true;
     s->n_updates = k;
@@ -1074,6 +1122,10 @@ void stage_destroy(stage_t* s) {
   for (auto& r : s->prof_pending) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
   for (auto e : s->prof_free) (void)hipEventDestroy(e);
   for (hipEvent_t e : s->ev_grad)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : s->ev_upd_g)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : s->ev_upd_v)
     if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : {s->ev_bwd[0], s->ev_bwd[1], s->ev_upd, s->ev_now, s->ev_m2s, s->ev_wjoin, s->ev_wg[0],
                       s->ev_wg[1], s->ev_wg[2], s->ev_wg[3], s->ev_wg[4]})

@@ -79,6 +79,14 @@ class Stage:
     def update(self, t: int, hp: B.UpdateHParams):
         B.delayed_update(self.handle, t, hp)
 
+    def set_update_overlap(self, on: bool):
+        """Overlap mode: the stage stream waits for an update only where the delay needs it."""
+        B.stage_set_update_overlap(self.handle, on)
+
+    def join_update(self):
+        """The stage stream waits for every update issued so far."""
+        B.stage_join_update(self.handle)
+
     def embed_indices(self, slot: int):
         T = self.shape.seq_len * self.shape.micro_batch
         ids = torch.empty(T, dtype=torch.int32, device=self.device)

@@ -66,12 +66,16 @@ def schedule_1f1b(M: int, warm: int):
 
 
 def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps: Iterable[int] = (),
-            device: str = "cuda:0", upd_steps: Iterable[int] = (), muon: bool = False):
+            device: str = "cuda:0", upd_steps: Iterable[int] = (), muon: bool = False,
+            early_update: bool = False):
     """T iterations of Alg. 1 on the GPU stage.  Returns losses (per step, per microbatch), outputs
     at y_steps, and at grad_steps the gradient g_t together with the master weights x_t it was taken
     at, at upd_steps the whole optimizer state before and after delayed_update(t) with the gradient
     it consumed (and, under "u_slot", the EF buffer iteration t uses), plus the final master / m / v /
-    u_prev and every EF buffer ("u_ring", buffer j = iterations j mod tau)."""
+    u_prev and every EF buffer ("u_ring", buffer j = iterations j mod tau).
+
+    early_update: the stage in overlap mode, and delayed_update(t) issued before step t's forwards
+    and backwards (it consumes g_{t-1}), so that it runs beside them."""
     import torch
     from paper_2606_30634_amd.stage import Stage
     dev = torch.device(device)
@@ -79,6 +83,8 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     ng = tau + 1
     st = Stage(shape_of(w, muon=muon or hp.optimizer == 1, max_delay=tau), device)
     st.load_master(params0)
+    if early_update:
+        st.set_update_overlap(True)
     names = list(params0)
     grad_steps, y_steps = set(grad_steps), set(y_steps)
     M = w.microbatches_per_step
@@ -92,6 +98,7 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
         return {n: st.view(pre + n).float().cpu().numpy().reshape(params0[n].shape).copy() for n in names}
 
     def state(g_idx=None, u_slot=None):
+        torch.cuda.synchronize(dev)   # the update stream too (overlap mode)
         d = {pre: grab(pre) for pre in ("", "m.", "v.", "u_prev.")}
         if g_idx is not None:
             d["g"] = grab(f"grad{g_idx}.")
@@ -99,9 +106,19 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
             d["u_slot"] = grab(ef_name(u_slot))
         return d
 
+    def update(t):
+        if t in upd_steps:
+            pre = state((t - hp.delay) % ng, t % tau)
+        st.update(t, hp)
+        if t in upd_steps:
+            res["upd"][t] = (pre, state(None, t % tau))
+
     for t in range(steps):
-        if t in grad_steps:
+        if t in grad_steps:   # x_t, before an early update(t) starts writing x_{t+1}
+            torch.cuda.synchronize(dev)
             res["x_at"][t] = {n: st.view(n).float().cpu().numpy().reshape(params0[n].shape).copy() for n in names}
+        if early_update:
+            update(t)
         inps = [to_device(datagen.step_inputs(w, t, i), w, dev) for i in range(M)]
         losses = [None] * M
         ys = [None] * M
@@ -132,11 +149,8 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
         if t in y_steps:
             res["ys"][t] = ys
         res["losses"].append(losses)
-        if t in upd_steps:
-            pre = state((t - hp.delay) % ng, t % tau)
-        st.update(t, hp)
-        if t in upd_steps:
-            res["upd"][t] = (pre, state(None, t % tau))
+        if not early_update:
+            update(t)
     torch.cuda.synchronize(dev)
     final = {}
     for pre in ("", "m.", "v.", "u_prev."):

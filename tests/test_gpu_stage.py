@@ -70,6 +70,21 @@ def test_tiny_fp32_20_steps(lam):
     _compare(w, g, o, 1e-4, (0, 1, 19), f"tiny lambda={lam}", lam)
 
 
+@pytest.mark.parametrize("w", ["tiny", "large-reduced"])
+def test_overlapped_early_update(w):
+    # overlap mode with delayed_update(t) issued before step t's forwards and backwards: the same
+    # trajectory (the update of iteration t reads only x_t and g_{t-1})
+    w = datagen.TINY if w == "tiny" else LARGE_R
+    tol = 1e-4 if w.dtype == "f32" else 2e-2
+    steps = 10
+    p0 = datagen.init_params(w)
+    log(f"{w.name}: {steps} steps, update issued first, overlap mode")
+    g = run_gpu(w, steps, hp_of(w), p0, grad_steps=(0, steps - 1), upd_steps=(1, 2, steps - 1), early_update=True)
+    o = run_oracle(w, steps, oracle.hparams_of(w), p0, grad_steps=(0, steps - 1))
+    _compare(w, g, o, tol, (0, steps - 1), f"{w.name} early update", w.ef_lambda,
+             state_tol=None if w.dtype == "f32" else 5e-2)
+
+
 @pytest.mark.parametrize("lam", [0.0, 1.0])
 def test_tiny_fp32_untied_last_stage(lam):
     # a last stage that is not the first: input activations, given targets, its own head matrix
