@@ -347,7 +347,11 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
 }
 
 // ------------------------------------------------------------------------------------------ dQ
-template <int HD>
+// DELTA: the pass that only sums delta_i = sum_j P_ij dP_ij over the keys, with the P and dP the dQ
+// pass recomputes, so that every row of dS = P (dP - delta) sums to zero.  (The shortcut
+// rowsum(dO O) with O stored in bf16 misses that by the rounding of O; once attention sharpens,
+// dP - delta cancels and the mismatch biases dQ and dK along the mean key.)
+template <int HD, bool DELTA = false>
 __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, int bz,
     unsigned char* __restrict__ smem) {
   using L = Lds<HD>;
@@ -382,7 +386,8 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
     }
   }
   const int64_t sidx = ((int64_t)b * a.Hq + h) * a.S + min(myq, a.S - 1);
-  const float lse2 = a.lse[sidx] * LOG2E, dl = a.delta[sidx];
+  const float lse2 = a.lse[sidx] * LOG2E, dl = DELTA ? 0.f : a.delta[sidx];
+  float rd = 0.f;  // DELTA: this lane's share of sum_j P_ij dP_ij
   wait_vm_lds<0>();  // register loads done before the ring starts (as in the forward)
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
@@ -415,6 +420,23 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
           dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Vs, t * 32, ks * 16), df[ks], dp[t], 0, 0, 0);
         }
       }
+      if constexpr (DELTA) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          if (HD == 64 && key0 + t * 32 + 31 <= q0) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) rd += fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) * dp[t][e];
+          } else {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int key = key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4);
+              const float p = key <= myq ? fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) : 0.f;
+              rd += p * dp[t][e];
+            }
+          }
+        }
+        continue;
+      }
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         // every key of the sub-tile is visible to every query: no mask (head dim 64 only; at 128
@@ -440,6 +462,12 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
       }
     }
   }
+  if constexpr (DELTA) {
+    rd += __shfl_xor(rd, 32, 64);  // the other half of the lane's query column
+    if (half == 0 && myq < a.S) a.delta[sidx] = rd;
+    wait_vm_lds<0>();  // no ring load may land in the LDS after the block ends
+    return;
+  }
   block_barrier();  // every wave is done with the last tile: the ring becomes the output staging
   store_rows_from_t<HD>(reinterpret_cast<float*>(smem), dq, 1.0f / sqrtf((float)HD),
                         (bf16*)a.dqkv + (int64_t)b * a.S * ld + h * HD, ld, qb * QB, a.S, a.rope_cos, a.rope_sin);
@@ -452,6 +480,16 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
   int unit, idx;  // unit: (batch, query head)
   xcd_item(blockIdx.x, nqb * a.Hq * a.B, nqb, unit, idx);
   bwd_dq_block<HD>(a, idx, unit % a.Hq, unit / a.Hq, smem);
+}
+
+// delta[b, h, i] = sum_j P_ij dP_ij, the grid of flash_bwd_dq
+template <int HD>
+__global__ void __launch_bounds__(NT) flash_bwd_delta(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int nqb = (a.S + QB - 1) / QB;
+  int unit, idx;
+  xcd_item(blockIdx.x, nqb * a.Hq * a.B, nqb, unit, idx);
+  bwd_dq_block<HD, true>(a, idx, unit % a.Hq, unit / a.Hq, smem);
 }
 
 // ------------------------------------------------------------------------------------------ dK, dV
@@ -646,7 +684,11 @@ void bwd_launch(const AttnArgs& a, hipStream_t st) {
     set_lds(flash_bwd_dkv<HD>, Lds<HD>::dkv_bytes());
     attr = true;
   }
-  if (!a.delta_ready) flash_delta<HD><<<(unsigned)cdiv((int64_t)a.B * a.S * a.Hq, 256), 256, 0, st>>>(a);
+  if (!a.delta_ready) {  // delta from the P and dP the backward recomputes
+    static bool dattr = false;
+    if (!dattr) { set_lds(flash_bwd_delta<HD>, Lds<HD>::dq_bytes()); dattr = true; }
+    flash_bwd_delta<HD><<<(unsigned)(cdiv(a.S, QB) * a.Hq * a.B), NT, Lds<HD>::dq_bytes(), st>>>(a);
+  }
   if constexpr (HD == 64) {
     // one launch for both (at head dim 128 the dK/dV register budget would halve dQ's occupancy)
     static bool fattr = false;

@@ -544,20 +544,23 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   after_wgrad(S, WG_O);
   int np = launch_rmsnorm_bwd(bf, S->dn, b.h, b.rstd2, S->wptr(vi, w.ffn_norm), dy, S->dh, S->rms_part, T, d, st);
   launch_colsum_partials(S->rms_part, np, d, g + w.ffn_norm, !first, st);
-  // output projection: do = dh Wo, with the attention backward's delta = rowsum(do o) in the
-  // epilogue ; dWo (+)= dh^T o
+  // output projection: do = dh Wo ; dWo (+)= dh^T o.  The attention backward's delta: on the bf16
+  // stage a pass of the attention backward sums P dP (o is stored in bf16, too coarse for
+  // rowsum(do o) once attention sharpens); on the fp32 stage rowsum(do o) in the product's epilogue
   GemmArgs go = gemm(T, S->hqd, d, S->dh, d, true, S->wptr(vi, w.wo), S->hqd, false, S->do_, S->hqd);
-  go.epi = 4;
-  go.aux = b.o;
-  go.ld_aux = S->hqd;
-  go.delta = S->delta;
-  go.delta_hd = sh.head_dim;
-  go.delta_S = sh.seq_len;
+  if (!bf) {
+    go.epi = 4;
+    go.aux = b.o;
+    go.ld_aux = S->hqd;
+    go.delta = S->delta;
+    go.delta_hd = sh.head_dim;
+    go.delta_S = sh.seq_len;
+  }
   run_gemm(S, go);
   run_wgrad(S, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta), WG_O);
   AttnArgs a = attn_args(S, b);
   a.dout = S->do_; a.dqkv = S->dqkv; a.delta = S->delta;
-  a.delta_ready = true;  // computed with do above
+  a.delta_ready = !bf;  // fp32: computed with do above
   a.rope_cos = S->cos_t;  // dq, dk come back w.r.t. the unrotated projections
   a.rope_sin = S->sin_t;
   after_wgrad(S, WG_QKV);
