@@ -387,7 +387,9 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
   }
   const int64_t sidx = ((int64_t)b * a.Hq + h) * a.S + min(myq, a.S - 1);
   const float lse2 = a.lse[sidx] * LOG2E, dl = DELTA ? 0.f : a.delta[sidx];
-  float rd = 0.f;  // DELTA: this lane's share of sum_j P_ij dP_ij
+  float rd[16];  // DELTA: this lane's share of sum_j P_ij dP_ij, one partial per accumulator slot
+#pragma unroll
+  for (int e = 0; e < 16; ++e) rd[e] = 0.f;
   wait_vm_lds<0>();  // register loads done before the ring starts (as in the forward)
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
@@ -425,13 +427,13 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
         for (int t = 0; t < 2; ++t) {
           if (HD == 64 && key0 + t * 32 + 31 <= q0) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) rd += fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) * dp[t][e];
+            for (int e = 0; e < 16; ++e) rd[e] += fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) * dp[t][e];
           } else {
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
               const int key = key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4);
               const float p = key <= myq ? fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) : 0.f;
-              rd += p * dp[t][e];
+              rd[e] += p * dp[t][e];
             }
           }
         }
@@ -463,8 +465,11 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
     }
   }
   if constexpr (DELTA) {
-    rd += __shfl_xor(rd, 32, 64);  // the other half of the lane's query column
-    if (half == 0 && myq < a.S) a.delta[sidx] = rd;
+    float sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) sum += rd[e];
+    sum += __shfl_xor(sum, 32, 64);  // the other half of the lane's query column
+    if (half == 0 && myq < a.S) a.delta[sidx] = sum;
     wait_vm_lds<0>();  // no ring load may land in the LDS after the block ends
     return;
   }

@@ -268,6 +268,96 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_vec(const T* __restrict__ dn,
   for (int c = threadIdx.x; c < d; c += 256) partial[(int64_t)blockIdx.x * d + c] = red[c];
 }
 
+// RMSNorm backward for wide rows (d = 4 * 64 * V * NI >= 2048): the block's four waves split
+// every row's columns, so a lane holds V * NI gains and dgamma sums instead of the whole row's
+// share; the row's dot product is the four wave sums added in wave order through LDS (two rows
+// in flight, a double-buffered exchange, one barrier per pair).  Each wave's dgamma columns are
+// its own: the block's partial row is written without a cross-wave reduction.
+template <typename T, int V, int NI>
+__global__ void __launch_bounds__(256) rmsnorm_bwd_slice(const T* __restrict__ dn, const T* __restrict__ x,
+                                                         const float* __restrict__ rstd,
+                                                         const T* __restrict__ gamma,
+                                                         const T* __restrict__ resid, T* __restrict__ dx,
+                                                         float* __restrict__ partial, int rows) {
+  constexpr int W = 64 * V * NI, d = 4 * W, U = 2;
+  static_assert(RMS_ROWS_VEC % U == 0, "row pairs");
+  using VT = typename Vec<T, V>::type;
+  __shared__ float sdot[2][U][4];
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int c0 = wave * W;
+  float gm[NI][V], dg[NI][V];
+#pragma unroll
+  for (int k = 0; k < NI; ++k) {
+    const VT gv = *reinterpret_cast<const VT*>(gamma + c0 + (lane + 64 * k) * V);
+#pragma unroll
+    for (int q = 0; q < V; ++q) { gm[k][q] = to_f32(gv[q]); dg[k][q] = 0.f; }
+  }
+#pragma unroll 1
+  for (int it = 0; it < RMS_ROWS_VEC / U; ++it) {
+    int r[U];
+    bool ok[U];
+    VT xv[U][NI], gv[U][NI], rv[U][NI];
+    float rs[U], dot[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      r[u] = blockIdx.x * RMS_ROWS_VEC + U * it + u;
+      ok[u] = r[u] < rows;
+      const int64_t base = (int64_t)(ok[u] ? r[u] : 0) * d + c0;
+      rs[u] = ok[u] ? rstd[r[u]] : 0.f;
+#pragma unroll
+      for (int k = 0; k < NI; ++k) {
+        const int64_t o = base + (lane + 64 * k) * V;
+        xv[u][k] = *reinterpret_cast<const VT*>(x + o);
+        gv[u][k] = *reinterpret_cast<const VT*>(dn + o);
+        if (resid) rv[u][k] = *reinterpret_cast<const VT*>(resid + o);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      dot[u] = 0.f;
+#pragma unroll
+      for (int k = 0; k < NI; ++k)
+#pragma unroll
+        for (int q = 0; q < V; ++q) {
+          const float xh = to_f32(xv[u][k][q]) * rs[u], g = to_f32(gv[u][k][q]);
+          dot[u] += g * gm[k][q] * xh;
+          dg[k][q] += g * xh;  // rs = 0 on a row past the end adds nothing
+        }
+      dot[u] = wave_sum(dot[u]);
+    }
+    const int buf = it & 1;
+    if (lane == 0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) sdot[buf][u][wave] = dot[u];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      dot[u] = (((sdot[buf][u][0] + sdot[buf][u][1]) + sdot[buf][u][2]) + sdot[buf][u][3]) / (float)d;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (!ok[u]) continue;
+      const int64_t base = (int64_t)r[u] * d + c0;
+#pragma unroll
+      for (int k = 0; k < NI; ++k) {
+        VT ov;
+#pragma unroll
+        for (int q = 0; q < V; ++q) {
+          const float xh = to_f32(xv[u][k][q]) * rs[u];
+          float v = rs[u] * (to_f32(gv[u][k][q]) * gm[k][q] - xh * dot[u]);
+          if (resid) v += to_f32(rv[u][k][q]);
+          ov[q] = from_f32<T>(v);
+        }
+        *reinterpret_cast<VT*>(dx + base + (lane + 64 * k) * V) = ov;
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < NI; ++k)
+#pragma unroll
+    for (int q = 0; q < V; ++q) partial[(int64_t)blockIdx.x * d + c0 + (lane + 64 * k) * V + q] = dg[k][q];
+}
+
 // ------------------------------------------------------------------ RoPE
 template <typename T>
 __global__ void __launch_bounds__(256) rope(T* __restrict__ qkv, int rows, int seq_len,
@@ -555,6 +645,12 @@ static int rmsb_t(const void* dn, const void* x, const float* r, const void* g, 
                                                   (const T*)res, (T*)dx, part, rows);                 \
     return (int)nv;                                                                                  \
   }
+#define RS(V, NI)                                                                                    \
+  if (align % (V * sizeof(T)) == 0) {                                                                \
+    rmsnorm_bwd_slice<T, V, NI><<<nv, 256, 0, st>>>((const T*)dn, (const T*)x, r, (const T*)g,        \
+                                                    (const T*)res, (T*)dx, part, rows);               \
+    return (int)nv;                                                                                  \
+  }
   // 16-byte vectors where d allows (8 bf16 or 4 fp32 elements per lane), else 8 or 4 bytes; any
   // other width, or rows not aligned to the vector, take the block-per-chunk kernel below
   constexpr bool B = sizeof(T) == 2;
@@ -565,11 +661,13 @@ static int rmsb_t(const void* dn, const void* x, const float* r, const void* g, 
     case 768: RB(4, 3) break;
     case 1024: if (B) { RB(8, 2) } else { RB(4, 4) } break;
     case 1536: if (B) { RB(8, 3) } else { RB(4, 6) } break;
-    case 2048: if (B) { RB(8, 4) } else { RB(4, 8) } break;
-    case 4096: if (B) { RB(8, 8) } break;
+    case 2048: if (B) { RS(8, 1) } else { RS(4, 2) } break;
+    case 3072: if (B) { RS(4, 3) } else { RS(4, 3) } break;
+    case 4096: if (B) { RS(8, 2) } else { RS(4, 4) } break;
     default: break;
   }
 #undef RB
+#undef RS
   const unsigned nb = (unsigned)cdiv(rows, RMS_CHUNK);
   rmsnorm_bwd<T><<<nb, 256, 0, st>>>((const T*)dn, (const T*)x, r, (const T*)g, (const T*)res, (T*)dx,
                                      part, rows, d);

@@ -121,7 +121,17 @@ LAST_TILED_R = datagen.LAST.with_(name="last-full-tiles", n_blocks=1, d_model=25
                                   head_dim=64, d_ffn=512, vocab=4096, seq_len=128, micro_batch=2)
 
 
-@pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, TILED_R, LAST_R, LAST_TILED_R], ids=lambda w: w.name)
+# the mid and large widths (d 2048, 4096: the column-split RMSNorm backward) with a ragged token
+# count (not a multiple of the 16 rows a block of the norm kernels covers)
+WIDE_MID_R = datagen.MID.with_(name="mid-width-reduced", n_blocks=1, d_model=2048, n_heads=16, n_kv_heads=16,
+                               head_dim=128, d_ffn=512, seq_len=45, micro_batch=2)
+WIDE_LARGE_R = datagen.LARGE.with_(name="large-width-reduced", n_blocks=1, d_model=4096, n_heads=32, n_kv_heads=8,
+                                   head_dim=128, d_ffn=512, seq_len=41, micro_batch=2,
+                                   microbatches_per_step=2, max_inflight=2)
+
+
+@pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, TILED_R, LAST_R, LAST_TILED_R, WIDE_MID_R, WIDE_LARGE_R],
+                         ids=lambda w: w.name)
 def test_reduced_bf16_stages(w):
     steps = 12
     p0 = datagen.init_params(w)
