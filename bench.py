@@ -202,8 +202,8 @@ def main():
                          "the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (one pipeline stage's "
-              "share on one MI355X); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the library runs one pipeline stage's share on one MI355X "
+              "and has no multi-GPU path; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
