@@ -75,7 +75,7 @@ enum { STAGE_MAX_DELAY = 8 };
  * [vocab, d_model].  The head keeps fp32 logits [tokens, vocab] per activation slot.  head_dim in {32, 64, 128};
  * n_heads a multiple of n_kv_heads; d_model a multiple of 64.  max_inflight >= 1 is the number
  * of activation slots (microbatches whose backward is pending).  optimizer 0: AdamW only;
- * 1: the arena also holds the Newton-Schulz workspace of delayed Muon (Alg. 2 of §4), about 12 (fp32
+ * 1: the arena also holds the Newton-Schulz workspace of delayed Muon (Alg. 2 of §4), 8 to 12 (fp32
  * stage: 8) bytes per element of the blocks' weight matrices plus their Gram matrices, so that
  * delayed_update accepts update_hparams_t.optimizer = 1.  max_delay in [0, 8] (0 is read as 1):
  * the largest delay delayed_update accepts; the arena holds max_delay + 1 gradient buffers and
@@ -99,8 +99,9 @@ typedef struct {
  * of §4) on every 2-D weight matrix of a block (wq, wk, wv, wo, wgate, wup, wdown, each on its
  * own) and AdamW on the embedding and the gains: M <- momentum M + (1 - momentum) c g;
  * O = Newton-Schulz(M) (ns_steps >= 1 quintic iterations on M / ||M||_F in the orientation with
- * rows <= cols, coefficients (3.4445, -4.7750, 2.0315); on a bf16 stage the iterate stays fp32
- * and enters the bf16 products as a hi + lo pair, A = X X^T and b A + c A A are bf16);
+ * rows <= cols, coefficients (3.4445, -4.7750, 2.0315); on a bf16 stage the iterate is held in
+ * fp32 or as a hi + lo pair of bf16 matrices and the product P X uses the pair, while
+ * A = hi hi^T and P = b A + c A A are bf16);
  * u = lr (update_rms sqrt(max(rows, cols)) O + weight_decay x_t); then the same standard or
  * Error-Feedback step as AdamW.  Needs a stage shaped with optimizer 1.
  * optimizer 2: Lion (§3.3's optimizer list) on every parameter, u = lr (sign(beta1 m + (1 - beta1)

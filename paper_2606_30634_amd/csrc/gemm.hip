@@ -6,6 +6,8 @@
 // thread, fp32 FMA.  bf16 workloads go to the MFMA kernel in gemm_mfma.hip.
 #include "common.h"
 #include "kernels.h"
+#include <cstdio>
+#include <cstdlib>
 
 bool gemm_mfma_try(const GemmArgs& g, hipStream_t st);  // gemm_mfma.hip
 
@@ -126,6 +128,11 @@ void launch_axpby(bool bf, void* y, const void* x, float alpha, float beta, int 
 void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st) {
   if (g.M == 0 || g.N == 0) return;
   if (bf && gemm_mfma_try(g, st)) return;
+  if (g.epi == GEMM_EPI_AXPBY_DUP || g.epi == GEMM_EPI_NS_SPLIT) {
+    // only the batched direct-to-LDS kernels implement these; callers check gemm_batched_tiles()
+    fprintf(stderr, "launch_gemm: epilogue %d needs whole tiles and bf16 operands\n", g.epi);
+    abort();
+  }
   if (g.batch > 1 || g.epi == GEMM_EPI_AXPBY) {
     // one product at a time, then the AXPBY pass
     const size_t es = bf ? 2 : 4, cs = g.out_f32 ? 4 : es;

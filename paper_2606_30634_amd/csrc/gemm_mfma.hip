@@ -141,6 +141,21 @@ __device__ __forceinline__ void tile_origin(const GemmArgs& g, int b, int& m0, i
   n0 = ((b % (GM * tiles_n)) / gsz) * BN;
 }
 
+// Tile b of a symmetric product (M == N, square tiles): the b-th tile (i, j) with i <= j, counted
+// row by row (T (T + 1) / 2 tiles for T tile rows).
+template <int BM, int BN>
+__device__ __forceinline__ void tri_origin(const GemmArgs& g, int b, int& m0, int& n0) {
+  static_assert(BM == BN, "square tiles");
+  const int T = g.M / BM;
+  int i = 0, first = 0;
+  while (i + 1 < T && b >= first + (T - i)) {
+    first += T - i;
+    ++i;
+  }
+  m0 = i * BM;
+  n0 = (i + b - first) * BN;
+}
+
 // Epilogue: per RP-row part (RP = 16 or 8) of each 32-row fragment row of the wave tile, stage
 // the fp32 accumulators through the wave's own LDS area and write 16-byte rows: split-K partials
 // to the workspace, or C with the beta / residual / SwiGLU-backward / RoPE / delta /
@@ -274,7 +289,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[W
 // GemmArgs::epi): bf16 output as is, SwiGLU backward, RoPE, SwiGLU forward, attention delta, plus
 // a residual row added, alpha (A B) + beta D.
 enum { EPI_PLAIN = 0, EPI_SWIGLU_BWD = 1, EPI_ROPE = 2, EPI_SWIGLU_FWD = 3, EPI_DELTA = 4, EPI_RESID = 5,
-       EPI_AXPBY = GEMM_EPI_AXPBY };
+       EPI_AXPBY = GEMM_EPI_AXPBY, EPI_AXPBY_DUP = GEMM_EPI_AXPBY_DUP, EPI_NS_SPLIT = GEMM_EPI_NS_SPLIT };
 
 // Output chunks leave with non-temporal stores and read-once epilogue operands arrive with
 // non-temporal loads: a product streams 10-150 MB of them through the 4 MB L2 of each XCD, which
@@ -299,6 +314,8 @@ __device__ __forceinline__ V ld_nt(const void* p) {
 template <int EPI> struct EpiIn { static constexpr bool loads = false; };
 template <> struct EpiIn<EPI_RESID> { static constexpr bool loads = true; bf16x8 r; };
 template <> struct EpiIn<EPI_AXPBY> { static constexpr bool loads = true; bf16x8 r; };
+template <> struct EpiIn<EPI_AXPBY_DUP> { static constexpr bool loads = true; bf16x8 r; };
+template <> struct EpiIn<EPI_NS_SPLIT> { static constexpr bool loads = true; bf16x8 a, b; };
 template <> struct EpiIn<EPI_SWIGLU_BWD> { static constexpr bool loads = true; bf16x8 a, b; };
 template <> struct EpiIn<EPI_DELTA> { static constexpr bool loads = true; bf16x8 o; };
 template <> struct EpiIn<EPI_ROPE> { static constexpr bool loads = true; f32x4 c0, c1, s0, s1; };
@@ -309,6 +326,12 @@ __device__ __forceinline__ void epi_load(EpiIn<EPI>& in, const GemmArgs& g, int 
     in.r = ld_nt<bf16x8>((const bf16*)g.resid + (int64_t)row * g.ldc + col);
   } else if constexpr (EPI == EPI_AXPBY) {
     in.r = ld_nt<bf16x8>((const bf16*)g.D + (int64_t)row * g.ldc + col);
+  } else if constexpr (EPI == EPI_AXPBY_DUP) {
+    in.r = ld_nt<bf16x8>((const bf16*)g.D + (int64_t)row * g.ld_aux + col);
+  } else if constexpr (EPI == EPI_NS_SPLIT) {  // hi and lo of the previous x
+    const bf16* dp = (const bf16*)g.D + (int64_t)row * g.ldc + col;
+    in.a = ld_nt<bf16x8>(dp);
+    in.b = ld_nt<bf16x8>(dp + g.N);
   } else if constexpr (EPI == EPI_SWIGLU_BWD) {
     const bf16* gu = (const bf16*)g.aux + (int64_t)row * g.ld_aux + col;
     in.a = ld_nt<bf16x8>(gu);
@@ -472,6 +495,29 @@ __device__ __forceinline__ void dma_epilogue(const GemmArgs& g, f32x16 (&acc)[WM
             for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
           }
           st_nt(Cb + o, ov);
+        } else if constexpr (EPI == EPI_AXPBY_DUP) {  // each value into two adjacent columns
+          bf16x8 d0, d1;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const bf16 u0 = (bf16)(g.alpha * v[q] + g.beta_d * (float)x.r[q]);
+            const bf16 u1 = (bf16)(g.alpha * v[q + 4] + g.beta_d * (float)x.r[q + 4]);
+            d0[2 * q] = u0; d0[2 * q + 1] = u0;
+            d1[2 * q] = u1; d1[2 * q + 1] = u1;
+          }
+          bf16* Cd = Cb + (int64_t)row * g.ldc + 2 * col;
+          st_nt(Cd, d0);
+          st_nt(Cd + 8, d1);
+        } else if constexpr (EPI == EPI_NS_SPLIT) {  // x = v + beta_d (hi + lo), then its hi/lo form
+          bf16x8 h8, l8;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float xv = v[q] + g.beta_d * ((float)x.a[q] + (float)x.b[q]);
+            const bf16 hq = (bf16)xv;
+            h8[q] = hq;
+            l8[q] = (bf16)(xv - (float)hq);
+          }
+          st_nt(Cb + o, h8);
+          st_nt(Cb + o + g.N, l8);
         } else {
           if constexpr (EPI == EPI_RESID) {
 #pragma unroll
@@ -484,6 +530,24 @@ __device__ __forceinline__ void dma_epilogue(const GemmArgs& g, f32x16 (&acc)[WM
 #pragma unroll
           for (int q = 0; q < 8; ++q) ov[q] = (bf16)v[q];
           st_nt(Cb + o, ov);
+        }
+      }
+    }
+    if constexpr (EPI == EPI_PLAIN && sizeof(OutT) == 2) {
+      if (g.sym && m0 != n0) {
+        // symmetric product, a tile above the diagonal: the part again at C[col, row], as 8-row
+        // column segments of the staged rows
+        constexpr int CT = WN * (RP / 8) / 64;  // segments per lane
+        static_assert(CT * 64 == WN * (RP / 8), "every lane writes the same number of segments");
+        bf16* Cb = (bf16*)g.C;
+#pragma unroll
+        for (int j = 0; j < CT; ++j) {
+          const int c = lane + 64 * j, cc = c % WN, rg = c / WN;
+          bf16x8 tv;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) tv[q] = (bf16)stg[(rg * 8 + q) * EP + cc];
+          const int row = m0 + wm0 + (p / NP) * 32 + RP * (p % NP) + rg * 8, col = n0 + wn0 + cc;
+          st_nt(Cb + (int64_t)col * g.ldc + row, tv);
         }
       }
     }
@@ -710,7 +774,11 @@ gemm_dma_kernel(GemmArgs g) {
   extern __shared__ __align__(16) unsigned char smem[];
   bf16* S = reinterpret_cast<bf16*>(smem);  // [NS][A tile | B tile]
 
-  const int tiles = (g.M / BM) * (g.N / BN);
+  const int tiles = g.sym ? (g.M / BM) * (g.M / BM + 1) / 2 : (g.M / BM) * (g.N / BN);
+  auto origin = [&](int b, int& m0_, int& n0_) {
+    if (g.sym) tri_origin<BM, BN>(g, b, m0_, n0_);
+    else tile_origin<BM, BN>(g, b, m0_, n0_);
+  };
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64), lane = threadIdx.x % 64;
   const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
   // split-K: this block covers slices [s0, s0 + nk) of every tile
@@ -758,7 +826,7 @@ gemm_dma_kernel(GemmArgs g) {
 
   int t = blockIdx.x;
   int m0, n0;
-  tile_origin<BM, BN>(g, t, m0, n0);
+  origin(t, m0, n0);
   const bf16* at = a_tile(m0);
   const bf16* bt = b_tile(n0);
   // slices NS - 1 and later ahead come from the next tile only when a tile has that many
@@ -770,7 +838,7 @@ gemm_dma_kernel(GemmArgs g) {
     const int tn = t + gridDim.x;
     const bool next = chain && tn < tiles;
     int m1 = m0, n1 = n0;
-    if (next) tile_origin<BM, BN>(g, tn, m1, n1);
+    if (next) origin(tn, m1, n1);
     const bf16* atn = a_tile(m1);
     const bf16* btn = b_tile(n1);
 
@@ -915,7 +983,8 @@ void launch_dma_one(const GemmArgs& g, int nblk, hipStream_t st) {
 template <int BM, int BN, int WM, int WN, typename OutT, int BKT, int NS>
 bool launch_dma_cfg(const GemmArgs& g, hipStream_t st) {
   if (g.M % BM || g.N % BN || g.K % BKT || g.K == 0 || (g.K / BKT) % g.ksplit) return false;
-  const int nblk = (g.M / BM) * (g.N / BN);
+  if (g.sym && (BM != BN || g.M != g.N || g.epi != 0 || g.resid || sizeof(OutT) != 2)) return false;
+  const int nblk = g.sym ? (g.M / BM) * (g.M / BM + 1) / 2 : (g.M / BM) * (g.N / BN);
   if constexpr (sizeof(OutT) == 4) {
     if (g.a_kmajor && g.b_kmajor) launch_dma_one<BM, BN, WM, WN, true, true, OutT, BKT, NS, EPI_PLAIN>(g, nblk, st);
     else if (g.a_kmajor) launch_dma_one<BM, BN, WM, WN, true, false, OutT, BKT, NS, EPI_PLAIN>(g, nblk, st);
@@ -931,7 +1000,7 @@ bool launch_dma_cfg(const GemmArgs& g, hipStream_t st) {
     break;
     switch (kind) {
       K_(EPI_PLAIN) K_(EPI_SWIGLU_BWD) K_(EPI_ROPE) K_(EPI_SWIGLU_FWD) K_(EPI_DELTA) K_(EPI_RESID)
-      K_(EPI_AXPBY)
+      K_(EPI_AXPBY) K_(EPI_AXPBY_DUP) K_(EPI_NS_SPLIT)
       default: return false;
     }
 #undef K_
@@ -968,14 +1037,16 @@ int device_cu_count() {
 bool gemm_mfma_try(const GemmArgs& g0, hipStream_t st) {
   // vector-load alignment: 8 elements along every contiguous dimension, rows in groups of 4
   if (g0.K % 8 || g0.M % 8 || g0.N % 8 || g0.lda % 8 || g0.ldb % 8 || g0.ldc % 8) return false;
-  if (g0.batch > 1 || g0.epi == EPI_AXPBY) {
+  if (g0.batch > 1 || g0.sym || g0.epi == EPI_AXPBY || g0.epi == EPI_AXPBY_DUP || g0.epi == EPI_NS_SPLIT) {
     // batched and AXPBY products run on the direct-to-LDS kernels only (full tiles, 16-byte
     // aligned operands and batch strides; AXPBY with bf16 output, fp32 output plain or
     // accumulating beta C); the caller loops over the others
     const bool ok = g0.a_kmajor && g0.M % 128 == 0 && g0.N % 128 == 0 && g0.K % 64 == 0 &&
-                    (g0.epi == 0 || (g0.epi == EPI_AXPBY && !g0.out_f32)) && !g0.resid &&
+                    (g0.epi == 0 || ((g0.epi == EPI_AXPBY || g0.epi == EPI_AXPBY_DUP || g0.epi == EPI_NS_SPLIT) &&
+                                     !g0.out_f32)) && !g0.resid &&
                     ((uintptr_t)g0.A | (uintptr_t)g0.B | (uintptr_t)g0.C | (uintptr_t)g0.D) % 16 == 0 &&
-                    (g0.sA | g0.sB | g0.sC | g0.sD) % 8 == 0;
+                    (g0.sA | g0.sB | g0.sC | g0.sD) % 8 == 0 &&
+                    (!g0.sym || (g0.M == g0.N && g0.epi == 0 && !g0.out_f32));
     if (!ok) return false;
     GemmArgs g = g0;
     g.ksplit = 1;

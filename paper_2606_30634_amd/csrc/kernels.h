@@ -114,8 +114,21 @@ struct GemmArgs {
   // C + b sC, D + b sD (elements)
   int batch = 1;
   int64_t sA = 0, sB = 0, sC = 0, sD = 0;
+  // sym: the product is symmetric (M == N, plain bf16 output): the direct-to-LDS kernels compute
+  // the tiles on and above the diagonal only and write each off-diagonal one also transposed; the
+  // other kernels ignore the flag (and compute every tile)
+  int sym = 0;
 };
 constexpr int GEMM_EPI_AXPBY = 6;
+// epilogue 7 (AXPBY with duplicated columns): C[r, 2c] = C[r, 2c + 1] = alpha (A B)[r, c] +
+// beta_d D[r, c], D of row stride ld_aux, C of row stride ldc (>= 2N).
+constexpr int GEMM_EPI_AXPBY_DUP = 7;
+// epilogue 8 (hi/lo split): x = (A B)[r, c] + beta_d (D[r, c] + D[r, N + c]) and C receives
+// hi = bf16(x) at column c and lo = bf16(x - hi) at N + c; C and D of row stride ldc (>= 2N), D
+// holding the same form of the previous x.
+constexpr int GEMM_EPI_NS_SPLIT = 8;
+// the batched direct-to-LDS kernels take a product (and epilogues 6-8) when it has whole tiles
+inline bool gemm_batched_tiles(int M, int N, int K) { return M % 128 == 0 && N % 128 == 0 && K % 64 == 0 && K > 0; }
 // y = alpha y + beta x over rows x cols (row stride ld), in place, bf16 or fp32 storage
 void launch_axpby(bool bf, void* y, const void* x, float alpha, float beta, int rows, int cols, int ld,
                   hipStream_t st);
@@ -160,11 +173,13 @@ void launch_muon_momentum(const MuonMat* mats, int nmat, int nblk, const float* 
                           const int* flag, float mu, double* partial, float* norm, hipStream_t st);
 // x[0] = M / (||M|| + 1e-7) in wide orientation (fp32)
 void launch_muon_prep(const MuonMat* mats, int nmat, int ntile, const float* M, const float* norm, hipStream_t st);
-// The bf16 operand form of fp32 iterates X [rows, n] (row stride n): S [rows, 4n] holds, per row,
-// [hi | hi | lo | hi] with hi = bf16(x) and lo = bf16(x - hi), so that the Gram product over
-// K = 3n of S[:, 0:3n] and S[:, n:4n] is hi hi^T + hi lo^T + lo hi^T, and a product L X is
-// L S[:, 0:n] + L S[:, 2n:3n] (row stride 4n)
+// The bf16 operand form of fp32 iterates X [rows, n] (row stride n): S [rows, 2n] holds, per row,
+// [hi | lo] with hi = bf16(x) and lo = bf16(x - hi), so that a product L X is L S[:, 0:n] +
+// L S[:, n:2n] (row stride 2n), or one product over K = 2 rows with S read as [2 rows, n] (rows
+// 2k, 2k + 1 = hi and lo of row k)
 void launch_muon_split(const float* X, bf16* S, int64_t rows, int n, hipStream_t st);
+// the inverse: X = hi + lo (n a multiple of 4)
+void launch_muon_join(const bf16* S, float* X, int64_t rows, int n, hipStream_t st);
 // W, u_prev and the compute copy (bf16 when bf) from O = x[fin]
 void launch_muon_apply(bool bf, const MuonMat* mats, int nmat, int ntile, int fin, float* W, float* up,
                        void* shadow, const int* flag, float lr, float wd, float rms, bool ef, float lam,

@@ -4,12 +4,16 @@
 // applies the orthogonalised update (standard, or the Error-Feedback form of §3.2).  The
 // Newton-Schulz products themselves are batched GEMMs launched by the stage.
 //
-// The iterate X stays in fp32 on every stage.  Rounding it to bf16 adds noise of relative size
-// 2^-9 in every direction, and the iteration multiplies the directions of small singular value by
-// up to a = 3.4445 per step: on the low-rank momenta of training that moves O by several percent.
-// Products that take X as an operand therefore use its hi + lo pair; the Gram matrix A and
-// P = b A + c A A enter as single bf16 matrices (rounding them perturbs X multiplicatively, which
-// the small singular directions do not amplify).
+// The iterate X is never rounded to bf16 alone.  That adds noise of relative size 2^-9 in every
+// direction, and the iteration multiplies the directions of small singular value by up to
+// a = 3.4445 per step: on the low-rank momenta of training that moves O by several percent.  X is
+// held in fp32, or as a pair hi + lo of bf16 matrices (hi = bf16(X), lo = bf16(X - hi), X to
+// about 2^-17 relative), and the product P X uses the pair.  The Gram matrix A = hi hi^T and
+// P = b A + c A A enter as single bf16 matrices: rounding them perturbs X multiplicatively, which
+// the small singular directions do not amplify, and A from hi alone differs from X X^T by about
+// as much as A's own bf16 rounding does.  On shapes of whole 128 x 128 tiles the
+// bf16 stage carries the pair from one step to the next (the product's epilogue forms the next
+// pair); other shapes keep X in fp32 and re-split it before each step.
 //
 // Per matrix W [rows, cols] with delayed gradient g (clipped by c):
 //   M <- mu M + (1 - mu) c g
@@ -20,6 +24,8 @@
 // Every reduction has a fixed order (per-chunk partial sums in fp64, summed in chunk order).
 #include "common.h"
 #include "kernels.h"
+#include <cstdio>
+#include <cstdlib>
 
 namespace {
 
@@ -152,7 +158,7 @@ __global__ void __launch_bounds__(MU_THREADS) muon_apply(const MuonMat* __restri
   }
 }
 
-// S row r = [hi | hi | lo | hi] of X row r, V consecutive columns per thread
+// S row r = [hi | lo] of X row r, V consecutive columns per thread
 template <int V>
 __global__ void __launch_bounds__(MU_THREADS) muon_split(const float* __restrict__ X, bf16* __restrict__ S,
                                                          int64_t rows, int n) {
@@ -162,7 +168,7 @@ __global__ void __launch_bounds__(MU_THREADS) muon_split(const float* __restrict
   const int64_t r = i / per_row;
   const int c = (int)(i % per_row) * V;
   const float* x = X + r * n + c;
-  bf16* s = S + r * 4 * n + c;
+  bf16* s = S + r * 2 * n + c;
   if constexpr (V == 4) {
     const f32x4 v = *reinterpret_cast<const f32x4*>(x);
     bf16x4 hi, lo;
@@ -172,16 +178,29 @@ __global__ void __launch_bounds__(MU_THREADS) muon_split(const float* __restrict
       lo[q] = (bf16)(v[q] - (float)hi[q]);
     }
     *reinterpret_cast<bf16x4*>(s) = hi;
-    *reinterpret_cast<bf16x4*>(s + n) = hi;
-    *reinterpret_cast<bf16x4*>(s + 2 * n) = lo;
-    *reinterpret_cast<bf16x4*>(s + 3 * n) = hi;
+    *reinterpret_cast<bf16x4*>(s + n) = lo;
   } else {
     const bf16 hi = (bf16)x[0], lo = (bf16)(x[0] - (float)hi);
     s[0] = hi;
-    s[n] = hi;
-    s[2 * n] = lo;
-    s[3 * n] = hi;
+    s[n] = lo;
   }
+}
+
+// X row r = hi + lo of S row r = [hi | lo], 4 consecutive columns per thread
+__global__ void __launch_bounds__(MU_THREADS) muon_join(const bf16* __restrict__ S, float* __restrict__ X,
+                                                        int64_t rows, int n) {
+  const int64_t per_row = n / 4;
+  const int64_t i = (int64_t)blockIdx.x * MU_THREADS + threadIdx.x;
+  if (i >= rows * per_row) return;
+  const int64_t r = i / per_row;
+  const int c = (int)(i % per_row) * 4;
+  const bf16* s = S + r * 2 * n + c;
+  const bf16x4 hi = *reinterpret_cast<const bf16x4*>(s);
+  const bf16x4 lo = *reinterpret_cast<const bf16x4*>(s + n);
+  f32x4 v;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) v[q] = (float)hi[q] + (float)lo[q];
+  *reinterpret_cast<f32x4*>(X + r * n + c) = v;
 }
 
 }  // namespace
@@ -205,6 +224,15 @@ void launch_muon_split(const float* X, bf16* S, int64_t rows, int n, hipStream_t
     muon_split<4><<<(unsigned)((rows * (n / 4) + MU_THREADS - 1) / MU_THREADS), MU_THREADS, 0, st>>>(X, S, rows, n);
   else
     muon_split<1><<<(unsigned)((rows * n + MU_THREADS - 1) / MU_THREADS), MU_THREADS, 0, st>>>(X, S, rows, n);
+}
+
+void launch_muon_join(const bf16* S, float* X, int64_t rows, int n, hipStream_t st) {
+  if (rows == 0 || n == 0) return;
+  if (n % 4) {
+    fprintf(stderr, "launch_muon_join: n = %d is not a multiple of 4\n", n);
+    abort();
+  }
+  muon_join<<<(unsigned)((rows * (n / 4) + MU_THREADS - 1) / MU_THREADS), MU_THREADS, 0, st>>>(S, X, rows, n);
 }
 
 void launch_muon_apply(bool bf, const MuonMat* mats, int nmat, int ntile, int fin, float* W, float* up,

@@ -126,7 +126,7 @@ struct stage {
   // Muon (shapes with optimizer 1): the blocks' weight matrices, grouped by their wide-orientation
   // shape for the batched Newton-Schulz products, and the ranges of the flat vector outside them
   // (AdamW: embedding, gains, padding)
-  struct MuonGroup { int m, n, nb; float* X[2]; bf16* S; void* A; void* P; };
+  struct MuonGroup { int m, n, nb; bool carry; float* X[2]; bf16* S[2]; void* A; void* P; };
   std::vector<MuonMat> muon;
   std::vector<MuonGroup> mgroups;
   std::vector<std::pair<int64_t, int64_t>> adamw_ranges;  // (offset, count)
@@ -337,9 +337,10 @@ size_t layout(stage* S, char* base) {
   S->row_loss = sh.last_stage ? (float*)carve(T * 4) : nullptr;
   // Muon: every block's wq, wk, wv, wo, wgate, wup, wdown; a group per wide-orientation shape
   // (m = min(rows, cols) <= n) holds the matrices' fp32 Newton-Schulz iterates [m, n] (ping-pong
-  // on the fp32 stage; one, updated in place, plus its bf16 hi/lo operand form [m, 4n] on the bf16
-  // stage), and their Gram products A = X X^T and P = b A + c A A [m, m] in the compute type,
-  // each kind contiguous over the group for the batched GEMMs
+  // on the fp32 stage; on the bf16 stage one, plus the bf16 hi/lo operand form [m, 2n]: ping-pong
+  // too when m and n are multiples of 128, as the iterate then stays in that form), and their Gram
+  // products A = X X^T [m, m] and P = b A + c A A in the compute type ([m, 2m] with each column
+  // twice when the hi/lo form is carried), each kind contiguous over the group for the batched GEMMs
   S->muon.clear();
   S->mgroups.clear();
   S->adamw_ranges.clear();
@@ -362,16 +363,21 @@ size_t layout(stage* S, char* base) {
       const int m = std::min(mx[k].rows, mx[k].cols), nn = std::max(mx[k].rows, mx[k].cols);
       size_t gi = 0;
       while (gi < S->mgroups.size() && (S->mgroups[gi].m != m || S->mgroups[gi].n != nn)) ++gi;
-      if (gi == S->mgroups.size()) S->mgroups.push_back({m, nn, 0, {nullptr, nullptr}, nullptr, nullptr, nullptr});
+      if (gi == S->mgroups.size())
+        S->mgroups.push_back({m, nn, 0, false, {nullptr, nullptr}, {nullptr, nullptr}, nullptr, nullptr});
       gidx[k] = (int)gi;
       slot[k] = S->mgroups[gi].nb++;
     }
     for (auto& gr : S->mgroups) {
-      gr.X[0] = (float*)carve((size_t)gr.nb * gr.m * gr.n * 4);
-      gr.X[1] = sh.dtype == 1 ? nullptr : (float*)carve((size_t)gr.nb * gr.m * gr.n * 4);
-      gr.S = sh.dtype == 1 ? (bf16*)carve((size_t)gr.nb * gr.m * gr.n * 4 * 2) : nullptr;
-      gr.A = carve((size_t)gr.nb * gr.m * gr.m * esz);
-      gr.P = carve((size_t)gr.nb * gr.m * gr.m * esz);
+      const size_t mn = (size_t)gr.nb * gr.m * gr.n, mm = (size_t)gr.nb * gr.m * gr.m;
+      gr.carry = sh.dtype == 1 && gemm_batched_tiles(gr.m, gr.m, 3 * gr.n) && gemm_batched_tiles(gr.m, gr.m, gr.m) &&
+                 gemm_batched_tiles(gr.m, gr.n, 2 * gr.m);
+      gr.X[0] = (float*)carve(mn * 4);
+      gr.X[1] = sh.dtype == 1 ? nullptr : (float*)carve(mn * 4);
+      gr.S[0] = sh.dtype == 1 ? (bf16*)carve(mn * 2 * 2) : nullptr;
+      gr.S[1] = gr.carry ? (bf16*)carve(mn * 2 * 2) : nullptr;
+      gr.A = carve(mm * esz);
+      gr.P = carve(mm * esz * (gr.carry ? 2 : 1));
     }
     int blk = 0, tile = 0;
     for (size_t k = 0; k < mx.size(); ++k) {
@@ -961,29 +967,57 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
       const int m = gr.m, n = gr.n;
       const int64_t mn = (int64_t)m * n, mm2 = (int64_t)m * m;
       const double fl = hp->ns_steps * 2.0 * gr.nb * (2.0 * mm2 * n + (double)mm2 * m);
-      if (s->bf) {
-        // X in fp32, its products from the hi/lo form S = [hi | hi | lo | hi]:
-        //   A  = S[:, 0:3n] S[:, n:4n]^T = hi hi^T + hi lo^T + lo hi^T     (bf16)
+      if (gr.carry) {
+        // X as its hi/lo form S = [hi | lo] from step to step (ping-pong):
+        //   A  = hi hi^T                                  (bf16, symmetric: the tiles on and above
+        //                                                  the diagonal, mirrored)
+        //   Pd = c A A + b A, each column twice: Pd[:, 2k] = Pd[:, 2k + 1] = P[:, k]   (bf16)
+        //   S' = form of (Pd Y + a (hi + lo)), Y [2m, n] rows 2k, 2k + 1 = hi_k, lo_k: Y is S
+        //        read with row stride n, so Pd Y = P hi + P lo in one product
+        //   and X = hi + lo of the last S for the update
+        GemmArgs g1[2], g3[2];
+        for (int q = 0; q < 2; ++q) {
+          g1[q] = gemm(m, m, n, gr.S[q], 2 * n, true, gr.S[q], 2 * n, true, gr.A, m);
+          g1[q].batch = gr.nb; g1[q].sA = g1[q].sB = 2 * mn; g1[q].sC = mm2; g1[q].sym = 1;
+          g3[q] = gemm(m, n, 2 * m, gr.P, 2 * m, true, gr.S[q], n, false, gr.S[q ^ 1], 2 * n);
+          g3[q].epi = GEMM_EPI_NS_SPLIT; g3[q].beta_d = ca; g3[q].D = gr.S[q];
+          g3[q].batch = gr.nb; g3[q].sA = 2 * mm2; g3[q].sB = g3[q].sC = g3[q].sD = 2 * mn;
+        }
+        GemmArgs g2 = gemm(m, m, m, gr.A, m, true, gr.A, m, true, gr.P, 2 * m);
+        g2.epi = GEMM_EPI_AXPBY_DUP; g2.alpha = cc; g2.beta_d = cb; g2.D = gr.A; g2.ld_aux = m;
+        g2.batch = gr.nb; g2.sA = g2.sB = g2.sD = mm2; g2.sC = 2 * mm2;
+        timed(s, STAGE_PROF_NS, fl, [&] {
+          launch_muon_split(gr.X[0], gr.S[0], (int64_t)gr.nb * m, n, us);
+          for (int it = 0; it < hp->ns_steps; ++it) {
+            launch_gemm(true, g1[it % 2], us);
+            launch_gemm(true, g2, us);
+            launch_gemm(true, g3[it % 2], us);
+          }
+          launch_muon_join(gr.S[hp->ns_steps % 2], gr.X[0], (int64_t)gr.nb * m, n, us);
+        }, us);
+      } else if (s->bf) {
+        // X in fp32, its products from the hi/lo form S = [hi | lo]:
+        //   A  = hi hi^T                                                     (bf16, symmetric)
         //   P  = c A A + b A                                                 (bf16)
         //   X <- P lo + a X, then X <- P hi + X                              (fp32, in place)
-        GemmArgs g1 = gemm(m, m, 3 * n, gr.S, 4 * n, true, gr.S + n, 4 * n, true, gr.A, m);
-        g1.batch = gr.nb; g1.sA = g1.sB = 4 * mn; g1.sC = mm2;
+        GemmArgs g1 = gemm(m, m, n, gr.S[0], 2 * n, true, gr.S[0], 2 * n, true, gr.A, m);
+        g1.batch = gr.nb; g1.sA = g1.sB = 2 * mn; g1.sC = mm2; g1.sym = 1;
         GemmArgs g2 = gemm(m, m, m, gr.A, m, true, gr.A, m, true, gr.P, m);
         g2.epi = GEMM_EPI_AXPBY; g2.alpha = cc; g2.beta_d = cb; g2.D = gr.A;
         g2.batch = gr.nb; g2.sA = g2.sB = g2.sC = g2.sD = mm2;
-        GemmArgs g3 = gemm(m, n, m, gr.P, m, true, gr.S + 2 * n, 4 * n, false, gr.X[0], n, true, ca);
-        g3.batch = gr.nb; g3.sA = mm2; g3.sB = 4 * mn; g3.sC = mn;
+        GemmArgs g3 = gemm(m, n, m, gr.P, m, true, gr.S[0] + n, 2 * n, false, gr.X[0], n, true, ca);
+        g3.batch = gr.nb; g3.sA = mm2; g3.sB = 2 * mn; g3.sC = mn;
         GemmArgs g4 = g3;
-        g4.B = gr.S;
+        g4.B = gr.S[0];
         g4.beta = 1.f;
         timed(s, STAGE_PROF_NS, fl, [&] {
-          launch_muon_split(gr.X[0], gr.S, (int64_t)gr.nb * m, n, us);
+          launch_muon_split(gr.X[0], gr.S[0], (int64_t)gr.nb * m, n, us);
           for (int it = 0; it < hp->ns_steps; ++it) {
             launch_gemm(true, g1, us);
             launch_gemm(true, g2, us);
             launch_gemm(true, g3, us);
             launch_gemm(true, g4, us);
-            if (it + 1 < hp->ns_steps) launch_muon_split(gr.X[0], gr.S, (int64_t)gr.nb * m, n, us);
+            if (it + 1 < hp->ns_steps) launch_muon_split(gr.X[0], gr.S[0], (int64_t)gr.nb * m, n, us);
           }
         }, us);
       } else {

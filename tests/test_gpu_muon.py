@@ -2,10 +2,13 @@
 ABI: the update in place (the oracle's rule on the GPU's own state and gradient before
 delayed_update(t), against the GPU's state after it) and free-running trajectories.  Muon runs on
 the blocks' weight matrices, AdamW on the embedding and the gains.  Tolerances: fp32 workload 1e-4;
-bf16 workloads 2e-2 on the Muon update and on losses (Newton-Schulz keeps its iterate in fp32 and
-takes bf16 Gram products: a bf16 emulation of that scheme on these workloads' momenta stays under
-7e-3 of float64 Newton-Schulz, where rounding the iterate itself to bf16 gives up to 8e-2); 1e-5
-on the momentum and on the AdamW parameters (fp32 arithmetic against float64)."""
+bf16 workloads 2e-2 on the Muon update and on losses (Newton-Schulz keeps its iterate in fp32, or
+as a hi + lo pair of bf16 matrices on shapes of whole tiles, and takes bf16 Gram products: a bf16
+emulation of either scheme on these workloads' momenta stays under 1e-2 of float64 Newton-Schulz,
+where rounding the iterate itself to bf16 gives up to 8e-2); 1e-5 on the momentum and on the AdamW
+parameters (fp32 arithmetic against float64).  The reduced workloads have whole-tile matrix shapes
+(the carried pair); the mixed one adds an FFN width of 320, whose [256, 320] matrices take the fp32
+iterate."""
 import numpy as np
 import pytest
 
@@ -16,6 +19,9 @@ from oracle.update import OptState, is_muon_matrix, iteration_update
 from test_gpu_stage import MID_R, LARGE_R, SMALL_R, TILED_R
 
 pytestmark = pytest.mark.gpu
+
+# one group of whole-tile shapes ([256, 256]) and one of the others ([256, 320])
+MIXED_R = SMALL_R.with_(name="small-mixed-muon", d_ffn=320)
 
 MUON = dict(optimizer="muon", momentum=0.95, update_rms=0.2, ns_steps=5)
 
@@ -76,7 +82,7 @@ def test_muon_tiny_fp32(lam):
     _report(f"muon tiny lambda={lam}", errs, tols)
 
 
-@pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, TILED_R], ids=lambda w: w.name)
+@pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, TILED_R, MIXED_R], ids=lambda w: w.name)
 def test_muon_reduced_bf16(w):
     steps = 6
     p0 = datagen.init_params(w)
