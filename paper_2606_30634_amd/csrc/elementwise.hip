@@ -26,6 +26,23 @@ __global__ void __launch_bounds__(256) embed_gather(const int32_t* __restrict__ 
   for (int j = threadIdx.x; j < d; j += blockDim.x) x0[dst + j] = ok ? E[src + j] : from_f32<T>(0.f);
 }
 
+// The same in 16-byte chunks, one wave per row and four rows per block (d a multiple of the
+// chunk, table and output 16-byte aligned).
+template <typename T>
+__global__ void __launch_bounds__(256) embed_gather_vec(const int32_t* __restrict__ tok,
+                                                        const T* __restrict__ E, T* __restrict__ x0,
+                                                        int rows, int d, int vocab) {
+  constexpr int V = 16 / (int)sizeof(T);
+  const int row = blockIdx.x * 4 + threadIdx.x / 64, lane = threadIdx.x % 64;
+  if (row >= rows) return;
+  const int t = tok[row];
+  const bool ok = t >= 0 && t < vocab;
+  const uint4* src = reinterpret_cast<const uint4*>(E + (int64_t)(ok ? t : 0) * d);
+  uint4* dst = reinterpret_cast<uint4*>(x0 + (int64_t)row * d);
+  const int nc = d / V;
+  for (int c = lane; c < nc; c += 64) dst[c] = ok ? src[c] : make_uint4(0u, 0u, 0u, 0u);
+}
+
 // ------------------------------------------------------------------ RMSNorm
 template <typename T>
 __global__ void __launch_bounds__(256) rmsnorm_fwd(const T* __restrict__ x,
@@ -594,6 +611,11 @@ __global__ void __launch_bounds__(1024) mean_kernel(const float* __restrict__ v,
 template <typename T>
 static void gather_t(const int32_t* tok, const void* E, void* x0, int rows, int d, int vocab,
                      hipStream_t st) {
+  if (rows <= 0) return;
+  if (d % (16 / (int)sizeof(T)) == 0 && ((uintptr_t)E | (uintptr_t)x0) % 16 == 0) {
+    embed_gather_vec<T><<<(unsigned)cdiv(rows, 4), 256, 0, st>>>(tok, (const T*)E, (T*)x0, rows, d, vocab);
+    return;
+  }
   embed_gather<T><<<rows, 256, 0, st>>>(tok, (const T*)E, (T*)x0, d, vocab);
 }
 void launch_embed_gather(bool bf, const int32_t* tok, const void* table, void* x0, int rows, int d,
