@@ -8,7 +8,7 @@ emulation of either scheme on these workloads' momenta stays under 1e-2 of float
 where rounding the iterate itself to bf16 gives up to 8e-2); 1e-5 on the momentum and on the AdamW
 parameters (fp32 arithmetic against float64).  The reduced workloads have whole-tile matrix shapes
 (the carried pair); the mixed one adds an FFN width of 320, whose [256, 320] matrices take the fp32
-iterate."""
+iterate; the small workload's update is also checked in place at full size."""
 import numpy as np
 import pytest
 
@@ -99,3 +99,16 @@ def test_muon_reduced_bf16(w):
         errs[f"final.{n}"] = rel(g["final"][""][n], ref)
         tols[f"final.{n}"] = 2e-2
     _report(f"muon {w.name}", errs, tols)
+
+
+def test_muon_update_small_full_size():
+    """The small workload at its full size: one step, then delayed_update(1), which consumes g_0, in
+    place on the GPU's own state.  Its two Newton-Schulz groups (twelve 768 x 768 matrices, nine
+    768 x 3072 ones) have whole tiles: the carried hi/lo pair, and symmetric Gram products that
+    compute 21 of their 36 tiles and mirror 15."""
+    w = datagen.SMALL
+    p0 = datagen.init_params(w)
+    log(f"muon {w.name}: 2 steps at full size")
+    g = run_gpu(w, 2, hp_of(w, **MUON), p0, upd_steps=(1,))
+    errs, tols = _update_in_place(w, g, w.ef_lambda, 2e-2)
+    _report("muon small full size", errs, tols)
