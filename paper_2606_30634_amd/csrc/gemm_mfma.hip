@@ -869,20 +869,30 @@ gemm_dma_kernel(GemmArgs g) {
       for (int i = 0; i < FM; ++i) af[0][i] = TA::frag(as, wm0 + i * 32, 0);
 #pragma unroll
       for (int j = 0; j < FN; ++j) bfr[0][j] = TB::frag(bs, wn0 + j * 32, 0);
+      // the next k-step's fragment reads go out between this step's MFMAs (one read after each
+      // MFMA; they write the other fragment buffer), so the LDS and matrix pipes work together
       static_for<BKT / 16>([&](auto KS) {
         constexpr int ks = KS, c = ks & 1;
+        __builtin_amdgcn_sched_barrier(0);
         if constexpr (ks + 1 < BKT / 16) {
 #pragma unroll
           for (int i = 0; i < FM; ++i) af[c ^ 1][i] = TA::frag(as, wm0 + i * 32, (ks + 1) * 16);
 #pragma unroll
           for (int j = 0; j < FN; ++j) bfr[c ^ 1][j] = TB::frag(bs, wn0 + j * 32, (ks + 1) * 16);
         }
-        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[c][i], bfr[c][j], acc[i][j], 0, 0, 0);
+        if constexpr (ks + 1 < BKT / 16) {
+          static_assert(FM * FN >= FM + FN, "one MFMA ahead of every fragment read");
+          static_for<FM + FN>([&](auto) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+          });
+          __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - (FM + FN), 0);
+        }
         __builtin_amdgcn_sched_barrier(0);
       });
     }
