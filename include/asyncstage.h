@@ -187,9 +187,27 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out,
  * "t <= 1" rule for tau = 1; the EF buffer of iteration t is t mod tau); write x_{t+1} to compute
  * version (t+1) mod 2.  Must be called once per t in increasing order; for t < tau (no pending
  * gradient) the weights are unchanged (u_{-1} = 0).  A non-finite
- * gradient norm leaves x, m, v and the EF buffer untouched (x_{t+1} = x_t) and is counted on the
- * device; see stage_poll_nonfinite.  STAGE_ESTATE on out-of-order t or an incomplete gradient. */
+ * gradient norm leaves x, m, v and the EF buffer untouched (x_{t+1} = x_t, the compute copy is
+ * written from x_t) and is counted on the device; see stage_poll_nonfinite.  Such an iteration still
+ * counts as having consumed its gradient: the bias-correction index of every update is
+ * k = t - tau + 1 (t + 1 with delay 0) whether or not earlier gradients were skipped, Error Feedback
+ * starts once tau gradients have been consumed, and an EF buffer the skipped iteration would have
+ * written keeps its contents.  The norm (two deterministic passes over the gradient) runs whether
+ * or not clipping is on, since it is also the non-finite check.  STAGE_ESTATE on out-of-order t or
+ * an incomplete gradient. */
 int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp);
+
+/* Resume a run at iteration next_t of a fixed-delay run (Alg. 1 carries x_t, the optimizer
+ * statistics, the EF buffers and the gradients not yet consumed from one iteration to the next).
+ * On a fresh stage (no delayed_update yet, no pending microbatch), after the caller has written
+ * through stage_tensor views the master weights x_next_t, m, v, every EF buffer ("u_prev.",
+ * "u_prev{j}.") and, for delay tau >= 1, the gradients g_s of steps s = next_t - tau .. next_t - 1
+ * into their buffers "grad{s mod (max_delay + 1)}.": marks those gradients complete and unconsumed,
+ * sets the count of consumed gradients to next_t - tau (next_t with delay 0) and copies the master
+ * weights into both compute versions (stage_sync_weights).  The next calls are stage_forward(...,
+ * step next_t, ...) and delayed_update(next_t).  delay in [0, max_delay] is the delay of the run
+ * being resumed.  STAGE_ESTATE when the stage has run an update or holds a pending microbatch. */
+int stage_resume(stage_t* s, int64_t next_t, int32_t delay);
 
 /* Stateless fused update (AdamW, Lion, NAdam or the AdamW weight prediction of hp; not Muon) over
  * flat device vectors of n elements:

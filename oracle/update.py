@@ -35,12 +35,22 @@ u is decoupled AdamW (§2: beta = (0.9, 0.95); App. E.1: weight decay 0.1, clipp
     g <- c g,  c = min(1, clip / (||g||_2 + 1e-6))        (global norm over the stage)
     m <- b1 m + (1 - b1) g;   v <- b2 v + (1 - b2) g^2
     u  = lr ( (m / (1 - b1^k)) / (sqrt(v / (1 - b2^k)) + eps) + wd x_t )
-with k the number of updates applied so far including this one, weight decay on the current
+with k the number of gradients consumed so far including this one, weight decay on the current
 weights x_t (the form Alg. 2 of §4 writes, U = eta (O + lambda X_t)), and the following readings
 where the paper is silent: eps = 1e-8; the clip epsilon 1e-6; weight decay on every parameter;
 step t = 0 changes nothing (the zero gradient g_{-1} is not fed to the statistics, so the first
 real update has k = 1); the EF buffer holds the whole previous update u_{t-2}, learning rate and
 weight decay included.
+
+A gradient whose global norm is not finite (a failure-detection reading; the paper is silent)
+is consumed without effect: the iteration leaves x, m, v and every Error-Feedback
+buffer as they are (x_{t+1} = x_t, the compute weights are x_{t+1}), but it still counts as an
+iteration that consumed a gradient, so k - the bias-correction index, the count of consumed
+gradients - advances, and Error Feedback starts once tau gradients have been consumed.  The EF
+buffer the skipped iteration would have written keeps its contents (zero before its first write),
+and a later iteration reads it as the update formed tau iterations earlier.  The skip is counted
+in OptState.n_skipped.  k is therefore t - tau + 1 at every iteration of a delay-tau run, whether
+or not earlier gradients were skipped.
 
 With optimizer "muon", u of every 2-D weight matrix of a decoder block is the one of Alg. 2
 (Delayed Muon, §4); the embedding and the RMSNorm gains keep AdamW:
@@ -145,10 +155,6 @@ def nadam_u(x, g, m, v, k: int, hp: "HParams"):
     return u, m1, v1
 
 
-class NonFiniteGradient(Exception):
-    pass
-
-
 def global_norm(grads: Dict[str, np.ndarray]) -> float:
     """||g||_2 over every tensor of the stage, accumulated in float64."""
     return math.sqrt(sum(float(np.sum(np.square(g.astype(np.float64)))) for g in grads.values()))
@@ -186,11 +192,12 @@ class OptState:
     v: Dict[str, np.ndarray]
     u_prev: Dict[str, np.ndarray]           # u_{t-2} at iteration t (zero before any update)
     pending: Optional[Dict[str, np.ndarray]] = None  # g_{t-1}, not yet consumed
-    n_updates: int = 0                      # updates applied so far
+    n_updates: int = 0                      # gradients consumed so far (applied or skipped)
     t: int = 0                              # next iteration index
     queue: List[Dict[str, np.ndarray]] = field(default_factory=list)   # delay >= 2: g_{t-tau} .. g_{t-1}
     x_compute: Optional[Dict[str, np.ndarray]] = None  # predict: the weights the next forward uses
     u_ring: List[Dict[str, np.ndarray]] = field(default_factory=list)  # delay >= 2: the last tau updates, oldest first
+    n_skipped: int = 0                      # gradients skipped for a non-finite norm
 
     @staticmethod
     def create(x: Dict[str, np.ndarray], dt=np.float64) -> "OptState":
@@ -201,9 +208,10 @@ class OptState:
 
     def copy(self) -> "OptState":
         cp = lambda d: None if d is None else {k: v.copy() for k, v in d.items()}
-        return OptState(cp(self.x), cp(self.m), cp(self.v), cp(self.u_prev), cp(self.pending),
-                        self.n_updates, self.t, [cp(g) for g in self.queue], [cp(u) for u in self.u_ring],
-                        cp(self.x_compute))
+        return OptState(x=cp(self.x), m=cp(self.m), v=cp(self.v), u_prev=cp(self.u_prev),
+                        pending=cp(self.pending), n_updates=self.n_updates, t=self.t,
+                        queue=[cp(g) for g in self.queue], x_compute=cp(self.x_compute),
+                        u_ring=[cp(u) for u in self.u_ring], n_skipped=self.n_skipped)
 
 
 def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> dict:
@@ -226,11 +234,15 @@ def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> d
         g_use = st.pending
     else:
         g_use = g_t
-    info = dict(applied=False, norm=0.0, clip=1.0)
-    if g_use is not None:
+    info = dict(applied=False, skipped=False, norm=0.0, clip=1.0)
+    if g_use is not None and not math.isfinite(global_norm(g_use)):
+        # consumed without effect: x, m, v, u_prev kept; k advances (see the module docstring)
+        st.n_updates += 1
+        st.n_skipped += 1
+        st.x_compute = {n: a.copy() for n, a in st.x.items()} if hp.predict == "updated" else None
+        info.update(skipped=True, norm=float("nan"))
+    elif g_use is not None:
         norm = global_norm(g_use)
-        if not math.isfinite(norm):
-            raise NonFiniteGradient(f"non-finite gradient norm at iteration {st.t}")
         c = clip_coefficient(norm, hp.clip_norm)
         k = st.n_updates + 1
         ef = hp.ef_lambda != 0.0 and st.n_updates >= 1   # "t <= 1": the first update is standard
@@ -267,12 +279,21 @@ def _iteration_update_tau(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams)
     """Iteration t with delay tau = hp.delay >= 2: consume g_{t-tau} once tau gradients wait, EF
     against the update formed tau iterations earlier once tau updates exist."""
     tau = hp.delay
-    info = dict(applied=False, norm=0.0, clip=1.0)
-    if len(st.queue) == tau:
+    info = dict(applied=False, skipped=False, norm=0.0, clip=1.0)
+    if len(st.queue) == tau and not math.isfinite(global_norm(st.queue[0])):
+        # consumed without effect; the EF buffer this iteration would write keeps what it holds:
+        # the update of iteration t - tau once the ring is full, zero before its first write
+        st.queue.pop(0)
+        keep = st.u_ring[0] if len(st.u_ring) == tau else {n: np.zeros_like(a) for n, a in st.x.items()}
+        st.u_ring.append({n: a.copy() for n, a in keep.items()})
+        if len(st.u_ring) > tau:
+            st.u_ring.pop(0)
+        st.n_updates += 1
+        st.n_skipped += 1
+        info.update(skipped=True, norm=float("nan"))
+    elif len(st.queue) == tau:
         g_use = st.queue.pop(0)
         norm = global_norm(g_use)
-        if not math.isfinite(norm):
-            raise NonFiniteGradient(f"non-finite gradient norm at iteration {st.t}")
         c = clip_coefficient(norm, hp.clip_norm)
         k = st.n_updates + 1
         ef = hp.ef_lambda != 0.0 and len(st.u_ring) == tau

@@ -17,7 +17,7 @@ EXPORTS = ["stage_required_bytes", "stage_init", "stage_num_tensors", "stage_ten
            "stage_tensor_by_name", "stage_sync_weights", "stage_forward", "stage_backward",
            "delayed_update", "delayed_update_flat", "stage_embed_indices", "stage_poll_nonfinite",
            "stage_grad_norm", "stage_profile_enable", "stage_profile_read", "stage_last_error",
-           "stage_destroy", "stage_set_update_overlap", "stage_join_update"]
+           "stage_destroy", "stage_set_update_overlap", "stage_join_update", "stage_resume"]
 PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_UPDATE, PROF_NORM, PROF_OTHER, PROF_NS = range(7)
 
 
@@ -70,6 +70,7 @@ def _load():
         "stage_profile_enable": (C.c_int, [vp, i32]),
         "stage_set_update_overlap": (C.c_int, [vp, i32]),
         "stage_join_update": (C.c_int, [vp]),
+        "stage_resume": (C.c_int, [vp, i64, i32]),
         "stage_profile_read": (C.c_int, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
         "stage_last_error": (C.c_char_p, []),
         "stage_destroy": (None, [vp]),
@@ -171,6 +172,10 @@ def stage_set_update_overlap(s: int, on: bool) -> None:
 
 def stage_join_update(s: int) -> None:
     _call("stage_join_update", s)
+
+
+def stage_resume(s: int, next_t: int, delay: int) -> None:
+    _call("stage_resume", s, next_t, delay)
 
 
 def stage_profile_enable(s: int, on: bool) -> None:

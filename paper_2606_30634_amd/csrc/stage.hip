@@ -924,9 +924,11 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
     HIP_OK(hipEventRecord(s->ev_now, s->st));
     HIP_OK(hipStreamWaitEvent(us, s->ev_now, 0));
   }
+  // The norm pass runs whether or not clipping is on: it is also the non-finite check (a skipped
+  // iteration leaves x, m, v and the EF buffer as they are, and still counts for k)
   const float* clip = nullptr;
   const int* flag = nullptr;
-  if (apply && hp->clip_norm > 0.f) {
+  if (apply) {
     timed(s, STAGE_PROF_NORM, 4.0 * s->n_flat, [&] {
       launch_grad_norm(s->grad[gb], false, s->n_flat, hp->clip_norm, s->upd_norm_part, s->upd_norm_out,
                        s->flag, s->skipped, device_cu_count(), us);
@@ -1098,6 +1100,31 @@ int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf
                       (hipStream_t)hip_stream);
   HIP_OK(hipGetLastError());
   return STAGE_OK;
+}
+
+int stage_resume(stage_t* s, int64_t next_t, int32_t delay) {
+  if (!s) return fail(STAGE_EINVAL, "null stage");
+  if (next_t < 0) return fail(STAGE_EINVAL, "next_t must be >= 0");
+  if (delay < 0 || delay > s->ndelay)
+    return fail(STAGE_EINVAL, "delay must be in [0, " + std::to_string(s->ndelay) + "] (the stage's max_delay)");
+  if (s->next_t != 0 || s->n_updates != 0) return fail(STAGE_ESTATE, "stage_resume needs a stage that has run no update");
+  for (const auto& sl : s->slots)
+    if (sl.pending) return fail(STAGE_ESTATE, "stage_resume with a pending microbatch");
+  // the gradients of steps next_t - delay .. next_t - 1 wait in their buffers, complete
+  for (int j = 0; j < s->ng; ++j) {
+    s->grad_step[j] = -1;
+    s->grad_count[j] = 0;
+    s->grad_consumed[j] = true;
+  }
+  for (int64_t st = std::max<int64_t>(0, next_t - delay); st < next_t; ++st) {
+    const int j = (int)(st % s->ng);
+    s->grad_step[j] = st;
+    s->grad_count[j] = 1;
+    s->grad_consumed[j] = false;
+  }
+  s->next_t = next_t;
+  s->n_updates = delay == 0 ? next_t : std::max<int64_t>(0, next_t - delay);  // gradients consumed so far
+  return stage_sync_weights(s);
 }
 
 int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts, int32_t* n_unique) {

@@ -79,6 +79,10 @@ class Stage:
     def update(self, t: int, hp: B.UpdateHParams):
         B.delayed_update(self.handle, t, hp)
 
+    def resume(self, next_t: int, delay: int = 1):
+        """Continue a run at iteration next_t from the state written through the views."""
+        B.stage_resume(self.handle, next_t, delay)
+
     def set_update_overlap(self, on: bool):
         """Overlap mode: the stage stream waits for an update only where the delay needs it."""
         B.stage_set_update_overlap(self.handle, on)

@@ -1,0 +1,121 @@
+"""Writes tests/golden/small_100_steps.npz: the float64 oracle's trajectory of the small workload
+(3 decoder blocks, d_model 768, 12 heads, SwiGLU 3072, seq 1024 x 8, vocab-32000 embedding on a
+first stage; AdamW, delay 1, Error Feedback lambda 1, clip 1.0, lr 1e-3) over 100 iterations of
+Alg. 1 (§2) with the Error-Feedback step of §3.2.
+
+Only the oracle and the seeded input generators are used; nothing comes from the HIP path.
+
+Stored (every array float64 unless noted):
+  loss[t], loss_abs[t]        surrogate loss sum(Y dY) of step t and sum |Y dY| (its condition)
+  offsets[name]               int64: start of the stored slice of each parameter (seeded)
+  {x,m,v,u_prev}@k/<name>     the slice of the master weights and optimizer state x_k, m_k, v_k,
+                              u_prev_k before iteration k's forward, k in STATE_AT
+  g@t/<name>                  the slice of the oracle's own gradient g_t (at its own x_t), t in GRAD_AT
+  norm.{dx,m,v,u_prev}@k/<name>  whole-tensor norms ||x_k - x_0||, ||m_k||, ||v_k||, ||u_prev_k||
+  y@t                         rows Y_ROWS of the stage output of step t (flattened tokens), t in Y_AT
+
+  python tests/golden/make_small_100.py [--steps 100] [--checkpoint DIR]
+"""
+from __future__ import annotations
+
+import argparse
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+
+import datagen  # noqa: E402
+import oracle  # noqa: E402
+from oracle import model  # noqa: E402
+from oracle.update import OptState, iteration_update  # noqa: E402
+
+STATE_AT = (2, 3, 10, 50, 100)
+GRAD_AT = (0, 1, 10, 50, 99)
+Y_AT = (0, 1, 10, 50, 99)
+SLICE = 512
+SLICE_SEED = 20250611
+Y_ROWS = (0, 1, 1023, 1024, 4095, 8191)
+OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "small_100_steps.npz")
+
+
+def slice_offsets(params):
+    rng = np.random.default_rng(SLICE_SEED)
+    return {n: int(rng.integers(0, v.size - SLICE + 1)) for n, v in params.items()}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--checkpoint", default="")
+    ap.add_argument("--out", default=OUT)
+    args = ap.parse_args()
+    w = datagen.SMALL
+    p0 = datagen.init_params(w)
+    offs = slice_offsets(p0)
+    hp = oracle.hparams_of(w)
+    st = OptState.create(p0, np.float64)
+    rec = {"loss": np.zeros(args.steps), "loss_abs": np.zeros(args.steps)}
+    for n, o in offs.items():
+        rec[f"offsets/{n}"] = np.array(o, dtype=np.int64)
+    x0 = {n: v.astype(np.float64) for n, v in p0.items()}
+    t0 = 0
+    ck = os.path.join(args.checkpoint, "small_100_ckpt.npz") if args.checkpoint else ""
+    if ck and os.path.exists(ck):
+        z = np.load(ck)
+        t0 = int(z["t"])
+        for pre, d in (("x", st.x), ("m", st.m), ("v", st.v), ("u_prev", st.u_prev)):
+            for n in d:
+                d[n] = z[f"{pre}/{n}"].copy()
+        st.pending = {n: z[f"pending/{n}"].copy() for n in st.x}
+        st.n_updates, st.t = int(z["n_updates"]), t0
+        for k in z.files:
+            if k.startswith("rec/"):
+                rec[k[4:]] = z[k].copy()
+        print(f"resumed at t = {t0}", flush=True)
+
+    def save_state(k):
+        for pre, d in (("x", st.x), ("m", st.m), ("v", st.v), ("u_prev", st.u_prev)):
+            for n, a in d.items():
+                rec[f"{pre}@{k}/{n}"] = a.ravel()[offs[n]:offs[n] + SLICE].copy()
+        for n in st.x:
+            rec[f"norm.dx@{k}/{n}"] = np.array(np.linalg.norm((st.x[n] - x0[n]).ravel()))
+            rec[f"norm.m@{k}/{n}"] = np.array(np.linalg.norm(st.m[n].ravel()))
+            rec[f"norm.v@{k}/{n}"] = np.array(np.linalg.norm(st.v[n].ravel()))
+            rec[f"norm.u_prev@{k}/{n}"] = np.array(np.linalg.norm(st.u_prev[n].ravel()))
+
+    for t in range(t0, args.steps):
+        tic = time.time()
+        if t in STATE_AT:
+            save_state(t)
+        inp = datagen.step_inputs(w, t, 0)
+        grads, outs = model.stage_step_grads(st.x, [inp], w, np.float64)
+        rec["loss"][t] = outs[0]["loss"]
+        rec["loss_abs"][t] = outs[0]["loss_abs"]
+        if t in GRAD_AT:
+            for n, a in grads.items():
+                rec[f"g@{t}/{n}"] = a.ravel()[offs[n]:offs[n] + SLICE].copy()
+        if t in Y_AT:
+            rec[f"y@{t}"] = outs[0]["y"].reshape(-1, w.d_model)[list(Y_ROWS)].copy()
+        iteration_update(st, grads, hp)
+        print(f"t = {t}: loss {rec['loss'][t]:.6e}, {time.time() - tic:.1f} s", flush=True)
+        if ck and (t + 1) % 5 == 0:
+            tmp = {f"{pre}/{n}": a for pre, d in (("x", st.x), ("m", st.m), ("v", st.v),
+                                                    ("u_prev", st.u_prev), ("pending", st.pending))
+                   for n, a in d.items()}
+            tmp.update({f"rec/{k}": v for k, v in rec.items()})
+            np.savez(ck + ".tmp.npz", t=t + 1, n_updates=st.n_updates, **tmp)
+            os.replace(ck + ".tmp.npz", ck)
+    if args.steps in STATE_AT:
+        save_state(args.steps)
+    store = {k: (v.astype(np.float32) if v.ndim and k.split("@")[0] in ("x", "m", "v", "u_prev", "g", "y")
+                 else v) for k, v in rec.items()}
+    np.savez_compressed(args.out, **store)
+    print(f"wrote {args.out}: {len(store)} arrays", flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -67,7 +67,7 @@ def schedule_1f1b(M: int, warm: int):
 
 def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps: Iterable[int] = (),
             device: str = "cuda:0", upd_steps: Iterable[int] = (), muon: bool = False,
-            early_update: bool = False):
+            early_update: bool = False, after_backward=None):
     """T iterations of Alg. 1 on the GPU stage.  Returns losses (per step, per microbatch), outputs
     at y_steps, and at grad_steps the gradient g_t together with the master weights x_t it was taken
     at, at upd_steps the whole optimizer state before and after delayed_update(t) with the gradient
@@ -75,7 +75,8 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     u_prev and every EF buffer ("u_ring", buffer j = iterations j mod tau).
 
     early_update: the stage in overlap mode, and delayed_update(t) issued before step t's forwards
-    and backwards (it consumes g_{t-1}), so that it runs beside them."""
+    and backwards (it consumes g_{t-1}), so that it runs beside them.
+    after_backward(t, stage): called after step t's backwards, before delayed_update(t)."""
     import torch
     from paper_2606_30634_amd.stage import Stage
     dev = torch.device(device)
@@ -136,6 +137,8 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
                            loss=loss_t[i] if w.last_stage else None)
             else:
                 st.backward(slot, dy=inp.get("dy"), microbatches_per_step=M)
+        if after_backward is not None:
+            after_backward(t, st)
         if t in grad_steps:
             res["grads"][t] = grab(f"grad{t % ng}.")
         for i in range(M):

@@ -147,3 +147,44 @@ def test_muon_replay(lam):
             expect = xs[t][k] - u - (lam * (u - us[-1]) if us and lam else 0.0)
             assert rel(xs[t + 1][k], expect) < 1e-9, (t, k)
             us.append(u)
+
+
+def _semi_orthogonal(shape, seed):
+    """An exactly semi-orthogonal matrix (orthonormal rows or columns) from a QR factorisation."""
+    m, n = shape
+    Q, _ = np.linalg.qr(np.random.default_rng(seed).standard_normal((max(m, n), min(m, n))))
+    return Q if m >= n else Q.T
+
+
+@pytest.mark.parametrize("shape", [(96, 32), (32, 96), (48, 48), (768, 3072)])
+def test_muon_scale_gives_update_rms(shape):
+    """The update RMS of §3 (0.2): s O has RMS 0.2 for an exactly semi-orthogonal O of any shape,
+    measured directly, not through the formula muon_scale implements."""
+    O = _semi_orthogonal(shape, 3)
+    np.testing.assert_allclose(O @ O.T if shape[0] <= shape[1] else O.T @ O, np.eye(min(shape)), atol=1e-12)
+    s = muon_scale(shape, 0.2)
+    assert abs(math.sqrt(np.mean((s * O) ** 2)) - 0.2) < 1e-12
+    s3 = muon_scale(shape, 0.35)
+    assert abs(math.sqrt(np.mean((s3 * O) ** 2)) - 0.35) < 1e-12
+
+
+@pytest.mark.parametrize("shape", [(96, 32), (32, 96), (40, 40)])
+def test_muon_update_rms_on_semi_orthogonal_momentum(shape):
+    """A first Muon update (wd 0, no clip) whose momentum is semi-orthogonal: Newton-Schulz maps
+    every singular value 1 / sqrt(min(m, n)) of the normalised momentum through the scalar quintic
+    to the same value q, so RMS(u) = lr 0.2 q exactly (the scalar recurrence computed here)."""
+    G = _semi_orthogonal(shape, 4)
+    hp = HParams(lr=3e-3, weight_decay=0.0, clip_norm=0.0, optimizer="muon", momentum=0.95, delay=0)
+    name = "blk0.wq"
+    st = OptState.create({name: np.zeros(shape)})
+    iteration_update(st, {name: G}, hp)
+    u = -st.x[name]
+    a, b, c = NS_COEFFS
+    M_fro = (1 - hp.momentum) * math.sqrt(min(shape))     # ||(1 - mu) G||_F
+    q = (1 - hp.momentum) / (M_fro + NS_EPS)
+    for _ in range(hp.ns_steps):
+        q = a * q + b * q ** 3 + c * q ** 5
+    rms = math.sqrt(np.mean(u ** 2))
+    assert abs(rms - hp.lr * 0.2 * q) < 1e-12 * hp.lr
+    # and u is parallel to G: every element scaled by the same factor
+    np.testing.assert_allclose(u, hp.lr * 0.2 * math.sqrt(max(shape)) * q * G, rtol=1e-10, atol=1e-16)

@@ -12,8 +12,7 @@ import torch
 
 from datagen import Workload, init_params, step_inputs
 from oracle import model, run
-from oracle.update import (HParams, NonFiniteGradient, OptState, flat_update, global_norm,
-                           iteration_update)
+from oracle.update import HParams, OptState, flat_update, global_norm, iteration_update
 
 R = np.random.default_rng(7)
 
@@ -138,16 +137,136 @@ def test_lambda_zero_is_standard_and_clipping_bound():
     assert clip_coefficient(0.5, 1.0) == 1.0
 
 
-def test_nonfinite_gradient_leaves_state_untouched():
-    hp = HParams(delay=1)
-    st = OptState.create({"w": np.ones(4)})
-    iteration_update(st, {"w": np.array([1.0, np.inf, 0, 0])}, hp)   # t=0: stash only
-    before = st.copy()
-    with pytest.raises(NonFiniteGradient):
-        iteration_update(st, {"w": np.zeros(4)}, hp)
-    np.testing.assert_array_equal(st.x["w"], before.x["w"])
-    np.testing.assert_array_equal(st.m["w"], before.m["w"])
-    assert st.n_updates == before.n_updates and st.t == before.t
+def _grad_seq(n, T, bad):
+    """x-independent gradient sequence; g_bad holds an infinity in one element."""
+    gs = [R.standard_normal(n) for _ in range(T)]
+    gs[bad] = gs[bad].copy()
+    gs[bad][3] = np.inf
+    return gs
+
+
+def test_nonfinite_gradient_is_skipped_with_k_advanced():
+    """A non-finite g_{t-1} leaves x, m, v and u_prev as they are, and the next update takes the
+    bias correction of the following index: torch AdamW (its own step counter advanced by hand,
+    no step taken for the bad gradient) on the same delayed sequence, lambda = 0."""
+    n, T, bad = 12, 8, 3
+    hp = HParams(lr=1e-2, clip_norm=0.0, ef_lambda=0.0, delay=1)
+    gs = _grad_seq(n, T, bad)
+    x0 = R.standard_normal(n)
+    st = OptState.create({"w": x0})
+    p, opt = _torch_adamw(x0, hp)
+    for t in range(T):
+        before = st.copy()
+        info = iteration_update(st, {"w": gs[t]}, hp)
+        if t == 0:
+            continue
+        if t - 1 == bad:   # consumes the bad gradient
+            assert info["skipped"] and not info["applied"] and st.n_skipped == 1
+            for f in ("x", "m", "v", "u_prev"):
+                np.testing.assert_array_equal(getattr(st, f)["w"], getattr(before, f)["w"])
+            opt.state[p]["step"] += 1      # torch: the iteration is counted, no step is taken
+            continue
+        p.grad = torch.tensor(gs[t - 1])
+        opt.step()
+        np.testing.assert_allclose(st.x["w"], p.detach().numpy(), rtol=1e-12, atol=1e-15)
+    assert st.n_updates == T - 1
+
+
+def test_nonfinite_gradient_ef_reads_last_applied_update():
+    """With Error Feedback after a skip, the EF term takes the update of the last applied
+    iteration (the EF buffer kept its contents): x_{t+1} = x_t - u - lambda (u - u_last)."""
+    n, T, bad, lam = 10, 7, 2, 1.0
+    hp = HParams(lr=1e-2, clip_norm=0.0, ef_lambda=lam, delay=1)
+    gs = _grad_seq(n, T, bad)
+    x0 = R.standard_normal(n)
+    st = OptState.create({"w": x0})
+    p, opt = _torch_adamw(np.zeros(n), hp)
+    u_last = None
+    for t in range(T):
+        x_t = st.x["w"].copy()
+        iteration_update(st, {"w": gs[t]}, hp)
+        if t == 0:
+            continue
+        if t - 1 == bad:
+            opt.state[p]["step"] += 1
+            np.testing.assert_array_equal(st.x["w"], x_t)
+            continue
+        u = _torch_u(p, opt, x_t, gs[t - 1], 0.0)
+        ref = x_t - u if u_last is None else x_t - u - lam * (u - u_last)
+        np.testing.assert_allclose(st.x["w"], ref, rtol=1e-12, atol=1e-15)
+        u_last = u
+
+
+@pytest.mark.parametrize("tau", [2, 3])
+def test_nonfinite_gradient_tau_keeps_ef_slot(tau):
+    """Delay tau: the skipped iteration's EF slot keeps its contents, so the iteration tau later
+    reads the update formed 2 tau iterations before it (zero before the ring's first write)."""
+    n, T = 9, 4 * tau + 3
+    hp = HParams(lr=1e-2, clip_norm=0.0, ef_lambda=float(tau), delay=tau)
+    for bad in (1, tau + 1):      # consumed at iteration bad + tau (ring still filling, ring full)
+        gs = _grad_seq(n, T, bad)
+        st = OptState.create({"w": R.standard_normal(n)})
+        slots = [np.zeros(n) for _ in range(tau)]     # the device ring: iteration t uses t mod tau
+        p, opt = _torch_adamw(np.zeros(n), hp)
+        for t in range(T):
+            x_t = st.x["w"].copy()
+            iteration_update(st, {"w": gs[t]}, hp)
+            if t < tau:
+                np.testing.assert_array_equal(st.x["w"], x_t)
+                continue
+            j = t - tau                 # the gradient consumed
+            if j == bad:
+                opt.state[p]["step"] += 1
+                np.testing.assert_array_equal(st.x["w"], x_t)
+                continue
+            u = _torch_u(p, opt, x_t, gs[j], 0.0)
+            ef = j >= tau              # tau gradients consumed before this one
+            ref = x_t - u - tau * (u - slots[t % tau]) if ef else x_t - u
+            np.testing.assert_allclose(st.x["w"], ref, rtol=1e-12, atol=1e-15)
+            slots[t % tau] = u
+
+
+@pytest.mark.parametrize("kind", ["tau2-ef", "predict", "delay1-ef"])
+def test_optstate_copy_round_trip(kind):
+    """copy() reproduces every field, shares no array with the original, and a run continued from
+    the copy equals the run continued from the original."""
+    hp = {"tau2-ef": HParams(lr=1e-2, ef_lambda=2.0, delay=2),
+          "predict": HParams(lr=1e-2, predict="updated"),
+          "delay1-ef": HParams(lr=1e-2, ef_lambda=1.0)}[kind]
+    gs = [{"w": R.standard_normal(6), "b": R.standard_normal(3)} for _ in range(9)]
+    st = OptState.create({"w": R.standard_normal(6), "b": R.standard_normal(3)})
+    for t in range(5):
+        iteration_update(st, gs[t], hp)
+    cp = st.copy()
+
+    def same(a, b):
+        if isinstance(a, dict):
+            assert a.keys() == b.keys()
+            for k in a:
+                np.testing.assert_array_equal(a[k], b[k])
+                assert a[k] is not b[k]
+        elif isinstance(a, list):
+            assert len(a) == len(b)
+            for u, v in zip(a, b):
+                same(u, v)
+        else:
+            assert a == b
+
+    import dataclasses
+    for f in dataclasses.fields(OptState):
+        a, b = getattr(st, f.name), getattr(cp, f.name)
+        assert (a is None) == (b is None), f.name
+        if a is not None:
+            same(a, b)
+    if kind == "tau2-ef":
+        assert len(cp.u_ring) == 2 and len(cp.queue) == 2 and cp.x_compute is None
+    if kind == "predict":
+        assert isinstance(cp.x_compute, dict) and cp.u_ring == []
+    for t in range(5, 9):
+        iteration_update(st, gs[t], hp)
+        iteration_update(cp, gs[t], hp)
+    same(st.x, cp.x)
+    same(st.m, cp.m)
 
 
 def test_flat_update_matches_iteration_update():
