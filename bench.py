@@ -3,12 +3,13 @@
 One step = one pass of the whole hot path over one optimizer step's input: delayed_update(t)
 (Alg. 1 with AdamW, Error Feedback lambda = 1, global-norm clipping at 1.0; it consumes g_{t-1}
 and is issued first, in the stage's overlap mode, so that it runs beside the step's work), then
-stage_forward and stage_backward of every microbatch of step t.  Default workload: the small bf16 stage (3 decoder blocks,
-d_model 768, 12 heads, SwiGLU 3072, seq 1024, microbatch 8, vocab-32000 embedding on the first
-stage), synthetic seeded inputs already resident in HBM.  Prints one JSON line.
+stage_forward and stage_backward of every microbatch of step t.  Default workload: the large bf16
+stage (4 decoder blocks, d_model 4096, 32 query / 8 key-value heads of 128, SwiGLU 14336, seq 4096,
+microbatch 2, eight microbatches per optimizer step in a 1F1B order with 4 activation slots:
+65536 tokens per step), synthetic seeded inputs already resident in HBM.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload small|mid|large|tiny|last] [--no-cpu-baseline]
-                  [--optimizer adamw|muon|lion|nadam] [--predict] [--delay TAU] [--vocab V]
+  python bench.py [--steps K] [--warmup W] [--workload large|mid|small|tiny|last] [--no-cpu-baseline]
+                  [--optimizer adamw|muon|lion|nadam|adan] [--predict] [--delay TAU] [--vocab V]
 
 With --optimizer muon the blocks' weight matrices take delayed Muon (Alg. 2: momentum 0.95, five
 quintic Newton-Schulz steps, update RMS 0.2) with Error Feedback lambda = 1, the embedding and gains
@@ -16,7 +17,7 @@ AdamW; the line then also reports the Newton-Schulz GEMMs as their own kernel cl
 (default 1) runs the fixed delay TAU of App. C (g_{t-TAU} consumed, Error Feedback lambda = TAU
 against the update formed TAU iterations earlier).  --workload last is the last stage of the small
 model's shape with its own LM head (vocab 49152; --vocab V sets another, e.g. 128256).  --optimizer
-lion|nadam and --predict (AdamW with SAPipe weight prediction from the updated state) select the
+lion|nadam|adan and --predict (AdamW with SAPipe weight prediction from the updated state) select the
 elementwise variants of the update, also for the update-only workload.
 """
 from __future__ import annotations
@@ -75,10 +76,12 @@ def measured_traffic(workload, kernel_class):
 
 
 def cpu_baseline(w, optimizer="adamw", predict=False):
-    """The oracle (float32, numpy) timed on whole optimizer steps of the workload -- all sequences
-    forward+backward, then the full delayed update -- repeated until at least 10 s of CPU work (at
-    most 4 steps) when one step is a bounded amount of work; otherwise on 2 of the step's sequences
-    plus the full update, extrapolated linearly in tokens."""
+    """The oracle (float32, numpy) timed on the machine's host cores.  A stage of width <= 1024: whole
+    optimizer steps of the workload -- all sequences forward+backward, then the full delayed update --
+    repeated until at least 10 s of CPU work (at most 4 steps).  A wider stage, whose step is hours of
+    CPU work: one decoder block forward+backward on one sequence (the unit every block and sequence of
+    the step repeats) and the delayed update on a 2^24-element slice of the flat vector (elementwise),
+    each repeated until a few seconds, scaled to the step's blocks, sequences and parameters."""
     import numpy as np
     import datagen
     import oracle
@@ -89,10 +92,46 @@ def cpu_baseline(w, optimizer="adamw", predict=False):
         cores = max(i.get("num_threads", 1) for i in threadpool_info()) or os.cpu_count()
     except Exception:
         cores = os.cpu_count()
-    n_seq = w.micro_batch if w.d_model <= 1024 else min(2, w.micro_batch)
+    kw = update_rule(optimizer, predict)
+    tokens_step = w.tokens_per_micro * w.microbatches_per_step
+    n_params = sum(int(np.prod(s)) for _, s, _ in datagen.param_specs(w))
+    if w.d_model > 1024:
+        ws = w.with_(n_blocks=1, micro_batch=1, microbatches_per_step=1)
+        p0 = {k: v.astype(np.float32) for k, v in datagen.init_params(ws).items()}
+        inp = datagen.step_inputs(ws, 0)
+        fb_s, reps = 0.0, 0
+        while reps < 3 and (reps == 0 or fb_s < 8.0):
+            t0 = time.perf_counter()
+            model.stage_step_grads(p0, [inp], ws, np.float32)
+            fb_s += time.perf_counter() - t0
+            reps += 1
+        n = 1 << 24
+        rule = dict(kw, optimizer="adamw") if optimizer == "muon" else kw   # Muon's matrices: not elementwise
+        hp = oracle.hparams_of(w, **(dict(rule, ef_lambda=0.0) if predict else rule))
+        st = OptState.create({"flat": np.random.default_rng(0).standard_normal(n).astype(np.float32) * 0.02},
+                             np.float32)
+        g = {"flat": np.random.default_rng(1).standard_normal(n).astype(np.float32) * 1e-3}
+        iteration_update(st, g, hp)
+        upd_s, ureps = 0.0, 0
+        while ureps < 8 and (ureps == 0 or upd_s < 2.0):
+            t0 = time.perf_counter()
+            iteration_update(st, g, hp)
+            upd_s += time.perf_counter() - t0
+            ureps += 1
+        seqs = w.micro_batch * w.microbatches_per_step
+        fb_step = fb_s / reps * w.n_blocks * seqs
+        upd_step = upd_s / ureps * n_params / n
+        step_s = fb_step + upd_step
+        return {"value": tokens_step / step_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+                "sample": f"float32 numpy oracle: one decoder block forward+backward on one {w.seq_len}-token "
+                          f"sequence ({fb_s / reps:.1f} s, {reps} reps) x {w.n_blocks} blocks x {seqs} sequences "
+                          f"per step, plus the delayed update ({hp.optimizer} + Error Feedback) on a 2^24-element slice "
+                          f"({upd_s / ureps:.2f} s, {ureps} reps) x {n_params / n:.1f} for {n_params} parameters; "
+                          f"{step_s:.0f} s per step extrapolated",
+                "measured_s": round(fb_s + upd_s, 2)}
+    n_seq = w.micro_batch
     ws = w.with_(micro_batch=n_seq)
     p0 = datagen.init_params(ws)
-    kw = update_rule(optimizer, predict)
     hp = oracle.hparams_of(ws, **(dict(kw, ef_lambda=0.0) if predict else kw))
     st = OptState.create(p0, np.float32)
     inp = datagen.step_inputs(ws, 0)
@@ -108,7 +147,6 @@ def cpu_baseline(w, optimizer="adamw", predict=False):
         fb_s += t1 - t0
         upd_s += t2 - t1
         reps += 1
-    tokens_step = w.tokens_per_micro * w.microbatches_per_step
     fb_per_token = fb_s / reps / (n_seq * w.seq_len)
     step_s = fb_per_token * tokens_step + upd_s / reps
     whole = n_seq * w.seq_len == tokens_step
@@ -117,14 +155,15 @@ def cpu_baseline(w, optimizer="adamw", predict=False):
     return {"value": tokens_step / step_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": f"float32 numpy oracle: {n_seq} of the step's {w.micro_batch * w.microbatches_per_step} "
                       f"sequences forward+backward ({fb_s / reps:.1f} s per step) plus the full delayed update "
-                      f"over {sum(v.size for v in p0.values())} parameters ({upd_s / reps:.1f} s per step); {how}",
+                      f"over {n_params} parameters ({upd_s / reps:.1f} s per step); {how}",
             "measured_s": round(fb_s + upd_s, 2)}
 
 
 def update_rule(optimizer, predict):
     """Keyword arguments of the update rule (hparams) for the optimizer options of this script."""
     kw = {"lion": dict(optimizer="lion", beta1=0.9, beta2=0.99, weight_decay=0.5),
-          "nadam": dict(optimizer="nadam", beta2=0.999)}.get(optimizer, dict(optimizer=optimizer))
+          "nadam": dict(optimizer="nadam", beta2=0.999),
+          "adan": dict(optimizer="adan", beta1=0.98, beta2=0.92, beta3=0.99)}.get(optimizer, dict(optimizer=optimizer))
     if predict:
         kw.update(predict="updated")
     return kw
@@ -133,9 +172,11 @@ def update_rule(optimizer, predict):
 def update_workload(steps, optimizer="adamw", predict=False):
     """The update-only workload: delayed_update_flat over a flat 1.0e9-element fp32 vector (x, m, v,
     EF buffer), one bf16 gradient N(0, 1e-3), bf16 compute copy; `steps` iterations timed with HIP
-    events on the stream.  36 algorithmic bytes per element (Lion, which keeps no v: 28; the
-    weight prediction, which has no EF buffer: 28).  A plain device copy of 4 GiB is timed in the
-    same process as the practical HBM ceiling."""
+    events on the stream, clipping off: 36 algorithmic bytes per element (Lion, which keeps no v: 28;
+    the weight prediction, which has no EF buffer: 28).  Then the same with clipping at 1.0: the
+    gradient's norm pass (grad_norm_flat, 2 more bytes per element) before every update.  The
+    library's streaming copy (hbm_stream_copy, 16-byte non-temporal accesses) of x's 4.0e9 bytes is timed
+    in the same process as the practical HBM ceiling."""
     import torch
     from paper_2606_30634_amd import binding as B
     from paper_2606_30634_amd.stage import hparams
@@ -152,35 +193,67 @@ def update_workload(steps, optimizer="adamw", predict=False):
     kw = update_rule(optimizer, predict)
     lam = 0.0 if predict else 1.0
     hp = hparams(lr=1e-3, ef_lambda=lam, clip_norm=0.0, **kw)
-    bpe = 2 + 2 + 8 + 8 + (0 if optimizer == "lion" else 8) + (8 if lam else 0)
+    hp_clip = hparams(lr=1e-3, ef_lambda=lam, clip_norm=1.0, **kw)
+    adan = optimizer == "adan"
+    bpe = 2 + 2 + 8 + 8 + (0 if optimizer == "lion" else 8) + (8 if lam else 0) + (16 if adan else 0)
+    d = torch.zeros(n, device=dev) if adan else None
+    gl = torch.zeros(n, device=dev) if adan else None
     stream = torch.cuda.current_stream(dev)
-    call = lambda t: B.delayed_update_flat(n, x.data_ptr(), g.data_ptr(), True, m.data_ptr(), v.data_ptr(),
-                                           up.data_ptr(), sh.data_ptr(), True, t, hp, None, stream.cuda_stream)
-    call(1)  # warm-up (t = 1: a real update)
+    ws_bytes = B.grad_norm_flat_workspace_bytes()
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    norm_out = torch.zeros(2, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    if adan:
+        call = lambda t, h, c: B.delayed_update_flat_adan(n, x.data_ptr(), g.data_ptr(), True, m.data_ptr(),
+                                                          v.data_ptr(), d.data_ptr(), gl.data_ptr(), up.data_ptr(),
+                                                          sh.data_ptr(), True, t, h, c, stream.cuda_stream)
+    else:
+        call = lambda t, h, c: B.delayed_update_flat(n, x.data_ptr(), g.data_ptr(), True, m.data_ptr(),
+                                                     v.data_ptr(), up.data_ptr(), sh.data_ptr(), True, t, h, c,
+                                                     stream.cuda_stream)
+    norm = lambda: B.grad_norm_flat(n, g.data_ptr(), True, 1.0, norm_out.data_ptr(), flag.data_ptr(),
+                                    ws.data_ptr(), ws_bytes, stream.cuda_stream)
+    log(f"bench: update-only workload, {n} elements, {steps} iterations without and with the norm pass")
+    call(1, hp, None)  # warm-up (t = 1: a real update)
     torch.cuda.synchronize(dev)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for t in range(2, 2 + steps):
-        call(t)
+        call(t, hp, None)
     e1.record(stream)
     torch.cuda.synchronize(dev)
     ms = e0.elapsed_time(e1) / steps
     gbs = bpe * n / (ms * 1e-3) / 1e9
-    del g, m, v, up, sh
-    src = x[: 1 << 30]  # 4 GiB
-    dst = torch.empty_like(src)
-    dst.copy_(src)
+    e0.record(stream)
+    for t in range(2 + steps, 2 + 2 * steps):
+        norm()
+        call(t, hp_clip, norm_out.data_ptr() + 4)
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    ms_clip = e0.elapsed_time(e1) / steps
+    gbs_clip = (bpe + 2) * n / (ms_clip * 1e-3) / 1e9
+    del g, m, v, up, sh, d, gl
+    src = x.view(torch.uint8)          # the 4.0e9 bytes of x
+    nb = src.numel() // 16 * 16
+    dst = torch.empty(nb, dtype=torch.uint8, device=dev)
+    if src.numel() < nb or dst.numel() < nb:
+        raise RuntimeError("copy ceiling: buffers smaller than the copy")
+    log(f"bench: streaming-copy ceiling, {nb} bytes")
+    B.hbm_stream_copy(dst.data_ptr(), src.data_ptr(), nb, stream.cuda_stream)
     torch.cuda.synchronize(dev)
     e0.record(stream)
     for _ in range(5):
-        dst.copy_(src)
+        B.hbm_stream_copy(dst.data_ptr(), src.data_ptr(), nb, stream.cuda_stream)
     e1.record(stream)
     torch.cuda.synchronize(dev)
-    copy_gbs = 2.0 * src.numel() * 4 / (e0.elapsed_time(e1) / 5 * 1e-3) / 1e9
+    copy_gbs = 2.0 * nb / (e0.elapsed_time(e1) / 5 * 1e-3) / 1e9
     return {"elements": n, "steps": steps, "rule": kw, "ef_lambda": lam, "bytes_per_element": bpe,
             "ms_per_step": round(ms, 4),
             "achieved_GBs": round(gbs, 1), "peak_GBs": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4),
-            "plain_copy_GBs": round(copy_gbs, 1), "frac_of_copy": round(gbs / copy_gbs, 4)}
+            "stream_copy_GBs": round(copy_gbs, 1), "frac_of_copy": round(gbs / copy_gbs, 4),
+            "with_clip_norm": {"bytes_per_element": bpe + 2, "ms_per_step": round(ms_clip, 4),
+                               "achieved_GBs": round(gbs_clip, 1), "frac": round(gbs_clip / PEAK_HBM_GBS, 4),
+                               "frac_of_copy": round(gbs_clip / copy_gbs, 4)}}
 
 
 def main():
@@ -188,9 +261,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="small")
+    ap.add_argument("--workload", default="large")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--optimizer", choices=("adamw", "muon", "lion", "nadam"), default="adamw")
+    ap.add_argument("--optimizer", choices=("adamw", "muon", "lion", "nadam", "adan"), default="adamw")
     ap.add_argument("--predict", action="store_true",
                     help="AdamW with SAPipe weight prediction from the updated state (no Error Feedback)")
     ap.add_argument("--delay", type=int, default=1)
@@ -224,7 +297,7 @@ def main():
     st = Stage(make_shape(w.n_blocks, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ffn, w.vocab,
                           w.first_stage, w.last_stage, w.tie_embedding, w.seq_len, w.micro_batch,
                           w.max_inflight, bf16=bf, rms_eps=w.rms_eps, rope_theta=w.rope_theta,
-                          muon=muon, max_delay=args.delay), "cuda:0")
+                          muon=muon, max_delay=args.delay, adan=args.optimizer == "adan"), "cuda:0")
     st.load_master(datagen.init_params(w))
     if args.predict and (args.optimizer != "adamw" or args.delay != 1):
         print("--predict applies to AdamW at delay 1", file=sys.stderr)
@@ -363,7 +436,8 @@ def main():
                    "optimizer": ("Muon (momentum 0.95, 5 Newton-Schulz steps, update RMS 0.2) on the block "
                                  "matrices, AdamW elsewhere" if muon else
                                  {"adamw": "AdamW", "lion": "Lion (betas 0.9, 0.99; wd 0.5)",
-                                  "nadam": "NAdam (betas 0.9, 0.999)"}[args.optimizer]) +
+                                  "nadam": "NAdam (betas 0.9, 0.999)",
+                                  "adan": "Adan (betas 0.98, 0.92, 0.99)"}[args.optimizer]) +
                                 (" with SAPipe weight prediction (updated state)" if args.predict else "") +
                                 f", delay {args.delay}, Error Feedback lambda {lam:g}, clip 1.0",
                    "parallelism": "1 GPU, one stage"},

@@ -77,7 +77,9 @@ enum { STAGE_MAX_DELAY = 8 };
  * of activation slots (microbatches whose backward is pending).  optimizer 0: AdamW only;
  * 1: the arena also holds the Newton-Schulz workspace of delayed Muon (Alg. 2 of §4), 8 to 12 (fp32
  * stage: 8) bytes per element of the blocks' weight matrices plus their Gram matrices, so that
- * delayed_update accepts update_hparams_t.optimizer = 1.  max_delay in [0, 8] (0 is read as 1):
+ * delayed_update accepts update_hparams_t.optimizer = 1; 2: the arena also holds Adan's two extra
+ * state vectors (8 bytes per parameter), so that delayed_update accepts optimizer = 4.  max_delay
+ * in [0, 8] (0 is read as 1):
  * the largest delay delayed_update accepts; the arena holds max_delay + 1 gradient buffers and
  * max_delay EF buffers. */
 typedef struct {
@@ -108,7 +110,12 @@ typedef struct {
  * c g) + weight_decay x_t), m <- beta2 m + (1 - beta2) c g (v unused).  optimizer 3: NAdam with the
  * momentum-decay schedule mu_k = beta1 (1 - 0.5 0.96^(k nadam_psi)): m, v as AdamW and u = lr
  * ((1 - mu_k) / (1 - P_k) c g + mu_{k+1} / (1 - P_k mu_{k+1}) m) / (sqrt(v / (1 - beta2^k)) + eps)
- * + lr weight_decay x_t, P_k = mu_1 ... mu_k.
+ * + lr weight_decay x_t, P_k = mu_1 ... mu_k.  optimizer 4: Adan (§3.3's optimizer list; the rule of
+ * the cited Adan work, betas as averaging weights, the paper's beta1 = 0.98) on every parameter,
+ * with diff = c g - c g_last (0 at the first update; g_last the clipped gradient the previous update
+ * consumed): m <- beta1 m + (1 - beta1) c g, d <- beta2 d + (1 - beta2) diff, n <- beta3 n + (1 -
+ * beta3) (c g + beta2 diff)^2 (n in the v slot), u = lr ((m / (1 - beta1^k) + beta2 d / (1 - beta2^k))
+ * / (sqrt(n / (1 - beta3^k)) + eps) + weight_decay x_t); needs a stage shaped with optimizer 2.
  * predict 1 (AdamW, delay 1, ef_lambda 0 only): SAPipe weight prediction with the updated
  * optimizer state (App. B.1) - the master takes the standard delayed step x_{t+1} = x_t -
  * u_{t-1}(g_{t-1}) while the compute copy receives x_{t+1} - u_t(g_{t-1}), AdamW fed g_{t-1} once
@@ -121,6 +128,7 @@ typedef struct {
   int32_t ns_steps;
   int32_t predict;
   float nadam_psi;
+  float beta3;
 } update_hparams_t;
 
 /* Bytes of device memory the stage needs (weights, optimizer state, max_delay + 1 gradient
@@ -222,6 +230,36 @@ int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf
                         float* v, float* u_prev, void* x_shadow, int32_t shadow_is_bf16,
                         int64_t t, const update_hparams_t* hp, const float* clip_scale_dev,
                         void* hip_stream);
+
+/* delayed_update_flat for Adan (hp->optimizer 4), whose rule keeps two more state vectors: d (the
+ * average of gradient differences) and g_last (the clipped gradient of the previous update), fp32,
+ * 16-byte aligned, read and written; v holds Adan's second moment n.  Every other argument and the
+ * delay / EF / shadow conventions as delayed_update_flat. */
+int delayed_update_flat_adan(int64_t n, float* x, const void* g_prev, int32_t g_is_bf16, float* m, float* v,
+                             float* d, float* g_last, float* u_prev, void* x_shadow, int32_t shadow_is_bf16,
+                             int64_t t, const update_hparams_t* hp, const float* clip_scale_dev, void* hip_stream);
+
+/* Device bytes of the workspace grad_norm_flat needs (partial sums of the first pass). */
+size_t grad_norm_flat_workspace_bytes(void);
+
+/* Global L2 norm of a flat gradient vector and its clip coefficient (the gradient clipping of §2 /
+ * App. E.1, c = min(1, clip_norm / (||g|| + 1e-6)), 1 when clip_norm <= 0 or the norm is not
+ * finite), the pass delayed_update runs over the stage's gradient, for a caller-held flat vector
+ * (with delayed_update_flat, whose clip_scale_dev can be out_dev + 1).  Two deterministic passes:
+ * contiguous ranges summed in double per block, then the partials in a fixed order.
+ *   g          n elements, fp32 or bf16 (g_is_bf16), device, 16-byte (bf16: 8-byte) aligned
+ *   out_dev    two floats, device: ||g||, c
+ *   nonfinite_dev  one int32, device, set to 1 when ||g|| is not finite and 0 otherwise; may be NULL
+ *   workspace  device scratch of >= grad_norm_flat_workspace_bytes(), 8-byte aligned, owned by
+ *              the caller; calls that share a workspace must not overlap
+ * Enqueued on hip_stream. */
+int grad_norm_flat(int64_t n, const void* g, int32_t g_is_bf16, float clip_norm, float* out_dev,
+                   int32_t* nonfinite_dev, void* workspace, size_t workspace_bytes, void* hip_stream);
+
+/* Measurement reference, not a step of the method: a streaming device copy of `bytes` (a multiple
+ * of 16; both pointers 16-byte aligned) with 16-byte non-temporal loads and stores, four chunks in
+ * flight per thread - the practical HBM ceiling the update pass's bandwidth is reported against. */
+int hbm_stream_copy(void* dst, const void* src, size_t bytes, void* hip_stream);
 
 /* Ascending unique token ids of the microbatch in `slot` and their counts (after its backward
  * on a first stage).  ids, counts: device int32 arrays of >= micro_batch*seq_len entries;

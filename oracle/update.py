@@ -17,6 +17,12 @@ Elementwise variants of u (the optimizer list of §3.3, on every parameter; same
     "nadam" (Dozat, 2016, the momentum-decay schedule of torch.optim.NAdam): mu_k = b1 (1 - 0.5 0.96^(k psi)),
             m, v as AdamW, u = lr ((1 - mu_k) / (1 - P_k) g + mu_{k+1} / (1 - P_k mu_{k+1}) m) /
             (sqrt(v / (1 - b2^k)) + eps) + lr wd x_t,   P_k = mu_1 ... mu_k
+    "adan"  (Xie et al., Adan, with the betas as averaging weights, (0.98, 0.92, 0.99) in its defaults):
+            diff = g - g_prev (0 at the first update), g_prev the clipped gradient of the previous update,
+            m <- b1 m + (1 - b1) g ;  d <- b2 d + (1 - b2) diff ;  n <- b3 n + (1 - b3) (g + b2 diff)^2
+            u = lr ((m / (1 - b1^k) + b2 d / (1 - b2^k)) / (sqrt(n / (1 - b3^k)) + eps) + wd x_t)
+            (n is kept in the v slot; d and g_prev are Adan's two extra state vectors; the decay is the
+            decoupled one on x_t, as for the other rules)
 and SAPipe weight prediction with the updated optimizer state (App. B.1, predict = "updated", AdamW):
 the master follows the standard delayed update x_{t+1} = x_t - u_{t-1}(g_{t-1}), while the next
 forward/backward runs at x~_{t+1} = x_{t+1} - u_t(g_{t-1}), the AdamW step from the state after the
@@ -89,6 +95,7 @@ class HParams:
     update_rms: float = 0.2      # Muon update RMS
     ns_steps: int = 5            # Newton-Schulz iterations
     nadam_psi: float = 0.004     # NAdam momentum decay
+    beta3: float = 0.99          # Adan: weight of the second-moment average
     predict: str = "none"        # "updated": SAPipe-WP with the updated optimizer state (AdamW)
 
 
@@ -155,6 +162,20 @@ def nadam_u(x, g, m, v, k: int, hp: "HParams"):
     return u, m1, v1
 
 
+def adan_u(x, g, m, n, d, g_prev, k: int, hp: "HParams"):
+    """One Adan evaluation (k-th update) on already-clipped g.  g_prev is the clipped gradient of the
+    previous update (ignored at k = 1, where the difference is zero).  Returns (u, m, n, d, g)."""
+    diff = np.zeros_like(g) if k == 1 else g - g_prev
+    m1 = hp.beta1 * m + (1.0 - hp.beta1) * g
+    d1 = hp.beta2 * d + (1.0 - hp.beta2) * diff
+    q = g + hp.beta2 * diff
+    n1 = hp.beta3 * n + (1.0 - hp.beta3) * q * q
+    denom = np.sqrt(n1 / (1.0 - hp.beta3 ** k)) + hp.eps
+    u = hp.lr * ((m1 / (1.0 - hp.beta1 ** k) + hp.beta2 * d1 / (1.0 - hp.beta2 ** k)) / denom
+                 + hp.weight_decay * x)
+    return u, m1, n1, d1, g.copy()
+
+
 def global_norm(grads: Dict[str, np.ndarray]) -> float:
     """||g||_2 over every tensor of the stage, accumulated in float64."""
     return math.sqrt(sum(float(np.sum(np.square(g.astype(np.float64)))) for g in grads.values()))
@@ -198,6 +219,8 @@ class OptState:
     x_compute: Optional[Dict[str, np.ndarray]] = None  # predict: the weights the next forward uses
     u_ring: List[Dict[str, np.ndarray]] = field(default_factory=list)  # delay >= 2: the last tau updates, oldest first
     n_skipped: int = 0                      # gradients skipped for a non-finite norm
+    adan_d: Optional[Dict[str, np.ndarray]] = None      # Adan: average of gradient differences
+    adan_gprev: Optional[Dict[str, np.ndarray]] = None  # Adan: clipped gradient of the previous update
 
     @staticmethod
     def create(x: Dict[str, np.ndarray], dt=np.float64) -> "OptState":
@@ -211,7 +234,8 @@ class OptState:
         return OptState(x=cp(self.x), m=cp(self.m), v=cp(self.v), u_prev=cp(self.u_prev),
                         pending=cp(self.pending), n_updates=self.n_updates, t=self.t,
                         queue=[cp(g) for g in self.queue], x_compute=cp(self.x_compute),
-                        u_ring=[cp(u) for u in self.u_ring], n_skipped=self.n_skipped)
+                        u_ring=[cp(u) for u in self.u_ring], n_skipped=self.n_skipped,
+                        adan_d=cp(self.adan_d), adan_gprev=cp(self.adan_gprev))
 
 
 def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> dict:
@@ -222,8 +246,8 @@ def iteration_update(st: OptState, g_t: Dict[str, np.ndarray], hp: HParams) -> d
         raise ValueError("delay must be >= 0")
     if hp.delay == 0 and hp.ef_lambda != 0.0:
         raise ValueError("Error Feedback needs a delayed gradient (delay >= 1)")
-    if hp.optimizer not in ("adamw", "muon", "lion", "nadam"):
-        raise ValueError("optimizer must be adamw, muon, lion or nadam")
+    if hp.optimizer not in ("adamw", "muon", "lion", "nadam", "adan"):
+        raise ValueError("optimizer must be adamw, muon, lion, nadam or adan")
     if hp.predict not in ("none", "updated"):
         raise ValueError("predict must be none or updated")
     if hp.predict == "updated" and (hp.optimizer != "adamw" or hp.ef_lambda != 0.0 or hp.delay != 1):
@@ -270,6 +294,12 @@ def _u_of(st: OptState, name: str, g, k: int, hp: HParams):
         u, st.m[name] = lion_u(st.x[name], g, st.m[name], hp)
     elif hp.optimizer == "nadam":
         u, st.m[name], st.v[name] = nadam_u(st.x[name], g, st.m[name], st.v[name], k, hp)
+    elif hp.optimizer == "adan":
+        if st.adan_d is None:
+            st.adan_d = {n: np.zeros_like(a) for n, a in st.x.items()}
+            st.adan_gprev = {n: np.zeros_like(a) for n, a in st.x.items()}
+        u, st.m[name], st.v[name], st.adan_d[name], st.adan_gprev[name] = adan_u(
+            st.x[name], g, st.m[name], st.v[name], st.adan_d[name], st.adan_gprev[name], k, hp)
     else:
         u, st.m[name], st.v[name] = adamw_u(st.x[name], g, st.m[name], st.v[name], k, hp)
     return u

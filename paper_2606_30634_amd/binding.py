@@ -17,7 +17,8 @@ EXPORTS = ["stage_required_bytes", "stage_init", "stage_num_tensors", "stage_ten
            "stage_tensor_by_name", "stage_sync_weights", "stage_forward", "stage_backward",
            "delayed_update", "delayed_update_flat", "stage_embed_indices", "stage_poll_nonfinite",
            "stage_grad_norm", "stage_profile_enable", "stage_profile_read", "stage_last_error",
-           "stage_destroy", "stage_set_update_overlap", "stage_join_update", "stage_resume"]
+           "stage_destroy", "stage_set_update_overlap", "stage_join_update", "stage_resume",
+           "grad_norm_flat_workspace_bytes", "grad_norm_flat", "hbm_stream_copy", "delayed_update_flat_adan"]
 PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_UPDATE, PROF_NORM, PROF_OTHER, PROF_NS = range(7)
 
 
@@ -34,7 +35,7 @@ class UpdateHParams(C.Structure):
                                          "ef_lambda")] + [("delay", C.c_int32), ("optimizer", C.c_int32),
                                                           ("momentum", C.c_float), ("update_rms", C.c_float),
                                                           ("ns_steps", C.c_int32), ("predict", C.c_int32),
-                                                          ("nadam_psi", C.c_float)]
+                                                          ("nadam_psi", C.c_float), ("beta3", C.c_float)]
 
 
 class StageError(RuntimeError):
@@ -71,6 +72,11 @@ def _load():
         "stage_set_update_overlap": (C.c_int, [vp, i32]),
         "stage_join_update": (C.c_int, [vp]),
         "stage_resume": (C.c_int, [vp, i64, i32]),
+        "grad_norm_flat_workspace_bytes": (sz, []),
+        "grad_norm_flat": (C.c_int, [i64, vp, i32, C.c_float, vp, vp, vp, sz, vp]),
+        "hbm_stream_copy": (C.c_int, [vp, vp, sz, vp]),
+        "delayed_update_flat_adan": (C.c_int, [i64, vp, vp, i32, vp, vp, vp, vp, vp, vp, i32, i64,
+                                               C.POINTER(UpdateHParams), vp, vp]),
         "stage_profile_read": (C.c_int, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
         "stage_last_error": (C.c_char_p, []),
         "stage_destroy": (None, [vp]),
@@ -148,6 +154,25 @@ def delayed_update_flat(n, x, g_prev, g_is_bf16, m, v, u_prev, x_shadow, shadow_
                         hp: UpdateHParams, clip_scale_dev, stream) -> None:
     _call("delayed_update_flat", n, x, g_prev, int(g_is_bf16), m, v, u_prev, x_shadow,
           int(shadow_is_bf16), t, C.byref(hp), clip_scale_dev, stream)
+
+
+def delayed_update_flat_adan(n, x, g_prev, g_is_bf16, m, v, d, g_last, u_prev, x_shadow, shadow_is_bf16, t,
+                             hp: UpdateHParams, clip_scale_dev, stream) -> None:
+    _call("delayed_update_flat_adan", n, x, g_prev, int(g_is_bf16), m, v, d, g_last, u_prev, x_shadow,
+          int(shadow_is_bf16), t, C.byref(hp), clip_scale_dev, stream)
+
+
+def grad_norm_flat_workspace_bytes() -> int:
+    return LIB.grad_norm_flat_workspace_bytes()
+
+
+def grad_norm_flat(n, g, g_is_bf16, clip_norm, out_dev, nonfinite_dev, workspace, workspace_bytes, stream) -> None:
+    _call("grad_norm_flat", n, g, int(g_is_bf16), clip_norm, out_dev, nonfinite_dev, workspace,
+          workspace_bytes, stream)
+
+
+def hbm_stream_copy(dst, src, nbytes, stream) -> None:
+    _call("hbm_stream_copy", dst, src, nbytes, stream)
 
 
 def stage_embed_indices(s: int, slot: int, ids, counts, n_unique) -> None:

@@ -5,7 +5,7 @@
 
 // ------------------------------------------------------------------ update (update.hip)
 // Elementwise update rules of the fused pass (UpdateScalars::opt)
-enum { UPD_ADAMW = 0, UPD_LION = 2, UPD_NADAM = 3, UPD_ADAMW_PREDICT = 4 };
+enum { UPD_ADAMW = 0, UPD_LION = 2, UPD_NADAM = 3, UPD_ADAMW_PREDICT = 4, UPD_ADAN = 5 };
 struct UpdateScalars {
   float lr, b1, b2, omb1, omb2, bc1, bc2, eps, wd, lam, one_plus_lam;
   int ef;     // 1: Error-Feedback form this call
@@ -13,6 +13,8 @@ struct UpdateScalars {
   int opt = UPD_ADAMW;
   float cg = 0.f, cm = 0.f;      // NAdam: lr (1 - mu_k) / (1 - P_k), lr mu_{k+1} / (1 - P_k mu_{k+1})
   float bc1n = 1.f, bc2n = 1.f;  // prediction: bias corrections of update k + 1
+  float b3 = 0.f, omb3 = 0.f, bc3 = 1.f;  // Adan: second-moment weight and its bias correction
+  int first = 0;                          // Adan: the first update (the gradient difference is 0)
 };
 size_t norm_scratch_bytes();
 // blocks: partial sums (and blocks of the first pass), at most norm_scratch_bytes() / 8; <= 0
@@ -24,8 +26,14 @@ void launch_grad_norm(const void* g, bool g_bf16, int64_t n, float clip, double*
 void launch_fused_update(int64_t n, float* x, const void* g, bool g_bf16, float* m, float* v,
                          float* up, void* shadow, int shadow_kind, const UpdateScalars& hs,
                          const float* clip, const int* flag, int blocks, hipStream_t st);
+// Adan (UPD_ADAN): x, m, n (the v slot), d, g_last, u_prev fp32; blocks as launch_fused_update
+void launch_fused_update_adan(int64_t n, float* x, const void* g, bool g_bf16, float* m, float* nn, float* d,
+                              float* g_last, float* up, void* shadow, int shadow_kind, const UpdateScalars& hs,
+                              const float* clip, const int* flag, int blocks, hipStream_t st);
 void launch_cast_copy(int64_t n, const float* src, void* dst, bool dst_bf16, hipStream_t st);
 void launch_zero(void* p, int64_t bytes, hipStream_t st);
+// bytes a multiple of 16, both pointers 16-byte aligned
+void launch_stream_copy(void* dst, const void* src, int64_t bytes, hipStream_t st);
 
 // compute units of the current device (gemm_mfma.hip; cached per device)
 int device_cu_count();

@@ -97,6 +97,9 @@ struct stage {
   // buffers (iteration t of a delay-tau run uses u_ring[t mod tau]; u_prev = u_ring[0])
   int ndelay = 1, ng = 2;
   float *master, *m, *v, *u_prev, *grad[STAGE_MAX_DELAY + 1], *u_ring[STAGE_MAX_DELAY];
+  // Adan's extra state (shapes with optimizer 2): the average of gradient differences and the
+  // clipped gradient of the previous update
+  float *adan_d = nullptr, *adan_gl = nullptr;
   void* ver[2];
   // scratch
   void *dA, *dB, *dh, *dn, *dgu, *do_, *dqkv, *dlog, *dhf;
@@ -230,7 +233,7 @@ int validate(const stage_shape_t* s) {
   if (s->d_model % 64 || s->d_ffn % 64) return fail(STAGE_EINVAL, "d_model, d_ffn must be multiples of 64");
   if (s->d_model > 4096) return fail(STAGE_EINVAL, "d_model > 4096 not supported");
   if (s->dtype != 0 && s->dtype != 1) return fail(STAGE_EINVAL, "dtype must be 0 (fp32) or 1 (bf16)");
-  if (s->optimizer != 0 && s->optimizer != 1) return fail(STAGE_EINVAL, "optimizer must be 0 or 1");
+  if (s->optimizer < 0 || s->optimizer > 2) return fail(STAGE_EINVAL, "optimizer must be 0, 1 (Muon workspace) or 2 (Adan state)");
   if (s->max_delay < 0 || s->max_delay > STAGE_MAX_DELAY)
     return fail(STAGE_EINVAL, "max_delay must be in [0, " + std::to_string(STAGE_MAX_DELAY) + "]");
   if (s->vocab < 0 || s->vocab >= (1 << 20)) return fail(STAGE_EINVAL, "vocab out of range [0, 2^20)");
@@ -285,6 +288,8 @@ size_t layout(stage* S, char* base) {
   for (int j = 0; j < S->ng; ++j) S->grad[j] = (float*)carve(n * 4);
   S->ver[0] = carve(n * esz);
   S->ver[1] = carve(n * esz);
+  S->adan_d = sh.optimizer == 2 ? (float*)carve(n * 4) : nullptr;
+  S->adan_gl = sh.optimizer == 2 ? (float*)carve(n * 4) : nullptr;
   // activation slots
   S->slots.assign(sh.max_inflight, Slot());
   for (auto& sl : S->slots) {
@@ -444,6 +449,10 @@ void register_tensors(stage* S) {
                        {"v.", S->v, 4, STAGE_DT_F32},    {"u_prev.", S->u_prev, 4, STAGE_DT_F32}};
   for (int j = 1; j < S->ndelay; ++j) vs.push_back({"u_prev" + std::to_string(j) + ".", S->u_ring[j], 4, STAGE_DT_F32});
   for (int j = 0; j < S->ng; ++j) vs.push_back({"grad" + std::to_string(j) + ".", S->grad[j], 4, STAGE_DT_F32});
+  if (S->adan_d) {
+    vs.push_back({"adan_d.", S->adan_d, 4, STAGE_DT_F32});
+    vs.push_back({"adan_gprev.", S->adan_gl, 4, STAGE_DT_F32});
+  }
   vs.push_back({"w0.", S->ver[0], S->esz, cdt});
   vs.push_back({"w1.", S->ver[1], S->esz, cdt});
   for (const auto& vv : vs)
@@ -852,8 +861,14 @@ UpdateScalars update_scalars(const update_hparams_t* hp, int64_t k, bool apply, 
   hs.one_plus_lam = 1.0f + hp->ef_lambda;
   hs.ef = ef ? 1 : 0;
   hs.apply = apply ? 1 : 0;
-  hs.opt = hp->optimizer == 2 ? UPD_LION : hp->optimizer == 3 ? UPD_NADAM
+  hs.opt = hp->optimizer == 2 ? UPD_LION : hp->optimizer == 3 ? UPD_NADAM : hp->optimizer == 4 ? UPD_ADAN
            : hp->predict ? UPD_ADAMW_PREDICT : UPD_ADAMW;
+  if (hs.opt == UPD_ADAN) {
+    hs.b3 = hp->beta3;
+    hs.omb3 = 1.0f - hp->beta3;
+    hs.bc3 = apply ? (float)(1.0 - std::pow((double)hp->beta3, kk)) : 1.f;
+    hs.first = k == 1 ? 1 : 0;
+  }
   if (apply && hs.opt == UPD_NADAM) {
     auto mu = [&](int64_t j) { return (double)hp->beta1 * (1.0 - 0.5 * std::pow(0.96, (double)j * hp->nadam_psi)); };
     double prod = 1.0;
@@ -871,8 +886,8 @@ UpdateScalars update_scalars(const update_hparams_t* hp, int64_t k, bool apply, 
 
 // Hyper-parameter checks shared by the stage and the flat update.
 int check_update_hparams(const update_hparams_t* hp) {
-  if (hp->optimizer < 0 || hp->optimizer > 3)
-    return fail(STAGE_EINVAL, "optimizer must be 0 (AdamW), 1 (Muon), 2 (Lion) or 3 (NAdam)");
+  if (hp->optimizer < 0 || hp->optimizer > 4)
+    return fail(STAGE_EINVAL, "optimizer must be 0 (AdamW), 1 (Muon), 2 (Lion), 3 (NAdam) or 4 (Adan)");
   if (hp->predict != 0 && hp->predict != 1) return fail(STAGE_EINVAL, "predict must be 0 or 1");
   if (hp->predict && (hp->optimizer != 0 || hp->ef_lambda != 0.f || hp->delay != 1))
     return fail(STAGE_EINVAL, "weight prediction (predict 1) needs AdamW, delay 1 and ef_lambda 0");
@@ -887,6 +902,8 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   if (int rc = check_update_hparams(hp)) return rc;
   if (hp->optimizer == 1 && s->sh.optimizer != 1)
     return fail(STAGE_EINVAL, "Muon needs a stage shaped with optimizer = 1 (its Newton-Schulz workspace)");
+  if (hp->optimizer == 4 && s->sh.optimizer != 2)
+    return fail(STAGE_EINVAL, "Adan needs a stage shaped with optimizer = 2 (its two extra state vectors)");
   if (hp->optimizer == 1 && (hp->ns_steps < 1 || hp->ns_steps > 32))
     return fail(STAGE_EINVAL, "ns_steps must be in [1, 32]");
   if (t != s->next_t) return fail(STAGE_ESTATE, "delayed_update: expected t = " + std::to_string(s->next_t));
@@ -1048,6 +1065,14 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
       launch_muon_apply(s->bf, s->muon_tab, nmat, s->muon_ntile, s->bf ? 0 : hp->ns_steps % 2, s->master, up, s->ver[vout],
                         flag, hp->lr, hp->weight_decay, hp->update_rms, ef, hp->ef_lambda, us);
     }, us);
+  } else if (hs.opt == UPD_ADAN) {
+    // x, m, n, d, g_last r+w; g read; the copy written; u_prev r+w with EF
+    const double ab = apply ? 40.0 + 4.0 + (s->bf ? 2.0 : 4.0) + (hp->ef_lambda != 0.f ? 8.0 : 0.0)
+                            : (4.0 + (s->bf ? 2.0 : 4.0));
+    timed(s, STAGE_PROF_UPDATE, ab * s->n_flat, [&] {
+      launch_fused_update_adan(s->n_flat, s->master, s->grad[gb], false, s->m, s->v, s->adan_d, s->adan_gl, up,
+                               s->ver[vout], s->bf ? 2 : 1, hs, clip, flag, device_cu_count(), us);
+    }, us);
   } else {
     timed(s, STAGE_PROF_UPDATE, ub * s->n_flat, [&] {
       launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v, up, s->ver[vout],
@@ -1085,6 +1110,7 @@ int delayed_update_flat(int64_t n, float* x, const void* g_prev, int32_t g_is_bf
   if (hp->delay < 1) return fail(STAGE_EINVAL, "delayed_update_flat implements a delay >= 1");
   if (int rc = check_update_hparams(hp)) return rc;
   if (hp->optimizer == 1) return fail(STAGE_EINVAL, "delayed_update_flat implements the elementwise rules (not Muon)");
+  if (hp->optimizer == 4) return fail(STAGE_EINVAL, "Adan keeps two more state vectors: delayed_update_flat_adan");
   if (hp->predict && !x_shadow) return fail(STAGE_EINVAL, "weight prediction writes the compute copy: x_shadow needed");
   if (n == 0) return STAGE_OK;
   if (!x || !g_prev || !m || !v) return fail(STAGE_EINVAL, "null vector");
@@ -1125,6 +1151,53 @@ int stage_resume(stage_t* s, int64_t next_t, int32_t delay) {
   s->next_t = next_t;
   s->n_updates = delay == 0 ? next_t : std::max<int64_t>(0, next_t - delay);  // gradients consumed so far
   return stage_sync_weights(s);
+}
+
+size_t grad_norm_flat_workspace_bytes(void) { return norm_scratch_bytes(); }
+
+int grad_norm_flat(int64_t n, const void* g, int32_t g_is_bf16, float clip_norm, float* out_dev,
+                   int32_t* nonfinite_dev, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  if (n < 0 || !out_dev) return fail(STAGE_EINVAL, "bad argument");
+  if (n > 0 && !g) return fail(STAGE_EINVAL, "null gradient");
+  if (!workspace || workspace_bytes < norm_scratch_bytes() || (uintptr_t)workspace % 8)
+    return fail(STAGE_EINVAL, "workspace must hold grad_norm_flat_workspace_bytes() bytes, 8-byte aligned");
+  if ((uintptr_t)g % (g_is_bf16 ? 8 : 16) || (uintptr_t)out_dev % 4)
+    return fail(STAGE_EINVAL, "g must be 16-byte (bf16: 8-byte) aligned");
+  launch_grad_norm(g, g_is_bf16 != 0, n, clip_norm, (double*)workspace, out_dev, (int*)nonfinite_dev, nullptr,
+                   device_cu_count(), (hipStream_t)hip_stream);
+  HIP_OK(hipGetLastError());
+  return STAGE_OK;
+}
+
+int hbm_stream_copy(void* dst, const void* src, size_t bytes, void* hip_stream) {
+  if (bytes % 16 || (uintptr_t)dst % 16 || (uintptr_t)src % 16 || (bytes && (!dst || !src)))
+    return fail(STAGE_EINVAL, "hbm_stream_copy: 16-byte aligned pointers and a multiple of 16 bytes");
+  launch_stream_copy(dst, src, (int64_t)bytes, (hipStream_t)hip_stream);
+  HIP_OK(hipGetLastError());
+  return STAGE_OK;
+}
+
+int delayed_update_flat_adan(int64_t n, float* x, const void* g_prev, int32_t g_is_bf16, float* m, float* v,
+                             float* d, float* g_last, float* u_prev, void* x_shadow, int32_t shadow_is_bf16,
+                             int64_t t, const update_hparams_t* hp, const float* clip_scale_dev, void* hip_stream) {
+  if (!hp || n < 0 || t < 0) return fail(STAGE_EINVAL, "bad argument");
+  if (hp->optimizer != 4) return fail(STAGE_EINVAL, "delayed_update_flat_adan needs optimizer 4 (Adan)");
+  if (hp->delay < 1) return fail(STAGE_EINVAL, "delayed_update_flat_adan implements a delay >= 1");
+  if (hp->predict) return fail(STAGE_EINVAL, "weight prediction is defined for AdamW only");
+  if (n == 0) return STAGE_OK;
+  if (!x || !g_prev || !m || !v || !d || !g_last) return fail(STAGE_EINVAL, "null vector");
+  if (hp->ef_lambda != 0.f && !u_prev) return fail(STAGE_EINVAL, "Error Feedback needs u_prev");
+  if (((uintptr_t)x | (uintptr_t)m | (uintptr_t)v | (uintptr_t)d | (uintptr_t)g_last | (uintptr_t)u_prev |
+       (uintptr_t)x_shadow) % 16 || (uintptr_t)g_prev % 8)
+    return fail(STAGE_EINVAL, "vectors must be 16-byte aligned (g_prev 8-byte)");
+  const int64_t tau = hp->delay;
+  const bool apply = t >= tau;
+  const UpdateScalars hs = update_scalars(hp, t - tau + 1, apply, hp->ef_lambda != 0.f && t >= 2 * tau);
+  launch_fused_update_adan(n, x, g_prev, g_is_bf16 != 0, m, v, d, g_last, hp->ef_lambda != 0.f ? u_prev : nullptr,
+                           x_shadow, x_shadow ? (shadow_is_bf16 ? 2 : 1) : 0, hs, clip_scale_dev, nullptr, 0,
+                           (hipStream_t)hip_stream);
+  HIP_OK(hipGetLastError());
+  return STAGE_OK;
 }
 
 int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts, int32_t* n_unique) {

@@ -218,6 +218,79 @@ __global__ void __launch_bounds__(256) fused_update_resident(int64_t n, float* _
   }
 }
 
+// Adan (Xie et al.) as the update function, one element group of 4: the clipped gradient gg, its
+// difference from the clipped gradient of the previous update (0 at the first), the three averages
+// m (gradient), d (differences), n (squared gg + b2 diff), then
+//   u = lr ((m / bc1 + b2 d / bc2) / (sqrt(n / bc3) + eps) + wd x_t)
+// and the standard or Error-Feedback step; g_last receives gg.  52 bytes per element with a bf16
+// gradient and copy: x, m, n, d, g_last, u_prev read and written, g read, the copy written.
+template <typename G, typename S, bool EF>
+__device__ __forceinline__ void adan_group(int64_t n, int64_t i, float* __restrict__ x, const G* __restrict__ g,
+                                           float* __restrict__ m, float* __restrict__ nn, float* __restrict__ d,
+                                           float* __restrict__ gl, float* __restrict__ up, S* __restrict__ shadow,
+                                           const UpdateScalars& hs, float c, bool skip) {
+  if (i >= n) return;
+  auto elem = [&](float gg, float& xv, float& mv, float& nv, float& dv, float& gv, float& uv) {
+    const float diff = hs.first ? 0.f : gg - gv;
+    mv = hs.b1 * mv + hs.omb1 * gg;
+    dv = hs.b2 * dv + hs.omb2 * diff;
+    const float q = gg + hs.b2 * diff;
+    nv = hs.b3 * nv + hs.omb3 * (q * q);
+    const float u = hs.lr * ((mv / hs.bc1 + hs.b2 * dv / hs.bc2) / (sqrtf(nv / hs.bc3) + hs.eps) + hs.wd * xv);
+    xv = (EF && hs.ef) ? xv - hs.one_plus_lam * u + hs.lam * uv : xv - u;
+    gv = gg;
+    uv = u;
+  };
+  if (i + 3 < n) {
+    float xr[4];
+    load4<float>(x, i, xr);
+    if (!skip) {
+      float gr[4], mr[4], nr[4], dr[4], lr[4], ur[4] = {0.f, 0.f, 0.f, 0.f};
+      load4<G>(g, i, gr);
+      load4<float>(m, i, mr);
+      load4<float>(nn, i, nr);
+      load4<float>(d, i, dr);
+      load4<float>(gl, i, lr);
+      if (EF) load4<float>(up, i, ur);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) elem(gr[j] * c, xr[j], mr[j], nr[j], dr[j], lr[j], ur[j]);
+      store4<float>(x, i, xr);
+      store4<float>(m, i, mr);
+      store4<float>(nn, i, nr);
+      store4<float>(d, i, dr);
+      store4<float>(gl, i, lr);
+      if (EF) store4<float>(up, i, ur);
+    }
+    if (shadow) store4<S>(shadow, i, xr);
+  } else {
+    for (int64_t k = i; k < n; ++k) {  // ragged tail
+      float xv = x[k];
+      if (!skip) {
+        float mv = m[k], nv = nn[k], dv = d[k], gv = gl[k], uv = EF ? up[k] : 0.f;
+        elem(to_f32(g[k]) * c, xv, mv, nv, dv, gv, uv);
+        x[k] = xv; m[k] = mv; nn[k] = nv; d[k] = dv; gl[k] = gv;
+        if (EF) up[k] = uv;
+      }
+      if (shadow) shadow[k] = from_f32<S>(xv);
+    }
+  }
+}
+
+// Grid-stride pass: a resident grid (blocks > 0 at launch) or one group of 4 elements per thread.
+template <typename G, typename S, bool EF>
+__global__ void __launch_bounds__(256) fused_update_adan(int64_t n, float* __restrict__ x, const G* __restrict__ g,
+                                                         float* __restrict__ m, float* __restrict__ nn,
+                                                         float* __restrict__ d, float* __restrict__ gl,
+                                                         float* __restrict__ up, S* __restrict__ shadow,
+                                                         UpdateScalars hs, const float* __restrict__ clip,
+                                                         const int* __restrict__ skip_flag) {
+  const bool skip = hs.apply == 0 || (skip_flag && skip_flag[0] != 0);
+  const float c = clip ? clip[0] : 1.0f;
+  const int64_t groups = (n + 3) / 4, stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups; q += stride)
+    adan_group<G, S, EF>(n, 4 * q, x, g, m, nn, d, gl, up, shadow, hs, c, skip);
+}
+
 template <typename S>
 __global__ void __launch_bounds__(256) cast_copy(int64_t n, const float* __restrict__ src,
                                                  S* __restrict__ dst) {
@@ -228,6 +301,24 @@ __global__ void __launch_bounds__(256) cast_copy(int64_t n, const float* __restr
     store4<S>(dst, i, r);
   } else {
     for (int64_t k = i; k < n; ++k) dst[k] = from_f32<S>(src[k]);
+  }
+}
+
+// Streaming copy of n16 16-byte chunks, four per thread in flight (one block-width apart), with
+// non-temporal loads and stores: the practical HBM ceiling the update pass is compared against.
+__global__ void __launch_bounds__(256) stream_copy(int64_t n16, const u32x4* __restrict__ src,
+                                                   u32x4* __restrict__ dst) {
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x * 4 + threadIdx.x;
+  u32x4 r[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t i = i0 + (int64_t)k * blockDim.x;
+    if (i < n16) r[k] = __builtin_nontemporal_load(src + i);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int64_t i = i0 + (int64_t)k * blockDim.x;
+    if (i < n16) __builtin_nontemporal_store(r[k], dst + i);
   }
 }
 
@@ -298,10 +389,34 @@ void launch_fused_update(int64_t n, float* x, const void* g, bool g_bf16, float*
 #undef UPD
 }
 
+void launch_fused_update_adan(int64_t n, float* x, const void* g, bool g_bf16, float* m, float* nn, float* d,
+                              float* g_last, float* up, void* shadow, int shadow_kind, const UpdateScalars& hs,
+                              const float* clip, const int* flag, int blocks, hipStream_t st) {
+  const int64_t groups = cdiv(n, 4);
+  const unsigned grid = (unsigned)(blocks > 0 && groups > (int64_t)blocks * 256 ? blocks : cdiv(groups, 256));
+  const bool ef = up != nullptr;
+#define ADAN(G, S, E) \
+  fused_update_adan<G, S, E><<<grid, 256, 0, st>>>(n, x, (const G*)g, m, nn, d, g_last, up, (S*)shadow, hs, clip, flag)
+  if (g_bf16) {
+    if (shadow_kind == 2) { if (ef) ADAN(bf16, bf16, true); else ADAN(bf16, bf16, false); }
+    else { if (ef) ADAN(bf16, float, true); else ADAN(bf16, float, false); }
+  } else {
+    if (shadow_kind == 2) { if (ef) ADAN(float, bf16, true); else ADAN(float, bf16, false); }
+    else { if (ef) ADAN(float, float, true); else ADAN(float, float, false); }
+  }
+#undef ADAN
+}
+
 void launch_cast_copy(int64_t n, const float* src, void* dst, bool dst_bf16, hipStream_t st) {
   const dim3 grid((unsigned)cdiv(cdiv(n, 4), 256));
   if (dst_bf16) cast_copy<bf16><<<grid, 256, 0, st>>>(n, src, (bf16*)dst);
   else cast_copy<float><<<grid, 256, 0, st>>>(n, src, (float*)dst);
+}
+
+void launch_stream_copy(void* dst, const void* src, int64_t bytes, hipStream_t st) {
+  const int64_t n16 = bytes / 16;
+  if (n16 == 0) return;
+  stream_copy<<<(unsigned)cdiv(n16, 256 * 4), 256, 0, st>>>(n16, (const u32x4*)src, (u32x4*)dst);
 }
 
 void launch_zero(void* p, int64_t bytes, hipStream_t st) {

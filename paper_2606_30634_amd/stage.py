@@ -16,19 +16,22 @@ _ESZ = {B.DT_F32: 4, B.DT_BF16: 2, B.DT_I32: 4}
 
 def make_shape(n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab, first_stage,
                last_stage, tie_embedding, seq_len, micro_batch, max_inflight=1, bf16=True,
-               rms_eps=1e-5, rope_theta=10000.0, muon=False, max_delay=1) -> B.StageShape:
+               rms_eps=1e-5, rope_theta=10000.0, muon=False, max_delay=1, adan=False) -> B.StageShape:
+    if muon and adan:
+        raise ValueError("a stage holds the Muon workspace or the Adan state, not both")
     return B.StageShape(n_blocks, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab,
                         int(first_stage), int(last_stage), int(tie_embedding), seq_len, micro_batch,
-                        max_inflight, 1 if bf16 else 0, rms_eps, rope_theta, 1 if muon else 0, max_delay)
+                        max_inflight, 1 if bf16 else 0, rms_eps, rope_theta, 1 if muon else (2 if adan else 0),
+                        max_delay)
 
 
 def hparams(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1, clip_norm=1.0,
             ef_lambda=1.0, delay=1, optimizer="adamw", momentum=0.95, update_rms=0.2,
-            ns_steps=5, predict="none", nadam_psi=0.004) -> B.UpdateHParams:
-    opt = {"adamw": 0, "muon": 1, "lion": 2, "nadam": 3}[optimizer]
+            ns_steps=5, predict="none", nadam_psi=0.004, beta3=0.99) -> B.UpdateHParams:
+    opt = {"adamw": 0, "muon": 1, "lion": 2, "nadam": 3, "adan": 4}[optimizer]
     pred = {"none": 0, "updated": 1}[predict]
     return B.UpdateHParams(lr, beta1, beta2, eps, weight_decay, clip_norm, ef_lambda, delay, opt,
-                           momentum, update_rms, ns_steps, pred, nadam_psi)
+                           momentum, update_rms, ns_steps, pred, nadam_psi, beta3)
 
 
 class Stage:

@@ -23,12 +23,12 @@ def rel(a, b) -> float:
     return float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-30))
 
 
-def shape_of(w, muon=False, max_delay=1):
+def shape_of(w, muon=False, max_delay=1, adan=False):
     from paper_2606_30634_amd.stage import make_shape
     return make_shape(w.n_blocks, w.d_model, w.n_heads, w.n_kv_heads, w.head_dim, w.d_ffn, w.vocab,
                       w.first_stage, w.last_stage, w.tie_embedding, w.seq_len, w.micro_batch,
                       w.max_inflight, bf16=(w.dtype == "bf16"), rms_eps=w.rms_eps,
-                      rope_theta=w.rope_theta, muon=muon, max_delay=max_delay)
+                      rope_theta=w.rope_theta, muon=muon, max_delay=max_delay, adan=adan)
 
 
 def hp_of(w, **kw):
@@ -82,7 +82,7 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     dev = torch.device(device)
     tau = max(hp.delay, 1)
     ng = tau + 1
-    st = Stage(shape_of(w, muon=muon or hp.optimizer == 1, max_delay=tau), device)
+    st = Stage(shape_of(w, muon=muon or hp.optimizer == 1, max_delay=tau, adan=hp.optimizer == 4), device)
     st.load_master(params0)
     if early_update:
         st.set_update_overlap(True)

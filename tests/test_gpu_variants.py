@@ -1,5 +1,5 @@
-"""GPU parity of the elementwise update variants against the oracle, through the C ABI: Lion and
-NAdam as the update function, and SAPipe weight prediction with the updated optimizer state (the
+"""GPU parity of the elementwise update variants against the oracle, through the C ABI: Lion,
+NAdam and Adan as the update function, and SAPipe weight prediction with the updated optimizer state (the
 compute copy receives x_{t+1} - u_t(g_{t-1})).  The fused flat update on 1,000,003 elements
 (ragged tail) at 1e-5 of the oracle's float64 rule; whole stages free-running at the usual bars
 (fp32 1e-4, bf16 2e-2 with m, v at 5e-2).
@@ -25,6 +25,9 @@ LION = dict(optimizer="lion", lr=5e-4, beta1=0.9, beta2=0.99, weight_decay=0.5)
 # 1 - beta2 alone differs by 1.3e-5 relative at beta2 = 0.999
 NADAM = dict(optimizer="nadam", beta1=float(np.float32(0.9)), beta2=float(np.float32(0.999)))
 PREDICT = dict(predict="updated", ef_lambda=0.0)
+# Adan with the betas of its authors' defaults (beta1 = 0.98 is the value the paper quotes), fp32-exact
+ADAN = dict(optimizer="adan", beta1=float(np.float32(0.98)), beta2=float(np.float32(0.92)),
+            beta3=float(np.float32(0.99)))
 
 
 def _lion_check(x0, m0, g, u_prev0, x1, m1, u1, hp, c=1.0, ef=False):
@@ -141,10 +144,10 @@ def _compare(w, g, o, tol, state_tol, label, compare_v=True):
         f"{k}={e:.2e}" for k, e in sorted(bad.items(), key=lambda kv: -kv[1])[:12])
 
 
-@pytest.mark.parametrize("kind", ["nadam", "predict"])
+@pytest.mark.parametrize("kind", ["nadam", "predict", "adan"])
 def test_variant_tiny_fp32(kind):
     w = datagen.TINY
-    kw = {"nadam": NADAM, "predict": PREDICT}[kind]
+    kw = {"nadam": NADAM, "predict": PREDICT, "adan": ADAN}[kind]
     p0 = datagen.init_params(w)
     steps = 12
     log(f"{kind} tiny fp32: {steps} steps")
@@ -184,13 +187,46 @@ def test_lion_tiny_fp32():
     assert max(errs.values()) <= 1e-4, {k: v for k, v in errs.items() if v > 1e-4}
 
 
-@pytest.mark.parametrize("kind", ["nadam", "predict"])
+@pytest.mark.parametrize("kind", ["nadam", "predict", "adan"])
 def test_variant_reduced_bf16(kind):
     w = SMALL_R
-    kw = {"nadam": NADAM, "predict": PREDICT}[kind]
+    kw = {"nadam": NADAM, "predict": PREDICT, "adan": ADAN}[kind]
     p0 = datagen.init_params(w)
     steps = 8
     log(f"{kind} {w.name}: {steps} steps")
     g = run_gpu(w, steps, hp_of(w, **kw), p0)
     o = run_oracle(w, steps, oracle.hparams_of(w, **kw), p0)
     _compare(w, g, o, 2e-2, 5e-2, f"{kind} {w.name}")
+
+
+@pytest.mark.parametrize("lam", [0.0, 1.0])
+def test_flat_update_adan(lam):
+    """delayed_update_flat_adan on 1,000,003 elements over 8 iterations (fp32 gradient, clip off,
+    fp32 compute copy): x, m, n, the difference average d, the last clipped gradient, the EF buffer
+    and the copy against the oracle's Adan at 1e-5."""
+    import torch
+    from paper_2606_30634_amd import binding as B
+    from paper_2606_30634_amd.stage import hparams
+    kw = dict(dict(lr=1e-3, clip_norm=0.0, ef_lambda=lam, delay=1), **ADAN)
+    hpg, hpo = hparams(**kw), HParams(**kw)
+    n = 1_000_003
+    dev = torch.device("cuda:0")
+    x0 = datagen.normal(27, "x", n, 0.02)
+    x = torch.from_numpy(x0).to(dev)
+    m, v, d, gl, up, sh = (torch.zeros(n, device=dev) for _ in range(6))
+    st = OptState.create({"w": x0.astype(np.float64)})
+    stream = torch.cuda.current_stream().cuda_stream
+    log(f"flat adan lambda={lam}: {n} elements")
+    for t in range(8):
+        gd = torch.from_numpy(datagen.normal(27, "g", n, 1e-3, step=max(t - 1, 0))).to(dev)
+        B.delayed_update_flat_adan(n, x.data_ptr(), gd.data_ptr(), False, m.data_ptr(), v.data_ptr(), d.data_ptr(),
+                                   gl.data_ptr(), up.data_ptr(), sh.data_ptr(), False, t, hpg, None, stream)
+        iteration_update(st, {"w": datagen.normal(27, "g", n, 1e-3, step=t).astype(np.float64)}, hpo)
+    torch.cuda.synchronize()
+    errs = {"x": rel(x.cpu().numpy(), st.x["w"]), "m": rel(m.cpu().numpy(), st.m["w"]),
+            "n": rel(v.cpu().numpy(), st.v["w"]), "d": rel(d.cpu().numpy(), st.adan_d["w"]),
+            "g_last": rel(gl.cpu().numpy(), st.adan_gprev["w"]), "copy": rel(sh.cpu().numpy(), st.x["w"])}
+    if lam:
+        errs["u_prev"] = rel(up.cpu().numpy(), st.u_prev["w"])
+    log(f"flat adan lambda={lam}: " + ", ".join(f"{k}={e:.2e}" for k, e in errs.items()))
+    assert max(errs.values()) < 1e-5, errs

@@ -149,3 +149,83 @@ def test_sapipe_master_is_the_standard_delayed_run():
     _, b, _ = _run(HParams(lr=1e-2, ef_lambda=0.0), x0, G)
     for xa, xb in zip(a, b):
         np.testing.assert_array_equal(xa, xb)
+
+
+# ---------------------------------------------------------------------------------------- Adan
+ADAN = dict(optimizer="adan", beta1=0.98, beta2=0.92, beta3=0.99)
+
+
+def test_adan_with_beta2_zero_is_adamw():
+    """beta2 = 0 takes the difference terms out: d is fed back with weight 0 and n averages g^2,
+    so Adan(beta1, 0, beta3) is AdamW(beta1, beta3) -- torch's AdamW with clipping, synchronous."""
+    hp = HParams(lr=1e-2, weight_decay=0.1, clip_norm=1.0, delay=0, **dict(ADAN, beta2=0.0))
+    x0 = R.standard_normal(30)
+    G = [R.standard_normal(30) * (0.05 if t % 2 else 3.0) for t in range(12)]
+    _, xs, _ = _run(hp, x0, G)
+    p = torch.nn.Parameter(torch.tensor(x0))
+    opt = torch.optim.AdamW([p], lr=hp.lr, betas=(hp.beta1, hp.beta3), eps=hp.eps,
+                            weight_decay=hp.weight_decay, foreach=False)
+    for t, g in enumerate(G):
+        p.grad = torch.tensor(g.copy())
+        torch.nn.utils.clip_grad_norm_([p], hp.clip_norm)
+        opt.step()
+        np.testing.assert_allclose(xs[t + 1], p.detach().numpy(), rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("lam", [0.0, 1.0])
+def test_adan_constant_gradient_closed_form(lam):
+    """A constant gradient has zero differences: d = 0, n / (1 - b3^k) = g^2, m / (1 - b1^k) = g,
+    so every update is lr (g / (|g| + eps) + wd x_t); delay 1: x_{t+1} = x_t - u (EF: - lam (u -
+    u_prev)), with x_1 = x_0."""
+    hp = HParams(lr=5e-3, weight_decay=0.0, clip_norm=0.0, ef_lambda=lam, delay=1, **ADAN)
+    g = R.standard_normal(16)
+    x0 = R.standard_normal(16)
+    _, xs, _ = _run(hp, x0, [g] * 8)
+    u = hp.lr * g / (np.abs(g) + hp.eps)
+    expect = [x0, x0]
+    for t in range(1, 8):
+        step = u if t == 1 or lam == 0 else u + lam * (u - u)
+        expect.append(expect[-1] - step)
+    for a, b in zip(xs, expect):
+        np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("lam", [0.0, 1.0])
+def test_adan_replay_with_explicit_sums(lam):
+    """Delay-1 Adan with clipping and decay, against a from-scratch rebuild of every update: the
+    three averages as explicit weighted sums over the clipped history of consumed gradients
+    (differences from the second consumed gradient on), with the bias corrections of the count."""
+    hp = HParams(lr=2e-3, weight_decay=0.1, clip_norm=0.5, ef_lambda=lam, delay=1, **ADAN)
+    T = 9
+    G = [R.standard_normal(12) * (0.1 if t % 3 else 2.0) for t in range(T)]
+    x0 = R.standard_normal(12)
+    _, xs, _ = _run(hp, x0, G)
+    clipped = []
+    x = x0.copy()
+    u_prev = None
+    assert np.array_equal(xs[1], x0)
+    for t in range(1, T):
+        g = G[t - 1]
+        clipped.append(g * min(1.0, hp.clip_norm / (np.linalg.norm(g) + 1e-6)))
+        k = len(clipped)
+        diffs = [np.zeros(12)] + [clipped[j] - clipped[j - 1] for j in range(1, k)]
+        m = sum((1 - hp.beta1) * hp.beta1 ** (k - 1 - j) * clipped[j] for j in range(k))
+        d = sum((1 - hp.beta2) * hp.beta2 ** (k - 1 - j) * diffs[j] for j in range(k))
+        n = sum((1 - hp.beta3) * hp.beta3 ** (k - 1 - j) * (clipped[j] + hp.beta2 * diffs[j]) ** 2
+                for j in range(k))
+        u = hp.lr * ((m / (1 - hp.beta1 ** k) + hp.beta2 * d / (1 - hp.beta2 ** k)) /
+                     (np.sqrt(n / (1 - hp.beta3 ** k)) + hp.eps) + hp.weight_decay * x)
+        x = x - u if (u_prev is None or lam == 0) else x - u - lam * (u - u_prev)
+        u_prev = u
+        np.testing.assert_allclose(xs[t + 1], x, rtol=1e-11, atol=1e-14)
+
+
+def test_adan_delay1_lags_synchronous_by_one_step():
+    hp0 = HParams(lr=1e-2, clip_norm=1.0, delay=0, **ADAN)
+    hp1 = HParams(lr=1e-2, clip_norm=1.0, delay=1, **ADAN)
+    x0 = R.standard_normal(20)
+    G = [R.standard_normal(20) for _ in range(10)]
+    _, xs0, _ = _run(hp0, x0, G)
+    _, xs1, _ = _run(hp1, x0, G)
+    for t in range(1, 10):
+        np.testing.assert_allclose(xs1[t + 1], xs0[t], rtol=1e-13, atol=1e-15)
