@@ -256,6 +256,17 @@ size_t grad_norm_flat_workspace_bytes(void);
 int grad_norm_flat(int64_t n, const void* g, int32_t g_is_bf16, float clip_norm, float* out_dev,
                    int32_t* nonfinite_dev, void* workspace, size_t workspace_bytes, void* hip_stream);
 
+/* grad_norm_flat for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same two passes, with the partial sums
+ * in a static device array of the library (1024 doubles, 8 KiB per GPU, held until the process
+ * ends) instead of a caller workspace.  It calls no hipMalloc, hipFree or allocating routine.  The
+ * first pass runs at most 1024 blocks whatever n is, so n has no scratch-imposed maximum; a grid that
+ * would need more partials is refused with STAGE_EINVAL.  Every call on a GPU shares that GPU's
+ * array (each call overwrites every partial it reads): calls that overlap on one GPU race.
+ * Arguments, results and alignment as grad_norm_flat. */
+int grad_norm_flat_noalloc(int64_t n, const void* g, int32_t g_is_bf16, float clip_norm, float* out_dev,
+                           int32_t* nonfinite_dev, void* hip_stream);
+
 /* Measurement reference, not a step of the method: a streaming device copy of `bytes` (a multiple
  * of 16; both pointers 16-byte aligned) with 16-byte non-temporal loads and stores, four chunks in
  * flight per thread - the practical HBM ceiling the update pass's bandwidth is reported against. */

@@ -18,7 +18,8 @@ EXPORTS = ["stage_required_bytes", "stage_init", "stage_num_tensors", "stage_ten
            "delayed_update", "delayed_update_flat", "stage_embed_indices", "stage_poll_nonfinite",
            "stage_grad_norm", "stage_profile_enable", "stage_profile_read", "stage_last_error",
            "stage_destroy", "stage_set_update_overlap", "stage_join_update", "stage_resume",
-           "grad_norm_flat_workspace_bytes", "grad_norm_flat", "hbm_stream_copy", "delayed_update_flat_adan"]
+           "grad_norm_flat_workspace_bytes", "grad_norm_flat", "hbm_stream_copy", "delayed_update_flat_adan",
+           "grad_norm_flat_noalloc"]
 PROF_GEMM, PROF_ATTN_FWD, PROF_ATTN_BWD, PROF_UPDATE, PROF_NORM, PROF_OTHER, PROF_NS = range(7)
 
 
@@ -75,6 +76,7 @@ def _load():
         "grad_norm_flat_workspace_bytes": (sz, []),
         "grad_norm_flat": (C.c_int, [i64, vp, i32, C.c_float, vp, vp, vp, sz, vp]),
         "hbm_stream_copy": (C.c_int, [vp, vp, sz, vp]),
+        "grad_norm_flat_noalloc": (C.c_int, [i64, vp, i32, C.c_float, vp, vp, vp]),
         "delayed_update_flat_adan": (C.c_int, [i64, vp, vp, i32, vp, vp, vp, vp, vp, vp, i32, i64,
                                                C.POINTER(UpdateHParams), vp, vp]),
         "stage_profile_read": (C.c_int, [vp, i32, C.POINTER(C.c_double), C.POINTER(i64), C.POINTER(C.c_double)]),
@@ -169,6 +171,10 @@ def grad_norm_flat_workspace_bytes() -> int:
 def grad_norm_flat(n, g, g_is_bf16, clip_norm, out_dev, nonfinite_dev, workspace, workspace_bytes, stream) -> None:
     _call("grad_norm_flat", n, g, int(g_is_bf16), clip_norm, out_dev, nonfinite_dev, workspace,
           workspace_bytes, stream)
+
+
+def grad_norm_flat_noalloc(n, g, g_is_bf16, clip_norm, out_dev, nonfinite_dev, stream) -> None:
+    _call("grad_norm_flat_noalloc", n, g, int(g_is_bf16), clip_norm, out_dev, nonfinite_dev, stream)
 
 
 def hbm_stream_copy(dst, src, nbytes, stream) -> None:

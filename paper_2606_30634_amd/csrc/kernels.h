@@ -17,6 +17,9 @@ struct UpdateScalars {
   int first = 0;                          // Adan: the first update (the gradient difference is 0)
 };
 size_t norm_scratch_bytes();
+// Device address of the current device's file-scope partial-sum array of the norm (norm_scratch_bytes()
+// bytes, looked up once per device); nullptr with *err the HIP error code when the lookup fails.
+double* norm_static_scratch(int* err);
 // blocks: partial sums (and blocks of the first pass), at most norm_scratch_bytes() / 8; <= 0
 // takes that maximum.
 void launch_grad_norm(const void* g, bool g_bf16, int64_t n, float clip, double* partial,

@@ -1169,6 +1169,27 @@ int grad_norm_flat(int64_t n, const void* g, int32_t g_is_bf16, float clip_norm,
   return STAGE_OK;
 }
 
+int grad_norm_flat_noalloc(int64_t n, const void* g, int32_t g_is_bf16, float clip_norm, float* out_dev,
+                           int32_t* nonfinite_dev, void* hip_stream) {
+  if (n < 0 || !out_dev) return fail(STAGE_EINVAL, "bad argument");
+  if (n > 0 && !g) return fail(STAGE_EINVAL, "null gradient");
+  if ((uintptr_t)g % (g_is_bf16 ? 8 : 16) || (uintptr_t)out_dev % 4)
+    return fail(STAGE_EINVAL, "g must be 16-byte (bf16: 8-byte) aligned");
+  // the first pass runs min(CUs, capacity) blocks, one partial each: the array's capacity bounds the
+  // grid, not n
+  const int blocks = device_cu_count();
+  if ((size_t)blocks * sizeof(double) > norm_scratch_bytes())
+    return fail(STAGE_EINVAL, "grad_norm_flat_noalloc: more partials than its static scratch holds");
+  int err = 0;
+  double* part = norm_static_scratch(&err);
+  if (!part) return fail(STAGE_EHIP, std::string("grad_norm_flat_noalloc: symbol lookup: ") +
+                                         hipGetErrorString((hipError_t)err));
+  launch_grad_norm(g, g_is_bf16 != 0, n, clip_norm, part, out_dev, (int*)nonfinite_dev, nullptr, blocks,
+                   (hipStream_t)hip_stream);
+  HIP_OK(hipGetLastError());
+  return STAGE_OK;
+}
+
 int hbm_stream_copy(void* dst, const void* src, size_t bytes, void* hip_stream) {
   if (bytes % 16 || (uintptr_t)dst % 16 || (uintptr_t)src % 16 || (bytes && (!dst || !src)))
     return fail(STAGE_EINVAL, "hbm_stream_copy: 16-byte aligned pointers and a multiple of 16 bytes");

@@ -357,9 +357,38 @@ void launch_update_t(int64_t n, float* x, const void* g, float* m, float* v, flo
   }
 }
 
+// Partial sums of the norm's first pass for callers that cannot allocate (grad_norm_flat_noalloc):
+// one array per GPU, held until the process ends.  Host code never passes its name to a kernel: the
+// name is a host-side stand-in, and the device address comes from hipGetSymbolAddress, per device.
+static __device__ __align__(256) double scratch[NORM_BLOCKS];
+
 }  // namespace
 
 size_t norm_scratch_bytes() { return NORM_BLOCKS * sizeof(double); }
+
+#include <mutex>
+double* norm_static_scratch(int* err) {
+  static std::mutex mu;
+  static double* addr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= 64) {
+    *err = e != hipSuccess ? (int)e : (int)hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));  // with device `dev` current
+    if (e != hipSuccess || !p) {
+      *err = e != hipSuccess ? (int)e : (int)hipErrorInvalidSymbol;
+      return nullptr;
+    }
+    addr[dev] = (double*)p;
+  }
+  *err = 0;
+  return addr[dev];
+}
 
 void launch_grad_norm(const void* g, bool g_bf16, int64_t n, float clip, double* partial,
                       float* out2, int* flag, unsigned long long* skipped, int blocks, hipStream_t st) {
