@@ -153,7 +153,8 @@ int stage_num_tensors(const stage_t* s, int32_t* count);
  *   [0, max_delay] (gradient buffers: step s accumulates into buffer s mod (max_delay + 1)) and
  *   "w0.", "w1." (the two compute versions, bf16 or fp32); "flat.master|m|v|u_prev|u_prev{j}|
  *   grad{j}|w0|w1" for the whole flat vectors (padding between tensors is zero and stays zero);
- *   "act{slot}.blk{i}.{x|rstd1|n1|qkv|o|lse|h|rstd2|n2|gu|z}" and "act{slot}.{x0|y|logits}"
+ *   "act{slot}.blk{i}.{x|rstd1|n1|qkv|o|lse|h|rstd2|n2|gu|z}" (on a bf16 stage also "o32", the
+ *   attention output in fp32) and "act{slot}.{x0|y|logits}"
  *   for the saved activations of an activation slot. */
 int stage_tensor(const stage_t* s, int32_t idx, const char** name, void** dev_ptr,
                  int64_t* numel, int32_t* dtype);

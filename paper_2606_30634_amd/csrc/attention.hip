@@ -75,6 +75,8 @@ __global__ void __launch_bounds__(TR) attn_fwd(AttnArgs a) {
   const float inv = 1.0f / l;
 #pragma unroll
   for (int c = 0; c < HD; ++c) out[rowo + c] = from_f32<T>(o[c] * inv);
+  if (a.o32)
+    for (int c = 0; c < HD; ++c) a.o32[rowo + c] = o[c] * inv;
   a.lse[((int64_t)b * a.Hq + h) * a.S + i] = m + logf(l);
 }
 
@@ -85,10 +87,14 @@ __global__ void __launch_bounds__(256) attn_delta(AttnArgs a) {
   if (idx >= (int64_t)a.B * a.Hq * a.S) return;
   const int i = idx % a.S, h = (idx / a.S) % a.Hq, b = idx / ((int64_t)a.S * a.Hq);
   const int64_t r = (int64_t)(b * a.S + i) * a.Hq * HD + h * HD;
-  const T* O = (const T*)a.o;
   const T* dO = (const T*)a.dout;
   float s = 0.f;
-  for (int c = 0; c < HD; ++c) s += to_f32(O[r + c]) * to_f32(dO[r + c]);
+  if (a.o32) {
+    for (int c = 0; c < HD; ++c) s += a.o32[r + c] * to_f32(dO[r + c]);
+  } else {
+    const T* O = (const T*)a.o;
+    for (int c = 0; c < HD; ++c) s += to_f32(O[r + c]) * to_f32(dO[r + c]);
+  }
   a.delta[idx] = s;
 }
 

@@ -13,8 +13,8 @@
 //   S^T = K Q^T (B = the wave's Q rows in registers) -> lane l owns query column l mod 32, so the
 //   online-softmax statistics of a query stay in one lane pair (l, l ^ 32); O^T += V^T P^T with P^T
 //   rebuilt from the S^T accumulators by one lane-pair exchange; lse = ln sum exp(S) is kept.
-// Backward (dS = P (dP - delta), delta = rowsum(dO O), P recomputed from lse), two kernels and no
-// float atomics: dQ (waves own queries, K and V tiles streamed) and dK/dV (waves own keys, Q and
+// Backward (dS = P (dP - delta), delta = rowsum(dO O) with O in fp32, P recomputed from lse), two
+// kernels and no float atomics: dQ (waves own queries, K and V tiles streamed) and dK/dV (waves own keys, Q and
 // dO tiles of every query head of the key/value head streamed).  Tiles are double-buffered through
 // registers: the next tile is fetched while the current one feeds the MFMAs.  Outputs leave through
 // LDS as 16-byte rows.  Query blocks with the longest causal range are scheduled first.
@@ -117,6 +117,26 @@ __device__ __forceinline__ bf16x8 acc_rows_to_b(const f32x16& s) {
   return r;
 }
 
+// The same operand from an accumulator split in two: hi = bf16(s) and lo = bf16(s - hi), so that
+// a product with hi and one with lo add up to the product with s to about 2^-17 relative (s - hi is
+// exact in fp32).
+template <int IB>
+__device__ __forceinline__ void acc_rows_to_b_split(const f32x16& s, bf16x8& hi, bf16x8& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float a = s[IB + 2 * q], b = s[IB + 2 * q + 1];
+    h[q] = pack2(a, b);
+    l[q] = pack2(a - __uint_as_float(h[q] << 16), b - __uint_as_float(h[q] & 0xffff0000u));
+  }
+  swap32(h[0], h[2]);
+  swap32(h[1], h[3]);
+  swap32(l[0], l[2]);
+  swap32(l[1], l[3]);
+  __builtin_memcpy(&hi, h, 16);
+  __builtin_memcpy(&lo, l, 16);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Streamed tiles: KB rows x HD of a head (row stride ld) land in a swizzled [KB][HD] LDS tile by
@@ -168,7 +188,8 @@ template <int HD>
 __device__ __forceinline__ void store_rows_from_t(float* __restrict__ stage, const f32x16* acc, float scale,
                                                   bf16* __restrict__ out, int ldo, int row0_wg, int S,
                                                   const float* rope_cos = nullptr,
-                                                  const float* rope_sin = nullptr) {
+                                                  const float* rope_sin = nullptr,
+                                                  float* __restrict__ out32 = nullptr) {
   constexpr int OP = HD + 4;  // fp32 staging pitch
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64, half = lane / 32, col = lane % 32;
 #pragma unroll
@@ -196,6 +217,11 @@ __device__ __forceinline__ void store_rows_from_t(float* __restrict__ stage, con
     } else {
 #pragma unroll
       for (int q = 0; q < 8; ++q) ov[q] = (bf16)sr[d + q];
+      if (out32) {  // the fp32 rows too (same layout)
+        float* o32 = out32 + (int64_t)row * ldo + d;
+        *reinterpret_cast<f32x4*>(o32) = f32x4{sr[d], sr[d + 1], sr[d + 2], sr[d + 3]};
+        *reinterpret_cast<f32x4*>(o32 + 4) = f32x4{sr[d + 4], sr[d + 5], sr[d + 6], sr[d + 7]};
+      }
     }
     *reinterpret_cast<bf16x8*>(out + (int64_t)row * ldo + d) = ov;
   }
@@ -228,7 +254,10 @@ struct Lds {
 };
 
 // ------------------------------------------------------------------------------------------ forward
-template <int HD>
+// HILO (a stage that keeps O in fp32 for the backward's delta): P enters the P V product as its
+// hi / lo bf16 pair, so that O, and the fp32 copy written to o32, carry P to about 2^-17 instead of
+// bf16's 2^-9; delta = rowsum(dO O) is then consistent with the P and dP the backward recomputes.
+template <int HD, bool HILO>
 __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
   using L = Lds<HD>;
   using TT = DmaRowTile<HD>;
@@ -331,10 +360,22 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
       }
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 pf = (kk % 2) ? acc_rows_to_b<8>(s[kk / 2]) : acc_rows_to_b<0>(s[kk / 2]);
+        if constexpr (HILO) {
+          bf16x8 ph, pl, vfr[DT];
+          if (kk % 2) acc_rows_to_b_split<8>(s[kk / 2], ph, pl);
+          else acc_rows_to_b_split<0>(s[kk / 2], ph, pl);
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Vs, dt * 32, kk * 16), pf, o[dt], 0, 0, 0);
+          for (int dt = 0; dt < DT; ++dt) vfr[dt] = frag_cols<HD>(Vs, dt * 32, kk * 16);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfr[dt], ph, o[dt], 0, 0, 0);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfr[dt], pl, o[dt], 0, 0, 0);
+        } else {
+          const bf16x8 pf = (kk % 2) ? acc_rows_to_b<8>(s[kk / 2]) : acc_rows_to_b<0>(s[kk / 2]);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Vs, dt * 32, kk * 16), pf, o[dt], 0, 0, 0);
+        }
       }
     }
   }
@@ -343,15 +384,14 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
     a.lse[((int64_t)b * a.Hq + h) * a.S + myq] = (m + log2f(lsum)) * 0.6931471805599453f;
   const float inv = lsum > 0.f ? 1.0f / lsum : 0.f;
   store_rows_from_t<HD>(reinterpret_cast<float*>(smem), o, inv,
-                        (bf16*)a.o + (int64_t)b * a.S * a.Hq * HD + h * HD, a.Hq * HD, qb * QB, a.S);
+                        (bf16*)a.o + (int64_t)b * a.S * a.Hq * HD + h * HD, a.Hq * HD, qb * QB, a.S, nullptr,
+                        nullptr, HILO ? a.o32 + (int64_t)b * a.S * a.Hq * HD + h * HD : nullptr);
 }
 
 // ------------------------------------------------------------------------------------------ dQ
-// DELTA: the pass that only sums delta_i = sum_j P_ij dP_ij over the keys, with the P and dP the dQ
-// pass recomputes, so that every row of dS = P (dP - delta) sums to zero.  (The shortcut
-// rowsum(dO O) with O stored in bf16 misses that by the rounding of O; once attention sharpens,
-// dP - delta cancels and the mismatch biases dQ and dK along the mean key.)
-template <int HD, bool DELTA = false>
+// delta_i = rowsum(dO O)_i comes with the backward's arguments, from O in fp32 (see flash_fwd's
+// HILO), so that every row of dS = P (dP - delta) sums to zero with the P and dP recomputed here.
+template <int HD>
 __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, int bz,
     unsigned char* __restrict__ smem) {
   using L = Lds<HD>;
@@ -386,10 +426,7 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
     }
   }
   const int64_t sidx = ((int64_t)b * a.Hq + h) * a.S + min(myq, a.S - 1);
-  const float lse2 = a.lse[sidx] * LOG2E, dl = DELTA ? 0.f : a.delta[sidx];
-  float rd[16];  // DELTA: this lane's share of sum_j P_ij dP_ij, one partial per accumulator slot
-#pragma unroll
-  for (int e = 0; e < 16; ++e) rd[e] = 0.f;
+  const float lse2 = a.lse[sidx] * LOG2E, dl = a.delta[sidx];
   wait_vm_lds<0>();  // register loads done before the ring starts (as in the forward)
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
@@ -422,23 +459,6 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
           dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Vs, t * 32, ks * 16), df[ks], dp[t], 0, 0, 0);
         }
       }
-      if constexpr (DELTA) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          if (HD == 64 && key0 + t * 32 + 31 <= q0) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) rd[e] += fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) * dp[t][e];
-          } else {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int key = key0 + t * 32 + 8 * (e / 4) + 4 * half + (e % 4);
-              const float p = key <= myq ? fast_exp2(__builtin_fmaf(s[t][e], sl2, -lse2)) : 0.f;
-              rd[e] += p * dp[t][e];
-            }
-          }
-        }
-        continue;
-      }
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         // every key of the sub-tile is visible to every query: no mask (head dim 64 only; at 128
@@ -464,15 +484,6 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
       }
     }
   }
-  if constexpr (DELTA) {
-    float sum = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) sum += rd[e];
-    sum += __shfl_xor(sum, 32, 64);  // the other half of the lane's query column
-    if (half == 0 && myq < a.S) a.delta[sidx] = sum;
-    wait_vm_lds<0>();  // no ring load may land in the LDS after the block ends
-    return;
-  }
   block_barrier();  // every wave is done with the last tile: the ring becomes the output staging
   store_rows_from_t<HD>(reinterpret_cast<float*>(smem), dq, 1.0f / sqrtf((float)HD),
                         (bf16*)a.dqkv + (int64_t)b * a.S * ld + h * HD, ld, qb * QB, a.S, a.rope_cos, a.rope_sin);
@@ -485,16 +496,6 @@ __global__ void __launch_bounds__(NT) flash_bwd_dq(AttnArgs a) {
   int unit, idx;  // unit: (batch, query head)
   xcd_item(blockIdx.x, nqb * a.Hq * a.B, nqb, unit, idx);
   bwd_dq_block<HD>(a, idx, unit % a.Hq, unit / a.Hq, smem);
-}
-
-// delta[b, h, i] = sum_j P_ij dP_ij, the grid of flash_bwd_dq
-template <int HD>
-__global__ void __launch_bounds__(NT) flash_bwd_delta(AttnArgs a) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int nqb = (a.S + QB - 1) / QB;
-  int unit, idx;
-  xcd_item(blockIdx.x, nqb * a.Hq * a.B, nqb, unit, idx);
-  bwd_dq_block<HD, true>(a, idx, unit % a.Hq, unit / a.Hq, smem);
 }
 
 // ------------------------------------------------------------------------------------------ dK, dV
@@ -656,15 +657,26 @@ __global__ void __launch_bounds__(256) flash_delta(AttnArgs a) {
   const int h = idx % a.Hq;
   const int64_t row = idx / a.Hq;  // b * S + i
   const int b = row / a.S, i = row % a.S;
-  const bf16* o = (const bf16*)a.o + row * a.Hq * HD + h * HD;
   const bf16* d = (const bf16*)a.dout + row * a.Hq * HD + h * HD;
   float acc = 0.f;
+  if (a.o32) {  // O in fp32 (the forward's own copy)
+    const float* o = a.o32 + row * a.Hq * HD + h * HD;
 #pragma unroll
-  for (int c = 0; c < HD; c += 8) {
-    const bf16x8 x = *reinterpret_cast<const bf16x8*>(o + c);
-    const bf16x8 y = *reinterpret_cast<const bf16x8*>(d + c);
+    for (int c = 0; c < HD; c += 8) {
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(o + c), x1 = *reinterpret_cast<const f32x4*>(o + c + 4);
+      const bf16x8 y = *reinterpret_cast<const bf16x8*>(d + c);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc += (float)x[j] * (float)y[j];
+      for (int j = 0; j < 4; ++j) acc += x0[j] * (float)y[j] + x1[j] * (float)y[j + 4];
+    }
+  } else {
+    const bf16* o = (const bf16*)a.o + row * a.Hq * HD + h * HD;
+#pragma unroll
+    for (int c = 0; c < HD; c += 8) {
+      const bf16x8 x = *reinterpret_cast<const bf16x8*>(o + c);
+      const bf16x8 y = *reinterpret_cast<const bf16x8*>(d + c);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc += (float)x[j] * (float)y[j];
+    }
   }
   a.delta[((int64_t)b * a.Hq + h) * a.S + i] = acc;
 }
@@ -674,11 +686,11 @@ void set_lds(K kernel, size_t bytes) {
   (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
-template <int HD>
+template <int HD, bool HILO>
 void fwd_launch(const AttnArgs& a, hipStream_t st) {
   static bool attr = false;
-  if (!attr) { set_lds(flash_fwd<HD>, Lds<HD>::fwd_bytes()); attr = true; }
-  flash_fwd<HD><<<(unsigned)(cdiv(a.S, QB) * a.Hq * a.B), NT, Lds<HD>::fwd_bytes(), st>>>(a);
+  if (!attr) { set_lds(flash_fwd<HD, HILO>, Lds<HD>::fwd_bytes()); attr = true; }
+  flash_fwd<HD, HILO><<<(unsigned)(cdiv(a.S, QB) * a.Hq * a.B), NT, Lds<HD>::fwd_bytes(), st>>>(a);
 }
 
 template <int HD>
@@ -689,10 +701,8 @@ void bwd_launch(const AttnArgs& a, hipStream_t st) {
     set_lds(flash_bwd_dkv<HD>, Lds<HD>::dkv_bytes());
     attr = true;
   }
-  if (!a.delta_ready) {  // delta from the P and dP the backward recomputes
-    static bool dattr = false;
-    if (!dattr) { set_lds(flash_bwd_delta<HD>, Lds<HD>::dq_bytes()); dattr = true; }
-    flash_bwd_delta<HD><<<(unsigned)(cdiv(a.S, QB) * a.Hq * a.B), NT, Lds<HD>::dq_bytes(), st>>>(a);
+  if (!a.delta_ready) {  // rowsum(dO O), from O in fp32 when the forward kept it
+    flash_delta<HD><<<(unsigned)cdiv((int64_t)a.B * a.S * a.Hq, 256), 256, 0, st>>>(a);
   }
   if constexpr (HD == 64) {
     // one launch for both (at head dim 128 the dK/dV register budget would halve dQ's occupancy)
@@ -710,9 +720,14 @@ void bwd_launch(const AttnArgs& a, hipStream_t st) {
 }  // namespace
 
 bool attention_mfma_fwd_try(const AttnArgs& a, hipStream_t st) {
-  if ((uintptr_t)a.qkv % 16 || (uintptr_t)a.o % 16) return false;
-  if (a.hd == 64) { fwd_launch<64>(a, st); return true; }
-  if (a.hd == 128) { fwd_launch<128>(a, st); return true; }
+  if ((uintptr_t)a.qkv % 16 || (uintptr_t)a.o % 16 || (uintptr_t)a.o32 % 16) return false;
+  if (a.o32) {
+    if (a.hd == 64) { fwd_launch<64, true>(a, st); return true; }
+    if (a.hd == 128) { fwd_launch<128, true>(a, st); return true; }
+    return false;
+  }
+  if (a.hd == 64) { fwd_launch<64, false>(a, st); return true; }
+  if (a.hd == 128) { fwd_launch<128, false>(a, st); return true; }
   return false;
 }
 

@@ -159,7 +159,8 @@ void launch_gemm(bool bf, const GemmArgs& g, hipStream_t st) {
     launch_gemm(bf, p, st);
     AttnArgs a{};
     a.B = g.M / g.delta_S; a.S = g.delta_S; a.Hq = g.N / g.delta_hd; a.Hkv = a.Hq; a.hd = g.delta_hd;
-    a.o = const_cast<void*>(g.aux); a.dout = g.C; a.delta = g.delta;
+    a.o = const_cast<void*>(g.aux); a.o32 = (float*)const_cast<void*>(g.aux);  // O in fp32
+    a.dout = g.C; a.delta = g.delta;
     launch_attention_delta(bf, a, st);
     return;
   }

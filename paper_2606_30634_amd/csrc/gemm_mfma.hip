@@ -317,7 +317,7 @@ template <> struct EpiIn<EPI_AXPBY> { static constexpr bool loads = true; bf16x8
 template <> struct EpiIn<EPI_AXPBY_DUP> { static constexpr bool loads = true; bf16x8 r; };
 template <> struct EpiIn<EPI_NS_SPLIT> { static constexpr bool loads = true; bf16x8 a, b; };
 template <> struct EpiIn<EPI_SWIGLU_BWD> { static constexpr bool loads = true; bf16x8 a, b; };
-template <> struct EpiIn<EPI_DELTA> { static constexpr bool loads = true; bf16x8 o; };
+template <> struct EpiIn<EPI_DELTA> { static constexpr bool loads = true; f32x4 o0, o1; };
 template <> struct EpiIn<EPI_ROPE> { static constexpr bool loads = true; f32x4 c0, c1, s0, s1; };
 
 template <int EPI>
@@ -337,7 +337,9 @@ __device__ __forceinline__ void epi_load(EpiIn<EPI>& in, const GemmArgs& g, int 
     in.a = ld_nt<bf16x8>(gu);
     in.b = ld_nt<bf16x8>(gu + g.N);
   } else if constexpr (EPI == EPI_DELTA) {
-    in.o = ld_nt<bf16x8>((const bf16*)g.aux + (int64_t)row * g.ld_aux + col);
+    const float* op = (const float*)g.aux + (int64_t)row * g.ld_aux + col;
+    in.o0 = ld_nt<f32x4>(op);
+    in.o1 = ld_nt<f32x4>(op + 4);
   } else if constexpr (EPI == EPI_ROPE) {
     if (col < g.rope_cols) {
       const int hh = g.rope_hd / 2, i0 = (col % g.rope_hd) % hh;
@@ -456,7 +458,7 @@ __device__ __forceinline__ void dma_epilogue(const GemmArgs& g, f32x16 (&acc)[WM
           st_nt(Cb + o, ov);
           float dot = 0.f;
 #pragma unroll
-          for (int q = 0; q < 8; ++q) dot += (float)ov[q] * (float)x.o[q];
+          for (int q = 0; q < 8; ++q) dot += (float)ov[q] * (q < 4 ? x.o0[q] : x.o1[q - 4]);
           // the head's delta_hd / 8 chunks sit in consecutive lanes (aligned groups)
           for (int m = 1; m < g.delta_hd / 8; m <<= 1) dot += __shfl_xor(dot, m, 64);
           if (col % g.delta_hd == 0) {

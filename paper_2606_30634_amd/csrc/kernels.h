@@ -114,9 +114,9 @@ struct GemmArgs {
   const float* rope_cos = nullptr; const float* rope_sin = nullptr;
   int rope_cols = 0, rope_hd = 0, rope_S = 0;
   int glu = 0; void* out2 = nullptr; int ld_out2 = 0;
-  // epilogue 4 (attention delta): the product is dO [M, N] (bf16, heads of delta_hd columns, rows
-  // b * delta_S + i) and aux the attention output O of the same layout; besides C, writes
-  // delta[(b Hq + h) delta_S + i] = sum over head h's columns of dO O (bf16-rounded dO).
+  // epilogue 4 (attention delta): the product is dO [M, N] (heads of delta_hd columns, rows
+  // b * delta_S + i) and aux the attention output O in fp32 of the same layout; besides C, writes
+  // delta[(b Hq + h) delta_S + i] = sum over head h's columns of dO O (dO rounded to C's type).
   float* delta = nullptr; int delta_hd = 0, delta_S = 0;
   // epilogue 6 (AXPBY): C = alpha (A B) + beta_d D, D of C's type and layout (leading dim ldc).
   float alpha = 1.f, beta_d = 0.f;
@@ -155,11 +155,14 @@ struct AttnArgs {
   int B, S, Hq, Hkv, hd;
   const void* qkv; void* o; float* lse;
   const void* dout; void* dqkv; float* delta;  // backward only; delta fp32 [B, Hq, s]
+  // fp32 copy of o (bf16 stage): the forward writes it when non-null; rowsum(dO O) reads it when
+  // non-null (else o)
+  float* o32 = nullptr;
   const float* rope_cos = nullptr; const float* rope_sin = nullptr;
   bool delta_ready = false;  // backward: delta already holds rowsum(dO O)
 };
 void launch_attention_fwd(bool bf, const AttnArgs& a, hipStream_t st);
-// delta = rowsum(dO O) per (batch, head, query) alone
+// delta = rowsum(dO O) per (batch, head, query) alone (O from o32 when set)
 void launch_attention_delta(bool bf, const AttnArgs& a, hipStream_t st);
 void launch_attention_bwd(bool bf, const AttnArgs& a, hipStream_t st);
 

@@ -44,6 +44,7 @@ struct BlockOff {  // element offsets of one block's weights in the flat paramet
 struct BlockAct {
   void *x, *n1, *qkv, *o, *h, *n2, *gu, *z;
   float *rstd1, *lse, *rstd2;
+  float* o32 = nullptr;  // bf16 stage: the attention output in fp32 (for the backward's delta)
 };
 
 struct Slot {
@@ -84,7 +85,13 @@ struct stage {
   // beside the activation-gradient chain: ev_m2s orders one after the stage stream's work so far,
   // ev_wg[k] marks the end of the last product of kind k (the stage stream waits on it before it
   // overwrites a buffer that product reads), ev_wjoin joins the stream back at the end.
+  // They go there only when the stage's products underfill the chip (wgrad_side): a block's
+  // [tokens, d_model] activation-gradient product of fewer than two 256 x 256 tiles per compute
+  // unit.  Products that fill it gain nothing from a second stream and would only run each other's
+  // kernels slower (measured on the large workload: 367 ms per step either way), so they run in
+  // order on the stage stream.
   hipStream_t wst = nullptr;
+  bool wgrad_side = true;
   hipEvent_t ev_m2s = nullptr, ev_wjoin = nullptr, ev_wg[5] = {};
   bool bf;
   size_t esz;  // bytes per compute element
@@ -200,6 +207,12 @@ enum { WG_DOWN = 0, WG_GU = 1, WG_O = 2, WG_QKV = 3, WG_HEAD = 4 };
 // weight-gradient product of kind k on the weight-gradient stream, after everything enqueued on
 // the stage stream so far (its inputs)
 void run_wgrad(stage* S, GemmArgs g, int k) {
+  if (!S->wgrad_side) {  // in order on the stage stream, with the split-K workspace
+    g.ws = S->gemm_ws;
+    g.ws_elems = S->gemm_ws ? GEMM_WS_ELEMS : 0;
+    timed(S, STAGE_PROF_GEMM, 2.0 * g.M * g.N * g.K, [&] { launch_gemm(S->bf, g, S->st); });
+    return;
+  }
   (void)hipEventRecord(S->ev_m2s, S->st);
   (void)hipStreamWaitEvent(S->wst, S->ev_m2s, 0);
   g.ws = S->gemm_ws;
@@ -210,9 +223,12 @@ void run_wgrad(stage* S, GemmArgs g, int k) {
 
 // the stage stream waits for the last weight-gradient product of kind k (and, the stream being in
 // order, for every product issued before it)
-void after_wgrad(stage* S, int k) { (void)hipStreamWaitEvent(S->st, S->ev_wg[k], 0); }
+void after_wgrad(stage* S, int k) {
+  if (S->wgrad_side) (void)hipStreamWaitEvent(S->st, S->ev_wg[k], 0);
+}
 
 void join_wgrad(stage* S) {
+  if (!S->wgrad_side) return;
   (void)hipEventRecord(S->ev_wjoin, S->wst);
   (void)hipStreamWaitEvent(S->st, S->ev_wjoin, 0);
 }
@@ -300,6 +316,7 @@ size_t layout(stage* S, char* base) {
       b.n1 = carve(T * d * esz);
       b.qkv = carve(T * qkvw * esz);
       b.o = carve(T * hqd * esz);
+      b.o32 = sh.dtype == 1 ? (float*)carve(T * hqd * 4) : nullptr;
       b.lse = (float*)carve((int64_t)sh.micro_batch * sh.n_heads * sh.seq_len * 4);
       b.h = carve(T * d * esz);
       b.rstd2 = (float*)carve(T * 4);
@@ -474,6 +491,7 @@ void register_tensors(stage* S) {
       S->named.push_back({p + "n1", b.n1, T * d, cdt});
       S->named.push_back({p + "qkv", b.qkv, T * S->qkvw, cdt});
       S->named.push_back({p + "o", b.o, T * S->hqd, cdt});
+      if (b.o32) S->named.push_back({p + "o32", b.o32, T * S->hqd, STAGE_DT_F32});
       S->named.push_back({p + "lse", b.lse, lse_n, STAGE_DT_F32});
       S->named.push_back({p + "h", b.h, T * d, cdt});
       S->named.push_back({p + "rstd2", b.rstd2, T, STAGE_DT_F32});
@@ -502,6 +520,7 @@ AttnArgs attn_args(const stage* S, const BlockAct& b) {
   a.B = S->sh.micro_batch; a.S = S->sh.seq_len; a.Hq = S->sh.n_heads; a.Hkv = S->sh.n_kv_heads;
   a.hd = S->sh.head_dim; a.qkv = b.qkv; a.o = b.o; a.lse = b.lse;
   a.dout = nullptr; a.dqkv = nullptr; a.delta = nullptr;
+  a.o32 = b.o32;
   return a;
 }
 
@@ -559,23 +578,22 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   after_wgrad(S, WG_O);
   int np = launch_rmsnorm_bwd(bf, S->dn, b.h, b.rstd2, S->wptr(vi, w.ffn_norm), dy, S->dh, S->rms_part, T, d, st);
   launch_colsum_partials(S->rms_part, np, d, g + w.ffn_norm, !first, st);
-  // output projection: do = dh Wo ; dWo (+)= dh^T o.  The attention backward's delta: on the bf16
-  // stage a pass of the attention backward sums P dP (o is stored in bf16, too coarse for
-  // rowsum(do o) once attention sharpens); on the fp32 stage rowsum(do o) in the product's epilogue
+  // output projection: do = dh Wo ; dWo (+)= dh^T o.  The attention backward's delta = rowsum(do o)
+  // in the product's epilogue, from o in fp32 (the bf16 stage's forward keeps an fp32 copy whose P V
+  // product took P as a hi / lo pair: delta then matches the P and dP the backward recomputes, where
+  // o rounded to bf16 would leave every dS row a nonzero sum once attention sharpens)
   GemmArgs go = gemm(T, S->hqd, d, S->dh, d, true, S->wptr(vi, w.wo), S->hqd, false, S->do_, S->hqd);
-  if (!bf) {
-    go.epi = 4;
-    go.aux = b.o;
-    go.ld_aux = S->hqd;
-    go.delta = S->delta;
-    go.delta_hd = sh.head_dim;
-    go.delta_S = sh.seq_len;
-  }
+  go.epi = 4;
+  go.aux = bf ? (const void*)b.o32 : b.o;
+  go.ld_aux = S->hqd;
+  go.delta = S->delta;
+  go.delta_hd = sh.head_dim;
+  go.delta_S = sh.seq_len;
   run_gemm(S, go);
   run_wgrad(S, gemm(d, S->hqd, T, S->dh, d, false, b.o, S->hqd, false, g + w.wo, S->hqd, true, beta), WG_O);
   AttnArgs a = attn_args(S, b);
   a.dout = S->do_; a.dqkv = S->dqkv; a.delta = S->delta;
-  a.delta_ready = !bf;  // fp32: computed with do above
+  a.delta_ready = true;  // computed with do above
   a.rope_cos = S->cos_t;  // dq, dk come back w.r.t. the unrotated projections
   a.rope_sin = S->sin_t;
   after_wgrad(S, WG_QKV);
@@ -621,6 +639,7 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
   S->T = shape->seq_len * shape->micro_batch;
   S->qkvw = (shape->n_heads + 2 * shape->n_kv_heads) * shape->head_dim;
   S->hqd = shape->n_heads * shape->head_dim;
+  S->wgrad_side = (int64_t)(S->T / 256) * (shape->d_model / 256) < 2 * (int64_t)device_cu_count();
   const size_t need = layout(S, nullptr);
   if (arena_bytes < need) {
     delete S;
