@@ -75,6 +75,26 @@ def measured_traffic(workload, kernel_class):
     return float(v) if v is not None else None
 
 
+def measured_mfma(workload, kernel_class):
+    """Counter-based matrix-core utilisation of a kernel class from the committed rocprofv3 --pmc summary of
+    this workload (SQ_VALU_MFMA_BUSY_CYCLES over the dispatch's cycles at the measured clock), or None when
+    there is none or the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"mfma_util_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    start = text.find("```json")
+    if start < 0:
+        return None
+    try:
+        rec = json.loads(text[start + 7:text.find("```", start + 7)])
+    except ValueError:
+        return None
+    if rec.get("sources_sha256") != kernel_sources_sha256():
+        return None
+    return rec.get("classes", {}).get(kernel_class)
+
+
 def cpu_baseline(w, optimizer="adamw", predict=False):
     """The oracle (float32, numpy) timed on the machine's host cores.  A stage of width <= 1024: whole
     optimizer steps of the workload -- all sequences forward+backward, then the full delayed update --
@@ -408,6 +428,10 @@ def main():
     roofline = {"kernel": dom, "bound": kd["bound"], "achieved": kd["achieved"], "peak": kd["peak"],
                 "unit": kd["unit"], "frac": kd["frac"],
                 "traffic": None if args.vocab else measured_traffic(args.workload + ("-bf16" if bf else "-f32"), dom)}
+    mc = None if args.vocab or args.optimizer != "adamw" else measured_mfma(args.workload + ("-bf16" if bf else "-f32"), dom)
+    if mc:
+        roofline["mfma_busy"] = mc.get("busy")
+        roofline["mfma_busy_clock_GHz"] = mc.get("clock")
     rc, skipped = B.stage_poll_nonfinite(st.handle)
     st.close()
 
