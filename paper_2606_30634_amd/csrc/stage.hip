@@ -1280,7 +1280,10 @@ int stage_profile_enable(stage_t* s, int32_t on) {
 
 int stage_profile_read(stage_t* s, int32_t cls, double* ms, int64_t* launches, double* work) {
   if (!s || cls < 0 || cls >= STAGE_PROF_NCLASS) return fail(STAGE_EINVAL, "bad argument");
+  // every stream a timed launch can be on: an update in flight (overlap mode) records on its own
   HIP_OK(hipStreamSynchronize(s->st));
+  for (hipStream_t x : {s->ust, s->wst})
+    if (x) HIP_OK(hipStreamSynchronize(x));
   prof_collect(s);
   if (ms) *ms = s->prof_ms[cls];
   if (launches) *launches = s->prof_n[cls];
