@@ -409,62 +409,110 @@ __global__ void __launch_bounds__(256) swiglu_fwd(const T* __restrict__ gu, T* _
   z[idx] = from_f32<T>(a * sigm(a) * b);
 }
 
-// ------------------------------------------------------------------ token sort (rank sort)
-// Key of position i: (token << 14) | i, with tokens outside [0, vocab) given the token value
-// vocab so that they sort after every valid one and belong to no embedding row.  The keys are
-// distinct, so key i goes to out[#{j : key_j < key_i}].  The count is split over SORT_PARTS ranges
-// of j (grid.y): a block counts, for 64 keys, the smaller keys of one range (its four waves each take
-// a quarter of the LDS-staged range; all lanes read the same word, a broadcast) and writes the
-// partial count; a second kernel adds the parts in order and scatters.
-constexpr int SORT_MAX = 16384;
-constexpr int SORT_PARTS = SORT_RANK_PARTS;
-constexpr int SORT_CHUNK = 2048;  // keys of one range (SORT_MAX / SORT_PARTS)
+// ------------------------------------------------------------------ token sort (radix sort)
+// Positions sorted by token, stably (equal tokens keep ascending positions): an LSD radix sort of the
+// keys key_i = token_i (tokens outside [0, vocab) keyed as vocab, so that they sort after every valid
+// one and belong to no embedding row; vocab < 2^17) carrying the positions, in three passes of 6-bit
+// digits.  A pass: per chunk of RADIX_CHUNK consecutive keys the digit counts (one wave walks the
+// chunk in rounds of 64 keys); one exclusive scan over (digit, chunk) in digit-major order; then the
+// stable scatter, where a key's place is its (digit, chunk) offset plus the number of keys with the
+// same digit before it in the chunk.  Within a round, the lanes holding a digit find each other from
+// six ballots of the digit's bits; the lowest of them advances the digit's running offset.  Integer
+// counts in a fixed order: the result is the same on every run.
+constexpr int RADIX_CHUNK = 1024, RADIX_BITS = 6, RADIX_DIG = 1 << RADIX_BITS, RADIX_PASSES = 3;
 __device__ __forceinline__ uint32_t token_key(const int32_t* tok, int i, int vocab) {
   const int t = tok[i];
-  return ((uint32_t)(t >= 0 && t < vocab ? t : vocab) << 14) | (uint32_t)i;
+  return (uint32_t)(t >= 0 && t < vocab ? t : vocab);
 }
-__global__ void __launch_bounds__(256) token_rank_part(const int32_t* __restrict__ tok, int n, int vocab,
-                                                       int part_len, int32_t* __restrict__ part) {
-  __shared__ u32x4 ks[SORT_CHUNK / 4];
-  __shared__ int cnt4[4][64];
-  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
-  const int i = blockIdx.x * 64 + lane;
-  const uint32_t mine = i < n ? token_key(tok, i, vocab) : 0xFFFFFFFFu;
-  const int c0 = blockIdx.y * part_len, m = max(0, min(part_len, n - c0));
-  const int m16 = (m + 15) & ~15;  // padded with keys that no valid key exceeds
-  uint32_t* kw = reinterpret_cast<uint32_t*>(ks);
-  for (int e = threadIdx.x; e < m16; e += 256) kw[e] = e < m ? token_key(tok, c0 + e, vocab) : 0xFFFFFFFFu;
-  __syncthreads();
-  int cnt = 0;
-  for (int q = wave; q < m16 / 4; q += 4) {
-    const u32x4 k = ks[q];
-    cnt += (k.x < mine) + (k.y < mine) + (k.z < mine) + (k.w < mine);
-  }
-  cnt4[wave][lane] = cnt;
-  __syncthreads();
-  if (wave == 0 && i < n)
-    part[(int64_t)blockIdx.y * n + i] = cnt4[0][lane] + cnt4[1][lane] + cnt4[2][lane] + cnt4[3][lane];
-}
-__global__ void __launch_bounds__(256) token_rank_scatter(const int32_t* __restrict__ tok, int n, int vocab,
-                                                          const int32_t* __restrict__ part,
-                                                          uint32_t* __restrict__ out) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  int r = 0;
+// lanes of the wave whose digit equals this lane's (among the active ones)
+__device__ __forceinline__ uint64_t digit_match(uint32_t dig, uint64_t active) {
+  uint64_t m = active;
 #pragma unroll
-  for (int y = 0; y < SORT_PARTS; ++y) r += part[(int64_t)y * n + i];
-  out[r] = token_key(tok, i, vocab);
+  for (int b = 0; b < RADIX_BITS; ++b) {
+    const uint64_t bal = __ballot((dig >> b) & 1u);
+    m &= ((dig >> b) & 1u) ? bal : ~bal;
+  }
+  return m;
+}
+// keys of pass 0 from the tokens (vals = positions), later passes from the previous pass's output
+__device__ __forceinline__ uint32_t radix_in(const int32_t* tok, const uint32_t* keys, int i, int vocab) {
+  return tok ? token_key(tok, i, vocab) : keys[i];
+}
+__global__ void __launch_bounds__(64) radix_count(const int32_t* __restrict__ tok, const uint32_t* __restrict__ keys,
+                                                  int n, int vocab, int shift, int nchunk, int32_t* __restrict__ hist) {
+  __shared__ int cnt[RADIX_DIG];
+  const int lane = threadIdx.x;
+  cnt[lane] = 0;  // RADIX_DIG == the wave's 64 lanes
+  __syncthreads();
+  const int c0 = blockIdx.x * RADIX_CHUNK, c1 = min(n, c0 + RADIX_CHUNK);
+  for (int r = c0; r < c1; r += 64) {
+    const int i = r + lane;
+    const bool on = i < c1;
+    const uint32_t dig = on ? (radix_in(tok, keys, i, vocab) >> shift) & (RADIX_DIG - 1) : 0u;
+    const uint64_t m = digit_match(dig, __ballot(on));
+    if (on && (m & ((1ull << lane) - 1)) == 0) cnt[dig] += __popcll(m);  // the digit's lowest lane
+    __syncthreads();
+  }
+  hist[(int64_t)lane * nchunk + blockIdx.x] = cnt[lane];
+}
+// exclusive scan of hist [RADIX_DIG][nchunk] in place, one block
+__global__ void __launch_bounds__(1024) radix_scan(int32_t* __restrict__ hist, int total) {
+  __shared__ int32_t part[1024];
+  const int per = (total + blockDim.x - 1) / blockDim.x;
+  const int lo = threadIdx.x * per, hi = min(total, lo + per);
+  int c = 0;
+  for (int q = lo; q < hi; ++q) c += hist[q];
+  part[threadIdx.x] = c;
+  __syncthreads();
+  for (int off = 1; off < (int)blockDim.x; off <<= 1) {  // inclusive Hillis-Steele scan
+    const int add = threadIdx.x >= off ? part[threadIdx.x - off] : 0;
+    __syncthreads();
+    part[threadIdx.x] += add;
+    __syncthreads();
+  }
+  int o = part[threadIdx.x] - c;
+  for (int q = lo; q < hi; ++q) {
+    const int v = hist[q];
+    hist[q] = o;
+    o += v;
+  }
+}
+__global__ void __launch_bounds__(64) radix_scatter(const int32_t* __restrict__ tok, const uint32_t* __restrict__ keys,
+                                                    const uint32_t* __restrict__ vals, int n, int vocab, int shift,
+                                                    int nchunk, const int32_t* __restrict__ offs,
+                                                    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out) {
+  __shared__ int base[RADIX_DIG];
+  const int lane = threadIdx.x;
+  base[lane] = offs[(int64_t)lane * nchunk + blockIdx.x];
+  __syncthreads();
+  const int c0 = blockIdx.x * RADIX_CHUNK, c1 = min(n, c0 + RADIX_CHUNK);
+  for (int r = c0; r < c1; r += 64) {
+    const int i = r + lane;
+    const bool on = i < c1;
+    const uint32_t key = on ? radix_in(tok, keys, i, vocab) : 0u;
+    const uint32_t dig = (key >> shift) & (RADIX_DIG - 1);
+    const uint64_t m = digit_match(dig, __ballot(on));
+    const int rank = __popcll(m & ((1ull << lane) - 1));
+    const int dst = on ? base[dig] + rank : 0;
+    __syncthreads();  // every lane has read its digit's offset before the offsets move on
+    if (on) {
+      keys_out[dst] = key;
+      vals_out[dst] = tok ? (uint32_t)i : vals[i];
+      if (rank == 0) base[dig] += __popcll(m);
+    }
+    __syncthreads();
+  }
 }
 
-// row_start[v] = first sorted index with token >= v (binary search), v in [0, vocab]
-__global__ void __launch_bounds__(256) token_row_start(const uint32_t* __restrict__ sorted, int n,
+// row_start[v] = first sorted index with token >= v (binary search over the sorted tokens), v in [0, vocab]
+__global__ void __launch_bounds__(256) token_row_start(const uint32_t* __restrict__ sorted_tok, int n,
                                                        int vocab, int32_t* __restrict__ row_start) {
   const int v = blockIdx.x * blockDim.x + threadIdx.x;
   if (v > vocab) return;
   int lo = 0, hi = n;
   while (lo < hi) {
     const int mid = (lo + hi) >> 1;
-    if ((int)(sorted[mid] >> 14) < v) lo = mid + 1; else hi = mid;
+    if ((int)sorted_tok[mid] < v) lo = mid + 1; else hi = mid;
   }
   row_start[v] = lo;
 }
@@ -498,7 +546,7 @@ __global__ void __launch_bounds__(1024) token_compact(const int32_t* __restrict_
 // dE[v] (+)= sum over the run of v in position order; rows without tokens get 0 (overwrite)
 template <typename T>
 __global__ void __launch_bounds__(256) embed_scatter(const T* __restrict__ dx0,
-                                                     const uint32_t* __restrict__ sorted,
+                                                     const uint32_t* __restrict__ sorted_pos,
                                                      const int32_t* __restrict__ row_start, int d,
                                                      float* __restrict__ de, int accumulate) {
   const int v = blockIdx.x;
@@ -506,7 +554,7 @@ __global__ void __launch_bounds__(256) embed_scatter(const T* __restrict__ dx0,
   if (accumulate && a == b) return;
   for (int j = threadIdx.x; j < d; j += blockDim.x) {
     float s = 0.f;
-    for (int q = a; q < b; ++q) s += to_f32(dx0[(int64_t)(sorted[q] & 0x3FFFu) * d + j]);
+    for (int q = a; q < b; ++q) s += to_f32(dx0[(int64_t)sorted_pos[q] * d + j]);
     const int64_t o = (int64_t)v * d + j;
     de[o] = accumulate ? de[o] + s : s;
   }
@@ -735,27 +783,44 @@ static void swf_t(const void* gu, void* z, int rows, int f, hipStream_t st) {
 void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st) {
   DISPATCH(bf, swf_t, gu, z, rows, f, st);
 }
-void launch_token_sort(const int32_t* tok, int n, int vocab, int32_t* rank_part, uint32_t* sorted,
-                       hipStream_t st) {
+int64_t token_sort_ws_elems(int n) { return 2 * (int64_t)n + (int64_t)RADIX_DIG * cdiv(n, RADIX_CHUNK); }
+void launch_token_sort(const int32_t* tok, int n, int vocab, int32_t* ws, uint32_t* sorted_tok,
+                       uint32_t* sorted_pos, hipStream_t st) {
   if (n <= 0) return;
-  const int part_len = cdiv(cdiv(n, SORT_PARTS), 16) * 16;  // <= SORT_CHUNK for n <= SORT_MAX
-  token_rank_part<<<dim3((unsigned)cdiv(n, 64), SORT_PARTS), 256, 0, st>>>(tok, n, vocab, part_len, rank_part);
-  token_rank_scatter<<<(unsigned)cdiv(n, 256), 256, 0, st>>>(tok, n, vocab, rank_part, sorted);
+  const int nchunk = (int)cdiv(n, RADIX_CHUNK);
+  uint32_t* tk = reinterpret_cast<uint32_t*>(ws);  // the ping-pong partner of (sorted_tok, sorted_pos)
+  uint32_t* tv = tk + n;
+  int32_t* hist = ws + 2 * (int64_t)n;
+  // passes 0 and 2 write the outputs, pass 1 the partner: the last pass ends in sorted_tok / sorted_pos
+  uint32_t* ok[RADIX_PASSES] = {sorted_tok, tk, sorted_tok};
+  uint32_t* ov[RADIX_PASSES] = {sorted_pos, tv, sorted_pos};
+  for (int p = 0; p < RADIX_PASSES; ++p) {
+    const int32_t* t0 = p == 0 ? tok : nullptr;
+    const uint32_t* ik = p == 0 ? nullptr : ok[p - 1];
+    const uint32_t* iv = p == 0 ? nullptr : ov[p - 1];
+    radix_count<<<(unsigned)nchunk, 64, 0, st>>>(t0, ik, n, vocab, p * RADIX_BITS, nchunk, hist);
+    radix_scan<<<1, 1024, 0, st>>>(hist, RADIX_DIG * nchunk);
+    radix_scatter<<<(unsigned)nchunk, 64, 0, st>>>(t0, ik, iv, n, vocab, p * RADIX_BITS, nchunk, hist, ok[p], ov[p]);
+  }
 }
-void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_start, int32_t* ids,
+void launch_token_runs(const uint32_t* sorted_tok, int n, int vocab, int32_t* row_start, int32_t* ids,
                        int32_t* counts, int32_t* n_unique, hipStream_t st) {
-  token_row_start<<<(unsigned)cdiv(vocab + 1, 256), 256, 0, st>>>(sorted, n, vocab, row_start);
+  token_row_start<<<(unsigned)cdiv(vocab + 1, 256), 256, 0, st>>>(sorted_tok, n, vocab, row_start);
   if (ids) token_compact<<<1, 1024, 0, st>>>(row_start, vocab, ids, counts, n_unique);
 }
-template <typename T>
-static void scat_t(const void* dx0, const uint32_t* sorted, const int32_t* rs, int V, int d,
-                   float* de, bool acc, hipStream_t st) {
-  embed_scatter<T><<<V, 256, 0, st>>>((const T*)dx0, sorted, rs, d, de, acc ? 1 : 0);
+void launch_token_compact(const int32_t* row_start, int vocab, int32_t* ids, int32_t* counts, int32_t* n_unique,
+                          hipStream_t st) {
+  token_compact<<<1, 1024, 0, st>>>(row_start, vocab, ids, counts, n_unique);
 }
-void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted,
+template <typename T>
+static void scat_t(const void* dx0, const uint32_t* sorted_pos, const int32_t* rs, int V, int d,
+                   float* de, bool acc, hipStream_t st) {
+  embed_scatter<T><<<V, 256, 0, st>>>((const T*)dx0, sorted_pos, rs, d, de, acc ? 1 : 0);
+}
+void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted_pos,
                           const int32_t* row_start, int vocab, int d, float* de, bool accumulate,
                           hipStream_t st) {
-  DISPATCH(bf, scat_t, dx0, sorted, row_start, vocab, d, de, accumulate, st);
+  DISPATCH(bf, scat_t, dx0, sorted_pos, row_start, vocab, d, de, accumulate, st);
 }
 
 void launch_ce_fwd(const float* logits, const int32_t* targets, int rows, int vocab, float* lse,

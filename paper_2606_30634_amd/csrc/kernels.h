@@ -65,15 +65,18 @@ inline int64_t rms_partial_rows(int rows) {
 void launch_rope(bool bf, void* qkv, int rows, int seq_len, int n_rot_heads, int head_dim, int ld,
                  const float* cos_t, const float* sin_t, bool inverse, hipStream_t st);
 void launch_swiglu_fwd(bool bf, const void* gu, void* z, int rows, int f, hipStream_t st);
-// token sort for the embedding gradient: keys (tok << 14 | pos) ascending, tokens outside
-// [0, vocab) keyed as vocab; n <= 16384
-// rank_part: scratch of SORT_RANK_PARTS * n int32
-constexpr int SORT_RANK_PARTS = 8;
-void launch_token_sort(const int32_t* tok, int n, int vocab, int32_t* rank_part, uint32_t* sorted,
-                       hipStream_t st);
-void launch_token_runs(const uint32_t* sorted, int n, int vocab, int32_t* row_start,
+// token sort for the embedding gradient: positions sorted by token, stably (equal tokens keep
+// ascending positions), tokens outside [0, vocab) keyed as vocab (after every valid one); vocab < 2^17.
+// ws: scratch of token_sort_ws_elems(n) int32.  sorted_tok / sorted_pos: n uint32 each.
+int64_t token_sort_ws_elems(int n);
+void launch_token_sort(const int32_t* tok, int n, int vocab, int32_t* ws, uint32_t* sorted_tok,
+                       uint32_t* sorted_pos, hipStream_t st);
+void launch_token_runs(const uint32_t* sorted_tok, int n, int vocab, int32_t* row_start,
                        int32_t* ids, int32_t* counts, int32_t* n_unique, hipStream_t st);
-void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted,
+// ascending unique ids and their counts from row_start (vocab + 1 entries)
+void launch_token_compact(const int32_t* row_start, int vocab, int32_t* ids, int32_t* counts, int32_t* n_unique,
+                          hipStream_t st);
+void launch_embed_scatter(bool bf, const void* dx0, const uint32_t* sorted_pos,
                           const int32_t* row_start, int vocab, int d, float* de, bool accumulate,
                           hipStream_t st);
 // cross-entropy rows of fp32 logits [rows, vocab]: the forward writes lse and the row loss

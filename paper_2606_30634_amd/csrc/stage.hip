@@ -53,6 +53,12 @@ struct Slot {
   void *hf;         // final norm output (last stage)
   float *rstdf, *logits, *lse_ce;  // head: final-norm statistics, fp32 logits, their row lse
   int32_t *tokens, *targets;
+  // first stage: the microbatch's positions sorted by token (stable) and the start of each token's
+  // run, sorted at forward time on the weight-gradient stream (the tokens are known then); the
+  // backward's embedding-gradient scatter waits for ev_sort
+  uint32_t *sorted_tok = nullptr, *sorted_pos = nullptr;
+  int32_t* row_start = nullptr;
+  hipEvent_t ev_sort = nullptr;
   int64_t step = -1;
   bool pending = false;
 };
@@ -115,8 +121,7 @@ struct stage {
   float* gemm_ws;
   int* flag;
   unsigned long long* skipped;
-  uint32_t* sorted;
-  int32_t *row_start, *rank_part;
+  int32_t* sort_ws;  // the token sort's scratch (its sorts run in order on one stream)
   std::vector<Slot> slots;
   // bookkeeping
   int64_t version_step[2] = {-1, -1};
@@ -263,7 +268,6 @@ int validate(const stage_shape_t* s) {
     return fail(STAGE_EINVAL, "tie_embedding needs a stage with both the embedding and the head");
   const int64_t T = (int64_t)s->seq_len * s->micro_batch;
   if (T > (1 << 24)) return fail(STAGE_EINVAL, "too many tokens per microbatch");
-  if (s->first_stage && T > 16384) return fail(STAGE_EINVAL, "first stage: at most 16384 tokens per microbatch");
   return STAGE_OK;
 }
 
@@ -326,6 +330,9 @@ size_t layout(stage* S, char* base) {
     }
     sl.y = carve(T * d * esz);
     sl.tokens = sh.first_stage ? (int32_t*)carve(T * 4) : nullptr;
+    sl.sorted_tok = sh.first_stage ? (uint32_t*)carve(T * 4) : nullptr;
+    sl.sorted_pos = sh.first_stage ? (uint32_t*)carve(T * 4) : nullptr;
+    sl.row_start = sh.first_stage ? (int32_t*)carve(((int64_t)sh.vocab + 1) * 4) : nullptr;
     sl.targets = sh.last_stage ? (int32_t*)carve(T * 4) : nullptr;
     sl.hf = sh.last_stage ? carve(T * d * esz) : nullptr;
     sl.rstdf = sh.last_stage ? (float*)carve(T * 4) : nullptr;
@@ -351,9 +358,7 @@ size_t layout(stage* S, char* base) {
   S->skipped = (unsigned long long*)carve(8);
   S->cos_t = (float*)carve((int64_t)sh.seq_len * (hd / 2) * 4);
   S->sin_t = (float*)carve((int64_t)sh.seq_len * (hd / 2) * 4);
-  S->sorted = sh.first_stage ? (uint32_t*)carve(T * 4) : nullptr;
-  S->rank_part = sh.first_stage ? (int32_t*)carve((int64_t)SORT_RANK_PARTS * T * 4) : nullptr;
-  S->row_start = sh.first_stage ? (int32_t*)carve(((int64_t)sh.vocab + 1) * 4) : nullptr;
+  S->sort_ws = sh.first_stage ? (int32_t*)carve(token_sort_ws_elems((int)T) * 4) : nullptr;
   S->dlog = sh.last_stage ? carve(T * (int64_t)sh.vocab * esz) : nullptr;
   S->dhf = sh.last_stage ? carve(T * d * esz) : nullptr;
   S->row_loss = sh.last_stage ? (float*)carve(T * 4) : nullptr;
@@ -661,6 +666,8 @@ int stage_init(const stage_shape_t* shape, void* arena, size_t arena_bytes, void
     for (int k = 0; k < S->ng && e == hipSuccess; ++k)
       e = hipEventCreateWithFlags(&S->ev_upd_g[k], hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&S->ev_now, hipEventDisableTiming);
+    for (auto& sl : S->slots)
+      if (e == hipSuccess && shape->first_stage) e = hipEventCreateWithFlags(&sl.ev_sort, hipEventDisableTiming);
     if (e != hipSuccess) {
       stage_destroy(S);
       return fail(STAGE_EHIP, std::string("stage_init: ") + hipGetErrorString(e));
@@ -774,6 +781,16 @@ int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens,
   if (sh.first_stage) {
     HIP_OK(hipMemcpyAsync(sl.tokens, tokens, (size_t)T * 4, hipMemcpyDeviceToDevice, st));
     launch_embed_gather(s->bf, sl.tokens, s->wptr(vi, s->off_embed), x0, T, d, sh.vocab, st);
+    // the embedding gradient's sort needs only the tokens: beside the forward, where there is a
+    // second stream
+    hipStream_t ss = s->wgrad_side ? s->wst : st;
+    if (ss != st) {
+      HIP_OK(hipEventRecord(s->ev_m2s, st));
+      HIP_OK(hipStreamWaitEvent(ss, s->ev_m2s, 0));
+    }
+    launch_token_sort(sl.tokens, T, sh.vocab, s->sort_ws, sl.sorted_tok, sl.sorted_pos, ss);
+    launch_token_runs(sl.sorted_tok, T, sh.vocab, sl.row_start, nullptr, nullptr, nullptr, ss);
+    HIP_OK(hipEventRecord(sl.ev_sort, ss));
   } else {
     HIP_OK(hipMemcpyAsync(x0, x_in, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
   }
@@ -848,9 +865,8 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   join_wgrad(s);  // every weight gradient is in g (the scatter below may add to the tied head's)
   if (sh.first_stage) {
     const void* dx0 = cur;
-    launch_token_sort(sl.tokens, T, sh.vocab, s->rank_part, s->sorted, st);
-    launch_token_runs(s->sorted, T, sh.vocab, s->row_start, nullptr, nullptr, nullptr, st);
-    launch_embed_scatter(bf, dx0, s->sorted, s->row_start, sh.vocab, d, g + s->off_embed,
+    HIP_OK(hipStreamWaitEvent(st, sl.ev_sort, 0));
+    launch_embed_scatter(bf, dx0, sl.sorted_pos, sl.row_start, sh.vocab, d, g + s->off_embed,
                          head_wrote_embed || !first, st);
   } else if (dx_out) {
     HIP_OK(hipMemcpyAsync(dx_out, cur, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
@@ -1246,8 +1262,8 @@ int stage_embed_indices(stage_t* s, int32_t slot, int32_t* ids, int32_t* counts,
   if (slot < 0 || slot >= s->sh.max_inflight) return fail(STAGE_EINVAL, "slot out of range");
   const Slot& sl = s->slots[slot];
   if (sl.step < 0) return fail(STAGE_ESTATE, "slot has not run forward");
-  launch_token_sort(sl.tokens, s->T, s->sh.vocab, s->rank_part, s->sorted, s->st);
-  launch_token_runs(s->sorted, s->T, s->sh.vocab, s->row_start, ids, counts, n_unique, s->st);
+  HIP_OK(hipStreamWaitEvent(s->st, sl.ev_sort, 0));
+  launch_token_compact(sl.row_start, s->sh.vocab, ids, counts, n_unique, s->st);
   HIP_OK(hipGetLastError());
   return STAGE_OK;
 }
@@ -1303,6 +1319,8 @@ void stage_destroy(stage_t* s) {
   for (auto e : s->prof_free) (void)hipEventDestroy(e);
   for (hipEvent_t e : s->ev_grad)
     if (e) (void)hipEventDestroy(e);
+  for (auto& sl : s->slots)
+    if (sl.ev_sort) (void)hipEventDestroy(sl.ev_sort);
   for (hipEvent_t e : s->ev_upd_g)
     if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : s->ev_upd_v)

@@ -12,7 +12,7 @@ pytestmark = pytest.mark.gpu
 REDUCED = dict(n_blocks=1, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, d_ffn=512, vocab=1000)
 
 
-@pytest.mark.parametrize("wname", ["small-reduced", "ragged", "max-tokens", "small"])
+@pytest.mark.parametrize("wname", ["small-reduced", "ragged", "16384-tokens", "32768-tokens", "few-ids", "small"])
 def test_gather_and_indices_bit_exact(wname):
     import torch
     from paper_2606_30634_amd.stage import Stage
@@ -20,8 +20,11 @@ def test_gather_and_indices_bit_exact(wname):
         "small": datagen.SMALL.with_(n_blocks=1),  # the gather and indices do not depend on depth
         "small-reduced": datagen.SMALL.with_(seq_len=96, micro_batch=2, **REDUCED),
         "ragged": datagen.SMALL.with_(seq_len=93, micro_batch=3, **REDUCED),  # 279 positions
-        # the first-stage limit of 16384 positions, over several LDS chunks of keys
-        "max-tokens": datagen.SMALL.with_(seq_len=2048, micro_batch=8, **dict(REDUCED, vocab=32000)),
+        # several 1024-key chunks of the radix sort, and twice the 16384 positions of the former rank sort
+        "16384-tokens": datagen.SMALL.with_(seq_len=2048, micro_batch=8, **dict(REDUCED, vocab=32000)),
+        "32768-tokens": datagen.SMALL.with_(seq_len=4096, micro_batch=8, **dict(REDUCED, vocab=32000)),
+        # 50 ids over 16384 positions: long runs of equal keys across chunks (the sort's stability)
+        "few-ids": datagen.SMALL.with_(seq_len=2048, micro_batch=8, **dict(REDUCED, vocab=50)),
     }[wname]
     log(f"gather/indices {wname}")
     dev = torch.device("cuda:0")
