@@ -15,6 +15,11 @@ Stored (every array float64 unless noted):
   y@t                         rows Y_ROWS of the stage output of step t (flattened tokens), t in Y_AT
 
   python tests/golden/make_small_100.py [--steps 100] [--checkpoint DIR]
+
+With --grad-noise EPS every gradient element is multiplied by (1 + EPS xi), xi standard normal from
+a generator seeded with (--noise-seed, t) at step t, before the update: the same method with a perturbation of the
+size of bf16 arithmetic, whose trajectory shows how far such perturbations alone carry two runs apart
+(--out names its file).
 """
 from __future__ import annotations
 
@@ -52,6 +57,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--checkpoint", default="")
     ap.add_argument("--out", default=OUT)
+    ap.add_argument("--grad-noise", type=float, default=0.0)
+    ap.add_argument("--noise-seed", type=int, default=0)
     args = ap.parse_args()
     w = datagen.SMALL
     p0 = datagen.init_params(w)
@@ -93,6 +100,9 @@ def main():
             save_state(t)
         inp = datagen.step_inputs(w, t, 0)
         grads, outs = model.stage_step_grads(st.x, [inp], w, np.float64)
+        if args.grad_noise > 0:
+            noise = np.random.default_rng([args.noise_seed, t])
+            grads = {n: a * (1.0 + args.grad_noise * noise.standard_normal(a.shape)) for n, a in grads.items()}
         rec["loss"][t] = outs[0]["loss"]
         rec["loss_abs"][t] = outs[0]["loss_abs"]
         if t in GRAD_AT:
