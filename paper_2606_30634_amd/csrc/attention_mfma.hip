@@ -562,54 +562,136 @@ __device__ __forceinline__ void bwd_dkv_block(const AttnArgs& a, int bx, int by,
     const float* Ls = reinterpret_cast<const float*>(Qs + 2 * L::TSZ);
     const float* Dl = Ls + KB;
     const int qs0 = (qblk0 + it % per_head) * KB;
+    if constexpr (HD == 128) {
+      // Both 32-query sub-tiles at once (one wave per SIMD at this head dim, so the wave's own
+      // instruction-level parallelism is what hides latency): the S and dP products of the two
+      // sub-tiles interleaved (four independent accumulator chains), then the softmax of each
+      // sub-tile beside the other's MFMAs.  A sub-tile whose queries all precede the wave's keys
+      // gets P = 0 from the causal mask, so it needs no branch.
+      f32x16 s2[2], dp2[2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int q0t = qs0 + t * 32;
-      if (q0t + 31 < k0) continue;  // every query of this sub-tile precedes every key of the wave
-      f32x16 s, dp;
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
+        for (int e = 0; e < 16; ++e) { s2[t][e] = 0.f; dp2[t][e] = 0.f; }
+      // the Q and dO fragments of the next 16-deep step are read while this step's MFMAs run
+      bf16x8 fq[2][2], fd[2][2];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Qs, t * 32, ks * 16), kf[ks], s, 0, 0, 0);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ds, t * 32, ks * 16), vf[ks], dp, 0, 0, 0);
+      for (int t = 0; t < 2; ++t) {
+        fq[0][t] = frag_rows<HD>(Qs, t * 32, 0);
+        fd[0][t] = frag_rows<HD>(Ds, t * 32, 0);
       }
-      // accumulator rows of this lane: t*32 + 8 (e/4) + 4 half + (e mod 4): four runs of 4
-      // consecutive query rows, so lse and delta arrive as 16-byte reads
-      // every query of the sub-tile sees every key of the wave and exists: no mask (head dim 64
-      // only, as in the dQ kernel)
-      const bool full = HD == 64 && q0t >= k0 + 31 && q0t + 31 < a.S;
+      static_for<KS>([&](auto KSI) {
+        constexpr int ks = KSI, c = ks & 1;
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (ks + 1 < KS) {
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const int r0 = t * 32 + 8 * e4 + 4 * half;
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(Ls + r0);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + r0);
-        if (full) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int e = 4 * e4 + j;
-            const float p = fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j] * LOG2E));
-            s[e] = p;
-            dp[e] = p * (dp[e] - d4[j]);
+          for (int t = 0; t < 2; ++t) {
+            fq[c ^ 1][t] = frag_rows<HD>(Qs, t * 32, (ks + 1) * 16);
+            fd[c ^ 1][t] = frag_rows<HD>(Ds, t * 32, (ks + 1) * 16);
           }
-        } else {
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          s2[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fq[c][t], kf[ks], s2[t], 0, 0, 0);
+          dp2[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fd[c][t], vf[ks], dp2[t], 0, 0, 0);
+        }
+        if constexpr (ks + 1 < KS) {
+          static_for<4>([&](auto) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+          });
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      // dV and dK of each sub-tile: 16 MFMAs, (g2, dt, dV or dK), whose dO or Q fragments (two
+      // transposing reads each) stream through a ring of 4 read 3 MFMAs ahead; the first three
+      // go out before the sub-tile's softmax
+      constexpr int NC = 2 * DT * 2, RA = 3;
+      auto cfrag = [&](auto QI, int t) {
+        constexpr int q = QI, g2 = q / (2 * DT), dt = (q / 2) % DT, isk = q % 2;
+        return frag_cols<HD>(isk ? Qs : Ds, dt * 32, t * 32 + g2 * 16);
+      };
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        bf16x8 fc[RA + 1];
+        static_for<RA>([&](auto QI) { fc[(int)QI] = cfrag(QI, t); });
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int r0 = t * 32 + 8 * e4 + 4 * half;
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(Ls + r0);
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + r0);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int e = 4 * e4 + j, q = qs0 + r0 + j;
-            const float p = (q >= mykey && q < a.S) ? fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j] * LOG2E)) : 0.f;
-            s[e] = p;
-            dp[e] = p * (dp[e] - d4[j]);
+            const float p = (q >= mykey && q < a.S) ? fast_exp2(__builtin_fmaf(s2[t][e], sl2, -l4[j] * LOG2E)) : 0.f;
+            s2[t][e] = p;
+            dp2[t][e] = p * (dp2[t][e] - d4[j]);
           }
         }
+        const bf16x8 pb0 = acc_rows_to_b<0>(s2[t]), pb1 = acc_rows_to_b<8>(s2[t]);
+        const bf16x8 sb0 = acc_rows_to_b<0>(dp2[t]), sb1 = acc_rows_to_b<8>(dp2[t]);
+        static_for<NC>([&](auto QI) {
+          constexpr int q = QI, g2 = q / (2 * DT), dt = (q / 2) % DT, isk = q % 2;
+          __builtin_amdgcn_sched_barrier(0);
+          if constexpr (q + RA < NC) fc[(q + RA) % (RA + 1)] = cfrag(std::integral_constant<int, q + RA>{}, t);
+          if constexpr (isk)
+            dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc[q % (RA + 1)], g2 ? sb1 : sb0, dk[dt], 0, 0, 0);
+          else
+            dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc[q % (RA + 1)], g2 ? pb1 : pb0, dv[dt], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        });
       }
+    } else {
 #pragma unroll
-      for (int g2 = 0; g2 < 2; ++g2) {
-        const bf16x8 pb = g2 ? acc_rows_to_b<8>(s) : acc_rows_to_b<0>(s);
-        const bf16x8 sb = g2 ? acc_rows_to_b<8>(dp) : acc_rows_to_b<0>(dp);
+      for (int t = 0; t < 2; ++t) {
+        const int q0t = qs0 + t * 32;
+        if (q0t + 31 < k0) continue;  // every query of this sub-tile precedes every key of the wave
+        f32x16 s, dp;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Ds, dt * 32, t * 32 + g2 * 16), pb, dv[dt], 0, 0, 0);
-          dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Qs, dt * 32, t * 32 + g2 * 16), sb, dk[dt], 0, 0, 0);
+        for (int e = 0; e < 16; ++e) { s[e] = 0.f; dp[e] = 0.f; }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Qs, t * 32, ks * 16), kf[ks], s, 0, 0, 0);
+          dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ds, t * 32, ks * 16), vf[ks], dp, 0, 0, 0);
+        }
+        // accumulator rows of this lane: t*32 + 8 (e/4) + 4 half + (e mod 4): four runs of 4
+        // consecutive query rows, so lse and delta arrive as 16-byte reads
+        // every query of the sub-tile sees every key of the wave and exists: no mask (head dim 64
+        // only, as in the dQ kernel)
+        const bool full = HD == 64 && q0t >= k0 + 31 && q0t + 31 < a.S;
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int r0 = t * 32 + 8 * e4 + 4 * half;
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(Ls + r0);
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + r0);
+          if (full) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int e = 4 * e4 + j;
+              const float p = fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j] * LOG2E));
+              s[e] = p;
+              dp[e] = p * (dp[e] - d4[j]);
+            }
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int e = 4 * e4 + j, q = qs0 + r0 + j;
+              const float p = (q >= mykey && q < a.S) ? fast_exp2(__builtin_fmaf(s[e], sl2, -l4[j] * LOG2E)) : 0.f;
+              s[e] = p;
+              dp[e] = p * (dp[e] - d4[j]);
+            }
+          }
+        }
+#pragma unroll
+        for (int g2 = 0; g2 < 2; ++g2) {
+          const bf16x8 pb = g2 ? acc_rows_to_b<8>(s) : acc_rows_to_b<0>(s);
+          const bf16x8 sb = g2 ? acc_rows_to_b<8>(dp) : acc_rows_to_b<0>(dp);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Ds, dt * 32, t * 32 + g2 * 16), pb, dv[dt], 0, 0, 0);
+            dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Qs, dt * 32, t * 32 + g2 * 16), sb, dk[dt], 0, 0, 0);
+          }
         }
       }
     }
