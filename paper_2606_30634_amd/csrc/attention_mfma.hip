@@ -450,17 +450,63 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
       // while the softmax of the second runs
       f32x16 s[2], dp[2];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 16; ++e) { s[t][e] = 0.f; dp[t][e] = 0.f; }
+      if constexpr (HD == 128) {
+        // the two sub-tiles' four accumulator chains interleaved, the K and V fragments of the
+        // next 16-deep step read while this step's MFMAs run
+        bf16x8 fk[2][2], fv[2][2];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s[t], 0, 0, 0);
-          dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Vs, t * 32, ks * 16), df[ks], dp[t], 0, 0, 0);
+        for (int t = 0; t < 2; ++t) {
+          fk[0][t] = frag_rows<HD>(Ks, t * 32, 0);
+          fv[0][t] = frag_rows<HD>(Vs, t * 32, 0);
         }
+        static_for<KS>([&](auto KSI) {
+          constexpr int ks = KSI, c = ks & 1;
+          __builtin_amdgcn_sched_barrier(0);
+          if constexpr (ks + 1 < KS) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+              fk[c ^ 1][t] = frag_rows<HD>(Ks, t * 32, (ks + 1) * 16);
+              fv[c ^ 1][t] = frag_rows<HD>(Vs, t * 32, (ks + 1) * 16);
+            }
+          }
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk[c][t], qf[ks], s[t], 0, 0, 0);
+            dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fv[c][t], df[ks], dp[t], 0, 0, 0);
+          }
+          if constexpr (ks + 1 < KS) {
+            static_for<4>([&](auto) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+            });
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        });
+      } else {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s[t], 0, 0, 0);
+            dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Vs, t * 32, ks * 16), df[ks], dp[t], 0, 0, 0);
+          }
       }
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
+        // at head dim 128 the K fragments of the sub-tile's dQ products (two transposing reads
+        // each) go through a ring of 4, read 3 products ahead, the first three before the softmax
+        constexpr int NC = 2 * DT, RA = 3;
+        bf16x8 fc[RA + 1];
+        if constexpr (HD == 128) {
+          static_for<RA>([&](auto QI) {
+            constexpr int q = QI;
+            fc[q] = frag_cols<HD>(Ks, (q % DT) * 32, t * 32 + (q / DT) * 16);
+          });
+          __builtin_amdgcn_sched_barrier(0);
+        }
         // every key of the sub-tile is visible to every query: no mask (head dim 64 only; at 128
         // the second code path costs the kernel its spill-free register budget)
         if (HD == 64 && key0 + t * 32 + 31 <= q0) {
@@ -474,12 +520,24 @@ __device__ __forceinline__ void bwd_dq_block(const AttnArgs& a, int bx, int by, 
             s[t][e] = p * (dp[t][e] - dl);
           }
         }
+        if constexpr (HD == 128) {
+          const bf16x8 b0 = acc_rows_to_b<0>(s[t]), b1 = acc_rows_to_b<8>(s[t]);
+          static_for<NC>([&](auto QI) {
+            constexpr int q = QI, g2 = q / DT, dt = q % DT;
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (q + RA < NC)
+              fc[(q + RA) % (RA + 1)] = frag_cols<HD>(Ks, ((q + RA) % DT) * 32, t * 32 + ((q + RA) / DT) * 16);
+            dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc[q % (RA + 1)], g2 ? b1 : b0, dq[dt], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+          });
+        } else {
 #pragma unroll
-        for (int g2 = 0; g2 < 2; ++g2) {
-          const bf16x8 bop = g2 ? acc_rows_to_b<8>(s[t]) : acc_rows_to_b<0>(s[t]);
+          for (int g2 = 0; g2 < 2; ++g2) {
+            const bf16x8 bop = g2 ? acc_rows_to_b<8>(s[t]) : acc_rows_to_b<0>(s[t]);
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-            dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Ks, dt * 32, t * 32 + g2 * 16), bop, dq[dt], 0, 0, 0);
+            for (int dt = 0; dt < DT; ++dt)
+              dq[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_cols<HD>(Ks, dt * 32, t * 32 + g2 * 16), bop, dq[dt], 0, 0, 0);
+          }
         }
       }
     }
