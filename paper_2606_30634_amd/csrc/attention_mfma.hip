@@ -311,15 +311,33 @@ __global__ void __launch_bounds__(NT) flash_fwd(AttnArgs a) {
     const bf16* Vs = Ks + L::TSZ;
     const int key0 = kb * KB;
     if (key0 <= q0 + 31) {  // some key of this block is visible to some query of this wave
+      // the two sub-tiles' score chains interleaved, the K fragments of the next 16-deep step
+      // read while this step's MFMAs run
       f32x16 s[2];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 16; ++e) s[t][e] = 0.f;
+      bf16x8 fk[2][2];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag_rows<HD>(Ks, t * 32, ks * 16), qf[ks], s[t], 0, 0, 0);
-      }
+      for (int t = 0; t < 2; ++t) fk[0][t] = frag_rows<HD>(Ks, t * 32, 0);
+      static_for<KS>([&](auto KSI) {
+        constexpr int ks = KSI, c = ks & 1;
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (ks + 1 < KS) {
+#pragma unroll
+          for (int t = 0; t < 2; ++t) fk[c ^ 1][t] = frag_rows<HD>(Ks, t * 32, (ks + 1) * 16);
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t) s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fk[c][t], qf[ks], s[t], 0, 0, 0);
+        if constexpr (ks + 1 < KS) {
+          static_for<2>([&](auto) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+          });
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
       // row maximum of the raw scores (the scale is positive), masked on the diagonal block
       float bm = -INFINITY;
       if (key0 + KB - 1 > q0) {
