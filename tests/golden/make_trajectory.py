@@ -1,7 +1,9 @@
-"""Writes tests/golden/small_100_steps.npz: the float64 oracle's trajectory of the small workload
-(3 decoder blocks, d_model 768, 12 heads, SwiGLU 3072, seq 1024 x 8, vocab-32000 embedding on a
-first stage; AdamW, delay 1, Error Feedback lambda 1, clip 1.0, lr 1e-3) over 100 iterations of
-Alg. 1 (§2) with the Error-Feedback step of §3.2.
+"""Writes the float64 oracle's trajectory of a bf16 workload at full size under Alg. 1 (§2) with the
+Error-Feedback step of §3.2 (AdamW, delay 1, lambda 1, clip 1.0, lr 1e-3): tests/golden/small_100_steps.npz,
+the small workload (3 decoder blocks, d_model 768, 12 heads, SwiGLU 3072, seq 1024 x 8, vocab-32000
+embedding on a first stage) over 100 iterations, and tests/golden/mid_10_steps.npz, the mid workload
+(a middle stage of 4 blocks, d_model 2048, 16 heads of 128, SwiGLU 8192, seq 2048 x 4, fed N(0, 1)
+activations) over 10 iterations.
 
 Only the oracle and the seeded input generators are used; nothing comes from the HIP path.
 
@@ -14,7 +16,9 @@ Stored (every array float64 unless noted):
   norm.{dx,m,v,u_prev}@k/<name>  whole-tensor norms ||x_k - x_0||, ||m_k||, ||v_k||, ||u_prev_k||
   y@t                         rows Y_ROWS of the stage output of step t (flattened tokens), t in Y_AT
 
-  python tests/golden/make_small_100.py [--steps 100] [--checkpoint DIR]
+  python tests/golden/make_trajectory.py [--workload small|mid] [--checkpoint DIR]
+      small: state before iterations 2, 3, 10, 50, 100; gradients and output rows of steps 0, 1,
+      10, 50, 99.  mid: state before iterations 2, 3, 10; gradients and output rows of steps 0, 1, 9.
 
 With --grad-noise EPS every gradient element is multiplied by (1 + EPS xi), xi standard normal from
 a generator seeded with (--noise-seed, t) at step t, before the update: the same method with a perturbation of the
@@ -38,13 +42,17 @@ import oracle  # noqa: E402
 from oracle import model  # noqa: E402
 from oracle.update import OptState, iteration_update  # noqa: E402
 
-STATE_AT = (2, 3, 10, 50, 100)
-GRAD_AT = (0, 1, 10, 50, 99)
-Y_AT = (0, 1, 10, 50, 99)
 SLICE = 512
 SLICE_SEED = 20250611
 Y_ROWS = (0, 1, 1023, 1024, 4095, 8191)
-OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "small_100_steps.npz")
+HERE = os.path.dirname(os.path.abspath(__file__))
+# per workload: iterations, state / gradient / output points, output file
+PLANS = {
+    "small": dict(steps=100, state_at=(2, 3, 10, 50, 100), grad_at=(0, 1, 10, 50, 99), y_at=(0, 1, 10, 50, 99),
+                  out=os.path.join(HERE, "small_100_steps.npz")),
+    "mid": dict(steps=10, state_at=(2, 3, 10), grad_at=(0, 1, 9), y_at=(0, 1, 9),
+                out=os.path.join(HERE, "mid_10_steps.npz")),
+}
 
 
 def slice_offsets(params):
@@ -54,13 +62,18 @@ def slice_offsets(params):
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--workload", default="small", choices=sorted(PLANS))
+    ap.add_argument("--steps", type=int, default=0)
     ap.add_argument("--checkpoint", default="")
-    ap.add_argument("--out", default=OUT)
+    ap.add_argument("--out", default="")
     ap.add_argument("--grad-noise", type=float, default=0.0)
     ap.add_argument("--noise-seed", type=int, default=0)
     args = ap.parse_args()
-    w = datagen.SMALL
+    plan = PLANS[args.workload]
+    args.steps = args.steps or plan["steps"]
+    args.out = args.out or plan["out"]
+    STATE_AT, GRAD_AT, Y_AT = plan["state_at"], plan["grad_at"], plan["y_at"]
+    w = datagen.WORKLOADS[args.workload]
     p0 = datagen.init_params(w)
     offs = slice_offsets(p0)
     hp = oracle.hparams_of(w)
@@ -70,7 +83,7 @@ def main():
         rec[f"offsets/{n}"] = np.array(o, dtype=np.int64)
     x0 = {n: v.astype(np.float64) for n, v in p0.items()}
     t0 = 0
-    ck = os.path.join(args.checkpoint, "small_100_ckpt.npz") if args.checkpoint else ""
+    ck = os.path.join(args.checkpoint, f"{args.workload}_ckpt.npz") if args.checkpoint else ""
     if ck and os.path.exists(ck):
         z = np.load(ck)
         t0 = int(z["t"])

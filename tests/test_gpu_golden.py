@@ -123,27 +123,30 @@ FREE_GRAD_AT = (0, 1)
 V_TOL = 2 * TOL
 
 
-@pytest.mark.timeout(900)
-def test_small_workload_100_steps():
+def _trajectory(w, z, label, at_step=None):
+    """Runs the stage free for len(z["loss"]) iterations on the workload's inputs, comparing with the
+    stored trajectory z: returns the stage (after its last update), the comparisons held to the bar
+    (errs, with their tolerances in tols) and those only reported (diag).  at_step(t, st, y, inp_h)
+    runs after step t's backward, before its update."""
     import torch
     from paper_2606_30634_amd.stage import Stage
-    from oracle import model
-    z = _load("small_100_steps.npz")
-    w = datagen.SMALL
     dev = torch.device("cuda:0")
     p0 = datagen.init_params(w)
     names = list(p0)
     offs = {n: int(z[f"offsets/{n}"]) for n in names}
     cnt = 512
     steps = len(z["loss"])
+    state_pts = sorted(int(k.split("@")[1].split("/")[0]) for k in z.files
+                       if k.startswith("norm.dx@") and k.split("/", 1)[1] == names[0])
+    grad_pts = sorted(int(k.split("@")[1]) for k in z.files if k.startswith("y@"))
     x0 = {n: torch.from_numpy(p0[n].reshape(-1)).double() for n in names}
     st = Stage(shape_of(w), "cuda:0")
     st.load_master(p0)
     hp = hp_of(w)
-    errs, tols, diag = {}, {}, {}
+    errs, diag = {}, {}
     y = torch.empty(w.micro_batch, w.seq_len, w.d_model, dtype=torch.bfloat16, device=dev)
     rows = [0, 1, 1023, 1024, 4095, 8191]
-    log(f"golden small: {steps} free-running iterations")
+    log(f"golden {label}: {steps} free-running iterations")
 
     def state_at(k):
         # held to the bar: weights and whole-tensor norms through step 10, m and v slices through
@@ -165,7 +168,53 @@ def test_small_workload_100_steps():
                 e = rel(full[offs[n]:offs[n] + cnt].cpu().numpy(), z[f"{pre}@{k}/{n}"])
                 (errs if pre != "u_prev" and k in FREE_MOMENT_AT else diag)[f"{pre}@{k}.{n}"] = e
 
-    def teacher_forced(t, inp_h, sensitivity):
+    for t in range(steps):
+        if t in state_pts:
+            state_at(t)
+        inp_h = datagen.step_inputs(w, t, 0)
+        inp = to_device(inp_h, w, dev)
+        if w.first_stage:
+            st.forward(0, t, tokens=inp["tokens"], y_out=y)
+        else:
+            st.forward(0, t, x_in=inp["x_in"], y_out=y)
+        st.backward(0, dy=inp["dy"])
+        if at_step is not None:
+            at_step(t, st, y, inp_h)
+        if t in grad_pts:
+            torch.cuda.synchronize()
+            out = errs if t in FREE_GRAD_AT else diag
+            for n in names:
+                g = st.view(f"grad{t % 2}.{n}").double()[offs[n]:offs[n] + cnt].cpu().numpy()
+                if np.linalg.norm(z[f"g@{t}/{n}"]) > 0:
+                    out[f"g@{t}.{n}"] = rel(g, z[f"g@{t}/{n}"])
+            yr = y.float().reshape(-1, w.d_model)[rows].cpu().numpy()
+            out[f"y@{t}"] = rel(yr, z[f"y@{t}"])
+        loss = float((y.double() * inp["dy"].double()).sum())
+        errs[f"loss@{t}"] = abs(loss - float(z["loss"][t])) / float(z["loss_abs"][t])
+        st.update(t, hp)
+    if steps in state_pts:
+        state_at(steps)
+    tols = {key: V_TOL for key in errs if key.startswith(("v@", "|v|@"))}
+    for k in sorted({int(key.split("@")[1].split(".")[0]) for key in diag}):
+        ks = {key: e for key, e in diag.items() if int(key.split("@")[1].split(".")[0]) == k}
+        log(f"  free-running step {k} (reported, not held to 2e-2): {len(ks)} values, median "
+            f"{float(np.median(list(ks.values()))):.2e}, max {max(ks.values()):.2e}")
+    return st, y, errs, tols, diag
+
+
+@pytest.mark.timeout(900)
+def test_small_workload_100_steps():
+    import torch
+    from oracle import model
+    z = _load("small_100_steps.npz")
+    w = datagen.SMALL
+    dev = torch.device("cuda:0")
+    p0 = datagen.init_params(w)
+    names = list(p0)
+    steps = len(z["loss"])
+    tf_errs = {}
+
+    def teacher_forced(st, y, t, inp_h, sensitivity):
         # the oracle's gradient at the GPU's own weights x_t (float64, from the fp32 master); with
         # `sensitivity`, also at the weights rounded to bf16, whose distance from the first is the
         # bf16 move the bar allows for
@@ -187,34 +236,13 @@ def test_small_workload_100_steps():
                 log(f"  {n}: GPU {e[f'g@{t}.{n}']:.2e}, bf16-weight move of the exact gradient {move:.2e}")
         return e, bars
 
-    for t in range(steps):
-        if t in (2, 3, 10, 50):
-            state_at(t)
-        inp_h = datagen.step_inputs(w, t, 0)
-        inp = to_device(inp_h, w, dev)
-        st.forward(0, t, tokens=inp["tokens"], y_out=y)
-        st.backward(0, dy=inp["dy"])
+    def at_step(t, st, y, inp_h):
         if t == 50:
-            e, _ = teacher_forced(t, inp_h, False)
-            errs.update({f"teacher-forced {k}": v for k, v in e.items()})
-        if t in (0, 1, 10, 50, 99):
-            torch.cuda.synchronize()
-            out = errs if t in FREE_GRAD_AT else diag
-            for n in names:
-                g = st.view(f"grad{t % 2}.{n}").double()[offs[n]:offs[n] + cnt].cpu().numpy()
-                if np.linalg.norm(z[f"g@{t}/{n}"]) > 0:
-                    out[f"g@{t}.{n}"] = rel(g, z[f"g@{t}/{n}"])
-            yr = y.float().reshape(-1, w.d_model)[rows].cpu().numpy()
-            out[f"y@{t}"] = rel(yr, z[f"y@{t}"])
-        loss = float((y.double() * inp["dy"].double()).sum())
-        errs[f"loss@{t}"] = abs(loss - float(z["loss"][t])) / float(z["loss_abs"][t])
-        st.update(t, hp)
-    state_at(steps)
-    tols.update({key: V_TOL for key in errs if key.startswith(("v@", "|v|@"))})
-    for k in sorted({int(key.split("@")[1].split(".")[0]) for key in diag}):
-        ks = {key: e for key, e in diag.items() if int(key.split("@")[1].split(".")[0]) == k}
-        log(f"  free-running step {k} (reported, not held to 2e-2): {len(ks)} values, median "
-            f"{float(np.median(list(ks.values()))):.2e}, max {max(ks.values()):.2e}")
+            e, _ = teacher_forced(st, y, t, inp_h, False)
+            tf_errs.update({f"teacher-forced {k}": v for k, v in e.items()})
+
+    st, y, errs, tols, _ = _trajectory(w, z, "small", at_step)
+    errs.update(tf_errs)
     _report(f"golden small {steps} free-running steps", errs, tols)
 
     # iteration `steps` teacher-forced: the gradient against the bar above, then the update
@@ -223,12 +251,22 @@ def test_small_workload_100_steps():
     inp = to_device(inp_h, w, dev)
     st.forward(0, t, tokens=inp["tokens"], y_out=y)
     st.backward(0, dy=inp["dy"])
-    tf, bars = teacher_forced(t, inp_h, True)
+    tf, bars = teacher_forced(st, y, t, inp_h, True)
     _report(f"golden small teacher-forced gradient {t}", tf, bars)
     rng = np.random.default_rng(11)
     nflat = st.tensors["flat.master"][1]
     sample = [(int(a) // 64 * 64, 65536) for a in rng.integers(0, nflat - 65536, size=16)]
-    e = _update_in_place(st, w, hp, t, sample)
+    e = _update_in_place(st, w, hp_of(w), t, sample)
     log(f"golden small: teacher-forced update {t} on 16 slices, worst rel {e:.3e}")
     assert e < 1e-5
     st.close()
+
+
+@pytest.mark.timeout(600)
+def test_mid_workload_10_steps():
+    # the mid workload at full size (a middle stage: d_model 2048, heads of 128, SwiGLU 8192, seq
+    # 2048 x 4) free-running over 10 iterations, within the window where the bf16 bar is well-posed
+    z = _load("mid_10_steps.npz")
+    st, _, errs, tols, _ = _trajectory(datagen.MID, z, "mid")
+    st.close()
+    _report(f"golden mid {len(z['loss'])} free-running steps", errs, tols)
