@@ -862,15 +862,19 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
     block_backward(s, vi, sl.blk[i], s->boff[i], cur, out, g, first);
     cur = out;
   }
-  join_wgrad(s);  // every weight gradient is in g (the scatter below may add to the tied head's)
   if (sh.first_stage) {
+    // the scatter reads the sorted positions and the activation gradient and writes the
+    // embedding's rows, which only a tied head's weight-gradient product also writes: it runs
+    // beside the remaining weight-gradient products
     const void* dx0 = cur;
     HIP_OK(hipStreamWaitEvent(st, sl.ev_sort, 0));
+    if (head_wrote_embed) after_wgrad(s, WG_HEAD);
     launch_embed_scatter(bf, dx0, sl.sorted_pos, sl.row_start, sh.vocab, d, g + s->off_embed,
                          head_wrote_embed || !first, st);
   } else if (dx_out) {
     HIP_OK(hipMemcpyAsync(dx_out, cur, (size_t)T * d * s->esz, hipMemcpyDeviceToDevice, st));
   }
+  join_wgrad(s);  // every weight gradient is in g
   HIP_OK(hipEventRecord(s->ev_bwd[vi], st));
   s->ev_bwd_set[vi] = true;
   HIP_OK(hipEventRecord(s->ev_grad[gb], st));
