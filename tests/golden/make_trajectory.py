@@ -20,9 +20,12 @@ Stored (every array float64 unless noted):
       small: state before iterations 2, 3, 10, 50, 100; gradients and output rows of steps 0, 1,
       10, 50, 99.  mid: state before iterations 2, 3, 10; gradients and output rows of steps 0, 1, 9.
 
-With --grad-noise EPS every gradient element is multiplied by (1 + EPS xi), xi standard normal from
-a generator seeded with (--noise-seed, t) at step t, before the update: the same method with a perturbation of the
-size of bf16 arithmetic, whose trajectory shows how far such perturbations alone carry two runs apart
+With --grad-noise EPS every gradient element g is perturbed before the update, by xi standard
+normal from a generator seeded with (--noise-seed, t) at step t: multiplied by (1 + EPS xi)
+(--noise-kind relative, which keeps every element's sign), or added EPS rms xi with rms the tensor's
+root mean square (--noise-kind additive: the shape of an accumulated rounding error, which can flip
+the sign of the tensor's smallest elements).  It is the same method with a perturbation of the size
+of bf16 arithmetic, whose trajectory shows how far such perturbations alone carry two runs apart
 (--out names its file).
 """
 from __future__ import annotations
@@ -68,6 +71,7 @@ def main():
     ap.add_argument("--out", default="")
     ap.add_argument("--grad-noise", type=float, default=0.0)
     ap.add_argument("--noise-seed", type=int, default=0)
+    ap.add_argument("--noise-kind", default="relative", choices=("relative", "additive"))
     args = ap.parse_args()
     plan = PLANS[args.workload]
     args.steps = args.steps or plan["steps"]
@@ -115,7 +119,11 @@ def main():
         grads, outs = model.stage_step_grads(st.x, [inp], w, np.float64)
         if args.grad_noise > 0:
             noise = np.random.default_rng([args.noise_seed, t])
-            grads = {n: a * (1.0 + args.grad_noise * noise.standard_normal(a.shape)) for n, a in grads.items()}
+            if args.noise_kind == "relative":
+                grads = {n: a * (1.0 + args.grad_noise * noise.standard_normal(a.shape)) for n, a in grads.items()}
+            else:
+                grads = {n: a + args.grad_noise * np.sqrt(np.mean(a * a)) * noise.standard_normal(a.shape)
+                         for n, a in grads.items()}
         rec["loss"][t] = outs[0]["loss"]
         rec["loss_abs"][t] = outs[0]["loss_abs"]
         if t in GRAD_AT:
