@@ -290,6 +290,9 @@ def main():
     ap.add_argument("--vocab", type=int, default=0, help="head vocabulary of a last-stage workload")
     ap.add_argument("--update-steps", type=int, default=50,
                     help="iterations of the update-only workload (1.0e9 fp32 elements); 0 skips it")
+    ap.add_argument("--overlap-mode", type=int, choices=(1, 2), default=None,
+                    help="update overlap mode (2: the update's elementwise pass in chunks beside the "
+                         "attention backwards); default 2 for the large and mid workloads, else 1")
     ap.add_argument("--calib-copy", action="store_true",
                     help="run one plain 1 GiB device-to-device copy first (a known-size reference for "
                          "the FETCH_SIZE / WRITE_SIZE counters)")
@@ -346,8 +349,13 @@ def main():
     warm = max(0, min(w.max_inflight - 1, M))
 
     # overlap mode: delayed_update(t) - it reads x_t and g_{t-1} only - is issued before step t's
-    # forwards and backwards and runs beside them on the stage's update stream
-    st.set_update_overlap(True)
+    # forwards and backwards and runs beside them on the stage's update stream.  Mode 2 runs its
+    # elementwise pass in chunks beside the step's attention backwards instead of beside the first
+    # forwards' products: measured 351-352 against 358-359 ms per step on the large workload and
+    # 14.9-15.0 against 15.1 on the mid one, while the small workload's attention backwards (under
+    # 0.2 ms) slow by more than the pass saves (2.89 against 2.83 ms).
+    mode = args.overlap_mode or (2 if args.workload in ("large", "mid") and not muon else 1)
+    st.set_update_overlap(mode)
 
     def step(t):
         st.update(t, hp)
@@ -464,6 +472,7 @@ def main():
                                   "adan": "Adan (betas 0.98, 0.92, 0.99)"}[args.optimizer]) +
                                 (" with SAPipe weight prediction (updated state)" if args.predict else "") +
                                 f", delay {args.delay}, Error Feedback lambda {lam:g}, clip 1.0",
+                   "update_overlap_mode": mode,
                    "parallelism": "1 GPU, one stage"},
         "roofline": roofline,
         "kernels": kern,

@@ -291,7 +291,18 @@ int stage_poll_nonfinite(stage_t* s, int64_t* skipped);
  * update).  A caller may then issue delayed_update(t) before step t's forwards and backwards, and
  * the update runs beside them on the stage's own stream (Alg. 1: x_{t+1} depends only on x_t and
  * g_{t-1}).  Reads of the master weights or optimizer state through stage_tensor() views must
- * follow stage_join_update() or a device synchronisation.  Turning it off joins. */
+ * follow stage_join_update() or a device synchronisation.  Turning it off joins.
+ * on = 2: as 1, and the elementwise pass of each delayed_update (AdamW, Lion, NAdam, the
+ * prediction; not Muon's or Adan's) is deferred in chunks, one per attention backward the stage
+ * runs in a step (n_blocks x the microbatches_per_step of the last stage_backward; chunks of at
+ * least 2^16 elements): each stage_backward launches the next chunk on the update stream as a
+ * block's attention backward starts, so that the pass's HBM traffic runs beside work bound by the
+ * matrix cores instead of beside the forward's products.  The results are those of mode 1
+ * (elementwise pass, bit for bit).  Chunks not launched by then are launched by the first call that
+ * needs the update: the forward that reads the version it writes, the backward that overwrites the
+ * gradient buffer it reads, the next delayed_update, stage_join_update, stage_sync_weights, or a
+ * change of mode; view reads must follow stage_join_update() (a device synchronisation alone does
+ * not launch them).  Other values: STAGE_EINVAL. */
 int stage_set_update_overlap(stage_t* s, int32_t on);
 
 /* The stage stream waits for every delayed_update issued so far (no-op when none is owed). */

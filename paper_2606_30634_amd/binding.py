@@ -197,8 +197,8 @@ def stage_grad_norm(s: int, which: int, norm_dev) -> None:
     _call("stage_grad_norm", s, which, norm_dev)
 
 
-def stage_set_update_overlap(s: int, on: bool) -> None:
-    _call("stage_set_update_overlap", s, int(on))
+def stage_set_update_overlap(s: int, mode: int) -> None:
+    _call("stage_set_update_overlap", s, int(mode))
 
 
 def stage_join_update(s: int) -> None:

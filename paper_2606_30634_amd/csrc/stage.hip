@@ -84,9 +84,29 @@ struct stage {
   // whole; ev_upd_v[v] marks the end of the update that wrote compute version v, ev_upd_g[j] of the
   // one that read gradient buffer j, and the first stage-stream call that reads that version or
   // overwrites that buffer waits on it (the flags say a wait is still owed).
-  bool overlap = false;
+  int overlap = 0;  // 0 off, 1 on, 2 on with the update's elementwise pass deferred (pend)
   hipEvent_t ev_upd_v[2] = {}, ev_upd_g[STAGE_MAX_DELAY + 1] = {};
   bool upd_owed_v[2] = {}, upd_owed_g[STAGE_MAX_DELAY + 1] = {}, upd_owed_all = false;
+  // Mode 2: the elementwise pass of the last delayed_update waits on the host as chunks
+  // [offset, offset + count) of the flat vector.  Each stage_backward that reaches a block's
+  // attention backward launches the next chunk on the update stream beside it (that work keeps the
+  // matrix cores busy and leaves HBM bandwidth idle, where the forward's products beside a whole
+  // pass would share it), and every call that needs the update's results launches the rest first.
+  // The other fields are the pass's arguments.
+  struct PendingPass {
+    std::vector<std::pair<int64_t, int64_t>> chunks;
+    size_t next = 0;
+    const float* g = nullptr;
+    float* up = nullptr;
+    void* shadow = nullptr;
+    UpdateScalars hs{};
+    const float* clip = nullptr;
+    const int* flag = nullptr;
+    double bytes = 0;  // HBM bytes per element
+    int vout = 0, gb = 0;
+    bool apply = false;
+  } pend;
+  int last_mb = 1;  // microbatches per step of the last stage_backward (attention backwards per block)
   // The weight-gradient products (fp32 output) of a backward run on a second stream of their own,
   // beside the activation-gradient chain: ev_m2s orders one after the stage stream's work so far,
   // ev_wg[k] marks the end of the last product of kind k (the stage stream waits on it before it
@@ -197,6 +217,31 @@ void timed(stage* S, int cls, double work, F&& launch, hipStream_t on = nullptr)
     (void)hipEventSynchronize(b);
     prof_collect(S);
   }
+}
+
+// Overlap mode 2: launches the next deferred chunk of the update pass on the update stream and
+// moves the update's completion events past it (a stage-stream wait issued before the launch would
+// not cover the chunk, so every such wait is preceded by flush_pending).
+void launch_pending_chunk(stage* S) {
+  auto& p = S->pend;
+  const int64_t o = p.chunks[p.next].first, n = p.chunks[p.next].second;
+  ++p.next;
+  timed(S, STAGE_PROF_UPDATE, p.bytes * n, [&] {
+    launch_fused_update(n, S->master + o, p.g + o, false, S->m + o, S->v + o, p.up ? p.up + o : nullptr,
+                        (char*)p.shadow + o * S->esz, S->bf ? 2 : 1, p.hs, p.clip, p.flag, device_cu_count(),
+                        S->ust);
+  }, S->ust);
+  (void)hipEventRecord(S->ev_upd, S->ust);
+  (void)hipEventRecord(S->ev_upd_v[p.vout], S->ust);
+  if (p.apply) (void)hipEventRecord(S->ev_upd_g[p.gb], S->ust);
+  if (p.next == p.chunks.size()) {
+    p.chunks.clear();
+    p.next = 0;
+  }
+}
+
+void flush_pending(stage* S) {
+  while (!S->pend.chunks.empty()) launch_pending_chunk(S);
 }
 
 // activation products on the stage stream (no split-K: the workspace belongs to the
@@ -602,6 +647,12 @@ void block_backward(stage* S, int vi, BlockAct& b, const BlockOff& w, const void
   a.rope_cos = S->cos_t;  // dq, dk come back w.r.t. the unrotated projections
   a.rope_sin = S->sin_t;
   after_wgrad(S, WG_QKV);
+  if (!S->pend.chunks.empty()) {
+    // a deferred chunk of the update pass (overlap mode 2) starts with the attention backward
+    (void)hipEventRecord(S->ev_now, st);
+    (void)hipStreamWaitEvent(S->ust, S->ev_now, 0);
+    launch_pending_chunk(S);
+  }
   timed(S, STAGE_PROF_ATTN_BWD, 2.0 * attn_fwd_flops(S), [&] { launch_attention_bwd(bf, a, st); });
   // qkv projection: dn1 = dqkv Wqkv ; dWqkv (+)= dqkv^T n1
   run_gemm(S, gemm(T, d, S->qkvw, S->dqkv, S->qkvw, true, S->wptr(vi, w.wqkv), d, false, S->dn, d));
@@ -729,6 +780,7 @@ int stage_tensor_by_name(const stage_t* s, const char* name, void** dev_ptr, int
 
 int stage_join_update(stage_t* s) {
   if (!s) return fail(STAGE_EINVAL, "null stage");
+  flush_pending(s);
   if (s->upd_owed_all) {
     HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd, 0));
     s->upd_owed_all = false;
@@ -740,8 +792,10 @@ int stage_join_update(stage_t* s) {
 
 int stage_set_update_overlap(stage_t* s, int32_t on) {
   if (!s) return fail(STAGE_EINVAL, "null stage");
+  if (on < 0 || on > 2) return fail(STAGE_EINVAL, "overlap mode must be 0, 1 or 2");
+  if (on < 2) flush_pending(s);
   if (!on) stage_join_update(s);
-  s->overlap = on != 0;
+  s->overlap = on;
   return STAGE_OK;
 }
 
@@ -771,6 +825,7 @@ int stage_forward(stage_t* s, int32_t slot, int64_t step, const int32_t* tokens,
   Slot& sl = s->slots[slot];
   if (sl.pending) return fail(STAGE_ESTATE, "slot holds a microbatch whose backward is pending");
   const int vi = (int)(step % 2);
+  if (vi == s->pend.vout) flush_pending(s);  // the deferred pass writes this version
   if (s->upd_owed_v[vi]) {
     HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd_v[vi], 0));
     s->upd_owed_v[vi] = false;
@@ -824,6 +879,8 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   if (microbatches_per_step <= 0) return fail(STAGE_EINVAL, "microbatches_per_step must be positive");
   const int64_t step = sl.step;
   const int gb = (int)(step % s->ng), vi = (int)(step % 2);
+  s->last_mb = microbatches_per_step;
+  if (s->pend.apply && gb == s->pend.gb) flush_pending(s);  // the deferred pass reads this buffer
   if (s->upd_owed_g[gb]) {
     HIP_OK(hipStreamWaitEvent(s->st, s->ev_upd_g[gb], 0));
     s->upd_owed_g[gb] = false;
@@ -885,6 +942,10 @@ int stage_backward(stage_t* s, int32_t slot, const void* dy, void* dx_out, int32
   return STAGE_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
 // Scalars of the fused elementwise pass for the k-th applied update (k >= 1 when apply): the
 // AdamW bias corrections, Lion's betas, NAdam's momentum-schedule coefficients (mu_j = b1 (1 -
 // 0.5 0.96^(j psi)), P_k = mu_1 ... mu_k, in double), and the bias corrections of update k + 1 for
@@ -933,6 +994,10 @@ int check_update_hparams(const update_hparams_t* hp) {
   return STAGE_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
 int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   if (!s || !hp) return fail(STAGE_EINVAL, "null argument");
   if (hp->delay < 0 || hp->delay > s->ndelay)
@@ -968,6 +1033,7 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
   // Order the update after the backwards whose gradient it reads (buffer gb) and after the last
   // use of the version it overwrites (parity vout); with no such backward on record, after
   // everything on the stage stream.
+  flush_pending(s);  // the previous update's deferred chunks go first
   hipStream_t us = s->ust;
   bool after_all = false;
   if (s->ev_bwd_set[vout]) HIP_OK(hipStreamWaitEvent(us, s->ev_bwd[vout], 0));
@@ -1113,10 +1179,31 @@ int delayed_update(stage_t* s, int64_t t, const update_hparams_t* hp) {
                                s->ver[vout], s->bf ? 2 : 1, hs, clip, flag, device_cu_count(), us);
     }, us);
   } else {
-    timed(s, STAGE_PROF_UPDATE, ub * s->n_flat, [&] {
-      launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v, up, s->ver[vout],
-                          s->bf ? 2 : 1, hs, clip, flag, device_cu_count(), us);
-    }, us);
+    // overlap mode 2: one chunk per attention backward the stage runs in a step (of at least 2^16
+    // elements, 1024-aligned), launched beside them; otherwise the whole pass now
+    const int64_t nchunk = s->overlap == 2
+        ? std::min<int64_t>((int64_t)s->sh.n_blocks * s->last_mb, s->n_flat >> 16) : 1;
+    if (nchunk > 1) {
+      auto& p = s->pend;
+      const int64_t per = (s->n_flat / nchunk + 1023) / 1024 * 1024;
+      for (int64_t o = 0; o < s->n_flat; o += per) p.chunks.emplace_back(o, std::min(per, s->n_flat - o));
+      p.next = 0;
+      p.g = s->grad[gb];
+      p.up = up;
+      p.shadow = s->ver[vout];
+      p.hs = hs;
+      p.clip = clip;
+      p.flag = flag;
+      p.bytes = ub;
+      p.vout = vout;
+      p.gb = gb;
+      p.apply = apply;
+    } else {
+      timed(s, STAGE_PROF_UPDATE, ub * s->n_flat, [&] {
+        launch_fused_update(s->n_flat, s->master, s->grad[gb], false, s->m, s->v, up, s->ver[vout],
+                            s->bf ? 2 : 1, hs, clip, flag, device_cu_count(), us);
+      }, us);
+    }
   }
   HIP_OK(hipGetLastError());
   // everything enqueued on the stage stream from here on runs after the update

@@ -86,9 +86,11 @@ class Stage:
         """Continue a run at iteration next_t from the state written through the views."""
         B.stage_resume(self.handle, next_t, delay)
 
-    def set_update_overlap(self, on: bool):
-        """Overlap mode: the stage stream waits for an update only where the delay needs it."""
-        B.stage_set_update_overlap(self.handle, on)
+    def set_update_overlap(self, mode: int):
+        """Overlap mode 1: the stage stream waits for an update only where the delay needs it; 2: also
+        the update's elementwise pass deferred in chunks beside the attention backwards (state views
+        after join_update()); 0: off."""
+        B.stage_set_update_overlap(self.handle, int(mode))
 
     def join_update(self):
         """The stage stream waits for every update issued so far."""

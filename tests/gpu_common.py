@@ -67,14 +67,15 @@ def schedule_1f1b(M: int, warm: int):
 
 def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps: Iterable[int] = (),
             device: str = "cuda:0", upd_steps: Iterable[int] = (), muon: bool = False,
-            early_update: bool = False, after_backward=None):
+            early_update: bool = False, after_backward=None, overlap_mode: int = 1):
     """T iterations of Alg. 1 on the GPU stage.  Returns losses (per step, per microbatch), outputs
     at y_steps, and at grad_steps the gradient g_t together with the master weights x_t it was taken
     at, at upd_steps the whole optimizer state before and after delayed_update(t) with the gradient
     it consumed (and, under "u_slot", the EF buffer iteration t uses), plus the final master / m / v /
     u_prev and every EF buffer ("u_ring", buffer j = iterations j mod tau).
 
-    early_update: the stage in overlap mode, and delayed_update(t) issued before step t's forwards
+    early_update: the stage in overlap mode (overlap_mode 1, or 2 with the update's elementwise pass
+    deferred beside the attention backwards), and delayed_update(t) issued before step t's forwards
     and backwards (it consumes g_{t-1}), so that it runs beside them.
     after_backward(t, stage): called after step t's backwards, before delayed_update(t)."""
     import torch
@@ -85,7 +86,7 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     st = Stage(shape_of(w, muon=muon or hp.optimizer == 1, max_delay=tau, adan=hp.optimizer == 4), device)
     st.load_master(params0)
     if early_update:
-        st.set_update_overlap(True)
+        st.set_update_overlap(overlap_mode)
     names = list(params0)
     grad_steps, y_steps = set(grad_steps), set(y_steps)
     M = w.microbatches_per_step
@@ -99,6 +100,8 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
         return {n: st.view(pre + n).float().cpu().numpy().reshape(params0[n].shape).copy() for n in names}
 
     def state(g_idx=None, u_slot=None):
+        if early_update and overlap_mode == 2:
+            st.join_update()          # launches the deferred chunks
         torch.cuda.synchronize(dev)   # the update stream too (overlap mode)
         d = {pre: grab(pre) for pre in ("", "m.", "v.", "u_prev.")}
         if g_idx is not None:
@@ -116,6 +119,8 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
 
     for t in range(steps):
         if t in grad_steps:   # x_t, before an early update(t) starts writing x_{t+1}
+            if early_update and overlap_mode == 2:
+                st.join_update()
             torch.cuda.synchronize(dev)
             res["x_at"][t] = {n: st.view(n).float().cpu().numpy().reshape(params0[n].shape).copy() for n in names}
         if early_update:
@@ -154,6 +159,8 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
         res["losses"].append(losses)
         if not early_update:
             update(t)
+    if early_update and overlap_mode == 2:
+        st.join_update()
     torch.cuda.synchronize(dev)
     final = {}
     for pre in ("", "m.", "v.", "u_prev."):

@@ -85,6 +85,41 @@ def test_overlapped_early_update(w):
              state_tol=None if w.dtype == "f32" else 5e-2)
 
 
+@pytest.mark.parametrize("w", ["tiny", "large-reduced"])
+def test_deferred_update_pass_bit_identical(w):
+    # overlap mode 2: the update's elementwise pass deferred in chunks launched beside the step's
+    # attention backwards gives the trajectory of mode 1 bit for bit (the pass is elementwise), and
+    # does run in chunks
+    from paper_2606_30634_amd import binding as B
+    w = datagen.TINY if w == "tiny" else LARGE_R
+    steps = 6
+    p0 = datagen.init_params(w)
+    runs, launches = {}, {}
+    for mode in (1, 2):
+        def hook(t, st, mode=mode):
+            if t == 0:
+                B.stage_profile_enable(st.handle, True)
+            if t == steps - 2:
+                launches[mode] = B.stage_profile_read(st.handle, B.PROF_UPDATE)[1]
+        log(f"{w.name}: {steps} steps, update issued first, overlap mode {mode}")
+        runs[mode] = run_gpu(w, steps, hp_of(w), p0, grad_steps=(0, steps - 1), y_steps=(0, steps - 1),
+                             upd_steps=(1, 2, steps - 1), early_update=True, overlap_mode=mode, after_backward=hook)
+    a, b = runs[1], runs[2]
+    log(f"{w.name}: update launches over iterations 1..{steps - 2}: mode 1 {launches[1]}, mode 2 {launches[2]}")
+    assert launches[1] == steps - 2 and launches[2] >= 2 * launches[1]
+    assert a["losses"] == b["losses"]
+    for t in a["ys"]:
+        for ya, yb in zip(a["ys"][t], b["ys"][t]):
+            assert np.array_equal(ya, yb), f"output of step {t}"
+    for pre in ("", "m.", "v.", "u_prev."):
+        for n in p0:
+            assert np.array_equal(a["final"][pre][n], b["final"][pre][n]), f"final {pre}{n}"
+    for t in a["upd"]:
+        for k in a["upd"][t][1]:
+            for n in p0:
+                assert np.array_equal(a["upd"][t][1][k][n], b["upd"][t][1][k][n]), f"state {k}{n} after update {t}"
+
+
 @pytest.mark.parametrize("lam", [0.0, 1.0])
 def test_tiny_fp32_untied_last_stage(lam):
     # a last stage that is not the first: input activations, given targets, its own head matrix
