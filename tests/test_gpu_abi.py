@@ -46,6 +46,9 @@ def test_call_order_errors():
     with pytest.raises(B.StageError) as e:
         st.update(3, hp)                                 # g_2 was never computed
     assert e.value.code == B.STAGE_ESTATE
+    with pytest.raises(B.StageError) as e:
+        st.set_update_overlap(3)                         # modes 0, 1, 2
+    assert e.value.code == B.STAGE_EINVAL
     torch.cuda.synchronize()
     st.close()
 
