@@ -173,6 +173,25 @@ def run_gpu(w, steps: int, hp, params0, grad_steps: Iterable[int] = (), y_steps:
     return res
 
 
+def run_oracle_noisy(w, steps: int, hp_oracle, params0, eps=0.012, seed=7, dt=np.float64):
+    """The oracle's iterations with every gradient perturbed before its update by additive noise of
+    eps times its tensor's rms (xi standard normal from a generator seeded with (seed, t)): an error
+    of the size and kind of bf16 accumulation, which changes the signs of a tensor's smallest
+    elements.  How far this run ends from the clean one is how far the method itself carries such
+    an error.  Returns the final x, m, v and EF buffer."""
+    from oracle import model
+    from oracle.update import OptState, iteration_update
+    st = OptState.create(params0, dt)
+    for t in range(steps):
+        x_t = st.x if st.x_compute is None else st.x_compute
+        inps = [datagen.step_inputs(w, t, i) for i in range(w.microbatches_per_step)]
+        grads, _ = model.stage_step_grads(x_t, inps, w, dt)
+        rng = np.random.default_rng([seed, t])
+        grads = {n: a + eps * np.sqrt(np.mean(a * a)) * rng.standard_normal(a.shape) for n, a in grads.items()}
+        iteration_update(st, grads, hp_oracle)
+    return {"": st.x, "m.": st.m, "v.": st.v, "u_prev.": st.u_prev}
+
+
 def oracle_grads_at(w, t, x_t, dt=np.float64):
     """The oracle's gradient g_t of step t's microbatches, taken at the given weights (teacher forcing)."""
     from oracle import model

@@ -6,7 +6,7 @@ import pytest
 
 import datagen
 import oracle
-from gpu_common import hp_of, log, oracle_grads_at, rel, run_gpu, run_oracle
+from gpu_common import hp_of, log, oracle_grads_at, rel, run_gpu, run_oracle, run_oracle_noisy
 
 pytestmark = pytest.mark.gpu
 
@@ -195,3 +195,15 @@ def test_reduced_bf16_100_steps(w):
     g = run_gpu(w, steps, hp_of(w), p0, grad_steps=(0, steps - 1), upd_steps=(1, steps - 1))
     o = run_oracle(w, steps, oracle.hparams_of(w), p0, grad_steps=(0, steps - 1))
     _compare(w, g, o, 2e-2, (0, steps - 1), f"{w.name} 100 steps", state_tol=1e-1)
+    # against the method's own sensitivity: the final weights, moments and EF buffer at most 1.5
+    # times as far (median over the parameters) from the float64 run as the float64 run with
+    # gradient noise of bf16 size ends up
+    noisy = run_oracle_noisy(w, steps, oracle.hparams_of(w), p0)
+    ratios = {}
+    for pre in ("", "m.", "v.", "u_prev."):
+        ge = [rel(g["final"][pre][n], o["final"][pre][n]) for n in p0]
+        ne = [rel(noisy[pre][n], o["final"][pre][n]) for n in p0]
+        ratios[pre or "x."] = float(np.median(ge)) / float(np.median(ne))
+    log(f"{w.name} 100 steps, final median error / noise-perturbed oracle's: " +
+        ", ".join(f"{k[:-1]}={r:.2f}" for k, r in ratios.items()))
+    assert all(r <= 1.5 for r in ratios.values()), ratios
