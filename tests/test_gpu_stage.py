@@ -165,6 +165,21 @@ WIDE_LARGE_R = datagen.LARGE.with_(name="large-width-reduced", n_blocks=1, d_mod
                                    microbatches_per_step=2, max_inflight=2)
 
 
+def _noise_envelope(w, steps, p0, g, o, label):
+    # against the method's own sensitivity: the final weights, moments and EF buffer at most 1.5
+    # times as far (median over the parameters) from the float64 run as the float64 run with
+    # gradient noise of bf16 size ends up
+    noisy = run_oracle_noisy(w, steps, oracle.hparams_of(w), p0)
+    ratios = {}
+    for pre in ("", "m.", "v.", "u_prev."):
+        ge = [rel(g["final"][pre][n], o["final"][pre][n]) for n in p0]
+        ne = [rel(noisy[pre][n], o["final"][pre][n]) for n in p0]
+        ratios[pre or "x."] = float(np.median(ge)) / float(np.median(ne))
+    log(f"{label}, final median error / noise-perturbed oracle's: " +
+        ", ".join(f"{k[:-1]}={r:.2f}" for k, r in ratios.items()))
+    assert all(r <= 1.5 for r in ratios.values()), ratios
+
+
 @pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, TILED_R, LAST_R, LAST_TILED_R, WIDE_MID_R, WIDE_LARGE_R],
                          ids=lambda w: w.name)
 def test_reduced_bf16_stages(w):
@@ -177,8 +192,10 @@ def test_reduced_bf16_stages(w):
     # bf16 free-running optimizer state: Adam turns noise-level gradient differences into lr-sized
     # differences of m / sqrt(v) wherever a gradient element is near zero, so m and v drift further
     # than the weights; they are held to 5e-2.  The EF buffer (the last update, sign-like wherever a
-    # gradient is at noise level) is checked teacher-forced only.
+    # gradient is at noise level) is checked teacher-forced, and with the rest of the final state
+    # against the noise-perturbed oracle run.
     _compare(w, g, o, 2e-2, (0, 1, steps - 1), w.name, state_tol=5e-2)
+    _noise_envelope(w, steps, p0, g, o, f"{w.name} {steps} steps")
 
 
 @pytest.mark.parametrize("w", [SMALL_R, MID_R, LARGE_R, LAST_R], ids=lambda w: w.name)
@@ -195,15 +212,4 @@ def test_reduced_bf16_100_steps(w):
     g = run_gpu(w, steps, hp_of(w), p0, grad_steps=(0, steps - 1), upd_steps=(1, steps - 1))
     o = run_oracle(w, steps, oracle.hparams_of(w), p0, grad_steps=(0, steps - 1))
     _compare(w, g, o, 2e-2, (0, steps - 1), f"{w.name} 100 steps", state_tol=1e-1)
-    # against the method's own sensitivity: the final weights, moments and EF buffer at most 1.5
-    # times as far (median over the parameters) from the float64 run as the float64 run with
-    # gradient noise of bf16 size ends up
-    noisy = run_oracle_noisy(w, steps, oracle.hparams_of(w), p0)
-    ratios = {}
-    for pre in ("", "m.", "v.", "u_prev."):
-        ge = [rel(g["final"][pre][n], o["final"][pre][n]) for n in p0]
-        ne = [rel(noisy[pre][n], o["final"][pre][n]) for n in p0]
-        ratios[pre or "x."] = float(np.median(ge)) / float(np.median(ne))
-    log(f"{w.name} 100 steps, final median error / noise-perturbed oracle's: " +
-        ", ".join(f"{k[:-1]}={r:.2f}" for k, r in ratios.items()))
-    assert all(r <= 1.5 for r in ratios.values()), ratios
+    _noise_envelope(w, steps, p0, g, o, f"{w.name} 100 steps")
