@@ -1,17 +1,18 @@
-"""Writes tests/golden/small_100_noise_profile.json: how far the small workload's float64 oracle
-trajectory moves over 100 iterations of Alg. 1 with Error Feedback when every gradient is perturbed
-by an error of the size of bf16 arithmetic, measured with the comparisons the GPU test makes
-against the clean trajectory (norm-wise relative errors of the stored slices, relative errors of
-the whole-tensor norms), as the median and the maximum over the parameters at every stored point.
-Two perturbations (make_trajectory.py --grad-noise 0.012 --noise-seed 7): relative (each element
-times 1 + 0.012 xi: no sign changes) and additive (0.012 times the tensor's rms times xi: the
-tensor's smallest elements change sign, as under an accumulated rounding error).
+"""Writes tests/golden/<workload>_<steps>_noise_profile.json: how far a workload's float64 oracle
+trajectory (small: 100 iterations of Alg. 1 with Error Feedback, mid: 10) moves when every
+gradient is perturbed by an error of the size of bf16 arithmetic, measured with the comparisons the
+GPU test makes against the clean trajectory (norm-wise relative errors of the stored slices,
+relative errors of the whole-tensor norms), as the median and the maximum over the parameters at
+every stored point.  Perturbations (make_trajectory.py --grad-noise 0.012 --noise-seed 7): additive
+(0.012 times the tensor's rms times xi: the tensor's smallest elements change sign, as under an
+accumulated rounding error) and, for the small workload, relative (each element times
+1 + 0.012 xi: no sign changes).
 
-Only oracle output is read: the clean trajectory (small_100_steps.npz) and the perturbed ones.
+Only oracle output is read: the clean trajectory (<workload>_<steps>_steps.npz) and the perturbed ones.
 
-  python tests/golden/make_trajectory.py --grad-noise 0.012 --noise-seed 7 --noise-kind relative --out REL.npz
-  python tests/golden/make_trajectory.py --grad-noise 0.012 --noise-seed 7 --noise-kind additive --out ADD.npz
-  python tests/golden/make_noise_profile.py REL.npz ADD.npz
+  python tests/golden/make_trajectory.py --workload W --grad-noise 0.012 --noise-seed 7 --noise-kind additive --out ADD.npz
+  python tests/golden/make_trajectory.py --workload W --grad-noise 0.012 --noise-seed 7 --noise-kind relative --out REL.npz
+  python tests/golden/make_noise_profile.py --workload W --additive ADD.npz [--relative REL.npz]
 """
 from __future__ import annotations
 
@@ -56,14 +57,23 @@ def profile(clean, noisy):
 
 
 def main():
-    clean = np.load(os.path.join(HERE, "small_100_steps.npz"))
+    import argparse
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", choices=("small", "mid"), default="small")
+    ap.add_argument("--additive", required=True)
+    ap.add_argument("--relative")
+    args = ap.parse_args()
+    name = {"small": "small_100", "mid": "mid_10"}[args.workload]
+    clean = np.load(os.path.join(HERE, f"{name}_steps.npz"))
     rec = {"grad_noise": 0.012, "noise_seed": 7}
-    for kind, path in zip(("relative", "additive"), sys.argv[1:3]):
+    for kind, path in (("relative", args.relative), ("additive", args.additive)):
+        if not path:
+            continue
         res = profile(clean, np.load(path))
         rec[kind] = res
         for k, v in res.items():
             print(f"{kind:8s} {k:14s} median {v['median']:.3e} max {v['max']:.3e} (n {v['n']})")
-    path = os.path.join(HERE, "small_100_noise_profile.json")
+    path = os.path.join(HERE, f"{name}_noise_profile.json")
     with open(path, "w") as f:
         json.dump(rec, f, indent=1)
     print(f"wrote {path}")

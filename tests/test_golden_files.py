@@ -1,14 +1,15 @@
-"""Consistency of the stored noise profile (tests/golden/small_100_noise_profile.json, written by
-make_noise_profile.py from oracle runs only), which the 100-iteration GPU test holds its later
-free-running points against.  CPU only: reads the JSON, runs nothing."""
+"""Consistency of the stored noise profiles (tests/golden/small_100_noise_profile.json and
+mid_10_noise_profile.json, written by make_noise_profile.py from oracle runs only), which the
+full-size GPU trajectory tests hold their later free-running points against.  CPU only: reads the
+JSON, runs nothing."""
 import json
 import os
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
-def _profile():
-    with open(os.path.join(GOLDEN, "small_100_noise_profile.json")) as f:
+def _profile(name="small_100"):
+    with open(os.path.join(GOLDEN, f"{name}_noise_profile.json")) as f:
         return json.load(f)
 
 
@@ -43,3 +44,16 @@ def test_perturbed_runs_separate_over_the_iterations():
         for q in ("x", "m", "v", "u_prev"):
             meds = [p[kind][f"{q}@{k}"]["median"] for k in (10, 50, 100)]
             assert meds[0] < meds[1] < meds[2], (kind, q, meds)
+
+
+def test_mid_profile_injected_noise():
+    # the mid workload's perturbed run (additive noise only): the same size at steps 0 and 1, no
+    # output change before the first update, and the weights and momentum separating from step 3
+    # to step 10
+    p = _profile("mid_10")["additive"]
+    for point in ("g@0", "g@1"):
+        assert abs(p[point]["median"] - 0.012) < 0.0006, (point, p[point])
+    for point in ("y@0", "y@1"):
+        assert p[point]["max"] == 0.0, point
+    for q in ("x", "m"):
+        assert p[f"{q}@3"]["median"] < p[f"{q}@10"]["median"], q
