@@ -127,10 +127,10 @@ FREE_GRAD_AT = (0, 1)
 # v is quadratic in the gradient: a gradient within 2e-2 gives v within about 4e-2
 V_TOL = 2 * TOL
 # Beyond the window, the free-running values are held against the method's own sensitivity: the
-# float64 oracle run of the same 100 iterations with every gradient element perturbed by 1.2 % of
-# its tensor's rms (make_trajectory.py --grad-noise 0.012 --noise-kind additive, an error of the
-# size and kind of bf16 accumulation: the smallest elements change sign) separates from the clean
-# run by the medians in small_100_noise_profile.json; the GPU's median error at each point may not
+# float64 oracle run of the same iterations with every gradient element perturbed by 1.2 % of its
+# tensor's rms (make_trajectory.py --grad-noise 0.012 --noise-kind additive, an error of the size
+# and kind of bf16 accumulation: the smallest elements change sign) separates from the clean run by
+# the medians in <workload>_<steps>_noise_profile.json; the GPU's median error at each point may not
 # exceed that by more than this factor.
 NOISE_ENVELOPE = 1.5
 
@@ -138,7 +138,8 @@ NOISE_ENVELOPE = 1.5
 def _trajectory(w, z, label, at_step=None):
     """Runs the stage free for len(z["loss"]) iterations on the workload's inputs, comparing with the
     stored trajectory z: returns the stage (after its last update), the comparisons held to the bar
-    (errs, with their tolerances in tols) and those only reported (diag).  at_step(t, st, y, inp_h)
+    (errs, with their tolerances in tols) and those beyond the 2e-2 window (diag), which the caller
+    holds against the noise-perturbed oracle run.  at_step(t, st, y, inp_h)
     runs after step t's backward, before its update."""
     import torch
     from paper_2606_30634_amd.stage import Stage
@@ -209,7 +210,7 @@ def _trajectory(w, z, label, at_step=None):
     tols = {key: V_TOL for key in errs if key.startswith(("v@", "|v|@"))}
     for k in sorted({int(key.split("@")[1].split(".")[0]) for key in diag}):
         ks = {key: e for key, e in diag.items() if int(key.split("@")[1].split(".")[0]) == k}
-        log(f"  free-running step {k} (reported, not held to 2e-2): {len(ks)} values, median "
+        log(f"  free-running step {k} (beyond the 2e-2 window): {len(ks)} values, median "
             f"{float(np.median(list(ks.values()))):.2e}, max {max(ks.values()):.2e}")
     return st, y, errs, tols, diag
 
