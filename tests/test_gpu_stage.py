@@ -85,13 +85,14 @@ def test_overlapped_early_update(w):
              state_tol=None if w.dtype == "f32" else 5e-2)
 
 
-@pytest.mark.parametrize("w", ["tiny", "large-reduced"])
-def test_deferred_update_pass_bit_identical(w):
+@pytest.mark.parametrize("case", ["tiny", "tiny-delay2", "large-reduced"])
+def test_deferred_update_pass_bit_identical(case):
     # overlap mode 2: the update's elementwise pass deferred in chunks launched beside the step's
     # attention backwards gives the trajectory of mode 1 bit for bit (the pass is elementwise), and
-    # does run in chunks
+    # does run in chunks; with a delay of 2 as well (gradient and EF rings)
     from paper_2606_30634_amd import binding as B
-    w = datagen.TINY if w == "tiny" else LARGE_R
+    w = LARGE_R if case == "large-reduced" else datagen.TINY
+    hp = hp_of(w, delay=2, ef_lambda=2.0) if case == "tiny-delay2" else hp_of(w)
     steps = 6
     p0 = datagen.init_params(w)
     runs, launches = {}, {}
@@ -102,8 +103,8 @@ def test_deferred_update_pass_bit_identical(w):
             if t == steps - 2:
                 launches[mode] = B.stage_profile_read(st.handle, B.PROF_UPDATE)[1]
         log(f"{w.name}: {steps} steps, update issued first, overlap mode {mode}")
-        runs[mode] = run_gpu(w, steps, hp_of(w), p0, grad_steps=(0, steps - 1), y_steps=(0, steps - 1),
-                             upd_steps=(1, 2, steps - 1), early_update=True, overlap_mode=mode, after_backward=hook)
+        runs[mode] = run_gpu(w, steps, hp, p0, grad_steps=(0, steps - 1), y_steps=(0, steps - 1),
+                             upd_steps=(2, 3, steps - 1), early_update=True, overlap_mode=mode, after_backward=hook)
     a, b = runs[1], runs[2]
     log(f"{w.name}: update launches over iterations 1..{steps - 2}: mode 1 {launches[1]}, mode 2 {launches[2]}")
     assert launches[1] == steps - 2 and launches[2] >= 2 * launches[1]
