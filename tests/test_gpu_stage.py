@@ -85,11 +85,13 @@ def test_overlapped_early_update(w):
              state_tol=None if w.dtype == "f32" else 5e-2)
 
 
-@pytest.mark.parametrize("case", ["tiny", "tiny-delay2", "large-reduced"])
+@pytest.mark.parametrize("case", ["tiny", "tiny-delay2", "tiny-skip", "large-reduced"])
 def test_deferred_update_pass_bit_identical(case):
     # overlap mode 2: the update's elementwise pass deferred in chunks launched beside the step's
     # attention backwards gives the trajectory of mode 1 bit for bit (the pass is elementwise), and
-    # does run in chunks; with a delay of 2 as well (gradient and EF rings)
+    # does run in chunks; with a delay of 2 as well (gradient and EF rings), and with an infinity
+    # in the gradient of step 2, whose update every chunk skips
+    import torch
     from paper_2606_30634_amd import binding as B
     w = LARGE_R if case == "large-reduced" else datagen.TINY
     hp = hp_of(w, delay=2, ef_lambda=2.0) if case == "tiny-delay2" else hp_of(w)
@@ -98,6 +100,10 @@ def test_deferred_update_pass_bit_identical(case):
     runs, launches = {}, {}
     for mode in (1, 2):
         def hook(t, st, mode=mode):
+            if case == "tiny-skip" and t == 2:
+                torch.cuda.synchronize()
+                st.view(f"grad0.{next(iter(p0))}")[5] = float("inf")
+                torch.cuda.synchronize()
             if t == 0:
                 B.stage_profile_enable(st.handle, True)
             if t == steps - 2:
@@ -108,6 +114,7 @@ def test_deferred_update_pass_bit_identical(case):
     a, b = runs[1], runs[2]
     log(f"{w.name}: update launches over iterations 1..{steps - 2}: mode 1 {launches[1]}, mode 2 {launches[2]}")
     assert launches[1] == steps - 2 and launches[2] >= 2 * launches[1]
+    assert a["skipped"] == b["skipped"] == (1 if case == "tiny-skip" else 0)
     assert a["losses"] == b["losses"]
     for t in a["ys"]:
         for ya, yb in zip(a["ys"][t], b["ys"][t]):
