@@ -431,6 +431,11 @@ def main():
                           "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4),
                           "work_per_launch": work / n}
     B.stage_profile_enable(st.handle, False)
+    if mode == 2 and "delayed_update" in kern and kern["delayed_update"]["launches"] > args.steps:
+        # its chunks share the chip with the attention backwards by design; the pass's own HBM
+        # roofline is the update-only workload's
+        kern["delayed_update"]["note"] = ("elementwise pass in chunks beside the attention backwards (overlap "
+                                          "mode 2); the pass alone: update_workload")
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
     kd = kern[dom]
     roofline = {"kernel": dom, "bound": kd["bound"], "achieved": kd["achieved"], "peak": kd["peak"],
